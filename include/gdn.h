@@ -1,0 +1,149 @@
+/*
+ * gdn.h — C ABI of the gated-delta-rule chunked forward and training backward
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper Sec. 4.1, Eq. (gdn), scalar gates b = w = beta and a
+ * scalar log-decay g — the KDA row of the family table with a scalar gate):
+ * for every sequence n and head h, a state S (d_k x d_v, fp32) evolves as
+ *
+ *     S_t = (I - beta_t k_t k_t^T) exp(g_t) S_{t-1} + beta_t k_t v_t^T,
+ *     o_t = S_t^T q_t,
+ *
+ * starting from S0 and ending at S_T.  gdn_fwd computes o, S_T and the state
+ * before every chunk of 64 tokens (the sequential inter-chunk carry of the
+ * paper's chunked form, Sec. 4.2).  gdn_bwd computes the gradients of the
+ * loss  sum(dO * o) + <dS_T, S_T>  with respect to q, k, v, g, beta and S0;
+ * it walks the chunks in reverse with an fp32 state-gradient carry (the
+ * reverse inter-chunk state scan, K#1 in Sec. 4.2) and differentiates the
+ * chunk-local triangular solve T = (I + A)^{-1} by reusing T (the WY /
+ * triangular-inverse VJP, K#2 in Sec. 4.2) without re-inverting.
+ *
+ * Family members (paper, table "One recurrence, five models"):
+ *   GDN_GATED_DELTA  the recurrence above;
+ *   GDN_DELTA        DeltaNet: g == 0 (g and dg are NULL);
+ *   GDN_DECAY_ONLY   scalar-decay SSD / Mamba-2: S_t = exp(g_t) S_{t-1} + k_t v_t^T
+ *                    (beta and dbeta are NULL).
+ *
+ * Layouts (row-major, token-major; every pointer is DEVICE memory unless
+ * stated otherwise):
+ *   q, k          [B, T, H, d_k]    io_dtype
+ *   v, o, dO      [B, T, H, d_v]    io_dtype
+ *   dq, dk        [B, T, H, d_k]    io_dtype
+ *   dv            [B, T, H, d_v]    io_dtype
+ *   g, beta       [B, T, H]         float32 (per-token scalars)
+ *   dg, dbeta     [B, T, H]         float32
+ *   S0, S_T, dS_T, dS0   [N, H, d_k, d_v]  float32, element S[k][v]
+ *   chunk_states  [sum_n ceil(L_n / 64), H, d_k, d_v]  float32
+ * Packed variable-length input: B = 1, T = sum_n L_n, sequence n occupies
+ * tokens [cu_seqlens[n], cu_seqlens[n+1]), N = num_seqs.  Otherwise N = B and
+ * every sequence has length T.  Sequence n's chunk states start at entry
+ * sum_{m<n} ceil(L_m / 64); entry c holds the state before the sequence's
+ * token 64 c (so its first entry equals S0).  The last chunk of a sequence may
+ * be partial.  Only chunk_states carries data from gdn_fwd to gdn_bwd.
+ *
+ * io_dtype GDN_BF16 means bfloat16 activations with fp32 gates and states; the
+ * chunk-local products then run on bf16 matrix cores with fp32 accumulation.
+ * GDN_F32 keeps every operand in fp32 (fp32 matrix cores).
+ *
+ * Supported: chunk == 64, d_k in {64, 128}, d_v in {64, 128, 256}, T >= 0,
+ * sequence lengths >= 0.  Anything else returns GDN_ERR_UNSUPPORTED.
+ *
+ * Non-finite inputs: a (sequence, head) stream whose inputs hold a NaN or Inf
+ * is recomputed token by token in fp32 in the operation order written above,
+ * so NaN/Inf land on exactly the outputs that order determines.
+ *
+ * Ownership and threading: the caller allocates every buffer, including the
+ * workspace (size from gdn_*_workspace_size).  The library never allocates,
+ * frees or synchronises; all work is enqueued on `stream` (a hipStream_t; NULL
+ * is the default stream) and the call returns without waiting.  There is no
+ * global mutable state: calls are reentrant and thread-safe; two calls that
+ * share a workspace must not overlap on the device.  Workspace contents are
+ * undefined between calls.
+ *
+ * Errors: every argument is validated on the host before anything is
+ * enqueued; on error nothing is launched and no output is touched.  Outputs
+ * whose byte ranges overlap an input or another output -> GDN_ERR_ALIAS.  A
+ * failed launch returns GDN_ERR_HIP.  Device faults surface at the caller's
+ * next synchronisation.  No C++ exception crosses this interface.
+ *
+ * Determinism: outputs are bitwise identical across runs for identical
+ * inputs (no floating-point atomics; every output element has one writer and a
+ * fixed reduction order).
+ */
+#ifndef GDN_H_
+#define GDN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GDN_OK = 0,
+  GDN_ERR_NULL = -1,        /* a required pointer is NULL */
+  GDN_ERR_SHAPE = -2,       /* negative or inconsistent sizes */
+  GDN_ERR_UNSUPPORTED = -3, /* chunk, d_k or d_v outside the supported set */
+  GDN_ERR_DTYPE = -4,       /* unknown io_dtype */
+  GDN_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required */
+  GDN_ERR_ALIAS = -6,       /* an output overlaps an input or another output */
+  GDN_ERR_VARLEN = -7,      /* cu_seqlens not 0-based, non-decreasing, ending at T */
+  GDN_ERR_HIP = -8,         /* a kernel launch failed */
+  GDN_ERR_VARIANT = -9      /* unknown variant, or a gate pointer that the
+                               variant forbids / requires */
+} gdn_status;
+
+typedef enum { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
+
+typedef enum {
+  GDN_GATED_DELTA = 0,
+  GDN_DELTA = 1,      /* g == 0: g and dg must be NULL */
+  GDN_DECAY_ONLY = 2  /* no delta term: beta and dbeta must be NULL */
+} gdn_variant;
+
+typedef struct {
+  int32_t B, T, H, dk, dv, chunk; /* chunk must be 64 */
+  int32_t num_seqs;               /* N: B, or the number of packed sequences */
+  /* Packed sequences: both NULL, or both non-NULL with identical contents
+   * [num_seqs + 1].  The host copy is read during the call (validation and
+   * chunk counts); the device copy is read by the kernels. */
+  const int32_t* cu_seqlens_host;
+  const int32_t* cu_seqlens_dev;
+  gdn_dtype io_dtype;
+  gdn_variant variant;
+} gdn_problem;
+
+/* Number of chunk states, sum_n ceil(L_n / 64); negative gdn_status on a
+ * malformed problem. */
+int64_t gdn_num_chunks(const gdn_problem* p);
+
+/* Bytes of device workspace gdn_fwd / gdn_bwd need (0 on a malformed problem).
+ * The workspace must be 256-byte aligned. */
+size_t gdn_fwd_workspace_size(const gdn_problem* p);
+size_t gdn_bwd_workspace_size(const gdn_problem* p);
+
+/* Forward.  S0 may be NULL (zero initial state).  Writes o, S_T and
+ * chunk_states. */
+gdn_status gdn_fwd(const gdn_problem* p, const void* q, const void* k, const void* v,
+                   const float* g, const float* beta, const float* S0, void* o, float* S_T,
+                   float* chunk_states, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward.  chunk_states must hold gdn_fwd's output for the same inputs.
+ * dS_T may be NULL (zero).  Writes dq, dk, dv, dg, dbeta and dS0. */
+gdn_status gdn_bwd(const gdn_problem* p, const void* q, const void* k, const void* v,
+                   const float* g, const float* beta, const float* chunk_states, const void* dO,
+                   const float* dS_T, void* dq, void* dk, void* dv, float* dg, float* dbeta,
+                   float* dS0, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* gdn_status_str(gdn_status s);
+
+/* Library version string. */
+const char* gdn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDN_H_ */

@@ -1,0 +1,626 @@
+// Training backward of the chunked gated delta rule on gfx950.  Only the
+// chunk states cross from the forward; everything else is recomputed.
+//
+//   prep   one block per (chunk, head): G, T = (I + A)^{-1}, W = T diag(beta e^G) K,
+//          and dV_loc = P^T dO with P = (Q K^T) * D.
+//   scan   the reverse inter-chunk state scan (paper Sec. 4.2, K#1): one block
+//          per (stream, value tile); an fp32 carry dh walks the chunks from the
+//          last to the first,
+//            dU' = dV_loc + Khat dh,   dh <- e^{G_last} dh + Q^T diag(e^G) dO - W^T dU',
+//          storing the carry that enters every chunk; dS0 is the final carry.
+//   grad   one block per (chunk, head): every chunk-local gradient, with the
+//          triangular-inverse VJP (paper Sec. 4.2, K#2) that reuses T in four
+//          triangular products, dA = -T^T dT T^T, and never re-inverts.
+//
+// The grad kernel avoids W and U: with R = diag(beta) V - diag(beta e^G) K h,
+//   U' = T R,   Y = T^T dU',   X = -Y h^T  (= T^T dW),   dT = dU' R^T,
+// which follow from W = T diag(beta e^G) K, U = T diag(beta) V, dW = -dU' h^T.
+// Per chunk, with h the state entering the chunk and dh the carry leaving it:
+//   dP  = dO U'^T,              dQ = diag(e^G) dO h^T + (dP * D) K
+//   dK  = (dP * D)^T Q + diag(e^{G_last - G}) U' dh^T + diag(beta e^G) X
+//         + (dB + dB^T) K,      dB = dA * beta_r * E   (strict lower)
+//   dV  = diag(beta) Y,         dbeta_r = v_r.Y_r + e^{G_r} k_r.X_r + sum_i dA_ri (K K^T)_ri E_ri
+//   dG_r = rowsum_r(Z) - colsum_r(Z) + e^{G_r} (q_r.(dO h^T)_r + beta_r k_r.X_r)
+//          - khat_r.dkhat_r,   Z = dA * A + dP * P,
+//   dG_last += e^{G_last} <h, dh> + sum_r khat_r.dkhat_r,   dg = reverse cumsum of dG.
+#pragma once
+
+#include "gdn_chunk.hpp"
+#include "gdn_launch.hpp"
+
+namespace gdn {
+
+template <int DK, int DV, typename OP, int VAR>
+__global__ __launch_bounds__(256) void k_prep_bwd(Geo geo, int H, const OP* __restrict__ q,
+                                                  const OP* __restrict__ k, const float* __restrict__ g,
+                                                  const float* __restrict__ beta, const OP* __restrict__ dO,
+                                                  float* __restrict__ gcum, OP* __restrict__ Wg,
+                                                  float* __restrict__ dvlg, int* __restrict__ flag) {
+  constexpr int LK = DK + pad_of<OP>();
+  constexpr int LC = CH + 4;
+  constexpr int LT = CH + pad_of<OP>();
+  constexpr int VS = 64;
+  constexpr int LVS = VS + pad_of<OP>();
+  __shared__ __align__(16) OP Qs[CH * LK];
+  __shared__ __align__(16) OP Ks[CH * LK];
+  __shared__ __align__(16) float As[VAR != VAR_DECAY ? CH * LC : 1];
+  __shared__ __align__(16) float Tf[VAR != VAR_DECAY ? CH * LC : 1];
+  __shared__ __align__(16) OP Ts[(VAR != VAR_DECAY && sizeof(OP) == 2) ? CH * LT : 1];
+  __shared__ __align__(16) OP PT[CH * LT];
+  __shared__ __align__(16) OP dOs[CH * LVS];
+  __shared__ __align__(16) float Xs[4 * 16 * 20];
+  __shared__ float Gs[CH], Bs[CH], GBs[CH];
+
+  const int ci = blockIdx.x, h = blockIdx.y;
+  const ChunkPos cp = chunk_pos(geo, ci);
+  const long tile = (long)ci * H + h;
+  bool ok = load_gates<VAR>(g, beta, cp.row0, H, h, cp.len, Gs, Bs);
+  ok &= load_rows<DK, LK>(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Qs);
+  ok &= load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
+  __syncthreads();
+  if (threadIdx.x < CH) {
+    gcum[tile * CH + threadIdx.x] = Gs[threadIdx.x];
+    GBs[threadIdx.x] = Bs[threadIdx.x] * expf(Gs[threadIdx.x]);
+  }
+  {
+    Tiles<CH, CH, 2, 2> p;
+    p.zero();
+    p.template mma<OP, DK>(KRow<OP, LK>{Qs}, KRow<OP, LK>{Ks});
+    p.each([&](int r, int i, float& x) {
+      PT[i * LT + r] = from_f<OP>(i <= r ? x * expf(Gs[r] - Gs[i]) : 0.f);
+    });
+  }
+  if constexpr (VAR != VAR_DECAY) {
+    Tiles<CH, CH, 2, 2> bm;
+    bm.zero();
+    bm.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{Ks});
+    bm.each([&](int r, int i, float& x) {
+      As[r * LC + i] = (i < r) ? Bs[r] * x * expf(Gs[r] - Gs[i]) : 0.f;
+    });
+    __syncthreads();
+    unit_lower_inverse<OP, LC, LT>(As, Tf, Ts, Xs);
+    const OP* Tp;
+    if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = Tf;
+    constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
+    Tiles<CH, DK, 2, 2> w;
+    w.zero();
+    w.template mma<OP, CH>(KRow<OP, LTT>{Tp}, kfun<OP>([&](int d, int i) {
+                             return from_f<OP>(GBs[i] * to_f(Ks[i * LK + d]));
+                           }));
+    OP* Wt = Wg + tile * CH * DK;
+    w.each([&](int r, int d, float& x) { Wt[r * DK + d] = from_f<OP>(x); });
+  }
+  // dV_loc = P^T dO, in slices of VS value columns
+  const OP* dop = dO + (cp.row0 * H + h) * DV;
+  float* dvl = dvlg + tile * CH * DV;
+  for (int c0 = 0; c0 < DV; c0 += VS) {
+    ok &= load_rows<VS, LVS>(dop + c0, (long)H * DV, cp.len, dOs);
+    __syncthreads();
+    Tiles<CH, VS, 2, 2> t;
+    t.zero();
+    t.template mma<OP, CH>(KRow<OP, LT>{PT}, KCol<OP, LVS>{dOs});
+    t.each([&](int i, int vv, float& x) { dvl[i * DV + c0 + vv] = x; });
+    __syncthreads();
+  }
+  const int bad = __syncthreads_or(!ok);
+  if (threadIdx.x == 0) flag[tile] = bad;
+}
+
+template <int DK, int DV, int BV, typename OP, int VAR>
+__global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __restrict__ q,
+                                                  const OP* __restrict__ k, const OP* __restrict__ dO,
+                                                  const float* __restrict__ dST, const float* __restrict__ gcum,
+                                                  const OP* __restrict__ Wg, const float* __restrict__ dvlg,
+                                                  OP* __restrict__ dhg, float* __restrict__ dS0,
+                                                  int* __restrict__ flag) {
+  constexpr int NVT = DV / BV;
+  constexpr bool DT_ = VAR != VAR_DECAY;  // delta term present
+  constexpr int LK = DK + pad_of<OP>();
+  constexpr int LB = BV + pad_of<OP>();
+  constexpr int LU = CH + pad_of<OP>();
+  __shared__ __align__(16) OP Ks[DT_ ? CH * LK : 1];
+  __shared__ __align__(16) OP Qs[CH * LK];
+  __shared__ __align__(16) OP Ws[DT_ ? CH * LK : 1];
+  __shared__ __align__(16) OP dhT[DT_ ? BV * LK : 1];
+  __shared__ __align__(16) OP dOs[CH * LB];
+  __shared__ __align__(16) OP dUT[DT_ ? BV * LU : 1];
+  __shared__ float Gs[CH], Gam[CH];
+
+  int s, vt;
+  scan_block_coords(blockIdx.x, geo.N * H, NVT, s, vt);
+  const int n = s / H, h = s - (s / H) * H, v0 = vt * BV;
+  const SeqPos sp = seq_pos(geo, n);
+
+  Tiles<DK, BV, 4, 1> dh;  // fp32 carry: gradient w.r.t. the state leaving the current chunk
+  bool ok = true;
+  const float* dSTp = dST ? dST + ((long)n * H + h) * DK * DV : nullptr;
+  dh.each([&](int d, int vv, float& x) {
+    x = dSTp ? dSTp[d * DV + v0 + vv] : 0.f;
+    ok &= finite_f(x);
+  });
+
+  for (int c = sp.nch - 1; c >= 0; --c) {
+    const long ci = sp.c0 + c;
+    const long tile = ci * H + h;
+    const long row0 = sp.row0 + (long)c * CH;
+    const int len = min(CH, sp.len - c * CH);
+    OP* dhp = dhg + tile * DK * DV;
+    dh.each([&](int d, int vv, float& x) {
+      const OP xo = from_f<OP>(x);
+      dhp[d * DV + v0 + vv] = xo;
+      if (DT_) dhT[vv * LK + d] = xo;
+    });
+    load_rows<DK, LK>(q + (row0 * H + h) * DK, (long)H * DK, len, Qs);
+    if constexpr (DT_) {
+      load_rows<DK, LK>(k + (row0 * H + h) * DK, (long)H * DK, len, Ks);
+      load_dense<CH, DK, LK>(Wg + tile * CH * DK, Ws);
+    }
+    load_rows<BV, LB>(dO + (row0 * H + h) * DV + v0, (long)H * DV, len, dOs);
+    if (threadIdx.x < CH) {
+      const float G = gcum[tile * CH + threadIdx.x];
+      Gs[threadIdx.x] = G;
+      Gam[threadIdx.x] = expf(G);
+    }
+    __syncthreads();
+    const float Gl = Gs[CH - 1];
+    if constexpr (DT_) {
+      // dU' = dV_loc + diag(e^{G_last - G}) K dh ; keep -dU'^T for the W^T product
+      Tiles<CH, BV, 4, 1> du;
+      du.zero();
+      du.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{dhT});
+      const float* dvl = dvlg + tile * CH * DV + v0;
+      du.each([&](int r, int vv, float& x) {
+        const float u = dvl[r * DV + vv] + expf(Gl - Gs[r]) * x;
+        dUT[vv * LU + r] = from_f<OP>(-u);
+      });
+      __syncthreads();
+    }
+    const float gl = Gam[CH - 1];
+    dh.each([&](int, int, float& x) { x *= gl; });
+    dh.template mma<OP, CH>(KCol<OP, LK>{Qs}, kfun<OP>([&](int vv, int r) {
+                              return from_f<OP>(Gam[r] * to_f(dOs[r * LB + vv]));
+                            }));
+    if constexpr (DT_) dh.template mma<OP, CH>(KCol<OP, LK>{Ws}, KRow<OP, LU>{dUT});
+    __syncthreads();
+  }
+  float* dS0p = dS0 + ((long)n * H + h) * DK * DV;
+  dh.each([&](int d, int vv, float& x) { dS0p[d * DV + v0 + vv] = x; });
+  const int bad = __syncthreads_or(!ok);
+  if (threadIdx.x == 0) flag[(long)s * NVT + vt] = bad;
+}
+
+// Bytes of the phase-dependent region of the grad kernel (LDS for bf16
+// operands, a per-block slice of the workspace for fp32 operands).
+template <int DK, typename OP>
+struct GradRegion {
+  static constexpr int P8 = 16 / (int)sizeof(OP);
+  static constexpr int LK = DK + P8, LT = CH + P8, LC = CH + 4;
+  static constexpr int VS = 32, LV = VS + P8;
+  static constexpr bool BF = sizeof(OP) == 2;
+  // phase 0: Qs, As, Tf (bf16 only), Xs
+  static constexpr int ph0 = CH * LK * (int)sizeof(OP) + CH * LC * 4 + (BF ? CH * LC * 4 : 0) + 4 * 16 * 20 * 4;
+  // phase 1: Vs, dOs, Rs, Ups, dUs, Ys, dVst [64][LV]; hs, dhs [DK][LV]; RT, dUT [VS][LT]
+  static constexpr int ph1 = (7 * CH * LV + 2 * DK * LV + 2 * VS * LT) * (int)sizeof(OP);
+  // phase 2: QT, KT [DK][LT]; SdT, M1, dPs, dPmT [64][LT]
+  static constexpr int ph2 = (2 * DK * LT + 4 * CH * LT) * (int)sizeof(OP);
+  static constexpr int bytes = ((ph0 > ph1 ? (ph0 > ph2 ? ph0 : ph2) : (ph1 > ph2 ? ph1 : ph2)) + 255) / 256 * 256;
+  static_assert(bytes == grad_region_bytes(DK, (int)sizeof(OP)), "host and device disagree");
+};
+
+// Sum over the 16 lanes that share a k-group (lanes l with equal l >> 4).
+__device__ __forceinline__ float sum16(float x) {
+  x += __shfl_xor(x, 1, WAVE);
+  x += __shfl_xor(x, 2, WAVE);
+  x += __shfl_xor(x, 4, WAVE);
+  x += __shfl_xor(x, 8, WAVE);
+  return x;
+}
+// Sum over the 4 k-groups (lanes l, l^16, l^32, l^48).
+__device__ __forceinline__ float sum_groups(float x) {
+  x += __shfl_xor(x, 16, WAVE);
+  x += __shfl_xor(x, 32, WAVE);
+  return x;
+}
+
+template <int DK, int DV, typename OP, int VAR>
+__global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __restrict__ q,
+                                                  const OP* __restrict__ k, const OP* __restrict__ v,
+                                                  const float* __restrict__ g, const float* __restrict__ beta,
+                                                  const float* __restrict__ states, const OP* __restrict__ dO,
+                                                  const OP* __restrict__ dhg, OP* __restrict__ dq,
+                                                  OP* __restrict__ dk, OP* __restrict__ dvo,
+                                                  float* __restrict__ dg, float* __restrict__ dbeta,
+                                                  int* __restrict__ flag, char* __restrict__ gscratch) {
+  typedef GradRegion<DK, OP> R;
+  constexpr bool BF = R::BF;
+  constexpr bool DT_ = VAR != VAR_DECAY;
+  constexpr int LK = R::LK, LT = R::LT, LC = R::LC, VS = R::VS, LV = R::LV;
+
+  // ---- persistent LDS
+  __shared__ __align__(16) OP Ks[CH * LK];
+  __shared__ __align__(16) OP Ts[DT_ ? CH * LT : 1];   // T (fp32 operands: T itself)
+  __shared__ __align__(16) OP TT[DT_ ? CH * LT : 1];   // T^T
+  __shared__ __align__(16) OP PT[CH * LT];             // P^T
+  __shared__ __align__(16) float Pf[BF ? CH * LC : 1]; // P in fp32 (bf16 operands)
+  __shared__ __align__(16) OP AE[DT_ ? CH * LT : 1];   // (K K^T)_ri E_ri, strict lower
+  __shared__ float Gs[CH], Gam[CH], Bs[CH], Dte[CH];
+  __shared__ float rowZ[2][CH], colZ[2][CH], rowA[2][CH];
+  __shared__ float dGs[CH], dBs[CH], hdh_w[4];
+  __shared__ __align__(16) char ulds[BF ? R::bytes : 16];
+  char* ub = BF ? ulds : gscratch + ((long)blockIdx.y * gridDim.x + blockIdx.x) * R::bytes;
+
+  const int ci = blockIdx.x, h = blockIdx.y;
+  const ChunkPos cp = chunk_pos(geo, ci);
+  const long tile = (long)ci * H + h;
+  const int w = wave_id(), l = lane_id();
+
+  // ================= phase 0: gates, P, A, T
+  OP* Qs = reinterpret_cast<OP*>(ub);
+  float* As = reinterpret_cast<float*>(ub + CH * LK * sizeof(OP));
+  float* Tf = BF ? As + CH * LC : reinterpret_cast<float*>(Ts);
+  float* Xs = As + CH * LC * (BF ? 2 : 1);
+  bool ok = load_gates<VAR>(g, beta, cp.row0, H, h, cp.len, Gs, Bs);
+  load_rows<DK, LK>(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Qs);
+  load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
+  __syncthreads();
+  if (threadIdx.x < CH) {
+    const int r = threadIdx.x;
+    Gam[r] = expf(Gs[r]);
+    Dte[r] = expf(Gs[CH - 1] - Gs[r]);
+  }
+  {
+    Tiles<CH, CH, 2, 2> p;
+    p.zero();
+    p.template mma<OP, DK>(KRow<OP, LK>{Qs}, KRow<OP, LK>{Ks});
+    p.each([&](int r, int i, float& x) {
+      const float pr = i <= r ? x * expf(Gs[r] - Gs[i]) : 0.f;
+      PT[i * LT + r] = from_f<OP>(pr);
+      if (BF) Pf[r * LC + i] = pr;
+    });
+  }
+  if constexpr (DT_) {
+    Tiles<CH, CH, 2, 2> bm;
+    bm.zero();
+    bm.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{Ks});
+    bm.each([&](int r, int i, float& x) {
+      const float ae = (i < r) ? x * expf(Gs[r] - Gs[i]) : 0.f;
+      AE[r * LT + i] = from_f<OP>(ae);
+      As[r * LC + i] = Bs[r] * ae;
+    });
+    __syncthreads();
+    unit_lower_inverse<OP, LC, LT>(As, Tf, Ts, Xs);
+    for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
+      const int r = idx >> 6, c = idx & 63;
+      TT[c * LT + r] = Ts[r * LT + c];
+    }
+  }
+  __syncthreads();
+
+  // ================= phase 1: value slices
+  OP* Vs = reinterpret_cast<OP*>(ub);
+  OP* dOs = Vs + CH * LV;
+  OP* Rs = dOs + CH * LV;
+  OP* Ups = Rs + CH * LV;
+  OP* dUs = Ups + CH * LV;
+  OP* Ys = dUs + CH * LV;
+  OP* dVst = Ys + CH * LV;
+  OP* hs = dVst + CH * LV;
+  OP* dhs = hs + DK * LV;
+  OP* RT = dhs + DK * LV;
+  OP* dUT = RT + VS * LT;
+
+  Tiles<CH, CH, 2, 2> dT, dP;
+  Tiles<CH, DK, 4, 1> X, dQa, dKh;
+  dT.zero(); dP.zero(); X.zero(); dQa.zero(); dKh.zero();
+  float dbY[4] = {0.f, 0.f, 0.f, 0.f};
+  float hdh = 0.f;
+  const float* hp = states + tile * DK * DV;
+  const OP* dhp = dhg + tile * DK * DV;
+  const OP* vp = v + (cp.row0 * H + h) * DV;
+  const OP* dop = dO + (cp.row0 * H + h) * DV;
+  OP* dvp = dvo + (cp.row0 * H + h) * DV;
+
+  for (int c0 = 0; c0 < DV; c0 += VS) {
+    ok &= load_rows<VS, LV>(vp + c0, (long)H * DV, cp.len, Vs);
+    load_rows<VS, LV>(dop + c0, (long)H * DV, cp.len, dOs);
+    for (int idx = threadIdx.x; idx < DK * VS / 4; idx += blockDim.x) {
+      const int d = idx / (VS / 4), c = (idx - d * (VS / 4)) * 4;
+      const float4 hx = *reinterpret_cast<const float4*>(hp + (long)d * DV + c0 + c);
+      const float hv[4] = {hx.x, hx.y, hx.z, hx.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const OP dv_ = dhp[(long)d * DV + c0 + c + j];
+        ok &= finite_f(hv[j]);
+        hdh += hv[j] * to_f(dv_);
+        hs[d * LV + c + j] = from_f<OP>(hv[j]);
+        dhs[d * LV + c + j] = dv_;
+      }
+    }
+    __syncthreads();
+    const OP* Up = Vs;  // U' of the scalar-decay member is V
+    if constexpr (DT_) {
+      // R = diag(beta) V - diag(beta e^G) K h
+      Tiles<CH, VS, 4, 1> rr;
+      rr.zero();
+      rr.template mma<OP, DK>(KRow<OP, LK>{Ks}, KCol<OP, LV>{hs});
+      rr.each([&](int r, int vv, float& x) {
+        const float rv = Bs[r] * (to_f(Vs[r * LV + vv]) - Gam[r] * x);
+        const OP ro = from_f<OP>(rv);
+        Rs[r * LV + vv] = ro;
+        RT[vv * LT + r] = ro;
+      });
+      __syncthreads();
+      // U' = T R
+      Tiles<CH, VS, 4, 1> up;
+      up.zero();
+      up.template mma<OP, CH>(KRow<OP, LT>{Ts}, KRow<OP, LT>{RT});
+      up.each([&](int r, int vv, float& x) { Ups[r * LV + vv] = from_f<OP>(x); });
+      Up = Ups;
+    }
+    // dU' = P^T dO + diag(e^{G_last - G}) K dh
+    {
+      Tiles<CH, VS, 4, 1> du;
+      du.zero();
+      du.template mma<OP, DK>(KRow<OP, LK>{Ks}, KCol<OP, LV>{dhs});
+      du.each([&](int r, int, float& x) { x *= Dte[r]; });
+      du.template mma<OP, CH>(KRow<OP, LT>{PT}, KCol<OP, LV>{dOs});
+      du.each([&](int r, int vv, float& x) {
+        const OP xo = from_f<OP>(x);
+        dUs[r * LV + vv] = xo;
+        if (DT_) dUT[vv * LT + r] = xo;
+        else dVst[r * LV + vv] = xo;  // scalar decay: dV = dU'
+      });
+    }
+    __syncthreads();
+    if constexpr (DT_) {
+      // Y = T^T dU'; dV = diag(beta) Y; dbeta_r += v_r . Y_r; keep -Y for X
+      Tiles<CH, VS, 4, 1> y;
+      y.zero();
+      y.template mma<OP, CH>(KRow<OP, LT>{TT}, KRow<OP, LT>{dUT});
+      y.each([&](int r, int vv, float& x) {
+        dVst[r * LV + vv] = from_f<OP>(Bs[r] * x);
+        Ys[r * LV + vv] = from_f<OP>(-x);
+      });
+#pragma unroll
+      for (int b = 0; b < y.TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = y.m0(0) + (l >> 4) * 4 + j, vv = y.n0(b) + (l & 15);
+          dbY[j] += to_f(Vs[r * LV + vv]) * y.acc[0][b][j];
+        }
+      __syncthreads();
+      dT.template mma<OP, VS>(KRow<OP, LV>{dUs}, KRow<OP, LV>{Rs});
+      X.template mma<OP, VS>(KRow<OP, LV>{Ys}, KRow<OP, LV>{hs});
+    }
+    dP.template mma<OP, VS>(KRow<OP, LV>{dOs}, KRow<OP, LV>{Up});
+    dQa.template mma<OP, VS>(KRow<OP, LV>{dOs}, KRow<OP, LV>{hs});
+    dKh.template mma<OP, VS>(KRow<OP, LV>{Up}, KRow<OP, LV>{dhs});
+    store_rows<VS, LV>(dvp + c0, (long)H * DV, cp.len, dVst);
+    __syncthreads();
+  }
+
+  // block-wide <h, dh> in a fixed order
+  hdh = wave_sum(hdh);
+  if (l == 0) hdh_w[w] = hdh;
+  // dbeta partial from Y: reduce over the 16 lanes of a k-group
+  if constexpr (DT_) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dbY[j] = sum16(dbY[j]);
+  }
+
+  // ================= phase 2: triangular VJP and the chunk-level gradients
+  OP* QT = reinterpret_cast<OP*>(ub);
+  OP* KT = QT + DK * LT;
+  OP* SdT = KT + DK * LT;  // dT^T, later dB + dB^T
+  OP* M1 = SdT + CH * LT;
+  OP* dPs = M1 + CH * LT;
+  OP* dPmT = dPs + CH * LT;
+  {
+    const OP* qp = q + (cp.row0 * H + h) * DK;
+    for (int idx = threadIdx.x; idx < CH * DK; idx += blockDim.x) {
+      const int r = idx % CH, d = idx / CH;
+      QT[d * LT + r] = r < cp.len ? qp[(long)r * H * DK + d] : from_f<OP>(0.f);
+      KT[d * LT + r] = Ks[r * LK + d];
+    }
+  }
+  Tiles<CH, CH, 2, 2> zs;  // Z = dA * A + dP * P, element by element
+  dP.each([&](int r, int i, float& x) {
+    const float dd = i <= r ? expf(Gs[r] - Gs[i]) : 0.f;
+    const float dpm = x * dd;
+    dPs[r * LT + i] = from_f<OP>(dpm);
+    dPmT[i * LT + r] = from_f<OP>(dpm);
+  });
+#pragma unroll
+  for (int a = 0; a < zs.TM; ++a)
+#pragma unroll
+    for (int b = 0; b < zs.TN; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = zs.m0(a) + (l >> 4) * 4 + j, i = zs.n0(b) + (l & 15);
+        const float pr = BF ? Pf[r * LC + i] : to_f(PT[i * LT + r]);
+        zs.acc[a][b][j] = dP.acc[a][b][j] * pr;
+      }
+  if constexpr (DT_) dT.each([&](int r, int c, float& x) { SdT[c * LT + r] = from_f<OP>(x); });
+  __syncthreads();
+
+  float rowA_l[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  if constexpr (DT_) {
+    // M1 = T^T dT
+    Tiles<CH, CH, 2, 2> m1;
+    m1.zero();
+    m1.template mma<OP, CH>(KRow<OP, LT>{TT}, KRow<OP, LT>{SdT});
+    m1.each([&](int r, int c, float& x) { M1[r * LT + c] = from_f<OP>(x); });
+    __syncthreads();
+    // dA = -(T^T dT) T^T, strict lower part
+    Tiles<CH, CH, 2, 2> da;
+    da.zero();
+    da.template mma<OP, CH>(KRow<OP, LT>{M1}, KRow<OP, LT>{Ts});
+#pragma unroll
+    for (int a = 0; a < da.TM; ++a)
+#pragma unroll
+      for (int b = 0; b < da.TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = da.m0(a) + (l >> 4) * 4 + j, i = da.n0(b) + (l & 15);
+          const float dA = (i < r) ? -da.acc[a][b][j] : 0.f;
+          const float ae = to_f(AE[r * LT + i]);
+          const float e = (i < r) ? expf(Gs[r] - Gs[i]) : 0.f;
+          zs.acc[a][b][j] += dA * Bs[r] * ae;
+          rowA_l[a][j] += dA * ae;
+          const float db = dA * Bs[r] * e;
+          if (i < r) {
+            SdT[r * LT + i] = from_f<OP>(db);
+            SdT[i * LT + r] = from_f<OP>(db);
+          } else if (i == r) {
+            SdT[r * LT + r] = from_f<OP>(0.f);
+          }
+        }
+  }
+  // row and column sums of Z, and the row sums of dA * (K K^T) * E, in fixed order
+  {
+    const int wm = w / 2, wn = w % 2;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float rs = zs.acc[a][0][j] + zs.acc[a][1][j];
+        rs = sum16(rs);
+        const float ra = sum16(rowA_l[a][j]);
+        const int r = zs.m0(a) + (l >> 4) * 4 + j;
+        if ((l & 15) == 0) {
+          rowZ[wn][r] = rs;
+          rowA[wn][r] = ra;
+        }
+      }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      float cs = 0.f;
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) cs += zs.acc[a][b][j];
+      cs = sum_groups(cs);
+      if ((l >> 4) == 0) colZ[wm][zs.n0(b) + (l & 15)] = cs;
+    }
+  }
+  __syncthreads();
+
+  // dQ = diag(e^G) dO h^T + (dP * D) K;   row sums q_r . (dO h^T)_r
+  float rq[4], rx[4], rk[4];
+  {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rq[j] = rx[j] = rk[j] = 0.f;
+#pragma unroll
+    for (int b = 0; b < dQa.TN; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = dQa.m0(0) + (l >> 4) * 4 + j, d = dQa.n0(b) + (l & 15);
+        const float qv = to_f(QT[d * LT + r]);
+        const float kv = to_f(Ks[r * LK + d]);
+        rq[j] += qv * dQa.acc[0][b][j];
+        rx[j] += kv * X.acc[0][b][j];
+        rk[j] += kv * dKh.acc[0][b][j];
+        dQa.acc[0][b][j] *= Gam[r];
+        dKh.acc[0][b][j] = Dte[r] * dKh.acc[0][b][j] + Bs[r] * Gam[r] * X.acc[0][b][j];
+      }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      rq[j] = sum16(rq[j]);
+      rx[j] = sum16(rx[j]);
+      rk[j] = sum16(rk[j]);
+    }
+  }
+  dQa.template mma<OP, CH>(KRow<OP, LT>{dPs}, KRow<OP, LT>{KT});
+  dKh.template mma<OP, CH>(KRow<OP, LT>{dPmT}, KRow<OP, LT>{QT});
+  if constexpr (DT_) dKh.template mma<OP, CH>(KRow<OP, LT>{SdT}, KRow<OP, LT>{KT});
+
+  // per-row scalars of this wave's rows -> dG, dbeta
+  if ((l & 15) == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = dQa.m0(0) + (l >> 4) * 4 + j;
+      float dG = (rowZ[0][r] + rowZ[1][r]) - (colZ[0][r] + colZ[1][r]);
+      dG += Gam[r] * (rq[j] + Bs[r] * rx[j]);
+      dG -= Dte[r] * rk[j];
+      dGs[r] = dG;
+      rk[j] = Dte[r] * rk[j];  // khat_r . dkhat_r
+      if (DT_) dBs[r] = (rowA[0][r] + rowA[1][r]) + Gam[r] * rx[j] + dbY[j];
+    }
+  }
+  // sum_r khat_r . dkhat_r in a fixed order: per-row values through LDS
+  __shared__ float kk_row[CH];
+  if ((l & 15) == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) kk_row[dQa.m0(0) + (l >> 4) * 4 + j] = rk[j];
+  }
+  __syncthreads();
+  // stage dq, dk (reusing QT / KT after every product has read them)
+  OP* dqst = QT;
+  OP* dkst = KT;
+  dQa.each([&](int r, int d, float& x) { dqst[r * LK + d] = from_f<OP>(x); });
+  dKh.each([&](int r, int d, float& x) { dkst[r * LK + d] = from_f<OP>(x); });
+  if (w == 0) {
+    // dG_last += e^{G_last} <h, dh> + sum_r khat_r . dkhat_r ; dg = reverse cumsum of dG
+    float kk = kk_row[l];
+    kk = wave_sum(kk);
+    float x = dGs[l];
+    if (l == CH - 1) x += Gam[CH - 1] * (((hdh_w[0] + hdh_w[1]) + hdh_w[2]) + hdh_w[3]) + kk;
+    // reverse inclusive scan: suffix sums
+    const float rev = __shfl(x, CH - 1 - l, WAVE);
+    const float sc = wave_incl_scan(rev);
+    const float dgv = __shfl(sc, CH - 1 - l, WAVE);
+    if (l < cp.len) {
+      const long o = (cp.row0 + l) * H + h;
+      if (VAR != VAR_DELTA) dg[o] = dgv;
+      if (DT_) dbeta[o] = dBs[l];
+    }
+  }
+  __syncthreads();
+  store_rows<DK, LK>(dq + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, dqst);
+  store_rows<DK, LK>(dk + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, dkst);
+  const int bad = __syncthreads_or(!ok);
+  if (threadIdx.x == 0) flag[tile] = bad;
+}
+
+// ---------------------------------------------------------------------------
+template <int DK, int DV, typename OP, int VAR>
+static hipError_t launch_bwd_t(const BwdArgs& a) {
+  constexpr int BV = SCAN_BV;
+  constexpr int NVT = DV / BV;
+  const Geo& geo = a.geo;
+  const int H = geo.H;
+  const BwdWs& w = a.ws;
+  if (geo.total_chunks > 0) {
+    hipLaunchKernelGGL((k_prep_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
+                       geo, H, (const OP*)a.q, (const OP*)a.k, a.g, a.beta, (const OP*)a.dO, w.gcum,
+                       (OP*)w.W, w.dvl, w.flag_prep);
+  }
+  const int NS = geo.N * H;
+  if (NS > 0) {
+    hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
+                       (const OP*)a.q, (const OP*)a.k, (const OP*)a.dO, a.dST, w.gcum, (const OP*)w.W,
+                       w.dvl, (OP*)w.dh, a.dS0, w.flag_scan);
+  }
+  if (geo.total_chunks > 0) {
+    hipLaunchKernelGGL((k_grad_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
+                       geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, a.states,
+                       (const OP*)a.dO, (const OP*)w.dh, (OP*)a.dq, (OP*)a.dk_, (OP*)a.dv_, a.dg, a.dbeta,
+                       w.flag_grad, (char*)w.grad_scratch);
+  }
+  return hipGetLastError();
+}
+
+template <int DT, int VAR>
+hipError_t launch_bwd_var(const BwdArgs& a) {
+  typedef typename op_of<DT>::type OP;
+  const int dk = a.dk, dv = a.dv;
+  if (dk == 64 && dv == 64) return launch_bwd_t<64, 64, OP, VAR>(a);
+  if (dk == 64 && dv == 128) return launch_bwd_t<64, 128, OP, VAR>(a);
+  if (dk == 64 && dv == 256) return launch_bwd_t<64, 256, OP, VAR>(a);
+  if (dk == 128 && dv == 64) return launch_bwd_t<128, 64, OP, VAR>(a);
+  if (dk == 128 && dv == 128) return launch_bwd_t<128, 128, OP, VAR>(a);
+  if (dk == 128 && dv == 256) return launch_bwd_t<128, 256, OP, VAR>(a);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace gdn

@@ -1,0 +1,180 @@
+// Chunk-local pieces shared by the forward and backward kernels: tile loads
+// and stores between HBM and LDS, the in-chunk gates, and the triangular
+// inverse T = (I + A)^{-1} of the delta rule's erase coupling (paper Sec. 4.2,
+// K#2: the forward computes T once per chunk and the backward reuses it).
+#pragma once
+
+#include "gdn_common.hpp"
+
+namespace gdn {
+
+template <typename T> constexpr int pad_of() { return 16 / (int)sizeof(T); }
+
+__device__ __forceinline__ bool finite8_bf16(uint4 u) {
+  // a bf16 value is non-finite when its 8 exponent bits are all ones
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+  bool ok = true;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    ok &= (w[i] & 0x7f80u) != 0x7f80u;
+    ok &= (w[i] & 0x7f800000u) != 0x7f800000u;
+  }
+  return ok;
+}
+__device__ __forceinline__ bool finite4_f32(uint4 u) {
+  return ((u.x & 0x7f800000u) != 0x7f800000u) & ((u.y & 0x7f800000u) != 0x7f800000u) &
+         ((u.z & 0x7f800000u) != 0x7f800000u) & ((u.w & 0x7f800000u) != 0x7f800000u);
+}
+template <typename T> __device__ __forceinline__ bool finite16B(uint4 u);
+template <> __device__ __forceinline__ bool finite16B<bf16>(uint4 u) { return finite8_bf16(u); }
+template <> __device__ __forceinline__ bool finite16B<float>(uint4 u) { return finite4_f32(u); }
+
+// Copy rows [0, len) of a 64 x D tile whose rows sit `rs` elements apart in
+// HBM into LDS dst[r * LD + d]; rows >= len are zero-filled.  Returns false
+// if any loaded value is NaN or Inf.
+template <int D, int LD, typename T>
+__device__ __forceinline__ bool load_rows(const T* __restrict__ src, long rs, int len, T* dst) {
+  constexpr int V = 16 / (int)sizeof(T);  // elements per 16-byte vector
+  constexpr int PER_ROW = D / V;
+  bool ok = true;
+  for (int idx = threadIdx.x; idx < CH * PER_ROW; idx += blockDim.x) {
+    const int r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
+    uint4 u = {0u, 0u, 0u, 0u};
+    if (r < len) {
+      u = *reinterpret_cast<const uint4*>(src + r * rs + c);
+      ok &= finite16B<T>(u);
+    }
+    *reinterpret_cast<uint4*>(dst + r * LD + c) = u;
+  }
+  return ok;
+}
+
+// Copy a contiguous R x D tile (row-major in HBM) into LDS with row stride LD.
+template <int R, int D, int LD, typename T>
+__device__ __forceinline__ void load_dense(const T* __restrict__ src, T* dst) {
+  constexpr int V = 16 / (int)sizeof(T);
+  constexpr int PER_ROW = D / V;
+  for (int idx = threadIdx.x; idx < R * PER_ROW; idx += blockDim.x) {
+    const int r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
+    *reinterpret_cast<uint4*>(dst + r * LD + c) = *reinterpret_cast<const uint4*>(src + (long)r * D + c);
+  }
+}
+
+// Write rows [0, len) of an LDS tile src[r * LD + d] (64 x D) to HBM rows `rs`
+// elements apart.
+template <int D, int LD, typename T>
+__device__ __forceinline__ void store_rows(T* __restrict__ dst, long rs, int len, const T* src) {
+  constexpr int V = 16 / (int)sizeof(T);
+  constexpr int PER_ROW = D / V;
+  for (int idx = threadIdx.x; idx < CH * PER_ROW; idx += blockDim.x) {
+    const int r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
+    if (r < len)
+      *reinterpret_cast<uint4*>(dst + r * rs + c) = *reinterpret_cast<const uint4*>(src + r * LD + c);
+  }
+}
+
+// In-chunk gates, computed by wave 0: G_r = sum_{s<=r} g_s (positions past the
+// chunk's end add 0, so G there equals the last valid G), beta_r (0 past the
+// end).  Returns false (on wave 0) if a loaded gate is non-finite.
+template <int VAR>
+__device__ __forceinline__ bool load_gates(const float* __restrict__ g, const float* __restrict__ beta,
+                                           long row0, int H, int h, int len, float* Gs, float* Bs) {
+  bool ok = true;
+  if (wave_id() == 0) {
+    const int r = lane_id();
+    float gv = 0.f, bv = 0.f;
+    if (r < len) {
+      if (VAR != VAR_DELTA) gv = g[(row0 + r) * H + h];
+      if (VAR != VAR_DECAY) bv = beta[(row0 + r) * H + h];
+    }
+    ok = finite_f(gv) && finite_f(bv);
+    Gs[r] = wave_incl_scan(gv);
+    Bs[r] = bv;
+  }
+  return ok;
+}
+
+// T = (I + A)^{-1} for the strictly lower-triangular 64 x 64 matrix A held in
+// fp32 in As (row stride LC).  The 16 x 16 diagonal blocks are inverted by
+// forward substitution (wave 0, one lane per column: row r of a block is
+// e_r - sum_{i<r} A_ri T_i); the blocks below the diagonal follow block row by
+// block row, T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj, on fp32 MFMA (wave j owns
+// block column j).  T lands in Tf (fp32, stride LC); for bf16 operands a copy
+// is rounded into Ts (stride LT).  Xs is a 4 x 16 x 20 fp32 scratch.
+// Must be called by all threads of the block.
+template <typename OP, int LC, int LT>
+__device__ void unit_lower_inverse(const float* As, float* Tf, OP* Ts, float* Xs) {
+  constexpr int LX = 20;
+  const int w = wave_id(), l = lane_id();
+  if (w == 0) {
+    const int base = (l >> 4) * 16, j = l & 15;
+    float col[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < r; ++i) s += As[(base + r) * LC + base + i] * col[i];
+      col[r] = (r == j) ? 1.f : (r > j ? -s : 0.f);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) Tf[(base + r) * LC + base + j] = col[r];
+  }
+  for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
+    const int r = idx >> 6, c = idx & 63;
+    if ((c >> 4) > (r >> 4)) Tf[r * LC + c] = 0.f;
+  }
+  __syncthreads();
+  for (int i = 1; i < 4; ++i) {
+    if (w < i) {
+      const int j = w;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int kb = j; kb < i; ++kb) {
+#pragma unroll
+        for (int k0 = 0; k0 < 16; k0 += 4) {
+          const float a = As[(16 * i + (l & 15)) * LC + 16 * kb + k0 + (l >> 4)];
+          const float b = Tf[(16 * kb + k0 + (l >> 4)) * LC + 16 * j + (l & 15)];
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) Xs[w * 16 * LX + (4 * (l >> 4) + jj) * LX + (l & 15)] = acc[jj];
+    }
+    __syncthreads();
+    if (w < i) {
+      const int j = w;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k0 = 0; k0 < 16; k0 += 4) {
+        const float a = Tf[(16 * i + (l & 15)) * LC + 16 * i + k0 + (l >> 4)];
+        const float b = Xs[w * 16 * LX + (k0 + (l >> 4)) * LX + (l & 15)];
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) Tf[(16 * i + 4 * (l >> 4) + jj) * LC + 16 * j + (l & 15)] = -acc[jj];
+    }
+    __syncthreads();
+  }
+  if constexpr (sizeof(OP) == 2) {
+    for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
+      const int r = idx >> 6, c = idx & 63;
+      Ts[r * LT + c] = from_f<OP>(Tf[r * LC + c]);
+    }
+    __syncthreads();
+  }
+}
+
+// XCD-aware placement of the (stream, value-tile) blocks of a state scan:
+// blocks are dealt to the 8 XCDs round robin, so the value tiles of one
+// stream get block ids that are equal modulo 8 and share that XCD's L2.
+__device__ __forceinline__ void scan_block_coords(int bid, int NS, int NVT, int& s, int& vt) {
+  if ((NS & 7) == 0) {
+    const int x = bid & 7, slot = bid >> 3;
+    s = (slot / NVT) * 8 + x;
+    vt = slot - (slot / NVT) * NVT;
+  } else {
+    s = bid / NVT;
+    vt = bid - s * NVT;
+  }
+}
+
+}  // namespace gdn

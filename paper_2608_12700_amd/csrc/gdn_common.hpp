@@ -1,0 +1,246 @@
+// Device-side building blocks shared by the gated-delta-rule kernels (gfx950).
+//
+// Matrix products run on 16x16 MFMA tiles: v_mfma_f32_16x16x32_bf16 for bf16
+// operands and v_mfma_f32_16x16x4_f32 for fp32 operands, always with fp32
+// accumulation.  Lane l of a wave owns row/column (l & 15) of a tile and the
+// k-group (l >> 4); the 16x16 fp32 result sits as C[4*(l>>4) + j][l & 15],
+// j = 0..3, in four accumulator registers.  Operands are read from LDS through
+// small "view" objects that map (outer index, k) to an element, so one product
+// routine serves every transpose the chunk algebra needs; a view whose k index
+// is contiguous turns into 16-byte LDS reads.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gdn_geo.hpp"
+
+namespace gdn {
+
+constexpr int CH = 64;  // chunk length (tokens)
+constexpr int WAVE = 64;
+
+typedef __bf16 bf16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+
+__device__ __forceinline__ float to_f(float x) { return x; }
+__device__ __forceinline__ float to_f(bf16 x) { return static_cast<float>(x); }
+template <typename T> __device__ __forceinline__ T from_f(float x);
+
+template <int DT> struct op_of;
+template <> struct op_of<DT_F32> { typedef float type; };
+template <> struct op_of<DT_BF16> { typedef bf16 type; };
+template <> __device__ __forceinline__ float from_f<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f<bf16>(float x) { return static_cast<bf16>(x); }
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
+__device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
+
+__device__ __forceinline__ bool finite_f(float x) {
+  return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
+}
+
+// ---------------------------------------------------------------------------
+// Operand views.  get(o, k): o is the row for an A operand (M x K) or the
+// column for a B operand (K x N); k is the contraction index.
+// ---------------------------------------------------------------------------
+
+// Element (o, k) at p[o * LD + k]: k contiguous.
+template <typename T, int LD>
+struct KRow {
+  const T* p;
+  static constexpr bool kVec = true;
+  __device__ __forceinline__ T get(int o, int k) const { return p[o * LD + k]; }
+  __device__ __forceinline__ const T* ptr(int o, int k) const { return p + o * LD + k; }
+};
+
+// Element (o, k) at p[k * LD + o]: o contiguous (a transposed use).
+template <typename T, int LD>
+struct KCol {
+  const T* p;
+  static constexpr bool kVec = false;
+  __device__ __forceinline__ T get(int o, int k) const { return p[k * LD + o]; }
+};
+
+// Element computed by a functor f(o, k) -> T.
+template <typename T, class F>
+struct KFun {
+  F f;
+  static constexpr bool kVec = false;
+  __device__ __forceinline__ T get(int o, int k) const { return f(o, k); }
+};
+template <typename T, class F>
+__device__ __forceinline__ KFun<T, F> kfun(F f) { return KFun<T, F>{f}; }
+
+template <typename OP> struct Mma;
+
+template <>
+struct Mma<bf16> {
+  static constexpr int KSTEP = 32;
+  typedef bf16x8 frag;
+  template <class V>
+  __device__ __forceinline__ static frag load(const V& v, int o, int k0) {
+    const int l = lane_id();
+    const int oo = o + (l & 15), kk = k0 + (l >> 4) * 8;
+    if constexpr (V::kVec) {
+      return *reinterpret_cast<const bf16x8*>(v.ptr(oo, kk));
+    } else {
+      frag r;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) r[j] = v.get(oo, kk + j);
+      return r;
+    }
+  }
+  __device__ __forceinline__ static f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <>
+struct Mma<float> {
+  static constexpr int KSTEP = 4;
+  typedef float frag;
+  template <class V>
+  __device__ __forceinline__ static frag load(const V& v, int o, int k0) {
+    const int l = lane_id();
+    return v.get(o + (l & 15), k0 + (l >> 4));
+  }
+  __device__ __forceinline__ static f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+};
+
+// A wave-level register-blocked product: the waves of a block form a WM x WN
+// grid over the (M/16) x (N/16) output tiles; wave (wm, wn) owns TM x TN tiles
+// and reuses each loaded fragment across its row or column of tiles.
+template <int M, int N, int WM, int WN>
+struct Tiles {
+  static_assert(M % (16 * WM) == 0 && N % (16 * WN) == 0, "tile grid");
+  static constexpr int TM = M / 16 / WM;
+  static constexpr int TN = N / 16 / WN;
+  f32x4 acc[TM][TN];
+
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  __device__ __forceinline__ static int m0(int a) { return ((wave_id() / WN) * TM + a) * 16; }
+  __device__ __forceinline__ static int n0(int b) { return ((wave_id() % WN) * TN + b) * 16; }
+
+  // acc += A (M x K) * B (K x N), K a multiple of the MFMA k-step.
+  template <typename OP, int K, class VA, class VB>
+  __device__ __forceinline__ void mma(const VA& A, const VB& B) {
+    typedef Mma<OP> X;
+#pragma unroll 2
+    for (int k0 = 0; k0 < K; k0 += X::KSTEP) {
+      typename X::frag fa[TM], fb[TN];
+#pragma unroll
+      for (int a = 0; a < TM; ++a) fa[a] = X::load(A, m0(a), k0);
+#pragma unroll
+      for (int b = 0; b < TN; ++b) fb[b] = X::load(B, n0(b), k0);
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) acc[a][b] = X::mma(fa[a], fb[b], acc[a][b]);
+    }
+  }
+
+  // Visit every owned element: f(row, col, value&).
+  template <class F>
+  __device__ __forceinline__ void each(F f) {
+    const int l = lane_id();
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float x = acc[a][b][j];
+          f(m0(a) + (l >> 4) * 4 + j, n0(b) + (l & 15), x);
+          acc[a][b][j] = x;
+        }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Chunk and sequence coordinates.
+// ---------------------------------------------------------------------------
+struct ChunkPos {
+  int n;     // sequence
+  int c;     // chunk index within the sequence
+  long row0; // global token row (b*T + t) of the chunk's first token
+  int len;   // tokens in this chunk (1..64)
+};
+
+__device__ __forceinline__ ChunkPos chunk_pos(const Geo& g, int ci) {
+  ChunkPos p;
+  if (g.cu == nullptr) {
+    p.n = ci / g.NT;
+    p.c = ci - p.n * g.NT;
+    const int t0 = p.c * CH;
+    p.row0 = (long)p.n * g.T + t0;
+    p.len = min(CH, g.T - t0);
+  } else {
+    int lo = 0, hi = g.N;  // find n with chunk_off[n] <= ci < chunk_off[n+1]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (g.chunk_off[mid] <= ci) lo = mid; else hi = mid;
+    }
+    // skip empty sequences that share the same offset
+    while (lo + 1 < g.N && g.chunk_off[lo + 1] <= ci) ++lo;
+    p.n = lo;
+    p.c = ci - g.chunk_off[lo];
+    const int t0 = g.cu[lo] + p.c * CH;
+    p.row0 = t0;
+    p.len = min(CH, g.cu[lo + 1] - t0);
+  }
+  return p;
+}
+
+struct SeqPos {
+  long row0;  // first token row
+  int len;    // tokens
+  int c0;     // first chunk (global chunk index)
+  int nch;    // chunks
+};
+
+__device__ __forceinline__ SeqPos seq_pos(const Geo& g, int n) {
+  SeqPos s;
+  if (g.cu == nullptr) {
+    s.row0 = (long)n * g.T;
+    s.len = g.T;
+    s.c0 = n * g.NT;
+    s.nch = g.NT;
+  } else {
+    s.row0 = g.cu[n];
+    s.len = g.cu[n + 1] - g.cu[n];
+    s.c0 = g.chunk_off[n];
+    s.nch = g.chunk_off[n + 1] - g.chunk_off[n];
+  }
+  return s;
+}
+
+// Inclusive prefix sum of one value per lane over a wave (Hillis-Steele; the
+// order of additions is fixed, so the result is deterministic).
+__device__ __forceinline__ float wave_incl_scan(float x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int off = 1; off < WAVE; off <<= 1) {
+    const float y = __shfl_up(x, off, WAVE);
+    if (l >= off) x += y;
+  }
+  return x;
+}
+
+// Fixed-order wave reduction (butterfly).
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = WAVE / 2; off > 0; off >>= 1) x += __shfl_xor(x, off, WAVE);
+  return x;
+}
+
+}  // namespace gdn

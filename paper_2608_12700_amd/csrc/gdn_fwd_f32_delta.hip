@@ -1,0 +1,5 @@
+// Instantiates the forward kernels for float operands, variant VAR_DELTA.
+#include "gdn_fwd.hpp"
+namespace gdn {
+template hipError_t launch_fwd_var<DT_F32, VAR_DELTA>(const FwdArgs&);
+}

@@ -1,0 +1,84 @@
+// Host-side launch interface between the C ABI (gdn_api.cpp) and the kernel
+// translation units.  Plain structs of device pointers and sizes.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include "gdn_geo.hpp"
+
+namespace gdn {
+
+// Forward workspace regions (device pointers into the caller's workspace).
+struct FwdWs {
+  int* chunk_off;  // [N+1] packed layout only
+  int* flag_prep;  // [chunks*H]   non-finite k, v, g, beta in the chunk
+  int* flag_out;   // [chunks*H]   non-finite q in the chunk
+  int* flag_scan;  // [N*H*NVT]    non-finite S0 slice
+  float* gcum;     // [chunks*H*64] in-chunk cumulative log-decay
+  void* W;         // [chunks*H*64*dk] operand dtype
+  float* U;        // [chunks*H*64*dv]
+  void* UpT;       // [chunks*H*dv*64] operand dtype, U' transposed
+  float* exact;    // exact-path scratch
+};
+
+struct FwdArgs {
+  Geo geo;
+  int dk, dv, variant;
+  const void *q, *k, *v;
+  const float *g, *beta, *S0;
+  void* o;
+  float* ST;
+  float* states;
+  FwdWs ws;
+  hipStream_t stream;
+};
+
+struct BwdWs {
+  int* chunk_off;
+  int* flag_prep;  // [chunks*H]   non-finite q, k, v, g, beta, dO in the chunk
+  int* flag_grad;  // [chunks*H]   non-finite chunk state in the chunk
+  int* flag_scan;  // [N*H*NVT]    non-finite dS_T slice
+  float* gcum;     // [chunks*H*64]
+  void* W;         // [chunks*H*64*dk] operand dtype
+  float* dvl;      // [chunks*H*64*dv] P^T dO
+  void* dh;        // [chunks*H*dk*dv] operand dtype: state gradient after each chunk
+  void* grad_scratch;  // [chunks*H*grad_region_bytes] fp32 operands only
+  float* exact;
+};
+
+struct BwdArgs {
+  Geo geo;
+  int dk, dv, variant;
+  const void *q, *k, *v;
+  const float *g, *beta, *states;
+  const void* dO;
+  const float* dST;
+  void *dq, *dk_, *dv_;
+  float *dg, *dbeta, *dS0;
+  BwdWs ws;
+  hipStream_t stream;
+};
+
+// value-tile width of the state scans
+constexpr int SCAN_BV = 32;
+
+// Bytes of the phase-dependent working region of the backward grad kernel
+// (held in LDS for bf16 operands and in the workspace, one slice per block,
+// for fp32 operands).  Must match GradRegion in gdn_bwd.hpp.
+constexpr int grad_region_bytes(int dk, int es) {
+  const int CHn = 64, P8 = 16 / es, LK = dk + P8, LT = CHn + P8, LC = CHn + 4, VS = 32, LV = VS + P8;
+  const bool bf = es == 2;
+  const int ph0 = CHn * LK * es + CHn * LC * 4 + (bf ? CHn * LC * 4 : 0) + 4 * 16 * 20 * 4;
+  const int ph1 = (7 * CHn * LV + 2 * dk * LV + 2 * VS * LT) * es;
+  const int ph2 = (2 * dk * LT + 4 * CHn * LT) * es;
+  const int m = ph0 > ph1 ? (ph0 > ph2 ? ph0 : ph2) : (ph1 > ph2 ? ph1 : ph2);
+  return (m + 255) / 256 * 256;
+}
+
+template <int DT, int VAR> hipError_t launch_fwd_var(const FwdArgs& a);
+template <int DT, int VAR> hipError_t launch_bwd_var(const BwdArgs& a);
+
+// chunk_off[n] = sum_{m<n} ceil((cu[m+1]-cu[m]) / 64), n = 0..N
+hipError_t launch_chunk_offsets(const int* cu, int N, int* chunk_off, hipStream_t stream);
+
+}  // namespace gdn

@@ -1,0 +1,242 @@
+"""Python binding of libgdn.so (argument marshalling only).
+
+Every step of the forward and backward runs in the library's HIP kernels; this
+module allocates outputs and workspace with torch, fills the C structs and
+passes raw device pointers plus the current HIP stream.  If the library has not
+been built, every entry point raises: there is no fallback.
+
+Names mirror the C ABI in include/gdn.h:
+  gdn_fwd(...) / gdn_bwd(...)       raw calls on pointers (ctypes)
+  fwd(...) / bwd(...)               torch-tensor conveniences built on them
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgdn.so")
+
+GDN_OK = 0
+STATUS = {0: "GDN_OK", -1: "GDN_ERR_NULL", -2: "GDN_ERR_SHAPE", -3: "GDN_ERR_UNSUPPORTED",
+          -4: "GDN_ERR_DTYPE", -5: "GDN_ERR_WORKSPACE", -6: "GDN_ERR_ALIAS", -7: "GDN_ERR_VARLEN",
+          -8: "GDN_ERR_HIP", -9: "GDN_ERR_VARIANT"}
+GDN_F32, GDN_BF16 = 0, 1
+VARIANTS = {"gated_delta": 0, "delta": 1, "decay_only": 2}
+CHUNK = 64
+
+
+class GdnError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {STATUS.get(code, code)}")
+        self.code = code
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+        ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
+        ("num_seqs", ctypes.c_int32),
+        ("cu_seqlens_host", ctypes.POINTER(ctypes.c_int32)),
+        ("cu_seqlens_dev", ctypes.c_void_p),
+        ("io_dtype", ctypes.c_int), ("variant", ctypes.c_int),
+    ]
+
+
+EXPORTED = ("gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_fwd",
+            "gdn_bwd", "gdn_status_str", "gdn_version")
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libgdn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2608_12700_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    P = ctypes.POINTER(Problem)
+    lib.gdn_num_chunks.argtypes = [P]
+    lib.gdn_num_chunks.restype = ctypes.c_int64
+    lib.gdn_fwd_workspace_size.argtypes = [P]
+    lib.gdn_fwd_workspace_size.restype = sz
+    lib.gdn_bwd_workspace_size.argtypes = [P]
+    lib.gdn_bwd_workspace_size.restype = sz
+    lib.gdn_fwd.argtypes = [P] + [vp] * 9 + [vp, sz, vp]
+    lib.gdn_fwd.restype = ctypes.c_int
+    lib.gdn_bwd.argtypes = [P] + [vp] * 14 + [vp, sz, vp]
+    lib.gdn_bwd.restype = ctypes.c_int
+    lib.gdn_status_str.argtypes = [ctypes.c_int]
+    lib.gdn_status_str.restype = ctypes.c_char_p
+    lib.gdn_version.argtypes = []
+    lib.gdn_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def make_problem(B, T, H, dk, dv, *, io_dtype=GDN_BF16, variant="gated_delta", cu_host=None,
+                 cu_dev_ptr=None, chunk=CHUNK):
+    """Fill a gdn_problem.  ``cu_host`` is an int32 numpy array kept alive by the caller."""
+    p = Problem()
+    p.B, p.T, p.H, p.dk, p.dv, p.chunk = B, T, H, dk, dv, chunk
+    if cu_host is not None:
+        p.num_seqs = len(cu_host) - 1
+        p.cu_seqlens_host = cu_host.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        p.cu_seqlens_dev = cu_dev_ptr
+    else:
+        p.num_seqs = B
+        p.cu_seqlens_host = None
+        p.cu_seqlens_dev = None
+    p.io_dtype = io_dtype
+    p.variant = VARIANTS[variant] if isinstance(variant, str) else int(variant)
+    return p
+
+
+# --- raw C-ABI calls (same names as the C functions) -----------------------
+
+def gdn_num_chunks(p: Problem) -> int:
+    return int(load().gdn_num_chunks(ctypes.byref(p)))
+
+
+def gdn_fwd_workspace_size(p: Problem) -> int:
+    return int(load().gdn_fwd_workspace_size(ctypes.byref(p)))
+
+
+def gdn_bwd_workspace_size(p: Problem) -> int:
+    return int(load().gdn_bwd_workspace_size(ctypes.byref(p)))
+
+
+def gdn_fwd(p, q, k, v, g, beta, S0, o, S_T, states, ws, ws_bytes, stream) -> int:
+    return int(load().gdn_fwd(ctypes.byref(p), q, k, v, g, beta, S0, o, S_T, states, ws, ws_bytes,
+                              stream))
+
+
+def gdn_bwd(p, q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg, dbeta, dS0, ws, ws_bytes,
+            stream) -> int:
+    return int(load().gdn_bwd(ctypes.byref(p), q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg,
+                              dbeta, dS0, ws, ws_bytes, stream))
+
+
+def gdn_status_str(code: int) -> str:
+    return load().gdn_status_str(code).decode()
+
+
+def gdn_version() -> str:
+    return load().gdn_version().decode()
+
+
+# --- torch conveniences ----------------------------------------------------
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_handle(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _check(t: torch.Tensor, name: str, dtype, device):
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+class Packed:
+    """Packed sequence offsets: a host int32 copy and a device int32 copy."""
+
+    def __init__(self, cu_seqlens, device):
+        import numpy as np
+        if isinstance(cu_seqlens, torch.Tensor):
+            host = cu_seqlens.detach().to("cpu", torch.int32).numpy()
+        else:
+            host = np.asarray(cu_seqlens, dtype=np.int32)
+        self.host = np.ascontiguousarray(host, dtype=np.int32)
+        self.dev = torch.from_numpy(self.host).to(device)
+
+    @property
+    def num_seqs(self) -> int:
+        return len(self.host) - 1
+
+
+def _problem_for(q, v, variant, packed: Optional[Packed]):
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    io = GDN_BF16 if q.dtype == torch.bfloat16 else GDN_F32
+    if packed is None:
+        return make_problem(B, T, H, dk, dv, io_dtype=io, variant=variant)
+    return make_problem(B, T, H, dk, dv, io_dtype=io, variant=variant, cu_host=packed.host,
+                        cu_dev_ptr=packed.dev.data_ptr())
+
+
+def fwd(q, k, v, g, beta, S0=None, *, variant="gated_delta", cu_seqlens=None, workspace=None):
+    """Forward: returns (o, S_T, chunk_states).  See include/gdn.h for layouts."""
+    dev = q.device
+    packed = None if cu_seqlens is None else (cu_seqlens if isinstance(cu_seqlens, Packed)
+                                              else Packed(cu_seqlens, dev))
+    p = _problem_for(q, v, variant, packed)
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, name, q.dtype, dev)
+    for name, t in (("g", g), ("beta", beta), ("S0", S0)):
+        if t is not None:
+            _check(t, name, torch.float32, dev)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    N = p.num_seqs
+    nch = gdn_num_chunks(p)
+    if nch < 0:
+        raise GdnError(nch, "gdn_num_chunks")
+    o = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    S_T = torch.empty((N, H, dk, dv), dtype=torch.float32, device=dev)
+    states = torch.empty((nch, H, dk, dv), dtype=torch.float32, device=dev)
+    wsb = gdn_fwd_workspace_size(p)
+    ws = workspace if workspace is not None else torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    rc = gdn_fwd(p, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S0), _ptr(o), _ptr(S_T),
+                 _ptr(states), _ptr(ws), ws.numel(), ctypes.c_void_p(_stream_handle(dev)))
+    if rc != GDN_OK:
+        raise GdnError(rc, "gdn_fwd")
+    return o, S_T, states
+
+
+def bwd(q, k, v, g, beta, chunk_states, dO, dS_T=None, *, variant="gated_delta", cu_seqlens=None,
+        workspace=None):
+    """Backward: returns (dq, dk, dv, dg, dbeta, dS0); dg / dbeta are None when the variant has no g / beta."""
+    dev = q.device
+    packed = None if cu_seqlens is None else (cu_seqlens if isinstance(cu_seqlens, Packed)
+                                              else Packed(cu_seqlens, dev))
+    p = _problem_for(q, v, variant, packed)
+    for name, t in (("q", q), ("k", k), ("v", v), ("dO", dO)):
+        _check(t, name, q.dtype, dev)
+    for name, t in (("g", g), ("beta", beta), ("chunk_states", chunk_states), ("dS_T", dS_T)):
+        if t is not None:
+            _check(t, name, torch.float32, dev)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    N = p.num_seqs
+    dq = torch.empty_like(q)
+    dk_ = torch.empty_like(k)
+    dvv = torch.empty_like(v)
+    dg = None if g is None else torch.empty((B, T, H), dtype=torch.float32, device=dev)
+    db = None if beta is None else torch.empty((B, T, H), dtype=torch.float32, device=dev)
+    dS0 = torch.empty((N, H, dk, dv), dtype=torch.float32, device=dev)
+    wsb = gdn_bwd_workspace_size(p)
+    ws = workspace if workspace is not None else torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    rc = gdn_bwd(p, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(chunk_states), _ptr(dO),
+                 _ptr(dS_T), _ptr(dq), _ptr(dk_), _ptr(dvv), _ptr(dg), _ptr(db), _ptr(dS0), _ptr(ws),
+                 ws.numel(), ctypes.c_void_p(_stream_handle(dev)))
+    if rc != GDN_OK:
+        raise GdnError(rc, "gdn_bwd")
+    return dq, dk_, dvv, dg, db, dS0
+
+
+__all__ = ["load", "make_problem", "Problem", "Packed", "GdnError", "fwd", "bwd", "gdn_fwd", "gdn_bwd",
+           "gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_status_str",
+           "gdn_version", "EXPORTED", "LIB_PATH", "VARIANTS"]

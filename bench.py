@@ -1,0 +1,286 @@
+#!/usr/bin/env python3
+"""Throughput of the gated-delta-rule forward + training backward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+One step = gdn_fwd then gdn_bwd (the whole hot path) over one batch of the
+throughput workload: bf16 I/O with fp32 gates and states, B=4, T=4096, H=16,
+d_k=d_v=128, chunk 64, seeded synthetic inputs already resident in HBM.
+Outputs and workspaces are allocated once, outside the timed region.
+
+The JSON line carries, besides tokens/s:
+  roofline      the dominant kernel (largest average duration among the
+                forward and backward stages), its algorithmic bytes per launch
+                divided by its average launch duration, measured live with HIP
+                events recorded on the launch stream around each stage of the
+                timed steps, against MI355X's 8 TB/s HBM peak;
+  cpu_baseline  the float64 oracle (fwd + bwd) on the host cores, on a bounded
+                sample of the same workload's (b, h) streams.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+CH = 64
+
+
+def kernel_model(B, T, H, dk, dv, es, N=None):
+    """Algorithmic bytes and flops per launch of every stage (compulsory traffic
+    of the kernel's own inputs and outputs, each moved once at its stored dtype).
+    """
+    N = B if N is None else N
+    nch = B * (-(-T // CH))
+    tiles = nch * H
+    g4 = 4 * CH  # one fp32 per token of a chunk
+    st = dk * dv * 4
+    per = {
+        "fwd_prep": (CH * dk * es + CH * dv * es + 2 * g4 + g4 + CH * dk * es + CH * dv * 4,
+                     2 * CH * CH * dk * 2 + CH ** 3 / 3 + 2 * CH * CH * dv),
+        "fwd_scan": (2 * CH * dk * es + CH * dv * 4 + g4 + st + CH * dv * es,
+                     2 * 2 * CH * dk * dv),
+        "fwd_out": (2 * CH * dk * es + g4 + st + CH * dv * es + CH * dv * es,
+                    2 * CH * CH * dk + 2 * CH * dk * dv + 2 * CH * CH * dv),
+        "bwd_prep": (2 * CH * dk * es + CH * dv * es + 2 * g4 + g4 + CH * dk * es + CH * dv * 4,
+                     3 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dv),
+        "bwd_scan": (3 * CH * dk * es + CH * dv * es + CH * dv * 4 + g4 + dk * dv * es,
+                     3 * 2 * CH * dk * dv),
+        "bwd_grad": (2 * CH * dk * es + 2 * CH * dv * es + 2 * g4 + st + dk * dv * es
+                     + 2 * CH * dk * es + CH * dv * es + 2 * g4,
+                     5 * 2 * CH * CH * dk + CH ** 3 / 3 + 4 * CH ** 3 + 5 * 2 * CH * dk * dv
+                     + 5 * 2 * CH * CH * dv),
+    }
+    out = {k: (b * tiles, f * tiles) for k, (b, f) in per.items()}
+    sio = 2 * N * H * dk * dv * 4  # S0 / S_T or dS_T / dS0
+    out["fwd_scan"] = (out["fwd_scan"][0] + sio, out["fwd_scan"][1])
+    out["bwd_scan"] = (out["bwd_scan"][0] + sio, out["bwd_scan"][1])
+    return out
+
+
+def path_model(B, T, H, dk, dv, es, N=None):
+    """The API's compulsory bytes for the forward and the backward."""
+    N = B if N is None else N
+    tok = B * T * H
+    nch = B * (-(-T // CH))
+    states = nch * H * dk * dv * 4
+    s = N * H * dk * dv * 4
+    fwd = tok * (2 * dk * es + dv * es + 8) + s + tok * dv * es + s + states
+    bwd = tok * (2 * dk * es + dv * es + 8) + states + tok * dv * es + s + tok * (2 * dk * es + dv * es + 8) + s
+    return fwd, bwd
+
+
+class Hip:
+    """The few HIP runtime calls the timing needs (events on the launch stream)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def event(self):
+        e = ctypes.c_void_p()
+        assert self.lib.hipEventCreate(ctypes.byref(e)) == 0
+        return e
+
+    def record(self, e, stream):
+        assert self.lib.hipEventRecord(e, ctypes.c_void_p(stream)) == 0
+
+    def ms(self, a, b):
+        x = ctypes.c_float()
+        assert self.lib.hipEventElapsedTime(ctypes.byref(x), a, b) == 0
+        return float(x.value)
+
+
+def _oracle_stream(args):
+    """One (b, h) stream through the float64 oracle: forward then backward."""
+    os.environ["OMP_NUM_THREADS"] = os.environ["OPENBLAS_NUM_THREADS"] = "1"
+    os.environ["MKL_NUM_THREADS"] = "1"
+    import numpy as np
+    from oracle import gdn_oracle as O
+    q, k, v, g, b, S0, dO, dST = args
+    f = lambda x: x[None].astype(np.float64)
+    O.fwd_streams(f(q), f(k), f(v), f(g), f(b), f(S0))
+    O.bwd_streams(f(q), f(k), f(v), f(g), f(b), f(S0), f(dO), f(dST))
+    return q.shape[0]
+
+
+def cpu_baseline(case, budget_s=15.0):
+    """Time the oracle on a bounded sample of the workload's streams, all host cores."""
+    import multiprocessing as mp
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    cores = max(1, min(cores, 16))
+    streams = [(b, h) for b in range(case.B) for h in range(case.H)]
+    per_stream_s = 2.5 * (case.T / 4096) * (case.dk * case.dv / 16384)
+    n = int(max(cores, min(len(streams), budget_s * cores / max(per_stream_s, 1e-3))))
+    n = min(n, len(streams))
+    sample = streams[:n]
+    tasks = [(case.q[b, :, h], case.k[b, :, h], case.v[b, :, h], case.g[b, :, h], case.beta[b, :, h],
+              case.S0[b, h], case.dO[b, :, h], case.dS_T[b, h]) for (b, h) in sample]
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(cores) as pool:
+        done = sum(pool.map(_oracle_stream, tasks, chunksize=1))
+    wall = time.perf_counter() - t0
+    token_heads = done
+    return {
+        "value": round(token_heads / case.H / wall, 1),
+        "unit": "tokens/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"{n} of {len(streams)} (b,h) streams of the workload, full T={case.T} each, "
+                   f"float64 token-serial fwd+bwd, one process per core; tokens/s counts all "
+                   f"{case.H} heads ({token_heads} token-heads in {wall:.1f} s)"),
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--stages", action="store_true", help="also print per-stage timings to stderr")
+    a = ap.parse_args(argv)
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); the path shards over "
+              f"(sequence, head) streams with no communication, so N GPUs run N independent copies.",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2608_12700_amd import gdn
+
+    case = W.config1()
+    # the oracle's worker processes are forked before anything touches the GPU
+    cpu = None if a.no_cpu_baseline else cpu_baseline(case, a.cpu_budget)
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    B, T, H, dk, dv = case.B, case.T, case.H, case.dk, case.dv
+    bf = torch.bfloat16
+    act = lambda x: torch.from_numpy(x).to(dev).to(bf).contiguous()
+    f32 = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+    q, k, v, dO = act(case.q), act(case.k), act(case.v), act(case.dO)
+    g, beta, S0, dST = f32(case.g), f32(case.beta), f32(case.S0), f32(case.dS_T)
+
+    p = gdn.make_problem(B, T, H, dk, dv, io_dtype=gdn.GDN_BF16, variant="gated_delta")
+    nch = gdn.gdn_num_chunks(p)
+    o = torch.empty_like(v)
+    S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
+    states = torch.empty((nch, H, dk, dv), dtype=torch.float32, device=dev)
+    dq, dk_, dv_ = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    dg, db = torch.empty_like(g), torch.empty_like(beta)
+    dS0 = torch.empty_like(S0)
+    wsf = torch.empty(gdn.gdn_fwd_workspace_size(p), dtype=torch.uint8, device=dev)
+    wsb = torch.empty(gdn.gdn_bwd_workspace_size(p), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+    hip = Hip()
+    ns = gdn.NUM_STAGES + 1
+
+    def step(evf=None, evb=None):
+        rc = gdn.gdn_fwd_ex(p, P(q), P(k), P(v), P(g), P(beta), P(S0), P(o), P(S_T), P(states), P(wsf),
+                            wsf.numel(), ctypes.c_void_p(stream), evf)
+        assert rc == 0, rc
+        rc = gdn.gdn_bwd_ex(p, P(q), P(k), P(v), P(g), P(beta), P(states), P(dO), P(dST), P(dq), P(dk_),
+                            P(dv_), P(dg), P(db), P(dS0), P(wsb), wsb.numel(), ctypes.c_void_p(stream), evb)
+        assert rc == 0, rc
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-step stage events, created before the timed region
+    evs = []
+    for _ in range(a.steps):
+        ef = (ctypes.c_void_p * ns)(*[hip.event() for _ in range(ns)])
+        eb = (ctypes.c_void_p * ns)(*[hip.event() for _ in range(ns)])
+        evs.append((ef, eb))
+    t0, t1 = hip.event(), hip.event()
+
+    torch.cuda.synchronize()
+    hip.record(t0, stream)
+    for i in range(a.steps):
+        step(evs[i][0], evs[i][1])
+    hip.record(t1, stream)
+    torch.cuda.synchronize()
+    total_ms = hip.ms(t0, t1)
+    ms_step = total_ms / a.steps
+
+    names = list(gdn.FWD_STAGES) + list(gdn.BWD_STAGES)
+    stage_ms = {nm: 0.0 for nm in names}
+    for ef, eb in evs:
+        for j in range(gdn.NUM_STAGES):
+            stage_ms[gdn.FWD_STAGES[j]] += hip.ms(ef[j], ef[j + 1]) / a.steps
+            stage_ms[gdn.BWD_STAGES[j]] += hip.ms(eb[j], eb[j + 1]) / a.steps
+    fwd_ms = sum(stage_ms[n] for n in gdn.FWD_STAGES)
+    bwd_ms = sum(stage_ms[n] for n in gdn.BWD_STAGES)
+
+    ok = all(bool(torch.isfinite(x).all()) for x in (o, S_T, dq, dk_, dv_, dg, db, dS0))
+
+    km = kernel_model(B, T, H, dk, dv, 2)
+    dom = max(km, key=lambda n: stage_ms[n])
+    dom_bytes, dom_flops = km[dom]
+    dom_s = stage_ms[dom] / 1e3
+    ach = dom_bytes / dom_s / 1e9
+    fwd_b, bwd_b = path_model(B, T, H, dk, dv, 2)
+
+    tokens = B * T
+    res = {
+        "metric": "GDN fwd+bwd tokens/s at B4 T4096 H16 d128 bf16; % of binding roofline",
+        "value": round(tokens / (ms_step / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded: q,k L2-normalised N(0,1); v,dO N(0,1); beta=sigmoid(N); "
+                "g=-0.1*softplus(N); S0 N(0,0.1^2); dS_T N(0,1))",
+        "config": {"workload": "gated delta rule fwd+bwd, bf16 I/O, fp32 state, B=4 T=4096 H=16 "
+                               "dk=dv=128 chunk=64", "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
+                   "chunk": CH, "global_batch": B, "seq_len": T, "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": int(dom_bytes),
+                     "avg_launch_ms": round(stage_ms[dom], 4),
+                     "mfma_tflops": round(dom_flops / dom_s / 1e12, 1)},
+        "path": {"fwd_ms": round(fwd_ms, 4), "bwd_ms": round(bwd_ms, 4),
+                 "fwd_hbm_frac": round(fwd_b / 8e12 / (fwd_ms / 1e3), 4),
+                 "bwd_hbm_frac": round(bwd_b / 8e12 / (bwd_ms / 1e3), 4),
+                 "bwd_tokens_per_s": round(tokens / (bwd_ms / 1e3), 1),
+                 "stage_ms": {k_: round(x, 4) for k_, x in stage_ms.items()},
+                 "outputs_finite": ok},
+    }
+    if a.stages:
+        for nm in names:
+            b_, f_ = km.get(nm, (0, 0))
+            t_ = stage_ms[nm] / 1e3
+            if t_ > 0 and b_:
+                print(f"{nm:10s} {stage_ms[nm]*1e3:9.1f} us  {b_/t_/1e9:8.1f} GB/s  {f_/t_/1e12:7.1f} TFLOP/s",
+                      file=sys.stderr)
+    if cpu is not None:
+        res["cpu_baseline"] = cpu
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

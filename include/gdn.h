@@ -136,6 +136,28 @@ gdn_status gdn_bwd(const gdn_problem* p, const void* q, const void* k, const voi
                    const float* dS_T, void* dq, void* dk, void* dv, float* dg, float* dbeta,
                    float* dS0, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Stages that gdn_fwd_ex / gdn_bwd_ex can bracket with events.  Forward:
+ * 0 chunk prep (UT transform), 1 forward state scan, 2 chunk output, 3 exact
+ * token-serial pass for non-finite streams.  Backward: 0 chunk prep, 1 reverse
+ * state scan, 2 chunk gradients, 3 exact pass. */
+#define GDN_NUM_STAGES 4
+
+/* gdn_fwd / gdn_bwd with optional per-stage timing.  `events` is NULL or an
+ * array of GDN_NUM_STAGES + 1 hipEvent_t handles created by the caller;
+ * events[i] is recorded on `stream` right before stage i is enqueued and
+ * events[GDN_NUM_STAGES] after the last one (a stage with nothing to do
+ * records two adjacent events).  The kernels are exactly those of
+ * gdn_fwd / gdn_bwd; argument checks and errors are the same. */
+gdn_status gdn_fwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
+                      const float* g, const float* beta, const float* S0, void* o, float* S_T,
+                      float* chunk_states, void* workspace, size_t workspace_bytes, void* stream,
+                      void* const* events);
+gdn_status gdn_bwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
+                      const float* g, const float* beta, const float* chunk_states, const void* dO,
+                      const float* dS_T, void* dq, void* dk, void* dv, float* dg, float* dbeta,
+                      float* dS0, void* workspace, size_t workspace_bytes, void* stream,
+                      void* const* events);
+
 /* Static description of a status code. */
 const char* gdn_status_str(gdn_status s);
 

@@ -186,6 +186,14 @@ size_t gdn_bwd_workspace_size(const gdn_problem* p) {
 gdn_status gdn_fwd(const gdn_problem* p, const void* q, const void* k, const void* v, const float* g,
                    const float* beta, const float* S0, void* o, float* S_T, float* chunk_states,
                    void* workspace, size_t workspace_bytes, void* stream) {
+  return gdn_fwd_ex(p, q, k, v, g, beta, S0, o, S_T, chunk_states, workspace, workspace_bytes, stream,
+                    nullptr);
+}
+
+gdn_status gdn_fwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
+                      const float* g, const float* beta, const float* S0, void* o, float* S_T,
+                      float* chunk_states, void* workspace, size_t workspace_bytes, void* stream,
+                      void* const* events) {
   try {
     Shape s;
     gdn_status st = check_problem(p, &s);
@@ -219,9 +227,11 @@ gdn_status gdn_fwd(const gdn_problem* p, const void* q, const void* k, const voi
     a.q = q; a.k = k; a.v = v; a.g = g; a.beta = beta; a.S0 = S0;
     a.o = o; a.ST = S_T; a.states = chunk_states; a.ws = w;
     a.stream = static_cast<hipStream_t>(stream);
-    if (s.N * s.H == 0) return GDN_OK;
-    if (s.packed && launch_chunk_offsets(p->cu_seqlens_dev, (int)s.N, w.chunk_off, a.stream) != hipSuccess)
-      return GDN_ERR_HIP;
+    a.events = reinterpret_cast<hipEvent_t const*>(events);
+    if (s.N * s.H == 0) {
+      for (int i = 0; i <= NUM_STAGES; ++i) stage_mark(a.events, i, a.stream);
+      return GDN_OK;
+    }
     hipError_t e;
     const bool bf = p->io_dtype == GDN_BF16;
     switch (p->variant) {
@@ -239,6 +249,15 @@ gdn_status gdn_bwd(const gdn_problem* p, const void* q, const void* k, const voi
                    const float* beta, const float* chunk_states, const void* dO, const float* dS_T,
                    void* dq, void* dk, void* dv, float* dg, float* dbeta, float* dS0, void* workspace,
                    size_t workspace_bytes, void* stream) {
+  return gdn_bwd_ex(p, q, k, v, g, beta, chunk_states, dO, dS_T, dq, dk, dv, dg, dbeta, dS0, workspace,
+                    workspace_bytes, stream, nullptr);
+}
+
+gdn_status gdn_bwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
+                      const float* g, const float* beta, const float* chunk_states, const void* dO,
+                      const float* dS_T, void* dq, void* dk, void* dv, float* dg, float* dbeta,
+                      float* dS0, void* workspace, size_t workspace_bytes, void* stream,
+                      void* const* events) {
   try {
     Shape s;
     gdn_status st = check_problem(p, &s);
@@ -278,9 +297,11 @@ gdn_status gdn_bwd(const gdn_problem* p, const void* q, const void* k, const voi
     a.dO = dO; a.dST = dS_T;
     a.dq = dq; a.dk_ = dk; a.dv_ = dv; a.dg = dg; a.dbeta = dbeta; a.dS0 = dS0; a.ws = w;
     a.stream = static_cast<hipStream_t>(stream);
-    if (s.N * s.H == 0) return GDN_OK;
-    if (s.packed && launch_chunk_offsets(p->cu_seqlens_dev, (int)s.N, w.chunk_off, a.stream) != hipSuccess)
-      return GDN_ERR_HIP;
+    a.events = reinterpret_cast<hipEvent_t const*>(events);
+    if (s.N * s.H == 0) {
+      for (int i = 0; i <= NUM_STAGES; ++i) stage_mark(a.events, i, a.stream);
+      return GDN_OK;
+    }
     hipError_t e;
     const bool bf = p->io_dtype == GDN_BF16;
     switch (p->variant) {

@@ -590,23 +590,32 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
   const Geo& geo = a.geo;
   const int H = geo.H;
   const BwdWs& w = a.ws;
+  stage_mark(a.events, 0, a.stream);
+  if (geo.cu != nullptr) {
+    const hipError_t e = launch_chunk_offsets(geo.cu, geo.N, const_cast<int*>(geo.chunk_off), a.stream);
+    if (e != hipSuccess) return e;
+  }
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_prep_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, a.g, a.beta, (const OP*)a.dO, w.gcum,
                        (OP*)w.W, w.dvl, w.flag_prep);
   }
+  stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
                        (const OP*)a.q, (const OP*)a.k, (const OP*)a.dO, a.dST, w.gcum, (const OP*)w.W,
                        w.dvl, (OP*)w.dh, a.dS0, w.flag_scan);
   }
+  stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_grad_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, a.states,
                        (const OP*)a.dO, (const OP*)w.dh, (OP*)a.dq, (OP*)a.dk_, (OP*)a.dv_, a.dg, a.dbeta,
                        w.flag_grad, (char*)w.grad_scratch);
   }
+  stage_mark(a.events, 3, a.stream);
+  stage_mark(a.events, 4, a.stream);
   return hipGetLastError();
 }
 

@@ -250,22 +250,31 @@ static hipError_t launch_fwd_t(const FwdArgs& a) {
   const Geo& geo = a.geo;
   const int H = geo.H;
   const FwdWs& w = a.ws;
+  stage_mark(a.events, 0, a.stream);
+  if (geo.cu != nullptr) {
+    const hipError_t e = launch_chunk_offsets(geo.cu, geo.N, const_cast<int*>(geo.chunk_off), a.stream);
+    if (e != hipSuccess) return e;
+  }
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_prep_fwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
                        geo, H, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, w.gcum, (OP*)w.W, w.U,
                        w.flag_prep);
   }
+  stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
                        (const OP*)a.k, (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, w.U, a.states,
                        a.ST, (OP*)w.UpT, w.flag_scan);
   }
+  stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_out_fwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, w.gcum, a.states,
                        (const OP*)w.UpT, (OP*)a.o, w.flag_out);
   }
+  stage_mark(a.events, 3, a.stream);
+  stage_mark(a.events, 4, a.stream);
   return hipGetLastError();
 }
 

@@ -31,6 +31,7 @@ struct FwdArgs {
   float* states;
   FwdWs ws;
   hipStream_t stream;
+  hipEvent_t const* events;  // nullptr, or NUM_STAGES + 1 events
 };
 
 struct BwdWs {
@@ -57,7 +58,15 @@ struct BwdArgs {
   float *dg, *dbeta, *dS0;
   BwdWs ws;
   hipStream_t stream;
+  hipEvent_t const* events;
 };
+
+constexpr int NUM_STAGES = 4;
+
+// Records events[i] on the stream when per-stage timing was requested.
+inline void stage_mark(hipEvent_t const* events, int i, hipStream_t stream) {
+  if (events) (void)hipEventRecord(events[i], stream);
+}
 
 // value-tile width of the state scans
 constexpr int SCAN_BV = 32;

@@ -47,7 +47,10 @@ class Problem(ctypes.Structure):
 
 
 EXPORTED = ("gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_fwd",
-            "gdn_bwd", "gdn_status_str", "gdn_version")
+            "gdn_bwd", "gdn_fwd_ex", "gdn_bwd_ex", "gdn_status_str", "gdn_version")
+NUM_STAGES = 4
+FWD_STAGES = ("fwd_prep", "fwd_scan", "fwd_out", "fwd_exact")
+BWD_STAGES = ("bwd_prep", "bwd_scan", "bwd_grad", "bwd_exact")
 
 _lib = None
 
@@ -72,6 +75,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gdn_fwd.restype = ctypes.c_int
     lib.gdn_bwd.argtypes = [P] + [vp] * 14 + [vp, sz, vp]
     lib.gdn_bwd.restype = ctypes.c_int
+    lib.gdn_fwd_ex.argtypes = [P] + [vp] * 9 + [vp, sz, vp, vp]
+    lib.gdn_fwd_ex.restype = ctypes.c_int
+    lib.gdn_bwd_ex.argtypes = [P] + [vp] * 14 + [vp, sz, vp, vp]
+    lib.gdn_bwd_ex.restype = ctypes.c_int
     lib.gdn_status_str.argtypes = [ctypes.c_int]
     lib.gdn_status_str.restype = ctypes.c_char_p
     lib.gdn_version.argtypes = []
@@ -121,6 +128,17 @@ def gdn_bwd(p, q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg, dbeta, dS0, w
             stream) -> int:
     return int(load().gdn_bwd(ctypes.byref(p), q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg,
                               dbeta, dS0, ws, ws_bytes, stream))
+
+
+def gdn_fwd_ex(p, q, k, v, g, beta, S0, o, S_T, states, ws, ws_bytes, stream, events) -> int:
+    return int(load().gdn_fwd_ex(ctypes.byref(p), q, k, v, g, beta, S0, o, S_T, states, ws, ws_bytes,
+                                 stream, events))
+
+
+def gdn_bwd_ex(p, q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg, dbeta, dS0, ws, ws_bytes,
+               stream, events) -> int:
+    return int(load().gdn_bwd_ex(ctypes.byref(p), q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg,
+                                 dbeta, dS0, ws, ws_bytes, stream, events))
 
 
 def gdn_status_str(code: int) -> str:
@@ -238,5 +256,6 @@ def bwd(q, k, v, g, beta, chunk_states, dO, dS_T=None, *, variant="gated_delta",
 
 
 __all__ = ["load", "make_problem", "Problem", "Packed", "GdnError", "fwd", "bwd", "gdn_fwd", "gdn_bwd",
+           "gdn_fwd_ex", "gdn_bwd_ex", "NUM_STAGES", "FWD_STAGES", "BWD_STAGES",
            "gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_status_str",
            "gdn_version", "EXPORTED", "LIB_PATH", "VARIANTS"]

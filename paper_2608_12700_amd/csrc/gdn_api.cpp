@@ -117,7 +117,7 @@ void layout_fwd(const Shape& s, char* base, FwdWs* w, size_t* total) {
   w->W = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->U = b.take<float>(tiles * kChunk * s.dv);
   w->UpT = b.take<char>(tiles * kChunk * s.dv * s.es);
-  w->exact = b.take<float>(exact_scratch_floats(s));
+  w->exact = nullptr;  // the exact forward needs no scratch
   *total = b.off;
 }
 
@@ -137,10 +137,11 @@ void layout_bwd(const Shape& s, char* base, BwdWs* w, size_t* total) {
   *total = b.off;
 }
 
-// The exact (token-serial) path keeps the states of one chunk per slot.
+// The exact (token-serial) backward keeps the states of one chunk per slot
+// (EXACT_SLOTS in gdn_exact.hpp).
 constexpr int kExactSlots = 16;
 size_t exact_scratch_floats(const Shape& s) {
-  return (size_t)kExactSlots * (kChunk + 1) * s.dk * s.dv;
+  return (size_t)kExactSlots * (kChunk + 2) * s.dk * s.dv;
 }
 
 Geo make_geo(const Shape& s, const gdn_problem* p, const int* chunk_off) {

@@ -26,6 +26,7 @@
 #pragma once
 
 #include "gdn_chunk.hpp"
+#include "gdn_exact.hpp"
 #include "gdn_launch.hpp"
 
 namespace gdn {
@@ -615,6 +616,12 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
                        w.flag_grad, (char*)w.grad_scratch);
   }
   stage_mark(a.events, 3, a.stream);
+  if (NS > 0) {
+    hipLaunchKernelGGL((k_exact_bwd<DK, DV, OP, VAR>), dim3(EXACT_SLOTS), dim3(DV), 0, a.stream, geo,
+                       (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, a.states,
+                       (const OP*)a.dO, a.dST, (OP*)a.dq, (OP*)a.dk_, (OP*)a.dv_, a.dg, a.dbeta, a.dS0,
+                       w.flag_prep, w.flag_grad, w.flag_scan, NVT, w.exact);
+  }
   stage_mark(a.events, 4, a.stream);
   return hipGetLastError();
 }

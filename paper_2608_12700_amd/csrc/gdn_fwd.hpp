@@ -16,6 +16,7 @@
 #pragma once
 
 #include "gdn_chunk.hpp"
+#include "gdn_exact.hpp"
 #include "gdn_launch.hpp"
 
 namespace gdn {
@@ -274,6 +275,11 @@ static hipError_t launch_fwd_t(const FwdArgs& a) {
                        (const OP*)w.UpT, (OP*)a.o, w.flag_out);
   }
   stage_mark(a.events, 3, a.stream);
+  if (NS > 0) {
+    hipLaunchKernelGGL((k_exact_fwd<DK, DV, OP, VAR>), dim3(NS), dim3(DV), 0, a.stream, geo, (const OP*)a.q,
+                       (const OP*)a.k, (const OP*)a.v, a.g, a.beta, a.S0, (OP*)a.o, a.ST, a.states,
+                       w.flag_prep, w.flag_out, w.flag_scan, NVT);
+  }
   stage_mark(a.events, 4, a.stream);
   return hipGetLastError();
 }

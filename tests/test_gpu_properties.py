@@ -1,0 +1,148 @@
+"""Tolerance-free properties of the HIP path, called through the C ABI:
+bitwise determinism, untouched guard bands around every output, the
+identity-state invariant, empty sequences, and host-side rejection of bad
+calls on a live device (nothing launched, outputs untouched)."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import workloads as W
+from tests import harness as Hn
+
+pytestmark = pytest.mark.gpu
+
+
+def _bits(t):
+    import torch
+    return t.contiguous().view(torch.uint8) if t.dtype != torch.bool else t
+
+
+def test_bitwise_determinism_five_runs():
+    import torch
+    case = W.config1()
+    first = Hn.run_device(case, keep_torch=True)
+    for rep in range(4):
+        again = Hn.run_device(case, keep_torch=True)
+        for nm, x in first.items():
+            if x is None:
+                continue
+            assert torch.equal(_bits(x), _bits(again[nm])), (rep, nm)
+
+
+def test_determinism_packed_and_variants():
+    import torch
+    for case in (W.config3("delta"), W.config3("decay_only")):
+        a = Hn.run_device(case, keep_torch=True)
+        b = Hn.run_device(case, keep_torch=True)
+        for nm, x in a.items():
+            if x is not None:
+                assert torch.equal(_bits(x), _bits(b[nm])), (case.name, nm)
+
+
+SENT = {"bf16": 0x7FA1, "f32": 0x7FC0DEAD}  # NaN payloads nothing in the path produces
+
+
+def _guarded(n, dtype, pad, io):
+    import torch
+    if dtype == torch.float32:
+        buf = torch.full((n + 2 * pad,), 0, dtype=torch.int32, device="cuda")
+        buf.fill_(np.int32(np.uint32(SENT["f32"]).view(np.int32)))
+        return buf.view(torch.float32)
+    buf = torch.full((n + 2 * pad,), 0, dtype=torch.int16, device="cuda")
+    buf.fill_(SENT["bf16"])
+    return buf.view(torch.bfloat16)
+
+
+@pytest.mark.parametrize("io", ["bf16", "f32"])
+def test_guard_bands_untouched(io):
+    """Outputs sit between sentinel-filled guard bands; ragged packed sequences
+    stress the tail chunks.  Every guard byte must survive both calls."""
+    import torch
+    from paper_2608_12700_amd import gdn
+    cu = np.array([0, 1, 64, 129, 130, 250], np.int32)
+    case = W.make_case(f"guard_{io}", B=1, T=int(cu[-1]), H=3, dk=64, dv=128, io_dtype=io, cu_seqlens=cu)
+    t = Hn.device_inputs(case)
+    act = torch.bfloat16 if io == "bf16" else torch.float32
+    packed = gdn.Packed(cu, "cuda")
+    p = gdn.make_problem(1, case.T, case.H, 64, 128, io_dtype=1 if io == "bf16" else 0, cu_host=packed.host,
+                         cu_dev_ptr=packed.dev.data_ptr())
+    nch = gdn.gdn_num_chunks(p)
+    N, H, T = len(cu) - 1, case.H, case.T
+    pad = 4096
+    sizes = {"o": (T * H * 128, act), "S_T": (N * H * 64 * 128, torch.float32),
+             "st": (nch * H * 64 * 128, torch.float32), "dq": (T * H * 64, act), "dk": (T * H * 64, act),
+             "dv": (T * H * 128, act), "dg": (T * H, torch.float32), "db": (T * H, torch.float32),
+             "dS0": (N * H * 64 * 128, torch.float32)}
+    bufs = {k: _guarded(n, dt, pad, io) for k, (n, dt) in sizes.items()}
+    ref = {k: b.clone() for k, b in bufs.items()}
+    P = lambda k: ctypes.c_void_p(bufs[k].data_ptr() + pad * bufs[k].element_size())
+    X = lambda x: ctypes.c_void_p(x.data_ptr())
+    wf = torch.empty(gdn.gdn_fwd_workspace_size(p), dtype=torch.uint8, device="cuda")
+    wb = torch.empty(gdn.gdn_bwd_workspace_size(p), dtype=torch.uint8, device="cuda")
+    s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    assert gdn.gdn_fwd(p, X(t["q"]), X(t["k"]), X(t["v"]), X(t["g"]), X(t["beta"]), X(t["S0"]), P("o"),
+                       P("S_T"), P("st"), X(wf), wf.numel(), s) == 0
+    assert gdn.gdn_bwd(p, X(t["q"]), X(t["k"]), X(t["v"]), X(t["g"]), X(t["beta"]), P("st"), X(t["dO"]),
+                       X(t["dS_T"]), P("dq"), P("dk"), P("dv"), P("dg"), P("db"), P("dS0"), X(wb), wb.numel(),
+                       s) == 0
+    torch.cuda.synchronize()
+    for k, b in bufs.items():
+        n = sizes[k][0]
+        bb, rr = b.view(torch.uint8), ref[k].view(torch.uint8)
+        es = b.element_size()
+        assert torch.equal(bb[:pad * es], rr[:pad * es]), f"{k}: guard before written"
+        assert torch.equal(bb[(pad + n) * es:], rr[(pad + n) * es:]), f"{k}: guard after written"
+        inner = b[pad:pad + n]
+        assert not torch.equal(inner.view(torch.uint8), ref[k][pad:pad + n].view(torch.uint8)), k
+
+
+def test_identity_state_when_beta_and_g_vanish():
+    import torch
+    from paper_2608_12700_amd import gdn
+    case = W.make_case("identity", B=2, T=300, H=2, dk=128, dv=64)
+    t = Hn.device_inputs(case)
+    zg, zb = torch.zeros_like(t["g"]), torch.zeros_like(t["beta"])
+    o, S_T, st = gdn.fwd(t["q"], t["k"], t["v"], zg, zb, t["S0"])
+    torch.cuda.synchronize()
+    assert torch.equal(S_T, t["S0"])
+    for c in range(st.shape[0] // 2):
+        assert torch.equal(st[c], t["S0"][0])
+
+
+def test_empty_sequences():
+    import torch
+    from paper_2608_12700_amd import gdn
+    case = W.make_case("empty", B=2, T=0, H=3, dk=64, dv=64)
+    t = Hn.device_inputs(case)
+    o, S_T, st = gdn.fwd(t["q"], t["k"], t["v"], t["g"], t["beta"], t["S0"])
+    dq, dk, dv, dg, db, dS0 = gdn.bwd(t["q"], t["k"], t["v"], t["g"], t["beta"], st, t["dO"], t["dS_T"])
+    torch.cuda.synchronize()
+    assert st.shape[0] == 0 and torch.equal(S_T, t["S0"]) and torch.equal(dS0, t["dS_T"])
+    cu = np.array([0, 0, 70, 70], np.int32)
+    case = W.make_case("empty_packed", B=1, T=70, H=2, dk=64, dv=64, cu_seqlens=cu)
+    dev, ref = Hn.run_device(case), Hn.run_oracle(case)
+    for d, r in zip(Hn.per_sequence(case, dev), Hn.per_sequence(case, ref)):
+        Hn.assert_parity(Hn.compare(d, r), 1e-2, "empty packed")
+
+
+def test_rejected_calls_leave_outputs_untouched():
+    import torch
+    from paper_2608_12700_amd import gdn
+    case = W.make_case("reject", B=1, T=64, H=2, dk=64, dv=64)
+    t = Hn.device_inputs(case)
+    p = gdn.make_problem(1, 64, 2, 64, 64)
+    o = torch.full_like(t["v"], 3.0)
+    S_T = torch.full_like(t["S0"], 3.0)
+    st = torch.full((1, 2, 64, 64), 3.0, device="cuda")
+    ws = torch.empty(gdn.gdn_fwd_workspace_size(p), dtype=torch.uint8, device="cuda")
+    X = lambda x: ctypes.c_void_p(x.data_ptr())
+    s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    rc = gdn.gdn_fwd(p, X(t["q"]), X(t["k"]), X(t["v"]), X(t["g"]), X(t["beta"]), X(t["S0"]), X(t["q"]),
+                     X(S_T), X(st), X(ws), ws.numel(), s)
+    assert rc == -6
+    rc = gdn.gdn_fwd(p, X(t["q"]), X(t["k"]), X(t["v"]), X(t["g"]), X(t["beta"]), X(t["S0"]), X(o), X(S_T),
+                     X(st), X(ws), ws.numel() - 1, s)
+    assert rc == -5
+    torch.cuda.synchronize()
+    assert bool((o == 3.0).all()) and bool((S_T == 3.0).all()) and bool((st == 3.0).all())

@@ -117,6 +117,7 @@ void layout_fwd(const Shape& s, char* base, FwdWs* w, size_t* total) {
   w->W = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->U = b.take<float>(tiles * kChunk * s.dv);
   w->UpT = b.take<char>(tiles * kChunk * s.dv * s.es);
+  w->KhT = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->exact = nullptr;  // the exact forward needs no scratch
   *total = b.off;
 }
@@ -130,8 +131,11 @@ void layout_bwd(const Shape& s, char* base, BwdWs* w, size_t* total) {
   w->flag_scan = b.take<int>((size_t)s.N * s.H * (s.dv / SCAN_BV));
   w->gcum = b.take<float>(tiles * kChunk);
   w->W = b.take<char>(tiles * kChunk * s.dk * s.es);
+  w->QgT = b.take<char>(tiles * kChunk * s.dk * s.es);
+  w->dOT = b.take<char>(tiles * kChunk * s.dv * s.es);
   w->dvl = b.take<float>(tiles * kChunk * s.dv);
   w->dh = b.take<char>(tiles * (size_t)s.dk * s.dv * s.es);
+  w->dUT = b.take<char>(tiles * kChunk * s.dv * s.es);
   w->grad_scratch = b.take<char>(s.es == 4 ? tiles * (size_t)grad_region_bytes((int)s.dk, 4) : 0);
   w->exact = b.take<float>(exact_scratch_floats(s));
   *total = b.off;

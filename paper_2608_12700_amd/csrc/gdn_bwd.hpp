@@ -31,11 +31,29 @@
 
 namespace gdn {
 
+// 4 consecutive elements of the operand type as one load/store unit.
+template <typename T> struct vec4_of;
+template <> struct vec4_of<bf16> { typedef uint2 type; };
+template <> struct vec4_of<float> { typedef uint4 type; };
+template <typename T> __device__ __forceinline__ T elem4(const typename vec4_of<T>::type& u, int j);
+template <> __device__ __forceinline__ bf16 elem4<bf16>(const uint2& u, int j) {
+  return __builtin_bit_cast(bf16, (unsigned short)((j < 2 ? u.x : u.y) >> ((j & 1) * 16)));
+}
+template <> __device__ __forceinline__ float elem4<float>(const uint4& u, int j) {
+  return elem16<float>(u, j);
+}
+template <typename T> __device__ __forceinline__ typename vec4_of<T>::type pack4(const T* x);
+template <> __device__ __forceinline__ uint2 pack4<bf16>(const bf16* x) {
+  return uint2{pack2(x[0], x[1]), pack2(x[2], x[3])};
+}
+template <> __device__ __forceinline__ uint4 pack4<float>(const float* x) { return pack16<float>(x); }
+
 template <int DK, int DV, typename OP, int VAR>
 __global__ __launch_bounds__(256) void k_prep_bwd(Geo geo, int H, const OP* __restrict__ q,
                                                   const OP* __restrict__ k, const float* __restrict__ g,
                                                   const float* __restrict__ beta, const OP* __restrict__ dO,
-                                                  float* __restrict__ gcum, OP* __restrict__ Wg,
+                                                  float* __restrict__ gcum, OP* __restrict__ WTg,
+                                                  OP* __restrict__ QgTg, OP* __restrict__ dOTg,
                                                   float* __restrict__ dvlg, int* __restrict__ flag) {
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
@@ -88,8 +106,20 @@ __global__ __launch_bounds__(256) void k_prep_bwd(Geo geo, int H, const OP* __re
     w.template mma<OP, CH>(KRow<OP, LTT>{Tp}, kfun<OP>([&](int d, int i) {
                              return from_f<OP>(GBs[i] * to_f(Ks[i * LK + d]));
                            }));
-    OP* Wt = Wg + tile * CH * DK;
-    w.each([&](int r, int d, float& x) { Wt[r * DK + d] = from_f<OP>(x); });
+    OP* Wt = WTg + tile * DK * CH;
+    w.each([&](int r, int d, float& x) { Wt[d * CH + r] = from_f<OP>(x); });
+  }
+  // (diag(e^G) Q)^T for the scan's injection term
+  constexpr int VE = 16 / (int)sizeof(OP);
+  {
+    OP* Qg = QgTg + tile * DK * CH;
+    for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
+      const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
+      OP vals[VE];
+#pragma unroll
+      for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(expf(Gs[r0 + j]) * to_f(Qs[(r0 + j) * LK + d]));
+      *reinterpret_cast<uint4*>(Qg + d * CH + r0) = pack16<OP>(vals);
+    }
   }
   // dV_loc = P^T dO, in slices of VS value columns
   const OP* dop = dO + (cp.row0 * H + h) * DV;
@@ -97,6 +127,14 @@ __global__ __launch_bounds__(256) void k_prep_bwd(Geo geo, int H, const OP* __re
   for (int c0 = 0; c0 < DV; c0 += VS) {
     ok &= load_rows<VS, LVS>(dop + c0, (long)H * DV, cp.len, dOs);
     __syncthreads();
+    OP* dOt = dOTg + tile * DV * CH + (long)c0 * CH;
+    for (int idx = threadIdx.x; idx < VS * CH / VE; idx += blockDim.x) {
+      const int vv = idx / (CH / VE), r0 = (idx - vv * (CH / VE)) * VE;
+      OP vals[VE];
+#pragma unroll
+      for (int j = 0; j < VE; ++j) vals[j] = dOs[(r0 + j) * LVS + vv];
+      *reinterpret_cast<uint4*>(dOt + vv * CH + r0) = pack16<OP>(vals);
+    }
     Tiles<CH, VS, 2, 2> t;
     t.zero();
     t.template mma<OP, CH>(KRow<OP, LT>{PT}, KCol<OP, LVS>{dOs});
@@ -107,32 +145,68 @@ __global__ __launch_bounds__(256) void k_prep_bwd(Geo geo, int H, const OP* __re
   if (threadIdx.x == 0) flag[tile] = bad;
 }
 
+// The reverse inter-chunk state scan (paper Sec. 4.2, K#1).  The fp32 carry dh
+// (the gradient w.r.t. the state leaving the chunk) stays in registers; the
+// prep kernel lays out every other operand for direct fragment loads (W^T,
+// (diag(e^G) Q)^T, dO^T, dV_loc), and the fragments of chunk c-1 are fetched
+// into registers while chunk c is processed:
+//   dU' = dV_loc + diag(e^{G_last - G}) K dh
+//   dh <- e^{G_last} dh + (diag(e^G) Q)^T dO - W^T dU'
 template <int DK, int DV, int BV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __restrict__ q,
-                                                  const OP* __restrict__ k, const OP* __restrict__ dO,
+__global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __restrict__ k,
                                                   const float* __restrict__ dST, const float* __restrict__ gcum,
-                                                  const OP* __restrict__ Wg, const float* __restrict__ dvlg,
-                                                  OP* __restrict__ dhg, float* __restrict__ dS0,
-                                                  int* __restrict__ flag) {
+                                                  const OP* __restrict__ WTg, const OP* __restrict__ QgTg,
+                                                  const OP* __restrict__ dOTg, const float* __restrict__ dvlg,
+                                                  OP* __restrict__ dhg, OP* __restrict__ dUTg,
+                                                  float* __restrict__ dS0, int* __restrict__ flag) {
   constexpr int NVT = DV / BV;
   constexpr bool DT_ = VAR != VAR_DECAY;  // delta term present
   constexpr int LK = DK + pad_of<OP>();
-  constexpr int LB = BV + pad_of<OP>();
   constexpr int LU = CH + pad_of<OP>();
-  __shared__ __align__(16) OP Ks[DT_ ? CH * LK : 1];
-  __shared__ __align__(16) OP Qs[CH * LK];
-  __shared__ __align__(16) OP Ws[DT_ ? CH * LK : 1];
-  __shared__ __align__(16) OP dhT[DT_ ? BV * LK : 1];
-  __shared__ __align__(16) OP dOs[CH * LB];
+  constexpr bool PF = sizeof(OP) == 2;
+  typedef Tiles<DK, BV, 4, 1> HT;  // dh slice
+  typedef Tiles<CH, BV, 4, 1> UT;  // dU' slice
+  __shared__ __align__(16) OP dhT[BV * LK];
   __shared__ __align__(16) OP dUT[DT_ ? BV * LU : 1];
-  __shared__ float Gs[CH], Gam[CH];
 
   int s, vt;
   scan_block_coords(blockIdx.x, geo.N * H, NVT, s, vt);
   const int n = s / H, h = s - (s / H) * H, v0 = vt * BV;
   const SeqPos sp = seq_pos(geo, n);
+  const int l = lane_id();
 
-  Tiles<DK, BV, 4, 1> dh;  // fp32 carry: gradient w.r.t. the state leaving the current chunk
+  struct Pre {
+    typename UT::template AFr<OP, DK> kf;
+    typename HT::template AFr<OP, CH> wt;
+    typename HT::template AFr<OP, CH> qg;
+    typename HT::template BFr<OP, CH> dob;
+    float dvl[UT::TN][4];
+    float dte[4];
+    float gl;
+  };
+  auto load_pre = [&](Pre& p, int c) {
+    const long tile = (long)(sp.c0 + c) * H + h;
+    const long row0 = sp.row0 + (long)c * CH;
+    const int len = min(CH, sp.len - c * CH);
+    p.qg.load(KRow<OP, CH>{QgTg + tile * DK * CH});
+    p.dob.load(KRow<OP, CH>{dOTg + tile * DV * CH + (long)v0 * CH});
+    const float Gl = gcum[tile * CH + CH - 1];
+    p.gl = expf(Gl);
+    p.kf.load(KRowM<OP>{k + (row0 * H + h) * DK, (long)H * DK, len});
+    if constexpr (DT_) p.wt.load(KRow<OP, CH>{WTg + tile * DK * CH});
+    {
+      const float* dv = dvlg + tile * CH * DV + v0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = UT::m0(0) + (l >> 4) * 4 + j;
+        p.dte[j] = expf(Gl - gcum[tile * CH + r]);
+#pragma unroll
+        for (int b = 0; b < UT::TN; ++b) p.dvl[b][j] = dv[r * DV + UT::n0(b) + (l & 15)];
+      }
+    }
+  };
+
+  HT dh;
   bool ok = true;
   const float* dSTp = dST ? dST + ((long)n * H + h) * DK * DV : nullptr;
   dh.each([&](int d, int vv, float& x) {
@@ -140,49 +214,56 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     ok &= finite_f(x);
   });
 
+  Pre cur, nxt;
+  if (sp.nch > 0) load_pre(cur, sp.nch - 1);
   for (int c = sp.nch - 1; c >= 0; --c) {
-    const long ci = sp.c0 + c;
-    const long tile = ci * H + h;
-    const long row0 = sp.row0 + (long)c * CH;
-    const int len = min(CH, sp.len - c * CH);
+    const long tile = (long)(sp.c0 + c) * H + h;
     OP* dhp = dhg + tile * DK * DV;
     dh.each([&](int d, int vv, float& x) {
       const OP xo = from_f<OP>(x);
       dhp[d * DV + v0 + vv] = xo;
-      if (DT_) dhT[vv * LK + d] = xo;
+      dhT[vv * LK + d] = xo;
     });
-    load_rows<DK, LK>(q + (row0 * H + h) * DK, (long)H * DK, len, Qs);
-    if constexpr (DT_) {
-      load_rows<DK, LK>(k + (row0 * H + h) * DK, (long)H * DK, len, Ks);
-      load_dense<CH, DK, LK>(Wg + tile * CH * DK, Ws);
-    }
-    load_rows<BV, LB>(dO + (row0 * H + h) * DV + v0, (long)H * DV, len, dOs);
-    if (threadIdx.x < CH) {
-      const float G = gcum[tile * CH + threadIdx.x];
-      Gs[threadIdx.x] = G;
-      Gam[threadIdx.x] = expf(G);
-    }
     __syncthreads();
-    const float Gl = Gs[CH - 1];
-    if constexpr (DT_) {
-      // dU' = dV_loc + diag(e^{G_last - G}) K dh ; keep -dU'^T for the W^T product
-      Tiles<CH, BV, 4, 1> du;
+    if (!PF) {
+      if (c < sp.nch - 1) load_pre(cur, c);
+    } else if (c > 0) {
+      load_pre(nxt, c - 1);
+    }
+    HT inj;  // (diag(e^G) Q)^T dO, independent of the carry
+    inj.zero();
+    inj.template mma<OP, CH>(cur.qg, cur.dob);
+    {
+      // dU' = dV_loc + diag(e^{G_last - G}) K dh (written for the gradient kernel for every
+      // family member; only the delta rule feeds it back into the carry)
+      UT du;
       du.zero();
-      du.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{dhT});
-      const float* dvl = dvlg + tile * CH * DV + v0;
-      du.each([&](int r, int vv, float& x) {
-        const float u = dvl[r * DV + vv] + expf(Gl - Gs[r]) * x;
-        dUT[vv * LU + r] = from_f<OP>(-u);
-      });
+      du.template mma<OP, DK>(cur.kf, KRow<OP, LK>{dhT});
+      OP* dUg = dUTg + tile * DV * CH + (long)v0 * CH;
+#pragma unroll
+      for (int b = 0; b < UT::TN; ++b) {
+        const int vv = UT::n0(b) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
+        OP u4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float u = cur.dvl[b][j] + cur.dte[j] * du.acc[0][b][j];
+          if (DT_) dUT[vv * LU + r0 + j] = from_f<OP>(-u);
+          u4[j] = from_f<OP>(u);
+        }
+        // dU' of this chunk for the gradient kernel, transposed (v, r)
+        *reinterpret_cast<typename vec4_of<OP>::type*>(dUg + vv * CH + r0) = pack4<OP>(u4);
+      }
       __syncthreads();
     }
-    const float gl = Gam[CH - 1];
-    dh.each([&](int, int, float& x) { x *= gl; });
-    dh.template mma<OP, CH>(KCol<OP, LK>{Qs}, kfun<OP>([&](int vv, int r) {
-                              return from_f<OP>(Gam[r] * to_f(dOs[r * LB + vv]));
-                            }));
-    if constexpr (DT_) dh.template mma<OP, CH>(KCol<OP, LK>{Ws}, KRow<OP, LU>{dUT});
-    __syncthreads();
+    const float gl = cur.gl;
+#pragma unroll
+    for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+      for (int b = 0; b < HT::TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dh.acc[a][b][j] = gl * dh.acc[a][b][j] + inj.acc[a][b][j];
+    if constexpr (DT_) dh.template mma<OP, CH>(cur.wt, KRow<OP, LU>{dUT});
+    if (PF) cur = nxt;
   }
   float* dS0p = dS0 + ((long)n * H + h) * DK * DV;
   dh.each([&](int d, int vv, float& x) { dS0p[d * DV + v0 + vv] = x; });
@@ -200,8 +281,8 @@ struct GradRegion {
   static constexpr bool BF = sizeof(OP) == 2;
   // phase 0: Qs, As, Tf (bf16 only), Xs
   static constexpr int ph0 = CH * LK * (int)sizeof(OP) + CH * LC * 4 + (BF ? CH * LC * 4 : 0) + 4 * 16 * 20 * 4;
-  // phase 1: Vs, dOs, Rs, Ups, dUs, Ys, dVst [64][LV]; hs, dhs [DK][LV]; RT, dUT [VS][LT]
-  static constexpr int ph1 = (7 * CH * LV + 2 * DK * LV + 2 * VS * LT) * (int)sizeof(OP);
+  // phase 1: Vs, dOs, Rs, Ups, dUs, Ys, dVst [64][LV]; hs, dhs [DK][LV]; hsT [VS][LK]; RT, dUT [VS][LT]
+  static constexpr int ph1 = (7 * CH * LV + 2 * DK * LV + VS * LK + 2 * VS * LT) * (int)sizeof(OP);
   // phase 2: QT, KT [DK][LT]; SdT, M1, dPs, dPmT [64][LT]
   static constexpr int ph2 = (2 * DK * LT + 4 * CH * LT) * (int)sizeof(OP);
   static constexpr int bytes = ((ph0 > ph1 ? (ph0 > ph2 ? ph0 : ph2) : (ph1 > ph2 ? ph1 : ph2)) + 255) / 256 * 256;
@@ -224,11 +305,12 @@ __device__ __forceinline__ float sum_groups(float x) {
 }
 
 template <int DK, int DV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __restrict__ q,
+__global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __restrict__ q,
                                                   const OP* __restrict__ k, const OP* __restrict__ v,
                                                   const float* __restrict__ g, const float* __restrict__ beta,
                                                   const float* __restrict__ states, const OP* __restrict__ dO,
-                                                  const OP* __restrict__ dhg, OP* __restrict__ dq,
+                                                  const OP* __restrict__ dhg, const OP* __restrict__ dUTg,
+                                                  OP* __restrict__ dq,
                                                   OP* __restrict__ dk, OP* __restrict__ dvo,
                                                   float* __restrict__ dg, float* __restrict__ dbeta,
                                                   int* __restrict__ flag, char* __restrict__ gscratch) {
@@ -241,12 +323,13 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
   __shared__ __align__(16) OP Ks[CH * LK];
   __shared__ __align__(16) OP Ts[DT_ ? CH * LT : 1];   // T (fp32 operands: T itself)
   __shared__ __align__(16) OP TT[DT_ ? CH * LT : 1];   // T^T
-  __shared__ __align__(16) OP PT[CH * LT];             // P^T
+  __shared__ __align__(16) OP PT[BF ? 1 : CH * LT];    // P^T (fp32 operands)
   __shared__ __align__(16) float Pf[BF ? CH * LC : 1]; // P in fp32 (bf16 operands)
   __shared__ __align__(16) OP AE[DT_ ? CH * LT : 1];   // (K K^T)_ri E_ri, strict lower
   __shared__ float Gs[CH], Gam[CH], Bs[CH], Dte[CH];
-  __shared__ float rowZ[2][CH], colZ[2][CH], rowA[2][CH];
-  __shared__ float dGs[CH], dBs[CH], hdh_w[4];
+  // per-row partial sums, one row of partials per wave column (wn) or row block (wm)
+  __shared__ float rowZ[2][CH], colZ[4][CH], rowA[2][CH], rqp[2][CH], rxp[2][CH], rkp[2][CH], dbYp[2][CH];
+  __shared__ float hdh_w[8];
   __shared__ __align__(16) char ulds[BF ? R::bytes : 16];
   char* ub = BF ? ulds : gscratch + ((long)blockIdx.y * gridDim.x + blockIdx.x) * R::bytes;
 
@@ -270,21 +353,21 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
     Dte[r] = expf(Gs[CH - 1] - Gs[r]);
   }
   {
-    Tiles<CH, CH, 2, 2> p;
+    Tiles<CH, CH, 4, 2> p;
     p.zero();
     p.template mma<OP, DK>(KRow<OP, LK>{Qs}, KRow<OP, LK>{Ks});
     p.each([&](int r, int i, float& x) {
-      const float pr = i <= r ? x * expf(Gs[r] - Gs[i]) : 0.f;
-      PT[i * LT + r] = from_f<OP>(pr);
+      const float pr = i <= r ? x * __expf(Gs[r] - Gs[i]) : 0.f;
       if (BF) Pf[r * LC + i] = pr;
+      else PT[i * LT + r] = from_f<OP>(pr);
     });
   }
   if constexpr (DT_) {
-    Tiles<CH, CH, 2, 2> bm;
+    Tiles<CH, CH, 4, 2> bm;
     bm.zero();
     bm.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{Ks});
     bm.each([&](int r, int i, float& x) {
-      const float ae = (i < r) ? x * expf(Gs[r] - Gs[i]) : 0.f;
+      const float ae = (i < r) ? x * __expf(Gs[r] - Gs[i]) : 0.f;
       AE[r * LT + i] = from_f<OP>(ae);
       As[r * LC + i] = Bs[r] * ae;
     });
@@ -307,11 +390,12 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
   OP* dVst = Ys + CH * LV;
   OP* hs = dVst + CH * LV;
   OP* dhs = hs + DK * LV;
-  OP* RT = dhs + DK * LV;
+  OP* hsT = dhs + DK * LV;
+  OP* RT = hsT + VS * LK;
   OP* dUT = RT + VS * LT;
 
-  Tiles<CH, CH, 2, 2> dT, dP;
-  Tiles<CH, DK, 4, 1> X, dQa, dKh;
+  Tiles<CH, CH, 4, 2> dT, dP;
+  Tiles<CH, DK, 4, 2> X, dQa, dKh;
   dT.zero(); dP.zero(); X.zero(); dQa.zero(); dKh.zero();
   float dbY[4] = {0.f, 0.f, 0.f, 0.f};
   float hdh = 0.f;
@@ -321,61 +405,53 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
   const OP* dop = dO + (cp.row0 * H + h) * DV;
   OP* dvp = dvo + (cp.row0 * H + h) * DV;
 
+  const OP* dUp = dUTg + tile * DV * CH;
   for (int c0 = 0; c0 < DV; c0 += VS) {
     ok &= load_rows<VS, LV>(vp + c0, (long)H * DV, cp.len, Vs);
     load_rows<VS, LV>(dop + c0, (long)H * DV, cp.len, dOs);
+    // h slice (fp32) -> hs (d, v) and hsT (v, d); dh slice -> dhs (d, v)
     for (int idx = threadIdx.x; idx < DK * VS / 4; idx += blockDim.x) {
       const int d = idx / (VS / 4), c = (idx - d * (VS / 4)) * 4;
       const float4 hx = *reinterpret_cast<const float4*>(hp + (long)d * DV + c0 + c);
+      const typename vec4_of<OP>::type dv4 = *reinterpret_cast<const typename vec4_of<OP>::type*>(dhp + (long)d * DV + c0 + c);
       const float hv[4] = {hx.x, hx.y, hx.z, hx.w};
+      OP h4[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const OP dv_ = dhp[(long)d * DV + c0 + c + j];
         ok &= finite_f(hv[j]);
-        hdh += hv[j] * to_f(dv_);
-        hs[d * LV + c + j] = from_f<OP>(hv[j]);
-        dhs[d * LV + c + j] = dv_;
+        hdh += hv[j] * to_f(elem4<OP>(dv4, j));
+        h4[j] = from_f<OP>(hv[j]);
+        hsT[(c + j) * LK + d] = h4[j];
+      }
+      *reinterpret_cast<typename vec4_of<OP>::type*>(hs + d * LV + c) = pack4<OP>(h4);
+      *reinterpret_cast<typename vec4_of<OP>::type*>(dhs + d * LV + c) = dv4;
+    }
+    // dU' slice from the reverse scan: dUT (v, r) and dUs (r, v)
+    {
+      constexpr int VE = 16 / (int)sizeof(OP);
+      for (int idx = threadIdx.x; idx < VS * CH / VE; idx += blockDim.x) {
+        const int vv = idx / (CH / VE), r = (idx - vv * (CH / VE)) * VE;
+        const uint4 u = *reinterpret_cast<const uint4*>(dUp + (long)(c0 + vv) * CH + r);
+        *reinterpret_cast<uint4*>(dUT + vv * LT + r) = u;
+#pragma unroll
+        for (int j = 0; j < VE; ++j) dUs[(r + j) * LV + vv] = elem16<OP>(u, j);
       }
     }
     __syncthreads();
     const OP* Up = Vs;  // U' of the scalar-decay member is V
     if constexpr (DT_) {
       // R = diag(beta) V - diag(beta e^G) K h
-      Tiles<CH, VS, 4, 1> rr;
+      Tiles<CH, VS, 4, 2> rr;
       rr.zero();
-      rr.template mma<OP, DK>(KRow<OP, LK>{Ks}, KCol<OP, LV>{hs});
+      rr.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{hsT});
       rr.each([&](int r, int vv, float& x) {
         const float rv = Bs[r] * (to_f(Vs[r * LV + vv]) - Gam[r] * x);
         const OP ro = from_f<OP>(rv);
         Rs[r * LV + vv] = ro;
         RT[vv * LT + r] = ro;
       });
-      __syncthreads();
-      // U' = T R
-      Tiles<CH, VS, 4, 1> up;
-      up.zero();
-      up.template mma<OP, CH>(KRow<OP, LT>{Ts}, KRow<OP, LT>{RT});
-      up.each([&](int r, int vv, float& x) { Ups[r * LV + vv] = from_f<OP>(x); });
-      Up = Ups;
-    }
-    // dU' = P^T dO + diag(e^{G_last - G}) K dh
-    {
-      Tiles<CH, VS, 4, 1> du;
-      du.zero();
-      du.template mma<OP, DK>(KRow<OP, LK>{Ks}, KCol<OP, LV>{dhs});
-      du.each([&](int r, int, float& x) { x *= Dte[r]; });
-      du.template mma<OP, CH>(KRow<OP, LT>{PT}, KCol<OP, LV>{dOs});
-      du.each([&](int r, int vv, float& x) {
-        const OP xo = from_f<OP>(x);
-        dUs[r * LV + vv] = xo;
-        if (DT_) dUT[vv * LT + r] = xo;
-        else dVst[r * LV + vv] = xo;  // scalar decay: dV = dU'
-      });
-    }
-    __syncthreads();
-    if constexpr (DT_) {
       // Y = T^T dU'; dV = diag(beta) Y; dbeta_r += v_r . Y_r; keep -Y for X
-      Tiles<CH, VS, 4, 1> y;
+      Tiles<CH, VS, 4, 2> y;
       y.zero();
       y.template mma<OP, CH>(KRow<OP, LT>{TT}, KRow<OP, LT>{dUT});
       y.each([&](int r, int vv, float& x) {
@@ -390,23 +466,33 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
           dbY[j] += to_f(Vs[r * LV + vv]) * y.acc[0][b][j];
         }
       __syncthreads();
+      // U' = T R
+      Tiles<CH, VS, 4, 2> up;
+      up.zero();
+      up.template mma<OP, CH>(KRow<OP, LT>{Ts}, KRow<OP, LT>{RT});
+      up.each([&](int r, int vv, float& x) { Ups[r * LV + vv] = from_f<OP>(x); });
+      Up = Ups;
+      __syncthreads();
       dT.template mma<OP, VS>(KRow<OP, LV>{dUs}, KRow<OP, LV>{Rs});
       X.template mma<OP, VS>(KRow<OP, LV>{Ys}, KRow<OP, LV>{hs});
     }
     dP.template mma<OP, VS>(KRow<OP, LV>{dOs}, KRow<OP, LV>{Up});
     dQa.template mma<OP, VS>(KRow<OP, LV>{dOs}, KRow<OP, LV>{hs});
     dKh.template mma<OP, VS>(KRow<OP, LV>{Up}, KRow<OP, LV>{dhs});
-    store_rows<VS, LV>(dvp + c0, (long)H * DV, cp.len, dVst);
+    store_rows<VS, LV>(dvp + c0, (long)H * DV, cp.len, DT_ ? dVst : dUs);  // scalar decay: dV = dU'
     __syncthreads();
   }
 
   // block-wide <h, dh> in a fixed order
   hdh = wave_sum(hdh);
   if (l == 0) hdh_w[w] = hdh;
-  // dbeta partial from Y: reduce over the 16 lanes of a k-group
+  // dbeta partial from Y: reduce over the 16 lanes of a k-group, one partial per wave column
   if constexpr (DT_) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) dbY[j] = sum16(dbY[j]);
+    for (int j = 0; j < 4; ++j) {
+      dbY[j] = sum16(dbY[j]);
+      if ((l & 15) == 0) dbYp[w % 2][(w / 2) * 16 + (l >> 4) * 4 + j] = dbY[j];
+    }
   }
 
   // ================= phase 2: triangular VJP and the chunk-level gradients
@@ -417,16 +503,23 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
   OP* dPs = M1 + CH * LT;
   OP* dPmT = dPs + CH * LT;
   {
+    constexpr int VE = 16 / (int)sizeof(OP);
     const OP* qp = q + (cp.row0 * H + h) * DK;
-    for (int idx = threadIdx.x; idx < CH * DK; idx += blockDim.x) {
-      const int r = idx % CH, d = idx / CH;
-      QT[d * LT + r] = r < cp.len ? qp[(long)r * H * DK + d] : from_f<OP>(0.f);
-      KT[d * LT + r] = Ks[r * LK + d];
+    for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
+      const int r = idx / (DK / VE), c = (idx - r * (DK / VE)) * VE;
+      const uint4 z = {0u, 0u, 0u, 0u};
+      const uint4 qv = r < cp.len ? *reinterpret_cast<const uint4*>(qp + (long)r * H * DK + c) : z;
+      const uint4 kv = *reinterpret_cast<const uint4*>(Ks + r * LK + c);
+#pragma unroll
+      for (int j = 0; j < VE; ++j) {
+        QT[(c + j) * LT + r] = elem16<OP>(qv, j);
+        KT[(c + j) * LT + r] = elem16<OP>(kv, j);
+      }
     }
   }
-  Tiles<CH, CH, 2, 2> zs;  // Z = dA * A + dP * P, element by element
+  Tiles<CH, CH, 4, 2> zs;  // Z = dA * A + dP * P, element by element
   dP.each([&](int r, int i, float& x) {
-    const float dd = i <= r ? expf(Gs[r] - Gs[i]) : 0.f;
+    const float dd = i <= r ? __expf(Gs[r] - Gs[i]) : 0.f;
     const float dpm = x * dd;
     dPs[r * LT + i] = from_f<OP>(dpm);
     dPmT[i * LT + r] = from_f<OP>(dpm);
@@ -444,16 +537,16 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
   if constexpr (DT_) dT.each([&](int r, int c, float& x) { SdT[c * LT + r] = from_f<OP>(x); });
   __syncthreads();
 
-  float rowA_l[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  float rowA_l[1][4] = {{0.f, 0.f, 0.f, 0.f}};
   if constexpr (DT_) {
     // M1 = T^T dT
-    Tiles<CH, CH, 2, 2> m1;
+    Tiles<CH, CH, 4, 2> m1;
     m1.zero();
     m1.template mma<OP, CH>(KRow<OP, LT>{TT}, KRow<OP, LT>{SdT});
     m1.each([&](int r, int c, float& x) { M1[r * LT + c] = from_f<OP>(x); });
     __syncthreads();
     // dA = -(T^T dT) T^T, strict lower part
-    Tiles<CH, CH, 2, 2> da;
+    Tiles<CH, CH, 4, 2> da;
     da.zero();
     da.template mma<OP, CH>(KRow<OP, LT>{M1}, KRow<OP, LT>{Ts});
 #pragma unroll
@@ -465,7 +558,7 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
           const int r = da.m0(a) + (l >> 4) * 4 + j, i = da.n0(b) + (l & 15);
           const float dA = (i < r) ? -da.acc[a][b][j] : 0.f;
           const float ae = to_f(AE[r * LT + i]);
-          const float e = (i < r) ? expf(Gs[r] - Gs[i]) : 0.f;
+          const float e = (i < r) ? __expf(Gs[r] - Gs[i]) : 0.f;
           zs.acc[a][b][j] += dA * Bs[r] * ae;
           rowA_l[a][j] += dA * ae;
           const float db = dA * Bs[r] * e;
@@ -481,34 +574,30 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
   {
     const int wm = w / 2, wn = w % 2;
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float rs = zs.acc[a][0][j] + zs.acc[a][1][j];
-        rs = sum16(rs);
-        const float ra = sum16(rowA_l[a][j]);
-        const int r = zs.m0(a) + (l >> 4) * 4 + j;
-        if ((l & 15) == 0) {
-          rowZ[wn][r] = rs;
-          rowA[wn][r] = ra;
-        }
+    for (int j = 0; j < 4; ++j) {
+      float rs = zs.acc[0][0][j] + zs.acc[0][1][j];
+      rs = sum16(rs);
+      const float ra = sum16(rowA_l[0][j]);
+      const int r = zs.m0(0) + (l >> 4) * 4 + j;
+      if ((l & 15) == 0) {
+        rowZ[wn][r] = rs;
+        rowA[wn][r] = ra;
       }
+    }
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       float cs = 0.f;
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) cs += zs.acc[a][b][j];
+      for (int j = 0; j < 4; ++j) cs += zs.acc[0][b][j];
       cs = sum_groups(cs);
       if ((l >> 4) == 0) colZ[wm][zs.n0(b) + (l & 15)] = cs;
     }
   }
   __syncthreads();
 
-  // dQ = diag(e^G) dO h^T + (dP * D) K;   row sums q_r . (dO h^T)_r
-  float rq[4], rx[4], rk[4];
+  // dQ = diag(e^G) dO h^T + (dP * D) K;   row sums q_r . (dO h^T)_r, k_r . X_r, k_r . dkhat_r
   {
+    float rq[4], rx[4], rk[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) rq[j] = rx[j] = rk[j] = 0.f;
 #pragma unroll
@@ -529,31 +618,17 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
       rq[j] = sum16(rq[j]);
       rx[j] = sum16(rx[j]);
       rk[j] = sum16(rk[j]);
+      if ((l & 15) == 0) {
+        const int r = dQa.m0(0) + (l >> 4) * 4 + j;
+        rqp[w % 2][r] = rq[j];
+        rxp[w % 2][r] = rx[j];
+        rkp[w % 2][r] = rk[j];
+      }
     }
   }
   dQa.template mma<OP, CH>(KRow<OP, LT>{dPs}, KRow<OP, LT>{KT});
   dKh.template mma<OP, CH>(KRow<OP, LT>{dPmT}, KRow<OP, LT>{QT});
   if constexpr (DT_) dKh.template mma<OP, CH>(KRow<OP, LT>{SdT}, KRow<OP, LT>{KT});
-
-  // per-row scalars of this wave's rows -> dG, dbeta
-  if ((l & 15) == 0) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = dQa.m0(0) + (l >> 4) * 4 + j;
-      float dG = (rowZ[0][r] + rowZ[1][r]) - (colZ[0][r] + colZ[1][r]);
-      dG += Gam[r] * (rq[j] + Bs[r] * rx[j]);
-      dG -= Dte[r] * rk[j];
-      dGs[r] = dG;
-      rk[j] = Dte[r] * rk[j];  // khat_r . dkhat_r
-      if (DT_) dBs[r] = (rowA[0][r] + rowA[1][r]) + Gam[r] * rx[j] + dbY[j];
-    }
-  }
-  // sum_r khat_r . dkhat_r in a fixed order: per-row values through LDS
-  __shared__ float kk_row[CH];
-  if ((l & 15) == 0) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) kk_row[dQa.m0(0) + (l >> 4) * 4 + j] = rk[j];
-  }
   __syncthreads();
   // stage dq, dk (reusing QT / KT after every product has read them)
   OP* dqst = QT;
@@ -561,19 +636,27 @@ __global__ __launch_bounds__(256) void k_grad_bwd(Geo geo, int H, const OP* __re
   dQa.each([&](int r, int d, float& x) { dqst[r * LK + d] = from_f<OP>(x); });
   dKh.each([&](int r, int d, float& x) { dkst[r * LK + d] = from_f<OP>(x); });
   if (w == 0) {
+    // per-row scalars (row r = lane), combined from the wave partials in a fixed order
+    const int r = l;
+    const float rq = rqp[0][r] + rqp[1][r], rx = rxp[0][r] + rxp[1][r];
+    const float kk_r = Dte[r] * (rkp[0][r] + rkp[1][r]);  // khat_r . dkhat_r
+    float x = (rowZ[0][r] + rowZ[1][r]) - (((colZ[0][r] + colZ[1][r]) + colZ[2][r]) + colZ[3][r]);
+    x += Gam[r] * (rq + Bs[r] * rx);
+    x -= kk_r;
+    const float db = (rowA[0][r] + rowA[1][r]) + Gam[r] * rx + (dbYp[0][r] + dbYp[1][r]);
     // dG_last += e^{G_last} <h, dh> + sum_r khat_r . dkhat_r ; dg = reverse cumsum of dG
-    float kk = kk_row[l];
-    kk = wave_sum(kk);
-    float x = dGs[l];
-    if (l == CH - 1) x += Gam[CH - 1] * (((hdh_w[0] + hdh_w[1]) + hdh_w[2]) + hdh_w[3]) + kk;
-    // reverse inclusive scan: suffix sums
+    const float kk = wave_sum(kk_r);
+    float hd = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) hd += hdh_w[i];
+    if (l == CH - 1) x += Gam[CH - 1] * hd + kk;
     const float rev = __shfl(x, CH - 1 - l, WAVE);
     const float sc = wave_incl_scan(rev);
     const float dgv = __shfl(sc, CH - 1 - l, WAVE);
     if (l < cp.len) {
       const long o = (cp.row0 + l) * H + h;
       if (VAR != VAR_DELTA) dg[o] = dgv;
-      if (DT_) dbeta[o] = dBs[l];
+      if (DT_) dbeta[o] = db;
     }
   }
   __syncthreads();
@@ -599,21 +682,21 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_prep_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, a.g, a.beta, (const OP*)a.dO, w.gcum,
-                       (OP*)w.W, w.dvl, w.flag_prep);
+                       (OP*)w.W, (OP*)w.QgT, (OP*)w.dOT, w.dvl, w.flag_prep);
   }
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
-                       (const OP*)a.q, (const OP*)a.k, (const OP*)a.dO, a.dST, w.gcum, (const OP*)w.W,
-                       w.dvl, (OP*)w.dh, a.dS0, w.flag_scan);
+                       (const OP*)a.k, a.dST, w.gcum, (const OP*)w.W, (const OP*)w.QgT, (const OP*)w.dOT,
+                       w.dvl, (OP*)w.dh, (OP*)w.dUT, a.dS0, w.flag_scan);
   }
   stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0) {
-    hipLaunchKernelGGL((k_grad_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
+    hipLaunchKernelGGL((k_grad_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, a.states,
-                       (const OP*)a.dO, (const OP*)w.dh, (OP*)a.dq, (OP*)a.dk_, (OP*)a.dv_, a.dg, a.dbeta,
-                       w.flag_grad, (char*)w.grad_scratch);
+                       (const OP*)a.dO, (const OP*)w.dh, (const OP*)w.dUT, (OP*)a.dq, (OP*)a.dk_, (OP*)a.dv_,
+                       a.dg, a.dbeta, w.flag_grad, (char*)w.grad_scratch);
   }
   stage_mark(a.events, 3, a.stream);
   if (NS > 0) {

@@ -10,6 +10,31 @@ namespace gdn {
 
 template <typename T> constexpr int pad_of() { return 16 / (int)sizeof(T); }
 
+// Element j of a 16-byte vector of T, and packing of T values into 16 bytes,
+// by explicit bit casts (no pointer type punning of register values).
+__device__ __forceinline__ uint32_t word_of(const uint4& u, int i) {
+  return i == 0 ? u.x : (i == 1 ? u.y : (i == 2 ? u.z : u.w));
+}
+template <typename T> __device__ __forceinline__ T elem16(const uint4& u, int j);
+template <> __device__ __forceinline__ bf16 elem16<bf16>(const uint4& u, int j) {
+  return __builtin_bit_cast(bf16, (unsigned short)(word_of(u, j >> 1) >> ((j & 1) * 16)));
+}
+template <> __device__ __forceinline__ float elem16<float>(const uint4& u, int j) {
+  return __builtin_bit_cast(float, word_of(u, j));
+}
+__device__ __forceinline__ uint32_t pack2(bf16 lo, bf16 hi) {
+  return (uint32_t)__builtin_bit_cast(unsigned short, lo) | ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
+}
+// 16 bytes of T from 16 / sizeof(T) values
+template <typename T> __device__ __forceinline__ uint4 pack16(const T* x);
+template <> __device__ __forceinline__ uint4 pack16<bf16>(const bf16* x) {
+  return uint4{pack2(x[0], x[1]), pack2(x[2], x[3]), pack2(x[4], x[5]), pack2(x[6], x[7])};
+}
+template <> __device__ __forceinline__ uint4 pack16<float>(const float* x) {
+  return uint4{__builtin_bit_cast(uint32_t, x[0]), __builtin_bit_cast(uint32_t, x[1]),
+               __builtin_bit_cast(uint32_t, x[2]), __builtin_bit_cast(uint32_t, x[3])};
+}
+
 __device__ __forceinline__ bool finite8_bf16(uint4 u) {
   // a bf16 value is non-finite when its 8 exponent bits are all ones
   const uint32_t w[4] = {u.x, u.y, u.z, u.w};

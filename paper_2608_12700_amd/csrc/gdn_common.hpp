@@ -56,6 +56,21 @@ struct KRow {
   __device__ __forceinline__ const T* ptr(int o, int k) const { return p + o * LD + k; }
 };
 
+// Element (o, k) at p[o * ld + k] with a runtime row stride; rows o >= rows
+// read as zero (tail chunks read straight from the token-major inputs).
+template <typename T>
+struct KRowM {
+  const T* p;
+  long ld;
+  int rows;
+  static constexpr bool kVec = false;
+  static constexpr bool kMasked = true;
+  __device__ __forceinline__ T get(int o, int k) const {
+    return o < rows ? p[o * ld + k] : static_cast<T>(0.f);
+  }
+  __device__ __forceinline__ const T* ptr(int o, int k) const { return p + o * ld + k; }
+};
+
 // Element (o, k) at p[k * LD + o]: o contiguous (a transposed use).
 template <typename T, int LD>
 struct KCol {
@@ -74,6 +89,9 @@ struct KFun {
 template <typename T, class F>
 __device__ __forceinline__ KFun<T, F> kfun(F f) { return KFun<T, F>{f}; }
 
+template <class V, class = void> struct is_masked { static constexpr bool value = false; };
+template <class V> struct is_masked<V, decltype((void)V::kMasked)> { static constexpr bool value = true; };
+
 template <typename OP> struct Mma;
 
 template <>
@@ -86,6 +104,12 @@ struct Mma<bf16> {
     const int oo = o + (l & 15), kk = k0 + (l >> 4) * 8;
     if constexpr (V::kVec) {
       return *reinterpret_cast<const bf16x8*>(v.ptr(oo, kk));
+    } else if constexpr (is_masked<V>::value) {
+      if (oo < v.rows) return *reinterpret_cast<const bf16x8*>(v.ptr(oo, kk));
+      frag z;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) z[j] = static_cast<bf16>(0.f);
+      return z;
     } else {
       frag r;
 #pragma unroll
@@ -147,6 +171,58 @@ struct Tiles {
 #pragma unroll
         for (int b = 0; b < TN; ++b) acc[a][b] = X::mma(fa[a], fb[b], acc[a][b]);
     }
+  }
+
+  // Fragments of A (this wave's rows) or B (this wave's columns) for the whole
+  // contraction, loaded ahead of the product (e.g. a chunk early).
+  template <typename OP, int K>
+  struct AFr {
+    typename Mma<OP>::frag f[K / Mma<OP>::KSTEP][TM];
+    template <class V>
+    __device__ __forceinline__ void load(const V& A) {
+#pragma unroll
+      for (int s = 0; s < K / Mma<OP>::KSTEP; ++s)
+#pragma unroll
+        for (int a = 0; a < TM; ++a) f[s][a] = Mma<OP>::load(A, m0(a), s * Mma<OP>::KSTEP);
+    }
+  };
+  template <typename OP, int K>
+  struct BFr {
+    typename Mma<OP>::frag f[K / Mma<OP>::KSTEP][TN];
+    template <class V>
+    __device__ __forceinline__ void load(const V& B) {
+#pragma unroll
+      for (int s = 0; s < K / Mma<OP>::KSTEP; ++s)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) f[s][b] = Mma<OP>::load(B, n0(b), s * Mma<OP>::KSTEP);
+    }
+  };
+
+  // acc += A * B with A's fragments already in registers.
+  template <typename OP, int K, class VB>
+  __device__ __forceinline__ void mma(const AFr<OP, K>& fa, const VB& B) {
+    typedef Mma<OP> X;
+#pragma unroll
+    for (int s = 0; s < K / X::KSTEP; ++s) {
+      typename X::frag fb[TN];
+#pragma unroll
+      for (int b = 0; b < TN; ++b) fb[b] = X::load(B, n0(b), s * X::KSTEP);
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) acc[a][b] = X::mma(fa.f[s][a], fb[b], acc[a][b]);
+    }
+  }
+  // acc += A * B with both operands' fragments already in registers.
+  template <typename OP, int K>
+  __device__ __forceinline__ void mma(const AFr<OP, K>& fa, const BFr<OP, K>& fb) {
+    typedef Mma<OP> X;
+#pragma unroll
+    for (int s = 0; s < K / X::KSTEP; ++s)
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) acc[a][b] = X::mma(fa.f[s][a], fb.f[s][b], acc[a][b]);
   }
 
   // Visit every owned element: f(row, col, value&).

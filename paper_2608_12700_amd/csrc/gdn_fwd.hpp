@@ -26,7 +26,7 @@ __global__ __launch_bounds__(256) void k_prep_fwd(Geo geo, int H, const OP* __re
                                                   const OP* __restrict__ v, const float* __restrict__ g,
                                                   const float* __restrict__ beta, float* __restrict__ gcum,
                                                   OP* __restrict__ Wg, float* __restrict__ Ug,
-                                                  int* __restrict__ flag) {
+                                                  OP* __restrict__ KhTg, int* __restrict__ flag) {
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
   constexpr int LT = CH + pad_of<OP>();
@@ -96,32 +96,82 @@ __global__ __launch_bounds__(256) void k_prep_fwd(Geo geo, int H, const OP* __re
     }
     ok &= load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
   }
+  // Khat^T[d][r] = exp(G_last - G_r) k_r[d], the scan's A operand for the carry
+  __syncthreads();
+  if (threadIdx.x < CH) GBs[threadIdx.x] = expf(Gs[CH - 1] - Gs[threadIdx.x]);
+  __syncthreads();
+  OP* Kh = KhTg + tile * DK * CH;
+  constexpr int VE = 16 / (int)sizeof(OP);
+  for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
+    const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
+    OP vals[VE];
+#pragma unroll
+    for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(GBs[r0 + j] * to_f(Ks[(r0 + j) * LK + d]));
+    *reinterpret_cast<uint4*>(Kh + d * CH + r0) = pack16<OP>(vals);
+  }
   const int bad = __syncthreads_or(!ok);
   if (threadIdx.x == 0) flag[tile] = bad;
 }
 
+// The forward inter-chunk scan.  Every operand except the carry arrives
+// pre-laid-out by the prep kernel (W row-major, Khat^T row-major, U in fp32), so
+// the A fragments of chunk c+1 are loaded from HBM/L2 straight into registers
+// while chunk c is computed; only h and U' pass through LDS (two barriers per
+// chunk).
 template <int DK, int DV, int BV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __restrict__ k,
-                                                  const OP* __restrict__ v, const float* __restrict__ S0,
-                                                  const float* __restrict__ gcum, const OP* __restrict__ Wg,
+__global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __restrict__ v,
+                                                  const float* __restrict__ S0, const float* __restrict__ gcum,
+                                                  const OP* __restrict__ Wg, const OP* __restrict__ KhTg,
                                                   const float* __restrict__ Ug, float* __restrict__ states,
                                                   float* __restrict__ ST, OP* __restrict__ UpTg,
                                                   int* __restrict__ flag) {
   constexpr int NVT = DV / BV;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LU = CH + pad_of<OP>();
-  __shared__ __align__(16) OP Ks[CH * LK];
-  __shared__ __align__(16) OP Ws[VAR != VAR_DECAY ? CH * LK : 1];
+  constexpr bool PF = sizeof(OP) == 2;  // prefetch a chunk ahead (bf16 fragments are compact)
+  typedef Tiles<DK, BV, 4, 1> HT;       // carried state slice h[:, v0:v0+BV]
+  typedef Tiles<CH, BV, 4, 1> UT;       // U' slice
   __shared__ __align__(16) OP hT[BV * LK];
   __shared__ __align__(16) OP UsT[BV * LU];
-  __shared__ float Gs[CH];
 
   int s, vt;
   scan_block_coords(blockIdx.x, geo.N * H, NVT, s, vt);
   const int n = s / H, h = s - (s / H) * H, v0 = vt * BV;
   const SeqPos sp = seq_pos(geo, n);
+  const int l = lane_id();
 
-  Tiles<DK, BV, 4, 1> hs;  // the carried state slice h[:, v0:v0+BV], fp32
+  struct Pre {
+    typename UT::template AFr<OP, DK> w;
+    typename HT::template AFr<OP, CH> kh;
+    float u[UT::TN][4];
+    float gl;
+  };
+  auto load_pre = [&](Pre& p, int c) {
+    const long tile = (long)(sp.c0 + c) * H + h;
+    if constexpr (VAR != VAR_DECAY) {
+      p.w.load(KRow<OP, DK>{Wg + tile * CH * DK});
+      const float* Ut = Ug + tile * CH * DV + v0;
+#pragma unroll
+      for (int b = 0; b < UT::TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p.u[b][j] = Ut[(UT::m0(0) + (l >> 4) * 4 + j) * DV + UT::n0(b) + (l & 15)];
+    } else {
+      const long row0 = sp.row0 + (long)c * CH;
+      const int len = min(CH, sp.len - c * CH);
+      const OP* vp = v + (row0 * H + h) * DV + v0;
+#pragma unroll
+      for (int b = 0; b < UT::TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = UT::m0(0) + (l >> 4) * 4 + j;
+          p.u[b][j] = r < len ? to_f(vp[(long)r * H * DV + UT::n0(b) + (l & 15)]) : 0.f;
+        }
+    }
+    p.kh.load(KRow<OP, CH>{KhTg + tile * DK * CH});
+    p.gl = expf(gcum[tile * CH + CH - 1]);
+  };
+
+  HT hs;
   bool ok = true;
   const float* S0p = S0 ? S0 + ((long)n * H + h) * DK * DV : nullptr;
   hs.each([&](int d, int vv, float& x) {
@@ -129,42 +179,51 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     ok &= finite_f(x);
   });
 
+  Pre cur, nxt;
+  if (sp.nch > 0) load_pre(cur, 0);
   for (int c = 0; c < sp.nch; ++c) {
-    const long ci = sp.c0 + c;
-    const long tile = ci * H + h;
-    const long row0 = sp.row0 + (long)c * CH;
-    const int len = min(CH, sp.len - c * CH);
+    const long tile = (long)(sp.c0 + c) * H + h;
     float* hp = states + tile * DK * DV;
     hs.each([&](int d, int vv, float& x) {
       hp[d * DV + v0 + vv] = x;
       hT[vv * LK + d] = from_f<OP>(x);
     });
-    load_rows<DK, LK>(k + (row0 * H + h) * DK, (long)H * DK, len, Ks);
-    if constexpr (VAR != VAR_DECAY) load_dense<CH, DK, LK>(Wg + tile * CH * DK, Ws);
-    if (threadIdx.x < CH) Gs[threadIdx.x] = gcum[tile * CH + threadIdx.x];
     __syncthreads();
-
-    Tiles<CH, BV, 4, 1> up;
+    if (!PF) {
+      if (c > 0) load_pre(cur, c);
+    } else if (c + 1 < sp.nch) {
+      load_pre(nxt, c + 1);
+    }
+    UT up;
     if constexpr (VAR != VAR_DECAY) {
       up.zero();
-      up.template mma<OP, DK>(KRow<OP, LK>{Ws}, KRow<OP, LK>{hT});
-      const float* Ut = Ug + tile * CH * DV + v0;
-      up.each([&](int r, int vv, float& x) { x = Ut[r * DV + vv] - x; });
+      up.template mma<OP, DK>(cur.w, KRow<OP, LK>{hT});
+#pragma unroll
+      for (int b = 0; b < UT::TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) up.acc[0][b][j] = cur.u[b][j] - up.acc[0][b][j];
     } else {
-      const OP* vp = v + (row0 * H + h) * DV + v0;
-      up.each([&](int r, int vv, float& x) { x = r < len ? to_f(vp[(long)r * H * DV + vv]) : 0.f; });
+#pragma unroll
+      for (int b = 0; b < UT::TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) up.acc[0][b][j] = cur.u[b][j];
     }
-    const float Gl = Gs[CH - 1];
     OP* Upt = UpTg + tile * DV * CH;
-    up.each([&](int r, int vv, float& x) {
-      if (VAR != VAR_DECAY) Upt[(v0 + vv) * CH + r] = from_f<OP>(x);
-      UsT[vv * LU + r] = from_f<OP>(x * expf(Gl - Gs[r]));
-    });
+#pragma unroll
+    for (int b = 0; b < UT::TN; ++b) {
+      const int vv = UT::n0(b) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const OP xo = from_f<OP>(up.acc[0][b][j]);
+        if (VAR != VAR_DECAY) Upt[(v0 + vv) * CH + r0 + j] = xo;
+        UsT[vv * LU + r0 + j] = xo;
+      }
+    }
     __syncthreads();
-    const float gl = expf(Gl);
+    const float gl = cur.gl;
     hs.each([&](int, int, float& x) { x *= gl; });
-    hs.template mma<OP, CH>(KCol<OP, LK>{Ks}, KRow<OP, LU>{UsT});
-    __syncthreads();
+    hs.template mma<OP, CH>(cur.kh, KRow<OP, LU>{UsT});
+    if (PF) cur = nxt;
   }
   float* STp = ST + ((long)n * H + h) * DK * DV;
   hs.each([&](int d, int vv, float& x) { STp[d * DV + v0 + vv] = x; });
@@ -259,13 +318,13 @@ static hipError_t launch_fwd_t(const FwdArgs& a) {
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_prep_fwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
                        geo, H, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, w.gcum, (OP*)w.W, w.U,
-                       w.flag_prep);
+                       (OP*)w.KhT, w.flag_prep);
   }
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
-                       (const OP*)a.k, (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, w.U, a.states,
+                       (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, (const OP*)w.KhT, w.U, a.states,
                        a.ST, (OP*)w.UpT, w.flag_scan);
   }
   stage_mark(a.events, 2, a.stream);

@@ -18,6 +18,7 @@ struct FwdWs {
   void* W;         // [chunks*H*64*dk] operand dtype
   float* U;        // [chunks*H*64*dv]
   void* UpT;       // [chunks*H*dv*64] operand dtype, U' transposed
+  void* KhT;       // [chunks*H*dk*64] operand dtype, (e^{G_last-G} K)^T
   float* exact;    // exact-path scratch
 };
 
@@ -40,9 +41,12 @@ struct BwdWs {
   int* flag_grad;  // [chunks*H]   non-finite chunk state in the chunk
   int* flag_scan;  // [N*H*NVT]    non-finite dS_T slice
   float* gcum;     // [chunks*H*64]
-  void* W;         // [chunks*H*64*dk] operand dtype
+  void* W;         // [chunks*H*dk*64] operand dtype, W^T
+  void* QgT;       // [chunks*H*dk*64] operand dtype, (diag(e^G) Q)^T
+  void* dOT;       // [chunks*H*dv*64] operand dtype, dO^T
   float* dvl;      // [chunks*H*64*dv] P^T dO
   void* dh;        // [chunks*H*dk*dv] operand dtype: state gradient after each chunk
+  void* dUT;       // [chunks*H*dv*64] operand dtype: dU' of each chunk, transposed
   void* grad_scratch;  // [chunks*H*grad_region_bytes] fp32 operands only
   float* exact;
 };
@@ -78,7 +82,7 @@ constexpr int grad_region_bytes(int dk, int es) {
   const int CHn = 64, P8 = 16 / es, LK = dk + P8, LT = CHn + P8, LC = CHn + 4, VS = 32, LV = VS + P8;
   const bool bf = es == 2;
   const int ph0 = CHn * LK * es + CHn * LC * 4 + (bf ? CHn * LC * 4 : 0) + 4 * 16 * 20 * 4;
-  const int ph1 = (7 * CHn * LV + 2 * dk * LV + 2 * VS * LT) * es;
+  const int ph1 = (7 * CHn * LV + 2 * dk * LV + VS * LK + 2 * VS * LT) * es;
   const int ph2 = (2 * dk * LT + 4 * CHn * LT) * es;
   const int m = ph0 > ph1 ? (ph0 > ph2 ? ph0 : ph2) : (ph1 > ph2 ? ph1 : ph2);
   return (m + 255) / 256 * 256;

@@ -40,19 +40,24 @@ def kernel_model(B, T, H, dk, dv, es, N=None):
     tiles = nch * H
     g4 = 4 * CH  # one fp32 per token of a chunk
     st = dk * dv * 4
+    qk = CH * dk * es  # one chunk of q or k (or a 64 x dk operand) in the I/O dtype
+    vv = CH * dv * es  # one chunk of v, o, dO (or a 64 x dv operand)
+    pp = CH * CH * es  # one 64 x 64 operand
     per = {
-        "fwd_prep": (CH * dk * es + CH * dv * es + 2 * g4 + g4 + CH * dk * es + CH * dv * 4,
-                     2 * CH * CH * dk * 2 + CH ** 3 / 3 + 2 * CH * CH * dv),
-        "fwd_scan": (2 * CH * dk * es + CH * dv * 4 + g4 + st + CH * dv * es,
-                     2 * 2 * CH * dk * dv),
-        "fwd_out": (2 * CH * dk * es + g4 + st + CH * dv * es + CH * dv * es,
-                    2 * CH * CH * dk + 2 * CH * dk * dv + 2 * CH * CH * dv),
-        "bwd_prep": (2 * CH * dk * es + CH * dv * es + 2 * g4 + g4 + CH * dk * es + CH * dv * 4,
-                     3 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dv),
-        "bwd_scan": (3 * CH * dk * es + CH * dv * es + CH * dv * 4 + g4 + dk * dv * es,
-                     3 * 2 * CH * dk * dv),
-        "bwd_grad": (2 * CH * dk * es + 2 * CH * dv * es + 2 * g4 + st + dk * dv * es
-                     + 2 * CH * dk * es + CH * dv * es + 2 * g4,
+        # q, k, v, g, beta -> gcum, W, U (fp32), Khat^T, P
+        "fwd_prep": (2 * qk + vv + 2 * g4 + g4 + 2 * qk + CH * dv * 4 + pp,
+                     3 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dk + 2 * CH * CH * dv),
+        # q, W, Khat^T, P, U, gcum -> chunk states, o
+        "fwd_scan": (3 * qk + pp + CH * dv * 4 + g4 + st + vv,
+                     3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
+        # q, k, g, beta, dO -> gcum, W^T, (diag(e^G) Q)^T, dO^T, P^T
+        "bwd_prep": (2 * qk + 2 * g4 + vv + g4 + 2 * qk + vv + pp,
+                     3 * 2 * CH * CH * dk + CH ** 3 / 3),
+        # k, gcum, W^T, Qg^T, dO^T, P^T -> dh (I/O dtype), dU'^T
+        "bwd_scan": (3 * qk + g4 + vv + pp + dk * dv * es + vv,
+                     3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
+        # q, k, v, g, beta, states, dO, dh, dU'^T -> dq, dk, dv, dg, dbeta
+        "bwd_grad": (2 * qk + vv + 2 * g4 + st + vv + dk * dv * es + vv + 2 * qk + vv + 2 * g4,
                      5 * 2 * CH * CH * dk + CH ** 3 / 3 + 4 * CH ** 3 + 5 * 2 * CH * dk * dv
                      + 5 * 2 * CH * CH * dv),
     }
@@ -227,8 +232,10 @@ def main(argv=None):
         for j in range(gdn.NUM_STAGES):
             stage_ms[gdn.FWD_STAGES[j]] += hip.ms(ef[j], ef[j + 1]) / a.steps
             stage_ms[gdn.BWD_STAGES[j]] += hip.ms(eb[j], eb[j + 1]) / a.steps
-    fwd_ms = sum(stage_ms[n] for n in gdn.FWD_STAGES)
-    bwd_ms = sum(stage_ms[n] for n in gdn.BWD_STAGES)
+    stage_ms.pop(None, None)  # a direction with fewer stages leaves the last one empty
+    names = [n for n in names if n is not None]
+    fwd_ms = sum(stage_ms[n] for n in gdn.FWD_STAGES if n is not None)
+    bwd_ms = sum(stage_ms[n] for n in gdn.BWD_STAGES if n is not None)
 
     ok = all(bool(torch.isfinite(x).all()) for x in (o, S_T, dq, dk_, dv_, dg, db, dS0))
 

@@ -137,9 +137,10 @@ gdn_status gdn_bwd(const gdn_problem* p, const void* q, const void* k, const voi
                    float* dS0, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Stages that gdn_fwd_ex / gdn_bwd_ex can bracket with events.  Forward:
- * 0 chunk prep (UT transform), 1 forward state scan, 2 chunk output, 3 exact
- * token-serial pass for non-finite streams.  Backward: 0 chunk prep, 1 reverse
- * state scan, 2 chunk gradients, 3 exact pass. */
+ * 0 chunk prep (UT transform and the masked in-chunk scores), 1 forward state
+ * scan with the chunk output, 2 exact token-serial pass for non-finite streams,
+ * 3 empty.  Backward: 0 chunk prep, 1 reverse state scan, 2 chunk gradients,
+ * 3 exact pass. */
 #define GDN_NUM_STAGES 4
 
 /* gdn_fwd / gdn_bwd with optional per-stage timing.  `events` is NULL or an

@@ -111,13 +111,12 @@ void layout_fwd(const Shape& s, char* base, FwdWs* w, size_t* total) {
   const size_t tiles = (size_t)s.chunks * s.H;
   w->chunk_off = b.take<int>(s.packed ? s.N + 1 : 0);
   w->flag_prep = b.take<int>(tiles);
-  w->flag_out = b.take<int>(tiles);
   w->flag_scan = b.take<int>((size_t)s.N * s.H * (s.dv / SCAN_BV));
   w->gcum = b.take<float>(tiles * kChunk);
   w->W = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->U = b.take<float>(tiles * kChunk * s.dv);
-  w->UpT = b.take<char>(tiles * kChunk * s.dv * s.es);
   w->KhT = b.take<char>(tiles * kChunk * s.dk * s.es);
+  w->P = b.take<char>(tiles * kChunk * kChunk * s.es);
   w->exact = nullptr;  // the exact forward needs no scratch
   *total = b.off;
 }
@@ -133,7 +132,7 @@ void layout_bwd(const Shape& s, char* base, BwdWs* w, size_t* total) {
   w->W = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->QgT = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->dOT = b.take<char>(tiles * kChunk * s.dv * s.es);
-  w->dvl = b.take<float>(tiles * kChunk * s.dv);
+  w->PT = b.take<char>(tiles * kChunk * kChunk * s.es);
   w->dh = b.take<char>(tiles * (size_t)s.dk * s.dv * s.es);
   w->dUT = b.take<char>(tiles * kChunk * s.dv * s.es);
   w->grad_scratch = b.take<char>(s.es == 4 ? tiles * (size_t)grad_region_bytes((int)s.dk, 4) : 0);

@@ -2,11 +2,11 @@
 // chunk states cross from the forward; everything else is recomputed.
 //
 //   prep   one block per (chunk, head): G, T = (I + A)^{-1}, W = T diag(beta e^G) K,
-//          and dV_loc = P^T dO with P = (Q K^T) * D.
+//          P = (Q K^T) * D, laid out for the scan.
 //   scan   the reverse inter-chunk state scan (paper Sec. 4.2, K#1): one block
 //          per (stream, value tile); an fp32 carry dh walks the chunks from the
 //          last to the first,
-//            dU' = dV_loc + Khat dh,   dh <- e^{G_last} dh + Q^T diag(e^G) dO - W^T dU',
+//            dU' = P^T dO + Khat dh,   dh <- e^{G_last} dh + Q^T diag(e^G) dO - W^T dU',
 //          storing the carry that enters every chunk; dS0 is the final carry.
 //   grad   one block per (chunk, head): every chunk-local gradient, with the
 //          triangular-inverse VJP (paper Sec. 4.2, K#2) that reuses T in four
@@ -31,99 +31,120 @@
 
 namespace gdn {
 
-// 4 consecutive elements of the operand type as one load/store unit.
-template <typename T> struct vec4_of;
-template <> struct vec4_of<bf16> { typedef uint2 type; };
-template <> struct vec4_of<float> { typedef uint4 type; };
-template <typename T> __device__ __forceinline__ T elem4(const typename vec4_of<T>::type& u, int j);
-template <> __device__ __forceinline__ bf16 elem4<bf16>(const uint2& u, int j) {
-  return __builtin_bit_cast(bf16, (unsigned short)((j < 2 ? u.x : u.y) >> ((j & 1) * 16)));
-}
-template <> __device__ __forceinline__ float elem4<float>(const uint4& u, int j) {
-  return elem16<float>(u, j);
-}
-template <typename T> __device__ __forceinline__ typename vec4_of<T>::type pack4(const T* x);
-template <> __device__ __forceinline__ uint2 pack4<bf16>(const bf16* x) {
-  return uint2{pack2(x[0], x[1]), pack2(x[2], x[3])};
-}
-template <> __device__ __forceinline__ uint4 pack4<float>(const float* x) { return pack16<float>(x); }
-
 template <int DK, int DV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_prep_bwd(Geo geo, int H, const OP* __restrict__ q,
+__global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __restrict__ q,
                                                   const OP* __restrict__ k, const float* __restrict__ g,
                                                   const float* __restrict__ beta, const OP* __restrict__ dO,
                                                   float* __restrict__ gcum, OP* __restrict__ WTg,
                                                   OP* __restrict__ QgTg, OP* __restrict__ dOTg,
-                                                  float* __restrict__ dvlg, int* __restrict__ flag) {
+                                                  OP* __restrict__ PTg, int* __restrict__ flag) {
+  constexpr bool DT_ = VAR != VAR_DECAY;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
   constexpr int LT = CH + pad_of<OP>();
   constexpr int VS = 64;
   constexpr int LVS = VS + pad_of<OP>();
-  __shared__ __align__(16) OP Qs[CH * LK];
-  __shared__ __align__(16) OP Ks[CH * LK];
-  __shared__ __align__(16) float As[VAR != VAR_DECAY ? CH * LC : 1];
-  __shared__ __align__(16) float Tf[VAR != VAR_DECAY ? CH * LC : 1];
-  __shared__ __align__(16) OP Ts[(VAR != VAR_DECAY && sizeof(OP) == 2) ? CH * LT : 1];
-  __shared__ __align__(16) OP PT[CH * LT];
-  __shared__ __align__(16) OP dOs[CH * LVS];
+  constexpr int VE = 16 / (int)sizeof(OP);
+  typedef typename vec4_of<OP>::type V4;
+  // LDS regions are reused by lifetime so that two blocks fit on a CU:
+  //   R1: Q, then T in fp32;  R2: K, then T in the operand dtype;
+  //   R3: (diag(beta e^G) K)^T;  R4: A in fp32, then dO slices.
+  constexpr int R1 = CH * LK * (int)sizeof(OP) > CH * LC * 4 ? CH * LK * (int)sizeof(OP) : CH * LC * 4;
+  constexpr int R2 = CH * LK * (int)sizeof(OP);
+  constexpr int R4 = CH * LC * 4 > CH * LVS * (int)sizeof(OP) ? CH * LC * 4 : CH * LVS * (int)sizeof(OP);
+  static_assert(CH * LT * (int)sizeof(OP) <= R2, "T fits where K was");
+  __shared__ __align__(16) char r1[R1];
+  __shared__ __align__(16) char r2[R2];
+  __shared__ __align__(16) OP KbT[DT_ ? DK * LT : 1];  // (diag(beta e^G) K)^T
+  __shared__ __align__(16) char r4[R4];
   __shared__ __align__(16) float Xs[4 * 16 * 20];
-  __shared__ float Gs[CH], Bs[CH], GBs[CH];
+  __shared__ float Gs[CH], Bs[CH], Gam[CH];
+  OP* Qs = reinterpret_cast<OP*>(r1);
+  float* Tf = reinterpret_cast<float*>(r1);
+  OP* Ks = reinterpret_cast<OP*>(r2);
+  OP* Ts = reinterpret_cast<OP*>(r2);
+  float* As = reinterpret_cast<float*>(r4);
+  OP* dOs = reinterpret_cast<OP*>(r4);
 
   const int ci = blockIdx.x, h = blockIdx.y;
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
+  const int l = lane_id();
   bool ok = load_gates<VAR>(g, beta, cp.row0, H, h, cp.len, Gs, Bs);
   ok &= load_rows<DK, LK>(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Qs);
   ok &= load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
   __syncthreads();
   if (threadIdx.x < CH) {
     gcum[tile * CH + threadIdx.x] = Gs[threadIdx.x];
-    GBs[threadIdx.x] = Bs[threadIdx.x] * expf(Gs[threadIdx.x]);
+    Gam[threadIdx.x] = __expf(Gs[threadIdx.x]);
   }
+  __syncthreads();
+  // P^T, written (i, r): the scan's A operand for P^T dO
   {
-    Tiles<CH, CH, 2, 2> p;
+    Tiles<CH, CH, 4, 2> p;
     p.zero();
     p.template mma<OP, DK>(KRow<OP, LK>{Qs}, KRow<OP, LK>{Ks});
-    p.each([&](int r, int i, float& x) {
-      PT[i * LT + r] = from_f<OP>(i <= r ? x * expf(Gs[r] - Gs[i]) : 0.f);
-    });
-  }
-  if constexpr (VAR != VAR_DECAY) {
-    Tiles<CH, CH, 2, 2> bm;
-    bm.zero();
-    bm.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{Ks});
-    bm.each([&](int r, int i, float& x) {
-      As[r * LC + i] = (i < r) ? Bs[r] * x * expf(Gs[r] - Gs[i]) : 0.f;
-    });
-    __syncthreads();
-    unit_lower_inverse<OP, LC, LT>(As, Tf, Ts, Xs);
-    const OP* Tp;
-    if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = Tf;
-    constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
-    Tiles<CH, DK, 2, 2> w;
-    w.zero();
-    w.template mma<OP, CH>(KRow<OP, LTT>{Tp}, kfun<OP>([&](int d, int i) {
-                             return from_f<OP>(GBs[i] * to_f(Ks[i * LK + d]));
-                           }));
-    OP* Wt = WTg + tile * DK * CH;
-    w.each([&](int r, int d, float& x) { Wt[d * CH + r] = from_f<OP>(x); });
+    OP* Pt = PTg + tile * CH * CH;
+#pragma unroll
+    for (int b = 0; b < p.TN; ++b) {
+      const int i = p.n0(b) + (l & 15), r0 = p.m0(0) + (l >> 4) * 4;
+      OP v4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = r0 + j;
+        v4[j] = from_f<OP>(i <= r ? p.acc[0][b][j] * __expf(Gs[r] - Gs[i]) : 0.f);
+      }
+      *reinterpret_cast<V4*>(Pt + i * CH + r0) = pack4<OP>(v4);
+    }
   }
   // (diag(e^G) Q)^T for the scan's injection term
-  constexpr int VE = 16 / (int)sizeof(OP);
   {
     OP* Qg = QgTg + tile * DK * CH;
     for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
       const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
       OP vals[VE];
 #pragma unroll
-      for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(expf(Gs[r0 + j]) * to_f(Qs[(r0 + j) * LK + d]));
+      for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Gam[r0 + j] * to_f(Qs[(r0 + j) * LK + d]));
       *reinterpret_cast<uint4*>(Qg + d * CH + r0) = pack16<OP>(vals);
     }
   }
-  // dV_loc = P^T dO, in slices of VS value columns
+  if constexpr (DT_) {
+    Tiles<CH, CH, 4, 2> bm;
+    bm.zero();
+    bm.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{Ks});
+    bm.each([&](int r, int i, float& x) {
+      As[r * LC + i] = (i < r) ? Bs[r] * x * __expf(Gs[r] - Gs[i]) : 0.f;
+    });
+    // (diag(beta e^G) K)^T for the W product
+    for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
+      const int i = idx / (DK / VE), d0 = (idx - i * (DK / VE)) * VE;
+      const uint4 kv = *reinterpret_cast<const uint4*>(Ks + i * LK + d0);
+      const float sc = Bs[i] * Gam[i];
+#pragma unroll
+      for (int j = 0; j < VE; ++j) KbT[(d0 + j) * LT + i] = from_f<OP>(sc * to_f(elem16<OP>(kv, j)));
+    }
+    __syncthreads();
+    unit_lower_inverse<OP, LC, LT>(As, Tf, Ts, Xs);  // Tf over Q, Ts over K: both are dead here
+    const OP* Tp;
+    if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
+    constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
+    // W = T diag(beta e^G) K, written transposed (d, r)
+    Tiles<CH, DK, 4, 2> w;
+    w.zero();
+    w.template mma<OP, CH>(KRow<OP, LTT>{Tp}, KRow<OP, LT>{KbT});
+    OP* Wt = WTg + tile * DK * CH;
+#pragma unroll
+    for (int b = 0; b < w.TN; ++b) {
+      const int d = w.n0(b) + (l & 15), r0 = w.m0(0) + (l >> 4) * 4;
+      OP v4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v4[j] = from_f<OP>(w.acc[0][b][j]);
+      *reinterpret_cast<V4*>(Wt + d * CH + r0) = pack4<OP>(v4);
+    }
+  }
+  // dO^T, in slices of VS value columns (dO slices reuse the A region)
+  __syncthreads();
   const OP* dop = dO + (cp.row0 * H + h) * DV;
-  float* dvl = dvlg + tile * CH * DV;
   for (int c0 = 0; c0 < DV; c0 += VS) {
     ok &= load_rows<VS, LVS>(dop + c0, (long)H * DV, cp.len, dOs);
     __syncthreads();
@@ -135,10 +156,6 @@ __global__ __launch_bounds__(256) void k_prep_bwd(Geo geo, int H, const OP* __re
       for (int j = 0; j < VE; ++j) vals[j] = dOs[(r0 + j) * LVS + vv];
       *reinterpret_cast<uint4*>(dOt + vv * CH + r0) = pack16<OP>(vals);
     }
-    Tiles<CH, VS, 2, 2> t;
-    t.zero();
-    t.template mma<OP, CH>(KRow<OP, LT>{PT}, KCol<OP, LVS>{dOs});
-    t.each([&](int i, int vv, float& x) { dvl[i * DV + c0 + vv] = x; });
     __syncthreads();
   }
   const int bad = __syncthreads_or(!ok);
@@ -148,15 +165,15 @@ __global__ __launch_bounds__(256) void k_prep_bwd(Geo geo, int H, const OP* __re
 // The reverse inter-chunk state scan (paper Sec. 4.2, K#1).  The fp32 carry dh
 // (the gradient w.r.t. the state leaving the chunk) stays in registers; the
 // prep kernel lays out every other operand for direct fragment loads (W^T,
-// (diag(e^G) Q)^T, dO^T, dV_loc), and the fragments of chunk c-1 are fetched
+// (diag(e^G) Q)^T, dO^T, P^T), and the fragments of chunk c-1 are fetched
 // into registers while chunk c is processed:
-//   dU' = dV_loc + diag(e^{G_last - G}) K dh
+//   dU' = P^T dO + diag(e^{G_last - G}) K dh
 //   dh <- e^{G_last} dh + (diag(e^G) Q)^T dO - W^T dU'
 template <int DK, int DV, int BV, typename OP, int VAR>
 __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __restrict__ k,
                                                   const float* __restrict__ dST, const float* __restrict__ gcum,
                                                   const OP* __restrict__ WTg, const OP* __restrict__ QgTg,
-                                                  const OP* __restrict__ dOTg, const float* __restrict__ dvlg,
+                                                  const OP* __restrict__ dOTg, const OP* __restrict__ PTg,
                                                   OP* __restrict__ dhg, OP* __restrict__ dUTg,
                                                   float* __restrict__ dS0, int* __restrict__ flag) {
   constexpr int NVT = DV / BV;
@@ -180,7 +197,7 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     typename HT::template AFr<OP, CH> wt;
     typename HT::template AFr<OP, CH> qg;
     typename HT::template BFr<OP, CH> dob;
-    float dvl[UT::TN][4];
+    typename UT::template AFr<OP, CH> pt;
     float dte[4];
     float gl;
   };
@@ -194,16 +211,9 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     p.gl = expf(Gl);
     p.kf.load(KRowM<OP>{k + (row0 * H + h) * DK, (long)H * DK, len});
     if constexpr (DT_) p.wt.load(KRow<OP, CH>{WTg + tile * DK * CH});
-    {
-      const float* dv = dvlg + tile * CH * DV + v0;
+    p.pt.load(KRow<OP, CH>{PTg + tile * CH * CH});
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = UT::m0(0) + (l >> 4) * 4 + j;
-        p.dte[j] = expf(Gl - gcum[tile * CH + r]);
-#pragma unroll
-        for (int b = 0; b < UT::TN; ++b) p.dvl[b][j] = dv[r * DV + UT::n0(b) + (l & 15)];
-      }
-    }
+    for (int j = 0; j < 4; ++j) p.dte[j] = __expf(Gl - gcum[tile * CH + UT::m0(0) + (l >> 4) * 4 + j]);
   };
 
   HT dh;
@@ -234,11 +244,16 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     inj.zero();
     inj.template mma<OP, CH>(cur.qg, cur.dob);
     {
-      // dU' = dV_loc + diag(e^{G_last - G}) K dh (written for the gradient kernel for every
+      // dU' = P^T dO + diag(e^{G_last - G}) K dh (written for the gradient kernel for every
       // family member; only the delta rule feeds it back into the carry)
       UT du;
       du.zero();
       du.template mma<OP, DK>(cur.kf, KRow<OP, LK>{dhT});
+#pragma unroll
+      for (int b = 0; b < UT::TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) du.acc[0][b][j] *= cur.dte[j];
+      du.template mma_raw<OP, CH / Mma<OP>::KSTEP>(cur.pt.f, cur.dob.f);  // + P^T dO
       OP* dUg = dUTg + tile * DV * CH + (long)v0 * CH;
 #pragma unroll
       for (int b = 0; b < UT::TN; ++b) {
@@ -246,7 +261,7 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
         OP u4[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float u = cur.dvl[b][j] + cur.dte[j] * du.acc[0][b][j];
+          const float u = du.acc[0][b][j];
           if (DT_) dUT[vv * LU + r0 + j] = from_f<OP>(-u);
           u4[j] = from_f<OP>(u);
         }
@@ -680,16 +695,16 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
     if (e != hipSuccess) return e;
   }
   if (geo.total_chunks > 0) {
-    hipLaunchKernelGGL((k_prep_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
+    hipLaunchKernelGGL((k_prep_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, a.g, a.beta, (const OP*)a.dO, w.gcum,
-                       (OP*)w.W, (OP*)w.QgT, (OP*)w.dOT, w.dvl, w.flag_prep);
+                       (OP*)w.W, (OP*)w.QgT, (OP*)w.dOT, (OP*)w.PT, w.flag_prep);
   }
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
                        (const OP*)a.k, a.dST, w.gcum, (const OP*)w.W, (const OP*)w.QgT, (const OP*)w.dOT,
-                       w.dvl, (OP*)w.dh, (OP*)w.dUT, a.dS0, w.flag_scan);
+                       (const OP*)w.PT, (OP*)w.dh, (OP*)w.dUT, a.dS0, w.flag_scan);
   }
   stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0) {

@@ -54,6 +54,26 @@ template <typename T> __device__ __forceinline__ bool finite16B(uint4 u);
 template <> __device__ __forceinline__ bool finite16B<bf16>(uint4 u) { return finite8_bf16(u); }
 template <> __device__ __forceinline__ bool finite16B<float>(uint4 u) { return finite4_f32(u); }
 
+// 4 consecutive elements of the operand type as one load/store unit.
+template <typename T> struct vec4_of;
+template <> struct vec4_of<bf16> { typedef uint2 type; };
+template <> struct vec4_of<float> { typedef uint4 type; };
+template <typename T> __device__ __forceinline__ T elem4(const typename vec4_of<T>::type& u, int j);
+template <> __device__ __forceinline__ bf16 elem4<bf16>(const uint2& u, int j) {
+  return __builtin_bit_cast(bf16, (unsigned short)((j < 2 ? u.x : u.y) >> ((j & 1) * 16)));
+}
+template <> __device__ __forceinline__ float elem4<float>(const uint4& u, int j) {
+  return elem16<float>(u, j);
+}
+template <typename T> __device__ __forceinline__ typename vec4_of<T>::type pack4(const T* x);
+template <> __device__ __forceinline__ uint2 pack4<bf16>(const bf16* x) {
+  return uint2{pack2(x[0], x[1]), pack2(x[2], x[3])};
+}
+template <> __device__ __forceinline__ uint4 pack4<float>(const float* x) { return pack16<float>(x); }
+
+// Backward chunk prep: everything the reverse scan needs per chunk, laid out
+// for direct MFMA fragment loads: P^T (P = (Q K^T) * D), W^T with
+// W = T diag(beta e^G) K, (diag(e^G) Q)^T and dO^T, plus the cumulative decay.
 // Copy rows [0, len) of a 64 x D tile whose rows sit `rs` elements apart in
 // HBM into LDS dst[r * LD + d]; rows >= len are zero-filled.  Returns false
 // if any loaded value is NaN or Inf.

@@ -225,6 +225,19 @@ struct Tiles {
         for (int b = 0; b < TN; ++b) acc[a][b] = X::mma(fa.f[s][a], fb.f[s][b], acc[a][b]);
   }
 
+  // acc += A * B from raw fragment arrays laid out like AFr / BFr of any
+  // Tiles with the same TM / TN ownership.
+  template <typename OP, int S>
+  __device__ __forceinline__ void mma_raw(const typename Mma<OP>::frag (&fa)[S][TM],
+                                          const typename Mma<OP>::frag (&fb)[S][TN]) {
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) acc[a][b] = Mma<OP>::mma(fa[s][a], fb[s][b], acc[a][b]);
+  }
+
   // Visit every owned element: f(row, col, value&).
   template <class F>
   __device__ __forceinline__ void each(F f) {

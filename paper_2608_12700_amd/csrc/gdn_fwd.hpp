@@ -1,18 +1,17 @@
 // Forward of the chunked gated delta rule on gfx950 (paper Sec. 4.2: parallel
 // work inside every chunk of 64 tokens, then a short sequential carry between
-// chunks).  Three kernels per call:
+// chunks).  Two kernels per call:
 //
 //   prep   one block per (chunk, head): in-chunk cumulative decay G, the erase
 //          coupling A = strict_lower(diag(beta) K K^T * exp(G_r - G_i)), the
-//          inverse T = (I + A)^{-1}, and the two applies
-//          W = T diag(beta e^G) K, U = T diag(beta) V.
-//   scan   one block per (stream, value tile of BV columns): the inter-chunk
-//          carry, chunk by chunk,  U' = U - W h,  h <- e^{G_last} h + Khat^T U'
-//          with Khat_r = e^{G_last - G_r} k_r; writes every h (the saved chunk
-//          states), U' and S_T.  The carry splits over value columns with no
-//          communication.
-//   out    one block per (chunk, head): O = diag(e^G) Q h + ((Q K^T) * D) U'
-//          with D_ri = e^{G_r - G_i} for i <= r (exponent formed only there).
+//          inverse T = (I + A)^{-1}, the two applies W = T diag(beta e^G) K and
+//          U = T diag(beta) V, Khat^T with Khat_r = e^{G_last - G_r} k_r, and
+//          P = (Q K^T) * D with D_ri = e^{G_r - G_i} for i <= r (exponent formed
+//          only there), all laid out for direct MFMA fragment loads.
+//   scan   one block per (stream, value tile of BV columns): chunk by chunk,
+//            U' = U - W h,   O = diag(e^G) Q h + P U',   h <- e^{G_last} h + Khat^T U',
+//          writing every h (the saved chunk states), the output tile and S_T.
+//          The carry splits over value columns with no communication.
 #pragma once
 
 #include "gdn_chunk.hpp"
@@ -22,115 +21,180 @@
 namespace gdn {
 
 template <int DK, int DV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_prep_fwd(Geo geo, int H, const OP* __restrict__ k,
-                                                  const OP* __restrict__ v, const float* __restrict__ g,
-                                                  const float* __restrict__ beta, float* __restrict__ gcum,
-                                                  OP* __restrict__ Wg, float* __restrict__ Ug,
-                                                  OP* __restrict__ KhTg, int* __restrict__ flag) {
+__global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __restrict__ q,
+                                                  const OP* __restrict__ k, const OP* __restrict__ v,
+                                                  const float* __restrict__ g, const float* __restrict__ beta,
+                                                  float* __restrict__ gcum, OP* __restrict__ Wg,
+                                                  float* __restrict__ Ug, OP* __restrict__ KhTg,
+                                                  OP* __restrict__ Pg, int* __restrict__ flag) {
+  constexpr bool DT_ = VAR != VAR_DECAY;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
   constexpr int LT = CH + pad_of<OP>();
   constexpr int VS = 64;  // value columns per slice of U
-  constexpr int LVS = VS + pad_of<OP>();
-  __shared__ __align__(16) OP Ks[CH * LK];
-  __shared__ __align__(16) float As[CH * LC];
-  __shared__ __align__(16) float Tf[CH * LC];
-  __shared__ __align__(16) OP Ts[sizeof(OP) == 2 ? CH * LT : 1];
-  __shared__ __align__(16) OP Vs[CH * LVS];
+  constexpr int VE = 16 / (int)sizeof(OP);
+  typedef typename vec4_of<OP>::type V4;
+  // LDS regions reused by lifetime (two blocks per CU):
+  //   R1: Q, then T in fp32;  R2: K, then T in the operand dtype;
+  //   R3: (diag(beta e^G) K)^T;  R4: A in fp32, then (diag(beta) V)^T slices.
+  constexpr int R1 = CH * LK * (int)sizeof(OP) > CH * LC * 4 ? CH * LK * (int)sizeof(OP) : CH * LC * 4;
+  constexpr int R2 = CH * LK * (int)sizeof(OP);
+  constexpr int R4 = CH * LC * 4 > VS * LT * (int)sizeof(OP) ? CH * LC * 4 : VS * LT * (int)sizeof(OP);
+  static_assert(CH * LT * (int)sizeof(OP) <= R2, "T fits where K was");
+  __shared__ __align__(16) char r1[R1];
+  __shared__ __align__(16) char r2[R2];
+  __shared__ __align__(16) OP KbT[DT_ ? DK * LT : 1];
+  __shared__ __align__(16) char r4[R4];
   __shared__ __align__(16) float Xs[4 * 16 * 20];
-  __shared__ float Gs[CH], Bs[CH], GBs[CH];
+  __shared__ float Gs[CH], Bs[CH], Gam[CH], Dte[CH];
+  OP* Qs = reinterpret_cast<OP*>(r1);
+  float* Tf = reinterpret_cast<float*>(r1);
+  OP* Ks = reinterpret_cast<OP*>(r2);
+  OP* Ts = reinterpret_cast<OP*>(r2);
+  float* As = reinterpret_cast<float*>(r4);
+  OP* VbT = reinterpret_cast<OP*>(r4);
 
   const int ci = blockIdx.x, h = blockIdx.y;
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
+  const int l = lane_id();
   bool ok = load_gates<VAR>(g, beta, cp.row0, H, h, cp.len, Gs, Bs);
-  if (VAR != VAR_DECAY) ok &= load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
+  ok &= load_rows<DK, LK>(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Qs);
+  ok &= load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
   __syncthreads();
   if (threadIdx.x < CH) {
-    gcum[tile * CH + threadIdx.x] = Gs[threadIdx.x];
-    GBs[threadIdx.x] = Bs[threadIdx.x] * expf(Gs[threadIdx.x]);
+    const int r = threadIdx.x;
+    gcum[tile * CH + r] = Gs[r];
+    Gam[r] = __expf(Gs[r]);
+    Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
   }
-  if constexpr (VAR != VAR_DECAY) {
-    // A = strict_lower(diag(beta) K K^T * exp(G_r - G_i))
-    Tiles<CH, CH, 2, 2> bm;
+  __syncthreads();
+  // P[r][i] = (q_r . k_i) e^{G_r - G_i} (i <= r): computed as K Q^T so that a
+  // lane's four accumulator rows are four consecutive i of one row r of P
+  {
+    Tiles<CH, CH, 4, 2> s;
+    s.zero();
+    s.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{Qs});
+    OP* Pt = Pg + tile * CH * CH;
+#pragma unroll
+    for (int b = 0; b < s.TN; ++b) {
+      const int r = s.n0(b) + (l & 15), i0 = s.m0(0) + (l >> 4) * 4;
+      OP v4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = i0 + j;
+        v4[j] = from_f<OP>(i <= r ? s.acc[0][b][j] * __expf(Gs[r] - Gs[i]) : 0.f);
+      }
+      *reinterpret_cast<V4*>(Pt + r * CH + i0) = pack4<OP>(v4);
+    }
+  }
+  if constexpr (DT_) {
+    Tiles<CH, CH, 4, 2> bm;
     bm.zero();
     bm.template mma<OP, DK>(KRow<OP, LK>{Ks}, KRow<OP, LK>{Ks});
     bm.each([&](int r, int i, float& x) {
-      As[r * LC + i] = (i < r) ? Bs[r] * x * expf(Gs[r] - Gs[i]) : 0.f;
+      As[r * LC + i] = (i < r) ? Bs[r] * x * __expf(Gs[r] - Gs[i]) : 0.f;
     });
-    __syncthreads();
+    // (diag(beta e^G) K)^T for the W product
+    for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
+      const int i = idx / (DK / VE), d0 = (idx - i * (DK / VE)) * VE;
+      const uint4 kv = *reinterpret_cast<const uint4*>(Ks + i * LK + d0);
+      const float sc = Bs[i] * Gam[i];
+#pragma unroll
+      for (int j = 0; j < VE; ++j) KbT[(d0 + j) * LT + i] = from_f<OP>(sc * to_f(elem16<OP>(kv, j)));
+    }
+  }
+  // Khat^T[d][r] = e^{G_last - G_r} k_r[d], the scan's A operand for the carry
+  {
+    OP* Kh = KhTg + tile * DK * CH;
+    for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
+      const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
+      OP vals[VE];
+#pragma unroll
+      for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Dte[r0 + j] * to_f(Ks[(r0 + j) * LK + d]));
+      *reinterpret_cast<uint4*>(Kh + d * CH + r0) = pack16<OP>(vals);
+    }
+  }
+  __syncthreads();  // Q and K are dead from here on
+  const OP* vp = v + (cp.row0 * H + h) * DV;
+  if constexpr (DT_) {
     unit_lower_inverse<OP, LC, LT>(As, Tf, Ts, Xs);
     const OP* Tp;
-    if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = Tf;
+    if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
     constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
-    // W = T diag(beta e^G) K
+    // W = T diag(beta e^G) K, computed as W^T = Kb^T T^T so a lane holds four
+    // consecutive d of one row r of W
     {
-      Tiles<CH, DK, 2, 2> w;
-      w.zero();
-      w.template mma<OP, CH>(KRow<OP, LTT>{Tp}, kfun<OP>([&](int d, int i) {
-                               return from_f<OP>(GBs[i] * to_f(Ks[i * LK + d]));
-                             }));
+      Tiles<DK, CH, 4, 2> wt;
+      wt.zero();
+      wt.template mma<OP, CH>(KRow<OP, LT>{KbT}, KRow<OP, LTT>{Tp});
       OP* Wt = Wg + tile * CH * DK;
-      w.each([&](int r, int d, float& x) { Wt[r * DK + d] = from_f<OP>(x); });
+#pragma unroll
+      for (int a = 0; a < wt.TM; ++a)
+#pragma unroll
+        for (int b = 0; b < wt.TN; ++b) {
+          const int r = wt.n0(b) + (l & 15), d0 = wt.m0(a) + (l >> 4) * 4;
+          OP v4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v4[j] = from_f<OP>(wt.acc[a][b][j]);
+          *reinterpret_cast<V4*>(Wt + r * DK + d0) = pack4<OP>(v4);
+        }
     }
-    // U = T diag(beta) V, in slices of VS value columns
-    const OP* vp = v + (cp.row0 * H + h) * DV;
+    // U = T diag(beta) V, per slice of VS value columns, as U^T = (diag(beta) V)^T T^T
     float* Ut = Ug + tile * CH * DV;
     for (int c0 = 0; c0 < DV; c0 += VS) {
-      ok &= load_rows<VS, LVS>(vp + c0, (long)H * DV, cp.len, Vs);
+      for (int idx = threadIdx.x; idx < CH * VS / VE; idx += blockDim.x) {
+        const int i = idx / (VS / VE), v0 = (idx - i * (VS / VE)) * VE;
+        uint4 vv = {0u, 0u, 0u, 0u};
+        if (i < cp.len) {
+          vv = *reinterpret_cast<const uint4*>(vp + (long)i * H * DV + c0 + v0);
+          ok &= finite16B<OP>(vv);
+        }
+#pragma unroll
+        for (int j = 0; j < VE; ++j) VbT[(v0 + j) * LT + i] = from_f<OP>(Bs[i] * to_f(elem16<OP>(vv, j)));
+      }
       __syncthreads();
-      Tiles<CH, VS, 2, 2> u;
-      u.zero();
-      u.template mma<OP, CH>(KRow<OP, LTT>{Tp}, kfun<OP>([&](int vv, int i) {
-                               return from_f<OP>(Bs[i] * to_f(Vs[i * LVS + vv]));
-                             }));
-      u.each([&](int r, int vv, float& x) { Ut[r * DV + c0 + vv] = x; });
+      Tiles<VS, CH, 4, 2> ut;
+      ut.zero();
+      ut.template mma<OP, CH>(KRow<OP, LT>{VbT}, KRow<OP, LTT>{Tp});
+#pragma unroll
+      for (int b = 0; b < ut.TN; ++b) {
+        const int r = ut.n0(b) + (l & 15), w0 = ut.m0(0) + (l >> 4) * 4;
+        *reinterpret_cast<float4*>(Ut + r * DV + c0 + w0) =
+            float4{ut.acc[0][b][0], ut.acc[0][b][1], ut.acc[0][b][2], ut.acc[0][b][3]};
+      }
       __syncthreads();
     }
   } else {
     // scalar-decay member: T = I, W = 0, U = V; only check v for non-finite values
-    const OP* vp = v + (cp.row0 * H + h) * DV;
-    for (int c0 = 0; c0 < DV; c0 += VS) {
-      ok &= load_rows<VS, LVS>(vp + c0, (long)H * DV, cp.len, Vs);
-      __syncthreads();
+    for (int idx = threadIdx.x; idx < CH * DV / VE; idx += blockDim.x) {
+      const int i = idx / (DV / VE), c = (idx - i * (DV / VE)) * VE;
+      if (i < cp.len) ok &= finite16B<OP>(*reinterpret_cast<const uint4*>(vp + (long)i * H * DV + c));
     }
-    ok &= load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
-  }
-  // Khat^T[d][r] = exp(G_last - G_r) k_r[d], the scan's A operand for the carry
-  __syncthreads();
-  if (threadIdx.x < CH) GBs[threadIdx.x] = expf(Gs[CH - 1] - Gs[threadIdx.x]);
-  __syncthreads();
-  OP* Kh = KhTg + tile * DK * CH;
-  constexpr int VE = 16 / (int)sizeof(OP);
-  for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
-    const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
-    OP vals[VE];
-#pragma unroll
-    for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(GBs[r0 + j] * to_f(Ks[(r0 + j) * LK + d]));
-    *reinterpret_cast<uint4*>(Kh + d * CH + r0) = pack16<OP>(vals);
   }
   const int bad = __syncthreads_or(!ok);
   if (threadIdx.x == 0) flag[tile] = bad;
 }
 
-// The forward inter-chunk scan.  Every operand except the carry arrives
-// pre-laid-out by the prep kernel (W row-major, Khat^T row-major, U in fp32), so
-// the A fragments of chunk c+1 are loaded from HBM/L2 straight into registers
-// while chunk c is computed; only h and U' pass through LDS (two barriers per
-// chunk).
+// The forward inter-chunk scan with the chunk output fused in.  Every operand
+// except the carry arrives pre-laid-out (W, P row-major, Khat^T, U in fp32, q
+// straight from the input), so the A fragments of chunk c+1 load from HBM/L2
+// into registers while chunk c is computed; only h and U' pass through LDS
+// (two barriers per chunk).
 template <int DK, int DV, int BV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __restrict__ v,
-                                                  const float* __restrict__ S0, const float* __restrict__ gcum,
-                                                  const OP* __restrict__ Wg, const OP* __restrict__ KhTg,
+__global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __restrict__ q,
+                                                  const OP* __restrict__ v, const float* __restrict__ S0,
+                                                  const float* __restrict__ gcum, const OP* __restrict__ Wg,
+                                                  const OP* __restrict__ KhTg, const OP* __restrict__ Pg,
                                                   const float* __restrict__ Ug, float* __restrict__ states,
-                                                  float* __restrict__ ST, OP* __restrict__ UpTg,
+                                                  float* __restrict__ ST, OP* __restrict__ o,
                                                   int* __restrict__ flag) {
   constexpr int NVT = DV / BV;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LU = CH + pad_of<OP>();
   constexpr bool PF = sizeof(OP) == 2;  // prefetch a chunk ahead (bf16 fragments are compact)
   typedef Tiles<DK, BV, 4, 1> HT;       // carried state slice h[:, v0:v0+BV]
-  typedef Tiles<CH, BV, 4, 1> UT;       // U' slice
+  typedef Tiles<CH, BV, 4, 1> UT;       // U' and output slices
   __shared__ __align__(16) OP hT[BV * LK];
   __shared__ __align__(16) OP UsT[BV * LU];
 
@@ -142,12 +206,17 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 
   struct Pre {
     typename UT::template AFr<OP, DK> w;
+    typename UT::template AFr<OP, DK> qf;
+    typename UT::template AFr<OP, CH> pf;
     typename HT::template AFr<OP, CH> kh;
     float u[UT::TN][4];
+    float gam[4];
     float gl;
   };
   auto load_pre = [&](Pre& p, int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
+    const long row0 = sp.row0 + (long)c * CH;
+    const int len = min(CH, sp.len - c * CH);
     if constexpr (VAR != VAR_DECAY) {
       p.w.load(KRow<OP, DK>{Wg + tile * CH * DK});
       const float* Ut = Ug + tile * CH * DV + v0;
@@ -156,8 +225,6 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
         for (int j = 0; j < 4; ++j) p.u[b][j] = Ut[(UT::m0(0) + (l >> 4) * 4 + j) * DV + UT::n0(b) + (l & 15)];
     } else {
-      const long row0 = sp.row0 + (long)c * CH;
-      const int len = min(CH, sp.len - c * CH);
       const OP* vp = v + (row0 * H + h) * DV + v0;
 #pragma unroll
       for (int b = 0; b < UT::TN; ++b)
@@ -167,8 +234,12 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
           p.u[b][j] = r < len ? to_f(vp[(long)r * H * DV + UT::n0(b) + (l & 15)]) : 0.f;
         }
     }
+    p.qf.load(KRowM<OP>{q + (row0 * H + h) * DK, (long)H * DK, len});
+    p.pf.load(KRow<OP, CH>{Pg + tile * CH * CH});
     p.kh.load(KRow<OP, CH>{KhTg + tile * DK * CH});
-    p.gl = expf(gcum[tile * CH + CH - 1]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) p.gam[j] = __expf(gcum[tile * CH + UT::m0(0) + (l >> 4) * 4 + j]);
+    p.gl = __expf(gcum[tile * CH + CH - 1]);
   };
 
   HT hs;
@@ -183,6 +254,8 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
   if (sp.nch > 0) load_pre(cur, 0);
   for (int c = 0; c < sp.nch; ++c) {
     const long tile = (long)(sp.c0 + c) * H + h;
+    const long row0 = sp.row0 + (long)c * CH;
+    const int len = min(CH, sp.len - c * CH);
     float* hp = states + tile * DK * DV;
     hs.each([&](int d, int vv, float& x) {
       hp[d * DV + v0 + vv] = x;
@@ -194,7 +267,9 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     } else if (c + 1 < sp.nch) {
       load_pre(nxt, c + 1);
     }
-    UT up;
+    UT up, ot;
+    ot.zero();
+    ot.template mma<OP, DK>(cur.qf, KRow<OP, LK>{hT});  // Q h
     if constexpr (VAR != VAR_DECAY) {
       up.zero();
       up.template mma<OP, DK>(cur.w, KRow<OP, LK>{hT});
@@ -208,21 +283,30 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
         for (int j = 0; j < 4; ++j) up.acc[0][b][j] = cur.u[b][j];
     }
-    OP* Upt = UpTg + tile * DV * CH;
 #pragma unroll
     for (int b = 0; b < UT::TN; ++b) {
       const int vv = UT::n0(b) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
+      OP u4[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const OP xo = from_f<OP>(up.acc[0][b][j]);
-        if (VAR != VAR_DECAY) Upt[(v0 + vv) * CH + r0 + j] = xo;
-        UsT[vv * LU + r0 + j] = xo;
+        u4[j] = from_f<OP>(up.acc[0][b][j]);
+        ot.acc[0][b][j] *= cur.gam[j];
       }
+      *reinterpret_cast<typename vec4_of<OP>::type*>(UsT + vv * LU + r0) = pack4<OP>(u4);
     }
     __syncthreads();
     const float gl = cur.gl;
     hs.each([&](int, int, float& x) { x *= gl; });
     hs.template mma<OP, CH>(cur.kh, KRow<OP, LU>{UsT});
+    ot.template mma<OP, CH>(cur.pf, KRow<OP, LU>{UsT});  // + P U'
+    OP* op = o + (row0 * H + h) * DV + v0;
+#pragma unroll
+    for (int b = 0; b < UT::TN; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = UT::m0(0) + (l >> 4) * 4 + j;
+        if (r < len) op[(long)r * H * DV + UT::n0(b) + (l & 15)] = from_f<OP>(ot.acc[0][b][j]);
+      }
     if (PF) cur = nxt;
   }
   float* STp = ST + ((long)n * H + h) * DK * DV;
@@ -231,81 +315,12 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
   if (threadIdx.x == 0) flag[(long)s * NVT + vt] = bad;
 }
 
-template <int DK, int DV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_out_fwd(Geo geo, int H, const OP* __restrict__ q,
-                                                 const OP* __restrict__ k, const OP* __restrict__ v,
-                                                 const float* __restrict__ gcum,
-                                                 const float* __restrict__ states,
-                                                 const OP* __restrict__ UpTg, OP* __restrict__ o,
-                                                 int* __restrict__ flag) {
-  constexpr int DVS = (sizeof(OP) == 2) ? (DV < 128 ? DV : 128) : 64;  // value columns per slice
-  constexpr int LK = DK + pad_of<OP>();
-  constexpr int LT = CH + pad_of<OP>();
-  constexpr int LH = DVS + pad_of<OP>();
-  __shared__ __align__(16) OP Qs[CH * LK];
-  __shared__ __align__(16) OP Ks[CH * LK];
-  __shared__ __align__(16) OP Hs[DK * LH];   // h[:, slice], row-major (d, v)
-  __shared__ __align__(16) OP Ps[CH * LT];
-  __shared__ __align__(16) OP UT[DVS * LT];  // U'^T slice (v, i); scalar decay: V slice (i, v)
-  static_assert(CH * LH <= DVS * LT, "V slice must fit the U' buffer");
-  __shared__ __align__(16) OP Os[CH * LH];
-  __shared__ float Gs[CH];
-
-  const int ci = blockIdx.x, h = blockIdx.y;
-  const ChunkPos cp = chunk_pos(geo, ci);
-  const long tile = (long)ci * H + h;
-  bool ok = load_rows<DK, LK>(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Qs);
-  load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
-  if (threadIdx.x < CH) Gs[threadIdx.x] = gcum[tile * CH + threadIdx.x];
-  __syncthreads();
-  {
-    Tiles<CH, CH, 2, 2> p;
-    p.zero();
-    p.template mma<OP, DK>(KRow<OP, LK>{Qs}, KRow<OP, LK>{Ks});
-    p.each([&](int r, int i, float& x) {
-      Ps[r * LT + i] = from_f<OP>(i <= r ? x * expf(Gs[r] - Gs[i]) : 0.f);
-    });
-  }
-  const float* hp = states + tile * DK * DV;
-  for (int c0 = 0; c0 < DV; c0 += DVS) {
-    for (int idx = threadIdx.x; idx < DK * DVS / 4; idx += blockDim.x) {
-      const int d = idx / (DVS / 4), c = (idx - d * (DVS / 4)) * 4;
-      const float4 x = *reinterpret_cast<const float4*>(hp + (long)d * DV + c0 + c);
-      Hs[d * LH + c + 0] = from_f<OP>(x.x);
-      Hs[d * LH + c + 1] = from_f<OP>(x.y);
-      Hs[d * LH + c + 2] = from_f<OP>(x.z);
-      Hs[d * LH + c + 3] = from_f<OP>(x.w);
-    }
-    if constexpr (VAR != VAR_DECAY) {
-      load_dense<DVS, CH, LT>(UpTg + tile * DV * CH + (long)c0 * CH, UT);
-    } else {
-      // V slice, row-major (i, v) with row stride LH; fits in UT (64*LH <= DVS*LT)
-      load_rows<DVS, LH>(v + (cp.row0 * H + h) * DV + c0, (long)H * DV, cp.len, UT);
-    }
-    __syncthreads();
-    Tiles<CH, DVS, 2, 2> ot;
-    ot.zero();
-    ot.template mma<OP, DK>(KRow<OP, LK>{Qs}, KCol<OP, LH>{Hs});
-    ot.each([&](int r, int, float& x) { x *= expf(Gs[r]); });
-    if constexpr (VAR != VAR_DECAY)
-      ot.template mma<OP, CH>(KRow<OP, LT>{Ps}, KRow<OP, LT>{UT});
-    else
-      ot.template mma<OP, CH>(KRow<OP, LT>{Ps}, KCol<OP, LH>{UT});
-    ot.each([&](int r, int vv, float& x) { Os[r * LH + vv] = from_f<OP>(x); });
-    __syncthreads();
-    store_rows<DVS, LH>(o + (cp.row0 * H + h) * DV + c0, (long)H * DV, cp.len, Os);
-    __syncthreads();
-  }
-  const int bad = __syncthreads_or(!ok);
-  if (threadIdx.x == 0) flag[tile] = bad;
-}
-
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 template <int DK, int DV, typename OP, int VAR>
 static hipError_t launch_fwd_t(const FwdArgs& a) {
-  constexpr int BV = 32;
+  constexpr int BV = SCAN_BV;
   constexpr int NVT = DV / BV;
   const Geo& geo = a.geo;
   const int H = geo.H;
@@ -316,29 +331,24 @@ static hipError_t launch_fwd_t(const FwdArgs& a) {
     if (e != hipSuccess) return e;
   }
   if (geo.total_chunks > 0) {
-    hipLaunchKernelGGL((k_prep_fwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
-                       geo, H, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, w.gcum, (OP*)w.W, w.U,
-                       (OP*)w.KhT, w.flag_prep);
+    hipLaunchKernelGGL((k_prep_fwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
+                       geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, w.gcum,
+                       (OP*)w.W, w.U, (OP*)w.KhT, (OP*)w.P, w.flag_prep);
   }
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
-                       (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, (const OP*)w.KhT, w.U, a.states,
-                       a.ST, (OP*)w.UpT, w.flag_scan);
+                       (const OP*)a.q, (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, (const OP*)w.KhT,
+                       (const OP*)w.P, w.U, a.states, a.ST, (OP*)a.o, w.flag_scan);
   }
   stage_mark(a.events, 2, a.stream);
-  if (geo.total_chunks > 0) {
-    hipLaunchKernelGGL((k_out_fwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(256), 0, a.stream,
-                       geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, w.gcum, a.states,
-                       (const OP*)w.UpT, (OP*)a.o, w.flag_out);
-  }
-  stage_mark(a.events, 3, a.stream);
   if (NS > 0) {
     hipLaunchKernelGGL((k_exact_fwd<DK, DV, OP, VAR>), dim3(NS), dim3(DV), 0, a.stream, geo, (const OP*)a.q,
                        (const OP*)a.k, (const OP*)a.v, a.g, a.beta, a.S0, (OP*)a.o, a.ST, a.states,
-                       w.flag_prep, w.flag_out, w.flag_scan, NVT);
+                       w.flag_prep, w.flag_prep, w.flag_scan, NVT);
   }
+  stage_mark(a.events, 3, a.stream);  // the chunk output is fused into the scan: stage 3 is empty
   stage_mark(a.events, 4, a.stream);
   return hipGetLastError();
 }

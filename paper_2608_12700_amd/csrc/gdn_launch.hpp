@@ -11,14 +11,13 @@ namespace gdn {
 // Forward workspace regions (device pointers into the caller's workspace).
 struct FwdWs {
   int* chunk_off;  // [N+1] packed layout only
-  int* flag_prep;  // [chunks*H]   non-finite k, v, g, beta in the chunk
-  int* flag_out;   // [chunks*H]   non-finite q in the chunk
+  int* flag_prep;  // [chunks*H]   non-finite q, k, v, g, beta in the chunk
   int* flag_scan;  // [N*H*NVT]    non-finite S0 slice
   float* gcum;     // [chunks*H*64] in-chunk cumulative log-decay
   void* W;         // [chunks*H*64*dk] operand dtype
   float* U;        // [chunks*H*64*dv]
-  void* UpT;       // [chunks*H*dv*64] operand dtype, U' transposed
   void* KhT;       // [chunks*H*dk*64] operand dtype, (e^{G_last-G} K)^T
+  void* P;         // [chunks*H*64*64] operand dtype, (Q K^T) * D
   float* exact;    // exact-path scratch
 };
 
@@ -44,7 +43,7 @@ struct BwdWs {
   void* W;         // [chunks*H*dk*64] operand dtype, W^T
   void* QgT;       // [chunks*H*dk*64] operand dtype, (diag(e^G) Q)^T
   void* dOT;       // [chunks*H*dv*64] operand dtype, dO^T
-  float* dvl;      // [chunks*H*64*dv] P^T dO
+  void* PT;        // [chunks*H*64*64] operand dtype, P^T
   void* dh;        // [chunks*H*dk*dv] operand dtype: state gradient after each chunk
   void* dUT;       // [chunks*H*dv*64] operand dtype: dU' of each chunk, transposed
   void* grad_scratch;  // [chunks*H*grad_region_bytes] fp32 operands only

@@ -49,7 +49,7 @@ class Problem(ctypes.Structure):
 EXPORTED = ("gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_fwd",
             "gdn_bwd", "gdn_fwd_ex", "gdn_bwd_ex", "gdn_status_str", "gdn_version")
 NUM_STAGES = 4
-FWD_STAGES = ("fwd_prep", "fwd_scan", "fwd_out", "fwd_exact")
+FWD_STAGES = ("fwd_prep", "fwd_scan", "fwd_exact", None)  # the output is fused into the scan
 BWD_STAGES = ("bwd_prep", "bwd_scan", "bwd_grad", "bwd_exact")
 
 _lib = None

@@ -57,7 +57,6 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   __shared__ __align__(16) char r2[R2];
   __shared__ __align__(16) OP KbT[DT_ ? DK * LT : 1];  // (diag(beta e^G) K)^T
   __shared__ __align__(16) char r4[R4];
-  __shared__ __align__(16) float Xs[4 * 16 * 20];
   __shared__ float Gs[CH], Bs[CH], Gam[CH];
   OP* Qs = reinterpret_cast<OP*>(r1);
   float* Tf = reinterpret_cast<float*>(r1);
@@ -124,7 +123,7 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
       for (int j = 0; j < VE; ++j) KbT[(d0 + j) * LT + i] = from_f<OP>(sc * to_f(elem16<OP>(kv, j)));
     }
     __syncthreads();
-    unit_lower_inverse<OP, LC, LT>(As, Tf, Ts, Xs);  // Tf over Q, Ts over K: both are dead here
+    unit_lower_inverse<OP, LC, LT, false>(As, Tf, Ts, (OP*)nullptr);  // Tf over Q, Ts over K: both are dead here
     const OP* Tp;
     if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
     constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
@@ -357,7 +356,6 @@ __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __re
   OP* Qs = reinterpret_cast<OP*>(ub);
   float* As = reinterpret_cast<float*>(ub + CH * LK * sizeof(OP));
   float* Tf = BF ? As + CH * LC : reinterpret_cast<float*>(Ts);
-  float* Xs = As + CH * LC * (BF ? 2 : 1);
   bool ok = load_gates<VAR>(g, beta, cp.row0, H, h, cp.len, Gs, Bs);
   load_rows<DK, LK>(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Qs);
   load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
@@ -387,7 +385,7 @@ __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __re
       As[r * LC + i] = Bs[r] * ae;
     });
     __syncthreads();
-    unit_lower_inverse<OP, LC, LT>(As, Tf, Ts, Xs);
+    unit_lower_inverse<OP, LC, LT, false>(As, Tf, Ts, (OP*)nullptr);
     for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
       const int r = idx >> 6, c = idx & 63;
       TT[c * LT + r] = Ts[r * LT + c];
@@ -522,8 +520,7 @@ __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __re
     const OP* qp = q + (cp.row0 * H + h) * DK;
     for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
       const int r = idx / (DK / VE), c = (idx - r * (DK / VE)) * VE;
-      const uint4 z = {0u, 0u, 0u, 0u};
-      const uint4 qv = r < cp.len ? *reinterpret_cast<const uint4*>(qp + (long)r * H * DK + c) : z;
+        const uint4 qv = keep16(r < cp.len, *reinterpret_cast<const uint4*>(qp + (long)clamp_row(r, cp.len) * H * DK + c));
       const uint4 kv = *reinterpret_cast<const uint4*>(Ks + r * LK + c);
 #pragma unroll
       for (int j = 0; j < VE; ++j) {
@@ -682,6 +679,531 @@ __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __re
 }
 
 // ---------------------------------------------------------------------------
+// Chunk gradients for bf16 operands.  One block of 8 waves per (chunk, head);
+// the value dimension is covered in slices of up to 128 columns (one slice for
+// d_v <= 128).  Compared with the generic kernel above:
+//   * the solve's VJP is taken in its short form: with U' = T R and
+//     Y = T^T dU', the gradient of A = diag(beta)(K K^T * E) is -Y U'^T
+//     (strict lower part), so no dT and no 64^3 products are needed;
+//   * every operand that is already laid out for a fragment load in HBM (the
+//     chunk state h in both orientations, dh, dU'^T, v) goes straight from
+//     global memory into registers, issued at kernel entry or one step ahead,
+//     instead of through LDS transposes;
+//   * the decay mask D (E is its strict lower part) is formed once and kept
+//     in registers next to P and A for the phase that needs it again.
+// ---------------------------------------------------------------------------
+template <int DK, int DV>
+struct GradBF {
+  static constexpr int VS = DV > 128 ? 128 : DV;
+  static constexpr int LK = DK + 8, LT = CH + 8, LC = CH + 4, LV = VS + 8;
+  static constexpr int WNk = DK / 16, WMk = 8 / WNk;
+  static constexpr int WNv = VS / 16, WMv = 8 / WNv;
+  typedef Tiles<CH, DK, WMk, WNk> TK;  // 64 x dk results: X, dQ, dK
+  typedef Tiles<VS, CH, WNv, WMv> TY;  // Y^T and U'^T
+  typedef Tiles<CH, CH, 4, 2> TC;      // P, A, dP, dA
+  static constexpr int PH0 = CH * LK * 2 + 2 * CH * LC * 4;
+  static constexpr int PH1 = (VS * LT + 3 * CH * LV) * 2;
+  static constexpr int PH2 = (2 * DK * LT + 3 * CH * LT) * 2;
+  static constexpr int UB = PH0 > PH1 ? (PH0 > PH2 ? PH0 : PH2) : (PH1 > PH2 ? PH1 : PH2);
+  static_assert(2 * CH * LK * 2 <= 2 * DK * LT * 2, "dq/dk staging fits where Q^T, K^T were");
+};
+
+__device__ __forceinline__ bf16x8 cvt8(const float (&x)[8]) {
+  bf16x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = from_f<bf16>(x[j]);
+  return r;
+}
+
+template <int DK, int DV, int VAR>
+__global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __restrict__ q,
+                                                 const bf16* __restrict__ k, const bf16* __restrict__ v,
+                                                 const float* __restrict__ g, const float* __restrict__ beta,
+                                                 const float* __restrict__ states, const bf16* __restrict__ dO,
+                                                 const bf16* __restrict__ dhg, const bf16* __restrict__ dUTg,
+                                                 bf16* __restrict__ dq, bf16* __restrict__ dk,
+                                                 bf16* __restrict__ dvo, float* __restrict__ dg,
+                                                 float* __restrict__ dbeta, int* __restrict__ flag) {
+  typedef GradBF<DK, DV> C;
+  typedef typename C::TK TK;
+  typedef typename C::TY TY;
+  typedef typename C::TC TC;
+  typedef Mma<bf16> M;
+  constexpr bool DT_ = VAR != VAR_DECAY;
+  constexpr int VS = C::VS, LK = C::LK, LT = C::LT, LC = C::LC, LV = C::LV;
+  constexpr int NDO = CH * VS / 8 / 512;  // 16-byte pieces of a dO slice per thread
+
+  __shared__ __align__(16) bf16 Ks[CH * LK];
+  __shared__ __align__(16) bf16 Ts[DT_ ? CH * LT : 1];
+  __shared__ __align__(16) bf16 TT[CH * LT];  // T^T (the identity for the scalar-decay member)
+  __shared__ __align__(16) float Gs[CH];
+  __shared__ __align__(16) float Gam[CH];
+  __shared__ __align__(16) float Bs[CH];
+  __shared__ __align__(16) float Dte[CH];
+  __shared__ float rowZ[2][CH], colZ[4][CH], rowA[2][CH];
+  __shared__ float rqp[C::WNk][CH], rxp[C::WNk][CH], rkp[C::WNk][CH], dbYp[C::WNv][CH];
+  __shared__ float hdh_w[8];
+  __shared__ __align__(16) char ub[C::UB];
+
+  const int ci = blockIdx.x, h = blockIdx.y;
+  const ChunkPos cp = chunk_pos(geo, ci);
+  const long tile = (long)ci * H + h;
+  const int w = wave_id(), l = lane_id();
+  const int len = cp.len;
+  const bf16* qp = q + (cp.row0 * H + h) * DK;
+  const bf16* kp = k + (cp.row0 * H + h) * DK;
+  const bf16* vp = v + (cp.row0 * H + h) * DV;
+  const bf16* dop = dO + (cp.row0 * H + h) * DV;
+  bf16* dvp = dvo + (cp.row0 * H + h) * DV;
+  const float* hp = states + tile * DK * DV;
+  const bf16* dhp = dhg + tile * DK * DV;
+  const bf16* dUp = dUTg + tile * DV * CH;
+  const long rsv = (long)H * DV;
+
+  // ---- operands of one value slice, loaded ahead of their use
+  struct PreA {
+    uint4 dov[NDO];                      // dO slice, staged to LDS
+    bf16x8 du[CH / 32][TY::TM];          // dU'^T rows: A fragments of Y^T
+    float hk[DK / 32][TY::TM][8];        // h^T: A fragments of (K h)^T
+    uint2 vb[TY::TM][TY::TN];            // v[r][v0..v0+3] in the Y^T accumulator layout
+  };
+  struct PreB {
+    float hx[VS / 32][TK::TN][8];        // h: B fragments of X and dQ
+    bf16x8 dh[VS / 32][TK::TN];          // dh: B fragments of dK
+  };
+  bool ok = true;
+  auto load_a = [&](PreA& p, int c0) {
+#pragma unroll
+    for (int t = 0; t < NDO; ++t) {
+      const int idx = threadIdx.x + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
+      p.dov[t] = keep16(r < len, *reinterpret_cast<const uint4*>(dop + clamp_row(r, len) * rsv + c0 + c));
+    }
+#pragma unroll
+    for (int s = 0; s < CH / 32; ++s)
+#pragma unroll
+      for (int a = 0; a < TY::TM; ++a) p.du[s][a] = M::load(KRow<bf16, CH>{dUp + (long)c0 * CH}, TY::m0(a), 32 * s);
+    if constexpr (DT_) {
+#pragma unroll
+      for (int s = 0; s < DK / 32; ++s)
+#pragma unroll
+        for (int a = 0; a < TY::TM; ++a)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            p.hk[s][a][j] = hp[(32 * s + 8 * (l >> 4) + j) * DV + c0 + TY::m0(a) + (l & 15)];
+#pragma unroll
+      for (int a = 0; a < TY::TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TY::TN; ++b) {
+          const int r = TY::n0(b) + (l & 15);
+          p.vb[a][b] =
+              keep8(r < len, *reinterpret_cast<const uint2*>(vp + clamp_row(r, len) * rsv + c0 + TY::m0(a) + 4 * (l >> 4)));
+        }
+    }
+  };
+  auto load_b = [&](PreB& p, int c0) {
+#pragma unroll
+    for (int s = 0; s < VS / 32; ++s)
+#pragma unroll
+      for (int b = 0; b < TK::TN; ++b) {
+        const float* src = hp + (TK::n0(b) + (l & 15)) * DV + c0 + 32 * s + 8 * (l >> 4);
+        const float4 x0 = *reinterpret_cast<const float4*>(src);
+        const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
+        p.hx[s][b][0] = x0.x; p.hx[s][b][1] = x0.y; p.hx[s][b][2] = x0.z; p.hx[s][b][3] = x0.w;
+        p.hx[s][b][4] = x1.x; p.hx[s][b][5] = x1.y; p.hx[s][b][6] = x1.z; p.hx[s][b][7] = x1.w;
+        p.dh[s][b] = M::load(KRow<bf16, DV>{dhp + c0}, TK::n0(b), 32 * s);
+      }
+  };
+
+  // ================= phase 0: gates, P, A, T
+  bf16* Qs = reinterpret_cast<bf16*>(ub);
+  float* As = reinterpret_cast<float*>(ub + CH * LK * 2);
+  float* Tf = As + CH * LC;
+  uint4 qk[2][CH * DK / 8 / 512];
+#pragma unroll
+  for (int t = 0; t < CH * DK / 8 / 512; ++t) {
+    const int idx = threadIdx.x + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
+    const long ro = clamp_row(r, len) * (long)H * DK + c;
+    qk[0][t] = keep16(r < len, *reinterpret_cast<const uint4*>(qp + ro));
+    qk[1][t] = keep16(r < len, *reinterpret_cast<const uint4*>(kp + ro));
+  }
+  ok &= load_gates<VAR>(g, beta, cp.row0, H, h, len, Gs, Bs);
+  PreA pa;
+  load_a(pa, 0);
+#pragma unroll
+  for (int t = 0; t < CH * DK / 8 / 512; ++t) {
+    const int idx = threadIdx.x + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
+    *reinterpret_cast<uint4*>(Qs + r * LK + c) = qk[0][t];
+    *reinterpret_cast<uint4*>(Ks + r * LK + c) = qk[1][t];
+  }
+  __syncthreads();
+  if (threadIdx.x < CH) {
+    const int r = threadIdx.x;
+    Gam[r] = __expf(Gs[r]);
+    Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
+  }
+  TC pm, ae;  // P = (Q K^T) * D and (K K^T) * E, kept for phase 2
+  float dd[TC::TN][4];  // D_ri = e^{G_r - G_i} for i <= r, else 0
+  pm.zero();
+  pm.template mma<bf16, DK>(KRow<bf16, LK>{Qs}, KRow<bf16, LK>{Ks});
+#pragma unroll
+  for (int b = 0; b < TC::TN; ++b)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = TC::m0(0) + 4 * (l >> 4) + j, i = TC::n0(b) + (l & 15);
+      dd[b][j] = i <= r ? __expf(Gs[r] - Gs[i]) : 0.f;
+      pm.acc[0][b][j] *= dd[b][j];
+    }
+  if constexpr (DT_) {
+    ae.zero();
+    ae.template mma<bf16, DK>(KRow<bf16, LK>{Ks}, KRow<bf16, LK>{Ks});
+#pragma unroll
+    for (int b = 0; b < TC::TN; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = TC::m0(0) + 4 * (l >> 4) + j, i = TC::n0(b) + (l & 15);
+        const float x = i < r ? ae.acc[0][b][j] * dd[b][j] : 0.f;
+        ae.acc[0][b][j] = x;
+        As[r * LC + i] = Bs[r] * x;
+      }
+    __syncthreads();
+    unit_lower_inverse<bf16, LC, LT, true>(As, Tf, Ts, TT);
+  } else {
+    for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
+      const int r = idx >> 6, c = idx & 63;
+      TT[r * LT + c] = from_f<bf16>(r == c ? 1.f : 0.f);
+    }
+  }
+  __syncthreads();
+
+  // ================= phase 1: value slices
+  bf16* RT = reinterpret_cast<bf16*>(ub);
+  bf16* Ys = RT + VS * LT;
+  bf16* Ups = Ys + CH * LV;
+  bf16* dOs = Ups + CH * LV;
+  TC dA, dP;
+  TK X, dQa, dKh;
+  dA.zero(); dP.zero(); X.zero(); dQa.zero(); dKh.zero();
+  float dbY[TY::TN];
+#pragma unroll
+  for (int b = 0; b < TY::TN; ++b) dbY[b] = 0.f;
+  float hdh = 0.f;
+
+  for (int c0 = 0; c0 < DV; c0 += VS) {
+    if (c0 > 0) {
+      __syncthreads();  // the previous slice's LDS operands are consumed
+      load_a(pa, c0);
+    }
+    PreB pb;
+    if constexpr (DT_) {
+      // R = diag(beta) (V - diag(e^G) K h), computed transposed, (K h)^T = h^T K^T,
+      // so that a lane needs v[r][v0..v0+3] as one 8-byte piece (the same
+      // piece the dbeta term uses) and writes R^T rows directly
+      TY kht;
+      kht.zero();
+#pragma unroll
+      for (int s = 0; s < DK / 32; ++s) {
+        bf16x8 fa[TY::TM];
+#pragma unroll
+        for (int a = 0; a < TY::TM; ++a) fa[a] = cvt8(pa.hk[s][a]);
+#pragma unroll
+        for (int b = 0; b < TY::TN; ++b) {
+          const bf16x8 fb = M::load(KRow<bf16, LK>{Ks}, TY::n0(b), 32 * s);
+#pragma unroll
+          for (int a = 0; a < TY::TM; ++a) kht.acc[a][b] = M::mma(fa[a], fb, kht.acc[a][b]);
+        }
+      }
+      load_b(pb, c0);
+#pragma unroll
+      for (int b = 0; b < TY::TN; ++b) {
+        const int r = TY::n0(b) + (l & 15);
+        const float br = Bs[r], gr = Gam[r];
+#pragma unroll
+        for (int a = 0; a < TY::TM; ++a) {
+          const int v0 = TY::m0(a) + 4 * (l >> 4);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float vx = to_f(elem4<bf16>(pa.vb[a][b], j));
+            ok &= finite_f(vx);
+            RT[(v0 + j) * LT + r] = from_f<bf16>(br * (vx - gr * kht.acc[a][b][j]));
+          }
+        }
+      }
+    } else {
+      load_b(pb, c0);
+    }
+    // Y^T = dU'^T T, so Y = T^T dU'.  dV = diag(beta) Y; keep -Y for dA and X
+    {
+      TY yt;
+      yt.zero();
+#pragma unroll
+      for (int s = 0; s < CH / 32; ++s) {
+        bf16x8 fb[TY::TN];
+#pragma unroll
+        for (int b = 0; b < TY::TN; ++b) fb[b] = M::load(KRow<bf16, LT>{TT}, TY::n0(b), 32 * s);
+#pragma unroll
+        for (int a = 0; a < TY::TM; ++a)
+#pragma unroll
+          for (int b = 0; b < TY::TN; ++b) yt.acc[a][b] = M::mma(pa.du[s][a], fb[b], yt.acc[a][b]);
+      }
+#pragma unroll
+      for (int b = 0; b < TY::TN; ++b) {
+        const int r = TY::n0(b) + (l & 15);
+        const float br = DT_ ? Bs[r] : 1.f;
+#pragma unroll
+        for (int a = 0; a < TY::TM; ++a) {
+          const int v0 = TY::m0(a) + 4 * (l >> 4);
+          bf16 d4[4], y4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float y = yt.acc[a][b][j];
+            d4[j] = from_f<bf16>(br * y);
+            y4[j] = from_f<bf16>(-y);
+            if (DT_) dbY[b] += to_f(elem4<bf16>(pa.vb[a][b], j)) * y;
+          }
+          if (r < len) *reinterpret_cast<uint2*>(dvp + r * rsv + c0 + v0) = pack4<bf16>(d4);
+          if (DT_) *reinterpret_cast<uint2*>(Ys + r * LV + v0) = pack4<bf16>(y4);
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < NDO; ++t) {
+      const int idx = threadIdx.x + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
+      *reinterpret_cast<uint4*>(dOs + r * LV + c) = pa.dov[t];
+    }
+    if constexpr (!DT_) {
+      // the scalar-decay member has U' = V
+      for (int idx = threadIdx.x; idx < CH * VS / 8; idx += blockDim.x) {
+        const int r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
+        const uint4 u = keep16(r < len, *reinterpret_cast<const uint4*>(vp + clamp_row(r, len) * rsv + c0 + c));
+        ok &= finite16B<bf16>(u);
+        *reinterpret_cast<uint4*>(Ups + r * LV + c) = u;
+      }
+    }
+    __syncthreads();
+    if constexpr (DT_) {
+      // U'^T = R^T T^T
+      TY ut;
+      ut.zero();
+      ut.template mma<bf16, CH>(KRow<bf16, LT>{RT}, KRow<bf16, LT>{Ts});
+#pragma unroll
+      for (int a = 0; a < TY::TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TY::TN; ++b) {
+          bf16 u4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) u4[j] = from_f<bf16>(ut.acc[a][b][j]);
+          *reinterpret_cast<uint2*>(Ups + (TY::n0(b) + (l & 15)) * LV + TY::m0(a) + 4 * (l >> 4)) =
+              pack4<bf16>(u4);
+        }
+      __syncthreads();
+      dA.template mma<bf16, VS>(KRow<bf16, LV>{Ys}, KRow<bf16, LV>{Ups});  // -Y U'^T
+    }
+    dP.template mma<bf16, VS>(KRow<bf16, LV>{dOs}, KRow<bf16, LV>{Ups});
+#pragma unroll
+    for (int s = 0; s < VS / 32; ++s) {
+      bf16x8 fh[TK::TN];
+#pragma unroll
+      for (int b = 0; b < TK::TN; ++b) {
+        fh[b] = cvt8(pb.hx[s][b]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) ok &= finite_f(pb.hx[s][b][j]);
+        if (TK::m0(0) == 0) {  // one wave row adds <h, dh> for its columns
+#pragma unroll
+          for (int j = 0; j < 8; ++j) hdh += pb.hx[s][b][j] * to_f(pb.dh[s][b][j]);
+        }
+      }
+#pragma unroll
+      for (int a = 0; a < TK::TM; ++a) {
+        const bf16x8 fo = M::load(KRow<bf16, LV>{dOs}, TK::m0(a), 32 * s);
+        const bf16x8 fu = M::load(KRow<bf16, LV>{Ups}, TK::m0(a), 32 * s);
+#pragma unroll
+        for (int b = 0; b < TK::TN; ++b) {
+          dQa.acc[a][b] = M::mma(fo, fh[b], dQa.acc[a][b]);
+          dKh.acc[a][b] = M::mma(fu, pb.dh[s][b], dKh.acc[a][b]);
+        }
+        if constexpr (DT_) {
+          const bf16x8 fy = M::load(KRow<bf16, LV>{Ys}, TK::m0(a), 32 * s);
+#pragma unroll
+          for (int b = 0; b < TK::TN; ++b) X.acc[a][b] = M::mma(fy, fh[b], X.acc[a][b]);
+        }
+      }
+    }
+  }
+
+  hdh = wave_sum(hdh);
+  if (l == 0) hdh_w[w] = hdh;
+  if constexpr (DT_) {
+    // dbeta partial v_r . Y_r: over the 4 lane groups, then one partial per wave row of Y^T
+#pragma unroll
+    for (int b = 0; b < TY::TN; ++b) {
+      const float s = sum_groups(dbY[b]);
+      if ((l >> 4) == 0) dbYp[w / C::WMv][TY::n0(b) + (l & 15)] = s;
+    }
+  }
+  __syncthreads();  // phase-1 LDS operands are consumed
+
+  // ================= phase 2: the chunk-level gradients
+  bf16* QT = reinterpret_cast<bf16*>(ub);
+  bf16* KT = QT + DK * LT;
+  bf16* dPs = KT + DK * LT;
+  bf16* dPmT = dPs + CH * LT;
+  bf16* SdT = dPmT + CH * LT;  // dB + dB^T, dB = dA * beta_r * E
+  for (int idx = threadIdx.x; idx < CH * DK / 8; idx += blockDim.x) {
+    const int r = idx & 63, c = (idx >> 6) * 8;  // lanes walk rows: conflict-free transposed writes
+    const uint4 qv = keep16(r < len, *reinterpret_cast<const uint4*>(qp + clamp_row(r, len) * (long)H * DK + c));
+    const uint4 kv = *reinterpret_cast<const uint4*>(Ks + r * LK + c);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      QT[(c + j) * LT + r] = elem16<bf16>(qv, j);
+      KT[(c + j) * LT + r] = elem16<bf16>(kv, j);
+    }
+  }
+  TC zs;  // Z = dA * A + dP * P
+  float rowA_l[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int b = 0; b < TC::TN; ++b) {
+    const int i = TC::n0(b) + (l & 15), r0 = TC::m0(0) + 4 * (l >> 4);
+    bf16 pt4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = r0 + j;
+      const float dpm = dP.acc[0][b][j] * dd[b][j];
+      dPs[r * LT + i] = from_f<bf16>(dpm);
+      pt4[j] = from_f<bf16>(dpm);
+      float z = dP.acc[0][b][j] * pm.acc[0][b][j];
+      if constexpr (DT_) {
+        // dB = dA * beta_r * E (strict lower); SdT = dB + dB^T, each entry
+        // written by exactly one lane: the owner of the lower-triangle element
+        const float da = i < r ? dA.acc[0][b][j] : 0.f;
+        z += da * Bs[r] * ae.acc[0][b][j];
+        rowA_l[j] += da * ae.acc[0][b][j];
+        if (i < r) {
+          const bf16 sd = from_f<bf16>(da * Bs[r] * dd[b][j]);
+          SdT[r * LT + i] = sd;
+          SdT[i * LT + r] = sd;
+        } else if (i == r) {
+          SdT[r * LT + r] = from_f<bf16>(0.f);
+        }
+      }
+      zs.acc[0][b][j] = z;
+    }
+    *reinterpret_cast<uint2*>(dPmT + i * LT + r0) = pack4<bf16>(pt4);
+  }
+  {
+    const int wm = w / 2, wn = w % 2;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float rs = sum16(zs.acc[0][0][j] + zs.acc[0][1][j]);
+      const float ra = sum16(rowA_l[j]);
+      const int r = TC::m0(0) + 4 * (l >> 4) + j;
+      if ((l & 15) == 0) {
+        rowZ[wn][r] = rs;
+        rowA[wn][r] = ra;
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < TC::TN; ++b) {
+      float cs = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cs += zs.acc[0][b][j];
+      cs = sum_groups(cs);
+      if ((l >> 4) == 0) colZ[wm][TC::n0(b) + (l & 15)] = cs;
+    }
+  }
+  __syncthreads();
+
+  // row sums q_r . (dO h^T)_r, k_r . X_r, k_r . (U' dh^T)_r, then the scalings
+  {
+    const int wn = w % C::WNk;
+#pragma unroll
+    for (int a = 0; a < TK::TM; ++a) {
+      const int r0 = TK::m0(a) + 4 * (l >> 4);
+      float rq[4] = {0.f, 0.f, 0.f, 0.f}, rx[4] = {0.f, 0.f, 0.f, 0.f}, rk[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int b = 0; b < TK::TN; ++b) {
+        const int d = TK::n0(b) + (l & 15);
+        const uint2 q4 = *reinterpret_cast<const uint2*>(QT + d * LT + r0);
+        const uint2 k4 = *reinterpret_cast<const uint2*>(KT + d * LT + r0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float qv = to_f(elem4<bf16>(q4, j)), kv = to_f(elem4<bf16>(k4, j));
+          rq[j] += qv * dQa.acc[a][b][j];
+          rx[j] += kv * X.acc[a][b][j];
+          rk[j] += kv * dKh.acc[a][b][j];
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        rq[j] = sum16(rq[j]);
+        rx[j] = sum16(rx[j]);
+        rk[j] = sum16(rk[j]);
+        if ((l & 15) == 0) {
+          rqp[wn][r0 + j] = rq[j];
+          rxp[wn][r0 + j] = rx[j];
+          rkp[wn][r0 + j] = rk[j];
+        }
+      }
+      const float4 g4 = *reinterpret_cast<const float4*>(Gam + r0);
+      const float4 e4 = *reinterpret_cast<const float4*>(Dte + r0);
+      const float4 b4 = *reinterpret_cast<const float4*>(Bs + r0);
+      const float gg[4] = {g4.x, g4.y, g4.z, g4.w}, ee[4] = {e4.x, e4.y, e4.z, e4.w};
+      const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+      for (int b = 0; b < TK::TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          dQa.acc[a][b][j] *= gg[j];
+          dKh.acc[a][b][j] = ee[j] * dKh.acc[a][b][j] + (DT_ ? bb[j] * gg[j] * X.acc[a][b][j] : 0.f);
+        }
+    }
+  }
+  dQa.template mma<bf16, CH>(KRow<bf16, LT>{dPs}, KRow<bf16, LT>{KT});
+  dKh.template mma<bf16, CH>(KRow<bf16, LT>{dPmT}, KRow<bf16, LT>{QT});
+  if constexpr (DT_) dKh.template mma<bf16, CH>(KRow<bf16, LT>{SdT}, KRow<bf16, LT>{KT});
+  __syncthreads();
+  bf16* dqst = QT;
+  bf16* dkst = QT + CH * LK;
+  dQa.each([&](int r, int d, float& x) { dqst[r * LK + d] = from_f<bf16>(x); });
+  dKh.each([&](int r, int d, float& x) { dkst[r * LK + d] = from_f<bf16>(x); });
+  if (w == 0) {
+    const int r = l;
+    float rq = 0.f, rx = 0.f, rk = 0.f;
+#pragma unroll
+    for (int i = 0; i < C::WNk; ++i) {
+      rq += rqp[i][r];
+      rx += rxp[i][r];
+      rk += rkp[i][r];
+    }
+    float dbv = 0.f;
+#pragma unroll
+    for (int i = 0; i < C::WNv; ++i) dbv += dbYp[i][r];
+    const float kk_r = Dte[r] * rk;  // khat_r . dkhat_r
+    float x = (rowZ[0][r] + rowZ[1][r]) - (((colZ[0][r] + colZ[1][r]) + colZ[2][r]) + colZ[3][r]);
+    x += Gam[r] * (rq + Bs[r] * rx);
+    x -= kk_r;
+    const float db = (rowA[0][r] + rowA[1][r]) + Gam[r] * rx + dbv;
+    const float kk = wave_sum(kk_r);
+    float hd = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) hd += hdh_w[i];
+    if (l == CH - 1) x += Gam[CH - 1] * hd + kk;
+    const float rev = __shfl(x, CH - 1 - l, WAVE);
+    const float sc = wave_incl_scan(rev);
+    const float dgv = __shfl(sc, CH - 1 - l, WAVE);
+    if (l < len) {
+      const long o = (cp.row0 + l) * H + h;
+      if (VAR != VAR_DELTA) dg[o] = dgv;
+      if (DT_) dbeta[o] = db;
+    }
+  }
+  __syncthreads();
+  store_rows<DK, LK>(dq + (cp.row0 * H + h) * DK, (long)H * DK, len, dqst);
+  store_rows<DK, LK>(dk + (cp.row0 * H + h) * DK, (long)H * DK, len, dkst);
+  const int bad = __syncthreads_or(!ok);
+  if (threadIdx.x == 0) flag[tile] = bad;
+}
+
+// ---------------------------------------------------------------------------
 template <int DK, int DV, typename OP, int VAR>
 static hipError_t launch_bwd_t(const BwdArgs& a) {
   constexpr int BV = SCAN_BV;
@@ -707,7 +1229,12 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
                        (const OP*)w.PT, (OP*)w.dh, (OP*)w.dUT, a.dS0, w.flag_scan);
   }
   stage_mark(a.events, 2, a.stream);
-  if (geo.total_chunks > 0) {
+  if (geo.total_chunks > 0 && sizeof(OP) == 2) {
+    hipLaunchKernelGGL((k_grad_bf<DK, DV, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
+                       (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, a.g, a.beta, a.states,
+                       (const bf16*)a.dO, (const bf16*)w.dh, (const bf16*)w.dUT, (bf16*)a.dq, (bf16*)a.dk_,
+                       (bf16*)a.dv_, a.dg, a.dbeta, w.flag_grad);
+  } else if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_grad_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, a.states,
                        (const OP*)a.dO, (const OP*)w.dh, (const OP*)w.dUT, (OP*)a.dq, (OP*)a.dk_, (OP*)a.dv_,

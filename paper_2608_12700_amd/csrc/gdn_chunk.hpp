@@ -84,11 +84,8 @@ __device__ __forceinline__ bool load_rows(const T* __restrict__ src, long rs, in
   bool ok = true;
   for (int idx = threadIdx.x; idx < CH * PER_ROW; idx += blockDim.x) {
     const int r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
-    uint4 u = {0u, 0u, 0u, 0u};
-    if (r < len) {
-      u = *reinterpret_cast<const uint4*>(src + r * rs + c);
-      ok &= finite16B<T>(u);
-    }
+    const uint4 u = keep16(r < len, *reinterpret_cast<const uint4*>(src + clamp_row(r, len) * rs + c));
+    ok &= finite16B<T>(u);
     *reinterpret_cast<uint4*>(dst + r * LD + c) = u;
   }
   return ok;
@@ -128,9 +125,14 @@ __device__ __forceinline__ bool load_gates(const float* __restrict__ g, const fl
   if (wave_id() == 0) {
     const int r = lane_id();
     float gv = 0.f, bv = 0.f;
-    if (r < len) {
-      if (VAR != VAR_DELTA) gv = g[(row0 + r) * H + h];
-      if (VAR != VAR_DECAY) bv = beta[(row0 + r) * H + h];
+    const long o = (row0 + clamp_row(r, len)) * H + h;
+    if (VAR != VAR_DELTA) {
+      const float x = g[o];
+      gv = r < len ? x : 0.f;
+    }
+    if (VAR != VAR_DECAY) {
+      const float x = beta[o];
+      bv = r < len ? x : 0.f;
     }
     ok = finite_f(gv) && finite_f(bv);
     Gs[r] = wave_incl_scan(gv);
@@ -140,72 +142,117 @@ __device__ __forceinline__ bool load_gates(const float* __restrict__ g, const fl
 }
 
 // T = (I + A)^{-1} for the strictly lower-triangular 64 x 64 matrix A held in
-// fp32 in As (row stride LC).  The 16 x 16 diagonal blocks are inverted by
-// forward substitution (wave 0, one lane per column: row r of a block is
-// e_r - sum_{i<r} A_ri T_i); the blocks below the diagonal follow block row by
-// block row, T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj, on fp32 MFMA (wave j owns
-// block column j).  T lands in Tf (fp32, stride LC); for bf16 operands a copy
-// is rounded into Ts (stride LT).  Xs is a 4 x 16 x 20 fp32 scratch.
-// Must be called by all threads of the block.
-template <typename OP, int LC, int LT>
-__device__ void unit_lower_inverse(const float* As, float* Tf, OP* Ts, float* Xs) {
-  constexpr int LX = 20;
-  const int w = wave_id(), l = lane_id();
+// fp32 in As (row stride LC), by blocked forward substitution over 16 x 16
+// blocks.
+//   Diagonal blocks: wave 0, one lane per (block, column); row r of a block's
+//   inverse is e_r - sum_{i<r} A_ri T_i, with the rows of A read as float4.
+//   Blocks below the diagonal: wave j builds block column j top-down,
+//   T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj, on fp32 MFMA with the column's
+//   finished blocks kept in accumulator registers.  The contraction index of
+//   every 16x16x4 product is enumerated as k = 4 * (lane group) + step, which
+//   makes an accumulator tile (lane holds rows 4g..4g+3 of column c) a ready B
+//   operand, so no block leaves registers until it is stored.
+// T lands in Tf (fp32, stride LC, zeros above the block diagonal); for bf16
+// operands a rounded copy goes to Ts (stride LT) and, if TRANS, T^T to TT.
+// Called by all threads of the block; ends with a barrier.
+template <typename OP, int LC, int LT, bool TRANS>
+__device__ void unit_lower_inverse(const float* As, float* Tf, OP* Ts, OP* TT) {
+  constexpr bool BF = sizeof(OP) == 2;
+  const int w = wave_id(), l = lane_id(), g = l >> 4, c = l & 15;
+  // the six blocks above the diagonal are zero (T^T: below it)
+  for (int idx = threadIdx.x; idx < 6 * 256; idx += blockDim.x) {
+    const int blk = idx >> 8, rr = (idx >> 4) & 15, cc = idx & 15;
+    const int bi = blk < 3 ? 0 : (blk < 5 ? 1 : 2);
+    const int bj = blk < 3 ? blk + 1 : (blk < 5 ? blk - 1 : 3);
+    const int r = 16 * bi + rr, col = 16 * bj + cc;
+    Tf[r * LC + col] = 0.f;
+    if constexpr (BF) Ts[r * LT + col] = from_f<OP>(0.f);
+    if constexpr (TRANS) TT[col * LT + r] = from_f<OP>(0.f);
+  }
   if (w == 0) {
-    const int base = (l >> 4) * 16, j = l & 15;
+    const int base = 16 * g;
     float col[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       float s = 0.f;
 #pragma unroll
-      for (int i = 0; i < r; ++i) s += As[(base + r) * LC + base + i] * col[i];
-      col[r] = (r == j) ? 1.f : (r > j ? -s : 0.f);
+      for (int q = 0; q < (r + 3) / 4; ++q) {
+        const float4 a = *reinterpret_cast<const float4*>(As + (base + r) * LC + base + 4 * q);
+        const float av[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          if (4 * q + t < r) s += av[t] * col[4 * q + t];
+      }
+      col[r] = (r == c) ? 1.f : (r > c ? -s : 0.f);
     }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) Tf[(base + r) * LC + base + j] = col[r];
-  }
-  for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
-    const int r = idx >> 6, c = idx & 63;
-    if ((c >> 4) > (r >> 4)) Tf[r * LC + c] = 0.f;
+    for (int r = 0; r < 16; ++r) {
+      Tf[(base + r) * LC + base + c] = col[r];
+      if constexpr (BF) Ts[(base + r) * LT + base + c] = from_f<OP>(col[r]);
+    }
+    if constexpr (TRANS) {
+      OP t16[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) t16[r] = from_f<OP>(col[r]);
+      if constexpr (BF) {
+        *reinterpret_cast<uint4*>(TT + (base + c) * LT + base) = pack16<OP>(t16);
+        *reinterpret_cast<uint4*>(TT + (base + c) * LT + base + 8) = pack16<OP>(t16 + 8);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) TT[(base + c) * LT + base + r] = t16[r];
+      }
+    }
   }
   __syncthreads();
-  for (int i = 1; i < 4; ++i) {
-    if (w < i) {
-      const int j = w;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      for (int kb = j; kb < i; ++kb) {
+  if (w < 3) {
+    const int j = w;
+    f32x4 tc[4];
 #pragma unroll
-        for (int k0 = 0; k0 < 16; k0 += 4) {
-          const float a = As[(16 * i + (l & 15)) * LC + 16 * kb + k0 + (l >> 4)];
-          const float b = Tf[(16 * kb + k0 + (l >> 4)) * LC + 16 * j + (l & 15)];
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+    for (int kb = 0; kb < 4; ++kb) {
+      tc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (kb == j) {
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) tc[kb][jj] = Tf[(16 * kb + 4 * g + jj) * LC + 16 * kb + c];
+      }
+    }
+#pragma unroll
+    for (int i = 1; i < 4; ++i) {
+      if (i <= j) continue;
+      f32x4 x = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < i; ++kb) {
+        if (kb < j) continue;
+        const float4 a = *reinterpret_cast<const float4*>(As + (16 * i + c) * LC + 16 * kb + 4 * g);
+        x = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, tc[kb][0], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, tc[kb][1], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, tc[kb][2], x, 0, 0, 0);
+        x = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, tc[kb][3], x, 0, 0, 0);
+      }
+      const float4 ti = *reinterpret_cast<const float4*>(Tf + (16 * i + c) * LC + 16 * i + 4 * g);
+      f32x4 t = {0.f, 0.f, 0.f, 0.f};
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti.x, x[0], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti.y, x[1], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti.z, x[2], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti.w, x[3], t, 0, 0, 0);
+      OP t4[4];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        tc[i][jj] = -t[jj];
+        t4[jj] = from_f<OP>(-t[jj]);
+        Tf[(16 * i + 4 * g + jj) * LC + 16 * j + c] = -t[jj];
+        if constexpr (BF) Ts[(16 * i + 4 * g + jj) * LT + 16 * j + c] = t4[jj];
+      }
+      if constexpr (TRANS) {
+        if constexpr (BF) {
+          *reinterpret_cast<uint2*>(TT + (16 * j + c) * LT + 16 * i + 4 * g) = uint2{pack2(t4[0], t4[1]), pack2(t4[2], t4[3])};
+        } else {
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) TT[(16 * j + c) * LT + 16 * i + 4 * g + jj] = t4[jj];
         }
       }
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) Xs[w * 16 * LX + (4 * (l >> 4) + jj) * LX + (l & 15)] = acc[jj];
     }
-    __syncthreads();
-    if (w < i) {
-      const int j = w;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int k0 = 0; k0 < 16; k0 += 4) {
-        const float a = Tf[(16 * i + (l & 15)) * LC + 16 * i + k0 + (l >> 4)];
-        const float b = Xs[w * 16 * LX + (k0 + (l >> 4)) * LX + (l & 15)];
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
-      }
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) Tf[(16 * i + 4 * (l >> 4) + jj) * LC + 16 * j + (l & 15)] = -acc[jj];
-    }
-    __syncthreads();
   }
-  if constexpr (sizeof(OP) == 2) {
-    for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
-      const int r = idx >> 6, c = idx & 63;
-      Ts[r * LT + c] = from_f<OP>(Tf[r * LC + c]);
-    }
-    __syncthreads();
-  }
+  __syncthreads();
 }
 
 // XCD-aware placement of the (stream, value-tile) blocks of a state scan:

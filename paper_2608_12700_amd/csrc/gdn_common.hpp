@@ -42,6 +42,16 @@ __device__ __forceinline__ bool finite_f(float x) {
   return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
 }
 
+// Masked tile rows: rows r >= len of a chunk are read from row len - 1
+// (len >= 1 for every chunk) and zeroed with a select afterwards.  Keeping
+// the load itself unconditional matters: a branch around a load forces the
+// wave to wait for it at the join, which serialises every masked load.
+__device__ __forceinline__ int clamp_row(int r, int len) { return r < len ? r : len - 1; }
+__device__ __forceinline__ uint4 keep16(bool keep, uint4 u) {
+  return uint4{keep ? u.x : 0u, keep ? u.y : 0u, keep ? u.z : 0u, keep ? u.w : 0u};
+}
+__device__ __forceinline__ uint2 keep8(bool keep, uint2 u) { return uint2{keep ? u.x : 0u, keep ? u.y : 0u}; }
+
 // ---------------------------------------------------------------------------
 // Operand views.  get(o, k): o is the row for an A operand (M x K) or the
 // column for a B operand (K x N); k is the contraction index.
@@ -66,7 +76,8 @@ struct KRowM {
   static constexpr bool kVec = false;
   static constexpr bool kMasked = true;
   __device__ __forceinline__ T get(int o, int k) const {
-    return o < rows ? p[o * ld + k] : static_cast<T>(0.f);
+    const T x = p[clamp_row(o, rows) * ld + k];
+    return o < rows ? x : static_cast<T>(0.f);
   }
   __device__ __forceinline__ const T* ptr(int o, int k) const { return p + o * ld + k; }
 };
@@ -105,11 +116,8 @@ struct Mma<bf16> {
     if constexpr (V::kVec) {
       return *reinterpret_cast<const bf16x8*>(v.ptr(oo, kk));
     } else if constexpr (is_masked<V>::value) {
-      if (oo < v.rows) return *reinterpret_cast<const bf16x8*>(v.ptr(oo, kk));
-      frag z;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) z[j] = static_cast<bf16>(0.f);
-      return z;
+      const uint4 u = *reinterpret_cast<const uint4*>(v.ptr(clamp_row(oo, v.rows), kk));
+      return __builtin_bit_cast(frag, keep16(oo < v.rows, u));
     } else {
       frag r;
 #pragma unroll

@@ -45,7 +45,6 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
   __shared__ __align__(16) char r2[R2];
   __shared__ __align__(16) OP KbT[DT_ ? DK * LT : 1];
   __shared__ __align__(16) char r4[R4];
-  __shared__ __align__(16) float Xs[4 * 16 * 20];
   __shared__ float Gs[CH], Bs[CH], Gam[CH], Dte[CH];
   OP* Qs = reinterpret_cast<OP*>(r1);
   float* Tf = reinterpret_cast<float*>(r1);
@@ -118,7 +117,7 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
   __syncthreads();  // Q and K are dead from here on
   const OP* vp = v + (cp.row0 * H + h) * DV;
   if constexpr (DT_) {
-    unit_lower_inverse<OP, LC, LT>(As, Tf, Ts, Xs);
+    unit_lower_inverse<OP, LC, LT, false>(As, Tf, Ts, (OP*)nullptr);
     const OP* Tp;
     if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
     constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
@@ -145,11 +144,9 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
     for (int c0 = 0; c0 < DV; c0 += VS) {
       for (int idx = threadIdx.x; idx < CH * VS / VE; idx += blockDim.x) {
         const int i = idx / (VS / VE), v0 = (idx - i * (VS / VE)) * VE;
-        uint4 vv = {0u, 0u, 0u, 0u};
-        if (i < cp.len) {
-          vv = *reinterpret_cast<const uint4*>(vp + (long)i * H * DV + c0 + v0);
-          ok &= finite16B<OP>(vv);
-        }
+        const uint4 vv =
+            keep16(i < cp.len, *reinterpret_cast<const uint4*>(vp + (long)clamp_row(i, cp.len) * H * DV + c0 + v0));
+        ok &= finite16B<OP>(vv);
 #pragma unroll
         for (int j = 0; j < VE; ++j) VbT[(v0 + j) * LT + i] = from_f<OP>(Bs[i] * to_f(elem16<OP>(vv, j)));
       }
@@ -169,7 +166,8 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
     // scalar-decay member: T = I, W = 0, U = V; only check v for non-finite values
     for (int idx = threadIdx.x; idx < CH * DV / VE; idx += blockDim.x) {
       const int i = idx / (DV / VE), c = (idx - i * (DV / VE)) * VE;
-      if (i < cp.len) ok &= finite16B<OP>(*reinterpret_cast<const uint4*>(vp + (long)i * H * DV + c));
+      ok &= finite16B<OP>(
+          keep16(i < cp.len, *reinterpret_cast<const uint4*>(vp + (long)clamp_row(i, cp.len) * H * DV + c)));
     }
   }
   const int bad = __syncthreads_or(!ok);
@@ -231,7 +229,8 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int r = UT::m0(0) + (l >> 4) * 4 + j;
-          p.u[b][j] = r < len ? to_f(vp[(long)r * H * DV + UT::n0(b) + (l & 15)]) : 0.f;
+          const float x = to_f(vp[(long)clamp_row(r, len) * H * DV + UT::n0(b) + (l & 15)]);
+          p.u[b][j] = r < len ? x : 0.f;
         }
     }
     p.qf.load(KRowM<OP>{q + (row0 * H + h) * DK, (long)H * DK, len});

@@ -689,6 +689,9 @@ __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __re
 //     chunk state h in both orientations, dh, dU'^T, v) goes straight from
 //     global memory into registers, issued at kernel entry or one step ahead,
 //     instead of through LDS transposes;
+//   * the 64 x d_k results (dQ, dK and X = -Y h^T) are accumulated transposed,
+//     d along the tile rows, so their row sums over d are mostly in-lane and
+//     the K^T, Q^T operands are read straight from the row-major tiles;
 //   * the decay mask D (E is its strict lower part) is formed once and kept
 //     in registers next to P and A for the phase that needs it again.
 // ---------------------------------------------------------------------------
@@ -696,16 +699,15 @@ template <int DK, int DV>
 struct GradBF {
   static constexpr int VS = DV > 128 ? 128 : DV;
   static constexpr int LK = DK + 8, LT = CH + 8, LC = CH + 4, LV = VS + 8;
-  static constexpr int WNk = DK / 16, WMk = 8 / WNk;
+  static constexpr int WMd = DK / 16, WNr = 8 / WMd;  // waves along d and along r of the d x 64 results
   static constexpr int WNv = VS / 16, WMv = 8 / WNv;
-  typedef Tiles<CH, DK, WMk, WNk> TK;  // 64 x dk results: X, dQ, dK
-  typedef Tiles<VS, CH, WNv, WMv> TY;  // Y^T and U'^T
+  typedef Tiles<DK, CH, WMd, WNr> TD;  // X^T, dQ^T, dK^T: d x 64
+  typedef Tiles<VS, CH, WNv, WMv> TY;  // Y^T, U'^T, (K h)^T: VS x 64
   typedef Tiles<CH, CH, 4, 2> TC;      // P, A, dP, dA
-  static constexpr int PH0 = CH * LK * 2 + 2 * CH * LC * 4;
+  static constexpr int PH0 = 2 * CH * LC * 4;
   static constexpr int PH1 = (VS * LT + 3 * CH * LV) * 2;
-  static constexpr int PH2 = (2 * DK * LT + 3 * CH * LT) * 2;
+  static constexpr int PH2 = 3 * CH * LT * 2 > 2 * CH * LK * 2 ? 3 * CH * LT * 2 : 2 * CH * LK * 2;
   static constexpr int UB = PH0 > PH1 ? (PH0 > PH2 ? PH0 : PH2) : (PH1 > PH2 ? PH1 : PH2);
-  static_assert(2 * CH * LK * 2 <= 2 * DK * LT * 2, "dq/dk staging fits where Q^T, K^T were");
 };
 
 __device__ __forceinline__ bf16x8 cvt8(const float (&x)[8]) {
@@ -725,14 +727,16 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
                                                  bf16* __restrict__ dvo, float* __restrict__ dg,
                                                  float* __restrict__ dbeta, int* __restrict__ flag) {
   typedef GradBF<DK, DV> C;
-  typedef typename C::TK TK;
+  typedef typename C::TD TD;
   typedef typename C::TY TY;
   typedef typename C::TC TC;
   typedef Mma<bf16> M;
   constexpr bool DT_ = VAR != VAR_DECAY;
   constexpr int VS = C::VS, LK = C::LK, LT = C::LT, LC = C::LC, LV = C::LV;
   constexpr int NDO = CH * VS / 8 / 512;  // 16-byte pieces of a dO slice per thread
+  constexpr int NQK = CH * DK / 8 / 512;  // 16-byte pieces of q (or k) per thread
 
+  __shared__ __align__(16) bf16 Qs[CH * LK];
   __shared__ __align__(16) bf16 Ks[CH * LK];
   __shared__ __align__(16) bf16 Ts[DT_ ? CH * LT : 1];
   __shared__ __align__(16) bf16 TT[CH * LT];  // T^T (the identity for the scalar-decay member)
@@ -741,14 +745,14 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   __shared__ __align__(16) float Bs[CH];
   __shared__ __align__(16) float Dte[CH];
   __shared__ float rowZ[2][CH], colZ[4][CH], rowA[2][CH];
-  __shared__ float rqp[C::WNk][CH], rxp[C::WNk][CH], rkp[C::WNk][CH], dbYp[C::WNv][CH];
+  __shared__ float rqp[C::WMd][CH], rxp[C::WMd][CH], rkp[C::WMd][CH], dbYp[C::WNv][CH];
   __shared__ float hdh_w[8];
   __shared__ __align__(16) char ub[C::UB];
 
   const int ci = blockIdx.x, h = blockIdx.y;
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
-  const int w = wave_id(), l = lane_id();
+  const int w = wave_id(), l = lane_id(), lg = l >> 4, lc = l & 15;
   const int len = cp.len;
   const bf16* qp = q + (cp.row0 * H + h) * DK;
   const bf16* kp = k + (cp.row0 * H + h) * DK;
@@ -768,8 +772,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     uint2 vb[TY::TM][TY::TN];            // v[r][v0..v0+3] in the Y^T accumulator layout
   };
   struct PreB {
-    float hx[VS / 32][TK::TN][8];        // h: B fragments of X and dQ
-    bf16x8 dh[VS / 32][TK::TN];          // dh: B fragments of dK
+    float hx[VS / 32][TD::TM][8];        // h: A fragments of X^T and dQ^T
+    bf16x8 dh[VS / 32][TD::TM];          // dh: A fragments of dK^T
   };
   bool ok = true;
   auto load_a = [&](PreA& p, int c0) {
@@ -788,15 +792,13 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
         for (int a = 0; a < TY::TM; ++a)
 #pragma unroll
-          for (int j = 0; j < 8; ++j)
-            p.hk[s][a][j] = hp[(32 * s + 8 * (l >> 4) + j) * DV + c0 + TY::m0(a) + (l & 15)];
+          for (int j = 0; j < 8; ++j) p.hk[s][a][j] = hp[(32 * s + 8 * lg + j) * DV + c0 + TY::m0(a) + lc];
 #pragma unroll
       for (int a = 0; a < TY::TM; ++a)
 #pragma unroll
         for (int b = 0; b < TY::TN; ++b) {
-          const int r = TY::n0(b) + (l & 15);
-          p.vb[a][b] =
-              keep8(r < len, *reinterpret_cast<const uint2*>(vp + clamp_row(r, len) * rsv + c0 + TY::m0(a) + 4 * (l >> 4)));
+          const int r = TY::n0(b) + lc;
+          p.vb[a][b] = keep8(r < len, *reinterpret_cast<const uint2*>(vp + clamp_row(r, len) * rsv + c0 + TY::m0(a) + 4 * lg));
         }
     }
   };
@@ -804,23 +806,22 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
     for (int s = 0; s < VS / 32; ++s)
 #pragma unroll
-      for (int b = 0; b < TK::TN; ++b) {
-        const float* src = hp + (TK::n0(b) + (l & 15)) * DV + c0 + 32 * s + 8 * (l >> 4);
+      for (int a = 0; a < TD::TM; ++a) {
+        const float* src = hp + (TD::m0(a) + lc) * DV + c0 + 32 * s + 8 * lg;
         const float4 x0 = *reinterpret_cast<const float4*>(src);
         const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
-        p.hx[s][b][0] = x0.x; p.hx[s][b][1] = x0.y; p.hx[s][b][2] = x0.z; p.hx[s][b][3] = x0.w;
-        p.hx[s][b][4] = x1.x; p.hx[s][b][5] = x1.y; p.hx[s][b][6] = x1.z; p.hx[s][b][7] = x1.w;
-        p.dh[s][b] = M::load(KRow<bf16, DV>{dhp + c0}, TK::n0(b), 32 * s);
+        p.hx[s][a][0] = x0.x; p.hx[s][a][1] = x0.y; p.hx[s][a][2] = x0.z; p.hx[s][a][3] = x0.w;
+        p.hx[s][a][4] = x1.x; p.hx[s][a][5] = x1.y; p.hx[s][a][6] = x1.z; p.hx[s][a][7] = x1.w;
+        p.dh[s][a] = M::load(KRow<bf16, DV>{dhp + c0}, TD::m0(a), 32 * s);
       }
   };
 
   // ================= phase 0: gates, P, A, T
-  bf16* Qs = reinterpret_cast<bf16*>(ub);
-  float* As = reinterpret_cast<float*>(ub + CH * LK * 2);
+  float* As = reinterpret_cast<float*>(ub);
   float* Tf = As + CH * LC;
-  uint4 qk[2][CH * DK / 8 / 512];
+  uint4 qk[2][NQK];
 #pragma unroll
-  for (int t = 0; t < CH * DK / 8 / 512; ++t) {
+  for (int t = 0; t < NQK; ++t) {
     const int idx = threadIdx.x + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
     const long ro = clamp_row(r, len) * (long)H * DK + c;
     qk[0][t] = keep16(r < len, *reinterpret_cast<const uint4*>(qp + ro));
@@ -830,7 +831,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   PreA pa;
   load_a(pa, 0);
 #pragma unroll
-  for (int t = 0; t < CH * DK / 8 / 512; ++t) {
+  for (int t = 0; t < NQK; ++t) {
     const int idx = threadIdx.x + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
     *reinterpret_cast<uint4*>(Qs + r * LK + c) = qk[0][t];
     *reinterpret_cast<uint4*>(Ks + r * LK + c) = qk[1][t];
@@ -849,7 +850,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   for (int b = 0; b < TC::TN; ++b)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int r = TC::m0(0) + 4 * (l >> 4) + j, i = TC::n0(b) + (l & 15);
+      const int r = TC::m0(0) + 4 * lg + j, i = TC::n0(b) + lc;
       dd[b][j] = i <= r ? __expf(Gs[r] - Gs[i]) : 0.f;
       pm.acc[0][b][j] *= dd[b][j];
     }
@@ -860,7 +861,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     for (int b = 0; b < TC::TN; ++b)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = TC::m0(0) + 4 * (l >> 4) + j, i = TC::n0(b) + (l & 15);
+        const int r = TC::m0(0) + 4 * lg + j, i = TC::n0(b) + lc;
         const float x = i < r ? ae.acc[0][b][j] * dd[b][j] : 0.f;
         ae.acc[0][b][j] = x;
         As[r * LC + i] = Bs[r] * x;
@@ -872,8 +873,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
       const int r = idx >> 6, c = idx & 63;
       TT[r * LT + c] = from_f<bf16>(r == c ? 1.f : 0.f);
     }
+    __syncthreads();
   }
-  __syncthreads();
 
   // ================= phase 1: value slices
   bf16* RT = reinterpret_cast<bf16*>(ub);
@@ -881,8 +882,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   bf16* Ups = Ys + CH * LV;
   bf16* dOs = Ups + CH * LV;
   TC dA, dP;
-  TK X, dQa, dKh;
-  dA.zero(); dP.zero(); X.zero(); dQa.zero(); dKh.zero();
+  TD Xt, dQt, dKt;  // X^T = -h Y^T, dQ^T (from dO h^T), dK^T (from U' dh^T)
+  dA.zero(); dP.zero(); Xt.zero(); dQt.zero(); dKt.zero();
   float dbY[TY::TN];
 #pragma unroll
   for (int b = 0; b < TY::TN; ++b) dbY[b] = 0.f;
@@ -915,11 +916,11 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
       load_b(pb, c0);
 #pragma unroll
       for (int b = 0; b < TY::TN; ++b) {
-        const int r = TY::n0(b) + (l & 15);
+        const int r = TY::n0(b) + lc;
         const float br = Bs[r], gr = Gam[r];
 #pragma unroll
         for (int a = 0; a < TY::TM; ++a) {
-          const int v0 = TY::m0(a) + 4 * (l >> 4);
+          const int v0 = TY::m0(a) + 4 * lg;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const float vx = to_f(elem4<bf16>(pa.vb[a][b], j));
@@ -947,11 +948,11 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
       }
 #pragma unroll
       for (int b = 0; b < TY::TN; ++b) {
-        const int r = TY::n0(b) + (l & 15);
+        const int r = TY::n0(b) + lc;
         const float br = DT_ ? Bs[r] : 1.f;
 #pragma unroll
         for (int a = 0; a < TY::TM; ++a) {
-          const int v0 = TY::m0(a) + 4 * (l >> 4);
+          const int v0 = TY::m0(a) + 4 * lg;
           bf16 d4[4], y4[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
@@ -992,8 +993,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
           bf16 u4[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) u4[j] = from_f<bf16>(ut.acc[a][b][j]);
-          *reinterpret_cast<uint2*>(Ups + (TY::n0(b) + (l & 15)) * LV + TY::m0(a) + 4 * (l >> 4)) =
-              pack4<bf16>(u4);
+          *reinterpret_cast<uint2*>(Ups + (TY::n0(b) + lc) * LV + TY::m0(a) + 4 * lg) = pack4<bf16>(u4);
         }
       __syncthreads();
       dA.template mma<bf16, VS>(KRow<bf16, LV>{Ys}, KRow<bf16, LV>{Ups});  // -Y U'^T
@@ -1001,30 +1001,30 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     dP.template mma<bf16, VS>(KRow<bf16, LV>{dOs}, KRow<bf16, LV>{Ups});
 #pragma unroll
     for (int s = 0; s < VS / 32; ++s) {
-      bf16x8 fh[TK::TN];
+      bf16x8 fh[TD::TM];
 #pragma unroll
-      for (int b = 0; b < TK::TN; ++b) {
-        fh[b] = cvt8(pb.hx[s][b]);
+      for (int a = 0; a < TD::TM; ++a) {
+        fh[a] = cvt8(pb.hx[s][a]);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) ok &= finite_f(pb.hx[s][b][j]);
-        if (TK::m0(0) == 0) {  // one wave row adds <h, dh> for its columns
+        for (int j = 0; j < 8; ++j) ok &= finite_f(pb.hx[s][a][j]);
+        if (TD::n0(0) == 0) {  // one wave column adds <h, dh> for its rows
 #pragma unroll
-          for (int j = 0; j < 8; ++j) hdh += pb.hx[s][b][j] * to_f(pb.dh[s][b][j]);
+          for (int j = 0; j < 8; ++j) hdh += pb.hx[s][a][j] * to_f(pb.dh[s][a][j]);
         }
       }
 #pragma unroll
-      for (int a = 0; a < TK::TM; ++a) {
-        const bf16x8 fo = M::load(KRow<bf16, LV>{dOs}, TK::m0(a), 32 * s);
-        const bf16x8 fu = M::load(KRow<bf16, LV>{Ups}, TK::m0(a), 32 * s);
+      for (int b = 0; b < TD::TN; ++b) {
+        const bf16x8 fo = M::load(KRow<bf16, LV>{dOs}, TD::n0(b), 32 * s);
+        const bf16x8 fu = M::load(KRow<bf16, LV>{Ups}, TD::n0(b), 32 * s);
 #pragma unroll
-        for (int b = 0; b < TK::TN; ++b) {
-          dQa.acc[a][b] = M::mma(fo, fh[b], dQa.acc[a][b]);
-          dKh.acc[a][b] = M::mma(fu, pb.dh[s][b], dKh.acc[a][b]);
+        for (int a = 0; a < TD::TM; ++a) {
+          dQt.acc[a][b] = M::mma(fh[a], fo, dQt.acc[a][b]);
+          dKt.acc[a][b] = M::mma(pb.dh[s][a], fu, dKt.acc[a][b]);
         }
         if constexpr (DT_) {
-          const bf16x8 fy = M::load(KRow<bf16, LV>{Ys}, TK::m0(a), 32 * s);
+          const bf16x8 fy = M::load(KRow<bf16, LV>{Ys}, TD::n0(b), 32 * s);
 #pragma unroll
-          for (int b = 0; b < TK::TN; ++b) X.acc[a][b] = M::mma(fy, fh[b], X.acc[a][b]);
+          for (int a = 0; a < TD::TM; ++a) Xt.acc[a][b] = M::mma(fh[a], fy, Xt.acc[a][b]);
         }
       }
     }
@@ -1037,32 +1037,20 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
     for (int b = 0; b < TY::TN; ++b) {
       const float s = sum_groups(dbY[b]);
-      if ((l >> 4) == 0) dbYp[w / C::WMv][TY::n0(b) + (l & 15)] = s;
+      if (lg == 0) dbYp[w / C::WMv][TY::n0(b) + lc] = s;
     }
   }
   __syncthreads();  // phase-1 LDS operands are consumed
 
   // ================= phase 2: the chunk-level gradients
-  bf16* QT = reinterpret_cast<bf16*>(ub);
-  bf16* KT = QT + DK * LT;
-  bf16* dPs = KT + DK * LT;
+  bf16* dPs = reinterpret_cast<bf16*>(ub);
   bf16* dPmT = dPs + CH * LT;
   bf16* SdT = dPmT + CH * LT;  // dB + dB^T, dB = dA * beta_r * E
-  for (int idx = threadIdx.x; idx < CH * DK / 8; idx += blockDim.x) {
-    const int r = idx & 63, c = (idx >> 6) * 8;  // lanes walk rows: conflict-free transposed writes
-    const uint4 qv = keep16(r < len, *reinterpret_cast<const uint4*>(qp + clamp_row(r, len) * (long)H * DK + c));
-    const uint4 kv = *reinterpret_cast<const uint4*>(Ks + r * LK + c);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      QT[(c + j) * LT + r] = elem16<bf16>(qv, j);
-      KT[(c + j) * LT + r] = elem16<bf16>(kv, j);
-    }
-  }
   TC zs;  // Z = dA * A + dP * P
   float rowA_l[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int b = 0; b < TC::TN; ++b) {
-    const int i = TC::n0(b) + (l & 15), r0 = TC::m0(0) + 4 * (l >> 4);
+    const int i = TC::n0(b) + lc, r0 = TC::m0(0) + 4 * lg;
     bf16 pt4[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -1095,8 +1083,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     for (int j = 0; j < 4; ++j) {
       const float rs = sum16(zs.acc[0][0][j] + zs.acc[0][1][j]);
       const float ra = sum16(rowA_l[j]);
-      const int r = TC::m0(0) + 4 * (l >> 4) + j;
-      if ((l & 15) == 0) {
+      const int r = TC::m0(0) + 4 * lg + j;
+      if (lc == 0) {
         rowZ[wn][r] = rs;
         rowA[wn][r] = ra;
       }
@@ -1107,69 +1095,81 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
       for (int j = 0; j < 4; ++j) cs += zs.acc[0][b][j];
       cs = sum_groups(cs);
-      if ((l >> 4) == 0) colZ[wm][TC::n0(b) + (l & 15)] = cs;
+      if (lg == 0) colZ[wm][TC::n0(b) + lc] = cs;
     }
   }
-  __syncthreads();
-
-  // row sums q_r . (dO h^T)_r, k_r . X_r, k_r . (U' dh^T)_r, then the scalings
+  // row sums q_r . (dO h^T)_r, k_r . X_r, k_r . (U' dh^T)_r (over d: in-lane over
+  // four d, then over the lane groups, then one partial per wave row), then the
+  // per-row scalings
   {
-    const int wn = w % C::WNk;
+    const int wd = w / C::WNr;
 #pragma unroll
-    for (int a = 0; a < TK::TM; ++a) {
-      const int r0 = TK::m0(a) + 4 * (l >> 4);
-      float rq[4] = {0.f, 0.f, 0.f, 0.f}, rx[4] = {0.f, 0.f, 0.f, 0.f}, rk[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < TD::TN; ++b) {
+      const int r = TD::n0(b) + lc;
+      float rq = 0.f, rx = 0.f, rk = 0.f;
 #pragma unroll
-      for (int b = 0; b < TK::TN; ++b) {
-        const int d = TK::n0(b) + (l & 15);
-        const uint2 q4 = *reinterpret_cast<const uint2*>(QT + d * LT + r0);
-        const uint2 k4 = *reinterpret_cast<const uint2*>(KT + d * LT + r0);
+      for (int a = 0; a < TD::TM; ++a) {
+        const int d0 = TD::m0(a) + 4 * lg;
+        const uint2 q4 = *reinterpret_cast<const uint2*>(Qs + r * LK + d0);
+        const uint2 k4 = *reinterpret_cast<const uint2*>(Ks + r * LK + d0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const float qv = to_f(elem4<bf16>(q4, j)), kv = to_f(elem4<bf16>(k4, j));
-          rq[j] += qv * dQa.acc[a][b][j];
-          rx[j] += kv * X.acc[a][b][j];
-          rk[j] += kv * dKh.acc[a][b][j];
+          rq += qv * dQt.acc[a][b][j];
+          rx += kv * Xt.acc[a][b][j];
+          rk += kv * dKt.acc[a][b][j];
         }
       }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        rq[j] = sum16(rq[j]);
-        rx[j] = sum16(rx[j]);
-        rk[j] = sum16(rk[j]);
-        if ((l & 15) == 0) {
-          rqp[wn][r0 + j] = rq[j];
-          rxp[wn][r0 + j] = rx[j];
-          rkp[wn][r0 + j] = rk[j];
-        }
+      rq = sum_groups(rq);
+      rx = sum_groups(rx);
+      rk = sum_groups(rk);
+      if (lg == 0) {
+        rqp[wd][r] = rq;
+        rxp[wd][r] = rx;
+        rkp[wd][r] = rk;
       }
-      const float4 g4 = *reinterpret_cast<const float4*>(Gam + r0);
-      const float4 e4 = *reinterpret_cast<const float4*>(Dte + r0);
-      const float4 b4 = *reinterpret_cast<const float4*>(Bs + r0);
-      const float gg[4] = {g4.x, g4.y, g4.z, g4.w}, ee[4] = {e4.x, e4.y, e4.z, e4.w};
-      const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
+      const float gr = Gam[r], er = Dte[r], bgr = DT_ ? Bs[r] * gr : 0.f;
 #pragma unroll
-      for (int b = 0; b < TK::TN; ++b)
+      for (int a = 0; a < TD::TM; ++a)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          dQa.acc[a][b][j] *= gg[j];
-          dKh.acc[a][b][j] = ee[j] * dKh.acc[a][b][j] + (DT_ ? bb[j] * gg[j] * X.acc[a][b][j] : 0.f);
+          dQt.acc[a][b][j] *= gr;
+          dKt.acc[a][b][j] = er * dKt.acc[a][b][j] + bgr * Xt.acc[a][b][j];
         }
     }
   }
-  dQa.template mma<bf16, CH>(KRow<bf16, LT>{dPs}, KRow<bf16, LT>{KT});
-  dKh.template mma<bf16, CH>(KRow<bf16, LT>{dPmT}, KRow<bf16, LT>{QT});
-  if constexpr (DT_) dKh.template mma<bf16, CH>(KRow<bf16, LT>{SdT}, KRow<bf16, LT>{KT});
   __syncthreads();
-  bf16* dqst = QT;
-  bf16* dkst = QT + CH * LK;
-  dQa.each([&](int r, int d, float& x) { dqst[r * LK + d] = from_f<bf16>(x); });
-  dKh.each([&](int r, int d, float& x) { dkst[r * LK + d] = from_f<bf16>(x); });
+  {
+    // dQ^T += K^T (dP * D)^T,  dK^T += Q^T (dP * D) + K^T (dB + dB^T); the K^T and
+    // Q^T fragments are read down the columns of the row-major tiles
+    typename TD::template AFr<bf16, CH> kt;
+    kt.load(KCol<bf16, LK>{Ks});
+    dQt.template mma<bf16, CH>(kt, KRow<bf16, LT>{dPs});
+    if constexpr (DT_) dKt.template mma<bf16, CH>(kt, KRow<bf16, LT>{SdT});
+    dKt.template mma<bf16, CH>(KCol<bf16, LK>{Qs}, KRow<bf16, LT>{dPmT});
+  }
+  __syncthreads();
+  bf16* dqst = reinterpret_cast<bf16*>(ub);
+  bf16* dkst = dqst + CH * LK;
+#pragma unroll
+  for (int a = 0; a < TD::TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TD::TN; ++b) {
+      const int r = TD::n0(b) + lc, d0 = TD::m0(a) + 4 * lg;
+      bf16 q4[4], k4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        q4[j] = from_f<bf16>(dQt.acc[a][b][j]);
+        k4[j] = from_f<bf16>(dKt.acc[a][b][j]);
+      }
+      *reinterpret_cast<uint2*>(dqst + r * LK + d0) = pack4<bf16>(q4);
+      *reinterpret_cast<uint2*>(dkst + r * LK + d0) = pack4<bf16>(k4);
+    }
   if (w == 0) {
     const int r = l;
     float rq = 0.f, rx = 0.f, rk = 0.f;
 #pragma unroll
-    for (int i = 0; i < C::WNk; ++i) {
+    for (int i = 0; i < C::WMd; ++i) {
       rq += rqp[i][r];
       rx += rxp[i][r];
       rk += rkp[i][r];

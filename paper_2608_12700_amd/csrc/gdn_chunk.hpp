@@ -145,7 +145,7 @@ __device__ __forceinline__ bool load_gates(const float* __restrict__ g, const fl
 // fp32 in As (row stride LC), by blocked forward substitution over 16 x 16
 // blocks.
 //   Diagonal blocks: wave 0, one lane per (block, column); row r of a block's
-//   inverse is e_r - sum_{i<r} A_ri T_i, with the rows of A read as float4.
+//   inverse is e_r - sum_{i<r} A_ri T_i.
 //   Blocks below the diagonal: wave j builds block column j top-down,
 //   T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj, on fp32 MFMA with the column's
 //   finished blocks kept in accumulator registers.  The contraction index of
@@ -156,7 +156,7 @@ __device__ __forceinline__ bool load_gates(const float* __restrict__ g, const fl
 // operands a rounded copy goes to Ts (stride LT) and, if TRANS, T^T to TT.
 // Called by all threads of the block; ends with a barrier.
 template <typename OP, int LC, int LT, bool TRANS>
-__device__ void unit_lower_inverse(const float* As, float* Tf, OP* Ts, OP* TT) {
+__device__ __forceinline__ void unit_lower_inverse(const float* As, float* Tf, OP* Ts, OP* TT) {
   constexpr bool BF = sizeof(OP) == 2;
   const int w = wave_id(), l = lane_id(), g = l >> 4, c = l & 15;
   // the six blocks above the diagonal are zero (T^T: below it)
@@ -170,20 +170,17 @@ __device__ void unit_lower_inverse(const float* As, float* Tf, OP* Ts, OP* TT) {
     if constexpr (TRANS) TT[col * LT + r] = from_f<OP>(0.f);
   }
   if (w == 0) {
+    // right-looking: once col_i is final, add its term to every later row, so
+    // consecutive FMAs are independent (the sum over i still runs in order)
     const int base = 16 * g;
-    float col[16];
+    float col[16], acc[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float s = 0.f;
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-      for (int q = 0; q < (r + 3) / 4; ++q) {
-        const float4 a = *reinterpret_cast<const float4*>(As + (base + r) * LC + base + 4 * q);
-        const float av[4] = {a.x, a.y, a.z, a.w};
+    for (int i = 0; i < 16; ++i) {
+      col[i] = (i == c) ? 1.f : (i > c ? -acc[i] : 0.f);
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-          if (4 * q + t < r) s += av[t] * col[4 * q + t];
-      }
-      col[r] = (r == c) ? 1.f : (r > c ? -s : 0.f);
+      for (int r = i + 1; r < 16; ++r) acc[r] += As[(base + r) * LC + base + i] * col[i];
     }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -205,39 +202,46 @@ __device__ void unit_lower_inverse(const float* As, float* Tf, OP* Ts, OP* TT) {
   }
   __syncthreads();
   if (w < 3) {
+    // block column j, right-looking over block rows: x_i accumulates
+    // A_ik T_kj as soon as T_kj is known, so only one 4-MFMA chain per block
+    // row lies on the critical path
     const int j = w;
-    f32x4 tc[4];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      tc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (kb == j) {
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) tc[kb][jj] = Tf[(16 * kb + 4 * g + jj) * LC + 16 * kb + c];
-      }
-    }
+    float4 ab[4][3], ti[4];
 #pragma unroll
     for (int i = 1; i < 4; ++i) {
-      if (i <= j) continue;
-      f32x4 x = {0.f, 0.f, 0.f, 0.f};
+      ti[i] = *reinterpret_cast<const float4*>(Tf + (16 * i + c) * LC + 16 * i + 4 * g);
 #pragma unroll
-      for (int kb = 0; kb < i; ++kb) {
-        if (kb < j) continue;
-        const float4 a = *reinterpret_cast<const float4*>(As + (16 * i + c) * LC + 16 * kb + 4 * g);
-        x = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, tc[kb][0], x, 0, 0, 0);
-        x = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, tc[kb][1], x, 0, 0, 0);
-        x = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, tc[kb][2], x, 0, 0, 0);
-        x = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, tc[kb][3], x, 0, 0, 0);
+      for (int kb = 0; kb < i; ++kb)
+        ab[i][kb] = *reinterpret_cast<const float4*>(As + (16 * i + c) * LC + 16 * kb + 4 * g);
+    }
+    f32x4 tk;  // T_kj of the latest finished block row k
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) tk[jj] = Tf[(16 * j + 4 * g + jj) * LC + 16 * j + c];
+    f32x4 x[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      if (k < j) continue;
+      // x_i += A_ik T_kj for every later block row i
+#pragma unroll
+      for (int i = k + 1; i < 4; ++i) {
+        x[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(ab[i][k].x, tk[0], x[i], 0, 0, 0);
+        x[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(ab[i][k].y, tk[1], x[i], 0, 0, 0);
+        x[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(ab[i][k].z, tk[2], x[i], 0, 0, 0);
+        x[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(ab[i][k].w, tk[3], x[i], 0, 0, 0);
       }
-      const float4 ti = *reinterpret_cast<const float4*>(Tf + (16 * i + c) * LC + 16 * i + 4 * g);
+      // T_{k+1,j} = -T_{k+1,k+1} x_{k+1}
+      const int i = k + 1;
       f32x4 t = {0.f, 0.f, 0.f, 0.f};
-      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti.x, x[0], t, 0, 0, 0);
-      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti.y, x[1], t, 0, 0, 0);
-      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti.z, x[2], t, 0, 0, 0);
-      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti.w, x[3], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti[i].x, x[i][0], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti[i].y, x[i][1], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti[i].z, x[i][2], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(ti[i].w, x[i][3], t, 0, 0, 0);
       OP t4[4];
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        tc[i][jj] = -t[jj];
+        tk[jj] = -t[jj];
         t4[jj] = from_f<OP>(-t[jj]);
         Tf[(16 * i + 4 * g + jj) * LC + 16 * j + c] = -t[jj];
         if constexpr (BF) Ts[(16 * i + 4 * g + jj) * LT + 16 * j + c] = t4[jj];

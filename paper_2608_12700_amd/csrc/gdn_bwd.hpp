@@ -197,8 +197,9 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     typename HT::template AFr<OP, CH> qg;
     typename HT::template BFr<OP, CH> dob;
     typename UT::template AFr<OP, CH> pt;
-    float dte[4];
-    float gl;
+    float gr[4];  // G of this lane's rows; exponentiated at use, so the prefetch never waits
+    float gl;     // G_last
+    int len;      // valid rows of the chunk
   };
   auto load_pre = [&](Pre& p, int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
@@ -206,13 +207,13 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     const int len = min(CH, sp.len - c * CH);
     p.qg.load(KRow<OP, CH>{QgTg + tile * DK * CH});
     p.dob.load(KRow<OP, CH>{dOTg + tile * DV * CH + (long)v0 * CH});
-    const float Gl = gcum[tile * CH + CH - 1];
-    p.gl = expf(Gl);
-    p.kf.load(KRowM<OP>{k + (row0 * H + h) * DK, (long)H * DK, len});
+    p.gl = gcum[tile * CH + CH - 1];
+    p.kf.load(KRowC<OP>{k + (row0 * H + h) * DK, (long)H * DK, len});  // rows past the end: masked in dU'
+    p.len = len;
     if constexpr (DT_) p.wt.load(KRow<OP, CH>{WTg + tile * DK * CH});
     p.pt.load(KRow<OP, CH>{PTg + tile * CH * CH});
 #pragma unroll
-    for (int j = 0; j < 4; ++j) p.dte[j] = __expf(Gl - gcum[tile * CH + UT::m0(0) + (l >> 4) * 4 + j]);
+    for (int j = 0; j < 4; ++j) p.gr[j] = gcum[tile * CH + UT::m0(0) + (l >> 4) * 4 + j];
   };
 
   HT dh;
@@ -223,9 +224,10 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     ok &= finite_f(x);
   });
 
-  Pre cur, nxt;
-  if (sp.nch > 0) load_pre(cur, sp.nch - 1);
-  for (int c = sp.nch - 1; c >= 0; --c) {
+  // One chunk of the reverse carry.  `prefetch` issues the loads of the
+  // previous chunk right after the barrier that opens this one; the two
+  // fragment buffers alternate, so nothing is copied.
+  auto step = [&](int c, const Pre& cur, auto&& prefetch) {
     const long tile = (long)(sp.c0 + c) * H + h;
     OP* dhp = dhg + tile * DK * DV;
     dh.each([&](int d, int vv, float& x) {
@@ -234,11 +236,7 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
       dhT[vv * LK + d] = xo;
     });
     __syncthreads();
-    if (!PF) {
-      if (c < sp.nch - 1) load_pre(cur, c);
-    } else if (c > 0) {
-      load_pre(nxt, c - 1);
-    }
+    prefetch();
     HT inj;  // (diag(e^G) Q)^T dO, independent of the carry
     inj.zero();
     inj.template mma<OP, CH>(cur.qg, cur.dob);
@@ -251,25 +249,30 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
 #pragma unroll
       for (int b = 0; b < UT::TN; ++b)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) du.acc[0][b][j] *= cur.dte[j];
+        for (int j = 0; j < 4; ++j) {
+          // rows past the chunk's end (their k was read from the last valid row) are zero
+          const int r = UT::m0(0) + (l >> 4) * 4 + j;
+          du.acc[0][b][j] = r < cur.len ? du.acc[0][b][j] * __expf(cur.gl - cur.gr[j]) : 0.f;
+        }
       du.template mma_raw<OP, CH / Mma<OP>::KSTEP>(cur.pt.f, cur.dob.f);  // + P^T dO
       OP* dUg = dUTg + tile * DV * CH + (long)v0 * CH;
 #pragma unroll
       for (int b = 0; b < UT::TN; ++b) {
         const int vv = UT::n0(b) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
-        OP u4[4];
+        OP u4[4], n4[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const float u = du.acc[0][b][j];
-          if (DT_) dUT[vv * LU + r0 + j] = from_f<OP>(-u);
+          n4[j] = from_f<OP>(-u);
           u4[j] = from_f<OP>(u);
         }
+        if (DT_) *reinterpret_cast<typename vec4_of<OP>::type*>(dUT + vv * LU + r0) = pack4<OP>(n4);
         // dU' of this chunk for the gradient kernel, transposed (v, r)
         *reinterpret_cast<typename vec4_of<OP>::type*>(dUg + vv * CH + r0) = pack4<OP>(u4);
       }
       __syncthreads();
     }
-    const float gl = cur.gl;
+    const float gl = expf(cur.gl);
 #pragma unroll
     for (int a = 0; a < HT::TM; ++a)
 #pragma unroll
@@ -277,7 +280,21 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
 #pragma unroll
         for (int j = 0; j < 4; ++j) dh.acc[a][b][j] = gl * dh.acc[a][b][j] + inj.acc[a][b][j];
     if constexpr (DT_) dh.template mma<OP, CH>(cur.wt, KRow<OP, LU>{dUT});
-    if (PF) cur = nxt;
+  };
+  const int nch = sp.nch;
+  if constexpr (PF) {
+    Pre p0, p1;
+    if (nch > 0) load_pre(p0, nch - 1);
+    for (int c = nch - 1; c >= 0; c -= 2) {
+      step(c, p0, [&] { if (c - 1 >= 0) load_pre(p1, c - 1); });
+      if (c - 1 >= 0) step(c - 1, p1, [&] { if (c - 2 >= 0) load_pre(p0, c - 2); });
+    }
+  } else {
+    Pre cur;
+    for (int c = nch - 1; c >= 0; --c) {
+      load_pre(cur, c);
+      step(c, cur, [] {});
+    }
   }
   float* dS0p = dS0 + ((long)n * H + h) * DK * DV;
   dh.each([&](int d, int vv, float& x) { dS0p[d * DV + v0 + vv] = x; });

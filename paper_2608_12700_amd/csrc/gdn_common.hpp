@@ -82,6 +82,19 @@ struct KRowM {
   __device__ __forceinline__ const T* ptr(int o, int k) const { return p + o * ld + k; }
 };
 
+// Element (o, k) at p[min(o, rows - 1) * ld + k]: rows past the end repeat the
+// last valid row.  For operands whose rows past a chunk's end only reach
+// results that are masked later, so the load needs no select (and no wait).
+template <typename T>
+struct KRowC {
+  const T* p;
+  long ld;
+  int rows;
+  static constexpr bool kVec = true;
+  __device__ __forceinline__ T get(int o, int k) const { return p[clamp_row(o, rows) * ld + k]; }
+  __device__ __forceinline__ const T* ptr(int o, int k) const { return p + clamp_row(o, rows) * ld + k; }
+};
+
 // Element (o, k) at p[k * LD + o]: o contiguous (a transposed use).
 template <typename T, int LD>
 struct KCol {

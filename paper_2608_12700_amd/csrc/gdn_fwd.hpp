@@ -208,8 +208,8 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     typename UT::template AFr<OP, CH> pf;
     typename HT::template AFr<OP, CH> kh;
     float u[UT::TN][4];
-    float gam[4];
-    float gl;
+    float gr[4];  // G of this lane's rows; exponentiated at use, so the prefetch never waits
+    float gl;     // G_last
   };
   auto load_pre = [&](Pre& p, int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
@@ -229,16 +229,18 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int r = UT::m0(0) + (l >> 4) * 4 + j;
-          const float x = to_f(vp[(long)clamp_row(r, len) * H * DV + UT::n0(b) + (l & 15)]);
-          p.u[b][j] = r < len ? x : 0.f;
+          // U' = V here; its rows past the chunk's end meet only zero columns of
+          // Khat^T and P, so the last valid row may stand in for them
+          p.u[b][j] = to_f(vp[(long)clamp_row(r, len) * H * DV + UT::n0(b) + (l & 15)]);
         }
     }
-    p.qf.load(KRowM<OP>{q + (row0 * H + h) * DK, (long)H * DK, len});
+    // q rows past the chunk's end only reach output rows that are not stored
+    p.qf.load(KRowC<OP>{q + (row0 * H + h) * DK, (long)H * DK, len});
     p.pf.load(KRow<OP, CH>{Pg + tile * CH * CH});
     p.kh.load(KRow<OP, CH>{KhTg + tile * DK * CH});
 #pragma unroll
-    for (int j = 0; j < 4; ++j) p.gam[j] = __expf(gcum[tile * CH + UT::m0(0) + (l >> 4) * 4 + j]);
-    p.gl = __expf(gcum[tile * CH + CH - 1]);
+    for (int j = 0; j < 4; ++j) p.gr[j] = gcum[tile * CH + UT::m0(0) + (l >> 4) * 4 + j];
+    p.gl = gcum[tile * CH + CH - 1];
   };
 
   HT hs;
@@ -249,9 +251,10 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     ok &= finite_f(x);
   });
 
-  Pre cur, nxt;
-  if (sp.nch > 0) load_pre(cur, 0);
-  for (int c = 0; c < sp.nch; ++c) {
+  // One chunk of the carry.  `prefetch` issues the loads of the next chunk
+  // right after the barrier that opens this one; the two fragment buffers
+  // alternate, so nothing is copied and no wait on the new loads is needed.
+  auto step = [&](int c, const Pre& cur, auto&& prefetch) {
     const long tile = (long)(sp.c0 + c) * H + h;
     const long row0 = sp.row0 + (long)c * CH;
     const int len = min(CH, sp.len - c * CH);
@@ -261,11 +264,7 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
       hT[vv * LK + d] = from_f<OP>(x);
     });
     __syncthreads();
-    if (!PF) {
-      if (c > 0) load_pre(cur, c);
-    } else if (c + 1 < sp.nch) {
-      load_pre(nxt, c + 1);
-    }
+    prefetch();
     UT up, ot;
     ot.zero();
     ot.template mma<OP, DK>(cur.qf, KRow<OP, LK>{hT});  // Q h
@@ -282,6 +281,9 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
         for (int j = 0; j < 4; ++j) up.acc[0][b][j] = cur.u[b][j];
     }
+    float gam[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) gam[j] = __expf(cur.gr[j]);
 #pragma unroll
     for (int b = 0; b < UT::TN; ++b) {
       const int vv = UT::n0(b) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
@@ -289,12 +291,12 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         u4[j] = from_f<OP>(up.acc[0][b][j]);
-        ot.acc[0][b][j] *= cur.gam[j];
+        ot.acc[0][b][j] *= gam[j];
       }
       *reinterpret_cast<typename vec4_of<OP>::type*>(UsT + vv * LU + r0) = pack4<OP>(u4);
     }
     __syncthreads();
-    const float gl = cur.gl;
+    const float gl = __expf(cur.gl);
     hs.each([&](int, int, float& x) { x *= gl; });
     hs.template mma<OP, CH>(cur.kh, KRow<OP, LU>{UsT});
     ot.template mma<OP, CH>(cur.pf, KRow<OP, LU>{UsT});  // + P U'
@@ -306,7 +308,21 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
         const int r = UT::m0(0) + (l >> 4) * 4 + j;
         if (r < len) op[(long)r * H * DV + UT::n0(b) + (l & 15)] = from_f<OP>(ot.acc[0][b][j]);
       }
-    if (PF) cur = nxt;
+  };
+  const int nch = sp.nch;
+  if constexpr (PF) {
+    Pre p0, p1;
+    if (nch > 0) load_pre(p0, 0);
+    for (int c = 0; c < nch; c += 2) {
+      step(c, p0, [&] { if (c + 1 < nch) load_pre(p1, c + 1); });
+      if (c + 1 < nch) step(c + 1, p1, [&] { if (c + 2 < nch) load_pre(p0, c + 2); });
+    }
+  } else {
+    Pre cur;
+    for (int c = 0; c < nch; ++c) {
+      load_pre(cur, c);
+      step(c, cur, [] {});
+    }
   }
   float* STp = ST + ((long)n * H + h) * DK * DV;
   hs.each([&](int d, int vv, float& x) { STp[d * DV + v0 + vv] = x; });

@@ -37,7 +37,8 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
                                                   const float* __restrict__ beta, const OP* __restrict__ dO,
                                                   float* __restrict__ gcum, OP* __restrict__ WTg,
                                                   OP* __restrict__ QgTg, OP* __restrict__ dOTg,
-                                                  OP* __restrict__ PTg, int* __restrict__ flag) {
+                                                  OP* __restrict__ PTg, OP* __restrict__ Tg,
+                                                  int* __restrict__ flag) {
   constexpr bool DT_ = VAR != VAR_DECAY;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
@@ -127,6 +128,11 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
     const OP* Tp;
     if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
     constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
+    // T itself, row-major, for the gradient kernel
+    for (int idx = threadIdx.x; idx < CH * CH / VE; idx += blockDim.x) {
+      const int r = idx / (CH / VE), c = (idx - r * (CH / VE)) * VE;
+      *reinterpret_cast<uint4*>(Tg + tile * CH * CH + r * CH + c) = *reinterpret_cast<const uint4*>(Tp + r * LTT + c);
+    }
     // W = T diag(beta e^G) K, written transposed (d, r)
     Tiles<CH, DK, 4, 2> w;
     w.zero();
@@ -283,11 +289,17 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
   };
   const int nch = sp.nch;
   if constexpr (PF) {
-    Pre p0, p1;
-    if (nch > 0) load_pre(p0, nch - 1);
-    for (int c = nch - 1; c >= 0; c -= 2) {
-      step(c, p0, [&] { if (c - 1 >= 0) load_pre(p1, c - 1); });
-      if (c - 1 >= 0) step(c - 1, p1, [&] { if (c - 2 >= 0) load_pre(p0, c - 2); });
+    // The prefetch always issues (before the first chunk it re-reads chunk 0):
+    // a conditional prefetch would leave one path with fewer memory operations
+    // in flight, and the wait counts, merged over both paths, would then wait
+    // for the loads just issued.
+    if (nch > 0) {
+      Pre p0, p1;
+      load_pre(p0, nch - 1);
+      for (int c = nch - 1; c >= 0; c -= 2) {
+        step(c, p0, [&] { load_pre(p1, max(c - 1, 0)); });
+        if (c - 1 >= 0) step(c - 1, p1, [&] { load_pre(p0, max(c - 2, 0)); });
+      }
     }
   } else {
     Pre cur;
@@ -721,10 +733,9 @@ struct GradBF {
   typedef Tiles<DK, CH, WMd, WNr> TD;  // X^T, dQ^T, dK^T: d x 64
   typedef Tiles<VS, CH, WNv, WMv> TY;  // Y^T, U'^T, (K h)^T: VS x 64
   typedef Tiles<CH, CH, 4, 2> TC;      // P, A, dP, dA
-  static constexpr int PH0 = 2 * CH * LC * 4;
   static constexpr int PH1 = (VS * LT + 3 * CH * LV) * 2;
   static constexpr int PH2 = 3 * CH * LT * 2 > 2 * CH * LK * 2 ? 3 * CH * LT * 2 : 2 * CH * LK * 2;
-  static constexpr int UB = PH0 > PH1 ? (PH0 > PH2 ? PH0 : PH2) : (PH1 > PH2 ? PH1 : PH2);
+  static constexpr int UB = PH1 > PH2 ? PH1 : PH2;
 };
 
 __device__ __forceinline__ bf16x8 cvt8(const float (&x)[8]) {
@@ -740,7 +751,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
                                                  const float* __restrict__ g, const float* __restrict__ beta,
                                                  const float* __restrict__ states, const bf16* __restrict__ dO,
                                                  const bf16* __restrict__ dhg, const bf16* __restrict__ dUTg,
-                                                 bf16* __restrict__ dq, bf16* __restrict__ dk,
+                                                 const bf16* __restrict__ Tg, bf16* __restrict__ dq, bf16* __restrict__ dk,
                                                  bf16* __restrict__ dvo, float* __restrict__ dg,
                                                  float* __restrict__ dbeta, int* __restrict__ flag) {
   typedef GradBF<DK, DV> C;
@@ -833,9 +844,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
       }
   };
 
-  // ================= phase 0: gates, P, A, T
-  float* As = reinterpret_cast<float*>(ub);
-  float* Tf = As + CH * LC;
+  // ================= phase 0: gates, P, A; T comes from the prep kernel
   uint4 qk[2][NQK];
 #pragma unroll
   for (int t = 0; t < NQK; ++t) {
@@ -844,6 +853,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     qk[0][t] = keep16(r < len, *reinterpret_cast<const uint4*>(qp + ro));
     qk[1][t] = keep16(r < len, *reinterpret_cast<const uint4*>(kp + ro));
   }
+  uint4 tq = {0u, 0u, 0u, 0u};  // 8 entries of T: row threadIdx.x / 8
+  if constexpr (DT_) tq = *reinterpret_cast<const uint4*>(Tg + tile * CH * CH + threadIdx.x * 8);
   ok &= load_gates<VAR>(g, beta, cp.row0, H, h, len, Gs, Bs);
   PreA pa;
   load_a(pa, 0);
@@ -852,6 +863,17 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     const int idx = threadIdx.x + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
     *reinterpret_cast<uint4*>(Qs + r * LK + c) = qk[0][t];
     *reinterpret_cast<uint4*>(Ks + r * LK + c) = qk[1][t];
+  }
+  if constexpr (DT_) {
+    const int r = threadIdx.x >> 3, c = (threadIdx.x & 7) * 8;
+    *reinterpret_cast<uint4*>(Ts + r * LT + c) = tq;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) TT[(c + j) * LT + r] = elem16<bf16>(tq, j);
+  } else {
+    for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
+      const int r = idx >> 6, c = idx & 63;
+      TT[r * LT + c] = from_f<bf16>(r == c ? 1.f : 0.f);
+    }
   }
   __syncthreads();
   if (threadIdx.x < CH) {
@@ -879,18 +901,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = TC::m0(0) + 4 * lg + j, i = TC::n0(b) + lc;
-        const float x = i < r ? ae.acc[0][b][j] * dd[b][j] : 0.f;
-        ae.acc[0][b][j] = x;
-        As[r * LC + i] = Bs[r] * x;
+        ae.acc[0][b][j] = i < r ? ae.acc[0][b][j] * dd[b][j] : 0.f;
       }
-    __syncthreads();
-    unit_lower_inverse<bf16, LC, LT, true>(As, Tf, Ts, TT);
-  } else {
-    for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
-      const int r = idx >> 6, c = idx & 63;
-      TT[r * LT + c] = from_f<bf16>(r == c ? 1.f : 0.f);
-    }
-    __syncthreads();
   }
 
   // ================= phase 1: value slices
@@ -1236,7 +1248,7 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_prep_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, a.g, a.beta, (const OP*)a.dO, w.gcum,
-                       (OP*)w.W, (OP*)w.QgT, (OP*)w.dOT, (OP*)w.PT, w.flag_prep);
+                       (OP*)w.W, (OP*)w.QgT, (OP*)w.dOT, (OP*)w.PT, (OP*)w.T, w.flag_prep);
   }
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
@@ -1249,7 +1261,8 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
   if (geo.total_chunks > 0 && sizeof(OP) == 2) {
     hipLaunchKernelGGL((k_grad_bf<DK, DV, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
                        (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, a.g, a.beta, a.states,
-                       (const bf16*)a.dO, (const bf16*)w.dh, (const bf16*)w.dUT, (bf16*)a.dq, (bf16*)a.dk_,
+                       (const bf16*)a.dO, (const bf16*)w.dh, (const bf16*)w.dUT, (const bf16*)w.T, (bf16*)a.dq,
+                       (bf16*)a.dk_,
                        (bf16*)a.dv_, a.dg, a.dbeta, w.flag_grad);
   } else if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_grad_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,

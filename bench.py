@@ -29,6 +29,118 @@ import time
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 CH = 64
+ROOT = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bf16_B4_T4096_H16_d128.json")
+STAGE_OF_KERNEL = {"k_prep_fwd": "fwd_prep", "k_scan_fwd": "fwd_scan", "k_prep_bwd": "bwd_prep",
+                   "k_scan_bwd": "bwd_scan", "k_grad_bf": "bwd_grad"}
+COPY_BYTES = 256 * 1024 * 1024
+
+
+def source_digest() -> str:
+    """Digest of every kernel source: measured traffic is reported only while it matches."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2608_12700_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hpp", ".hip", ".cpp", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(stage: str):
+    """HBM bytes per launch of `stage` from the committed counter summary, or None
+    when there is none or the kernels changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_digest") != source_digest():
+        return None
+    k = t.get("kernels", {}).get(stage)
+    return None if k is None else k["hbm_bytes_per_launch"]
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    out = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            out += list(csv.DictReader(fh))
+    return out
+
+
+def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, command):
+    """Turn FETCH_SIZE / WRITE_SIZE passes (KiB per dispatch) over the bench and
+    over a plain copy of COPY_BYTES into HBM bytes per launch of each stage."""
+    def per_kernel(d, counter):
+        acc = {}
+        for r in _counter_rows(d):
+            if r["Counter_Name"] != counter:
+                continue
+            for k, st in STAGE_OF_KERNEL.items():
+                if k in r["Kernel_Name"]:
+                    acc.setdefault(st, []).append(float(r["Counter_Value"]))
+        return {st: sum(v) / len(v) for st, v in acc.items()}
+
+    def copy_kib(d, counter):
+        vals = [float(r["Counter_Value"]) for r in _counter_rows(d) if r["Counter_Name"] == counter]
+        return max(vals)  # the copy is the largest dispatch of the calibration run
+    fscale = COPY_BYTES / 1024.0 / copy_kib(calib_fetch_dir, "FETCH_SIZE")
+    wscale = COPY_BYTES / 1024.0 / copy_kib(calib_write_dir, "WRITE_SIZE")
+    f, w = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+    km = kernel_model(4, 4096, 16, 128, 128, 2)
+    kern = {}
+    for st in sorted(f):
+        b = (f[st] * fscale + w.get(st, 0.0) * wscale) * 1024.0
+        kern[st] = {"fetch_kib": round(f[st], 1), "write_kib": round(w.get(st, 0.0), 1),
+                    "hbm_bytes_per_launch": int(b), "algorithmic_bytes_per_launch": int(km[st][0]),
+                    "ratio": round(b / km[st][0], 3)}
+    return {"source_digest": source_digest(), "command": command,
+            "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4),
+            "calibration": f"plain device copy of {COPY_BYTES} bytes (bench.py --copy-kernel)",
+            "kernels": kern}
+
+
+def summarize_trace(trace_dir, command):
+    """Markdown table of a `rocprofv3 --kernel-trace --stats --output-format csv` run."""
+    import csv
+    import glob
+    import re
+    f = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)[0]
+    with open(f) as fh:
+        rows = list(csv.DictReader(fh))
+
+    def short(n):
+        m = re.search(r"gdn\d*(k_\w+?)I(.*?)EE", n)
+        if not m:
+            return n[:60]
+        nums = re.findall(r"Li(\d+)E", m.group(2))
+        return f"{m.group(1)}<{','.join(nums)}>" + (" bf16" if "DF16b" in m.group(2) else "")
+    out = ["# Kernel trace: gated delta rule fwd+bwd, bf16 I/O, B=4 T=4096 H=16 dk=dv=128", "",
+           "Command (from the repository root, one MI355X):", "", "```", command, "```", "",
+           "| kernel | calls | average (us) | total (us) | % |", "|---|---:|---:|---:|---:|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        if float(r["Percentage"]) < 0.2:
+            continue
+        out.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                   f"{float(r['TotalDurationNs']) / 1e3:.1f} | {float(r['Percentage']):.1f} |")
+    return "\n".join(out) + "\n"
+
+
+def copy_kernel():
+    """A plain device copy of COPY_BYTES, three times: the counter calibration run."""
+    import torch
+    a_ = torch.randn(COPY_BYTES // 4, device="cuda")
+    b_ = torch.empty_like(a_)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b_.copy_(a_)
+    torch.cuda.synchronize()
+    print(f"copied {COPY_BYTES} bytes x3", flush=True)
 
 
 def kernel_model(B, T, H, dk, dv, es, N=None):
@@ -50,14 +162,14 @@ def kernel_model(B, T, H, dk, dv, es, N=None):
         # q, W, Khat^T, P, U, gcum -> chunk states, o
         "fwd_scan": (3 * qk + pp + CH * dv * 4 + g4 + st + vv,
                      3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
-        # q, k, g, beta, dO -> gcum, W^T, (diag(e^G) Q)^T, dO^T, P^T
-        "bwd_prep": (2 * qk + 2 * g4 + vv + g4 + 2 * qk + vv + pp,
+        # q, k, g, beta, dO -> gcum, W^T, (diag(e^G) Q)^T, dO^T, P^T, T
+        "bwd_prep": (2 * qk + 2 * g4 + vv + g4 + 2 * qk + vv + 2 * pp,
                      3 * 2 * CH * CH * dk + CH ** 3 / 3),
         # k, gcum, W^T, Qg^T, dO^T, P^T -> dh (I/O dtype), dU'^T
         "bwd_scan": (3 * qk + g4 + vv + pp + dk * dv * es + vv,
                      3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
-        # q, k, v, g, beta, states, dO, dh, dU'^T -> dq, dk, dv, dg, dbeta
-        "bwd_grad": (2 * qk + vv + 2 * g4 + st + vv + dk * dv * es + vv + 2 * qk + vv + 2 * g4,
+        # q, k, v, g, beta, T, states, dO, dh, dU'^T -> dq, dk, dv, dg, dbeta
+        "bwd_grad": (2 * qk + vv + 2 * g4 + pp + st + vv + dk * dv * es + vv + 2 * qk + vv + 2 * g4,
                      5 * 2 * CH * CH * dk + CH ** 3 / 3 + 4 * CH ** 3 + 5 * 2 * CH * dk * dv
                      + 5 * 2 * CH * CH * dv),
     }
@@ -156,7 +268,29 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--stages", action="store_true", help="also print per-stage timings to stderr")
+    ap.add_argument("--copy-kernel", action="store_true",
+                    help="only run a plain device copy (calibrates the HBM byte counters)")
+    ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="write the traffic summary from four rocprofv3 --pmc output folders")
+    ap.add_argument("--summarize-trace", metavar="TRACE", help="write the kernel-trace summary of a "
+                    "rocprofv3 --kernel-trace --stats --output-format csv folder")
+    ap.add_argument("--command", default="", help="the profiling command recorded in the summary")
     a = ap.parse_args(argv)
+    if a.copy_kernel:
+        copy_kernel()
+        return 0
+    if a.summarize_trace:
+        md = summarize_trace(a.summarize_trace, a.command)
+        with open(os.path.join(ROOT, "profiles", "kernel_trace_bf16_B4_T4096_H16_d128.md"), "w") as fh:
+            fh.write(md)
+        print(md)
+        return 0
+    if a.summarize_counters:
+        t = summarize_counters(*a.summarize_counters, a.command)
+        with open(TRAFFIC_FILE, "w") as fh:
+            json.dump(t, fh, indent=1)
+        print(json.dumps(t))
+        return 0
     if a.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); the path shards over "
               f"(sequence, head) streams with no communication, so N GPUs run N independent copies.",
@@ -265,7 +399,7 @@ def main(argv=None):
                                "dk=dv=128 chunk=64", "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "chunk": CH, "global_batch": B, "seq_len": T, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom),
                      "algorithmic_bytes_per_launch": int(dom_bytes),
                      "avg_launch_ms": round(stage_ms[dom], 4),
                      "mfma_tflops": round(dom_flops / dom_s / 1e12, 1)},

@@ -117,6 +117,7 @@ void layout_fwd(const Shape& s, char* base, FwdWs* w, size_t* total) {
   w->U = b.take<float>(tiles * kChunk * s.dv);
   w->KhT = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->P = b.take<char>(tiles * kChunk * kChunk * s.es);
+  w->Qg = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->exact = nullptr;  // the exact forward needs no scratch
   *total = b.off;
 }

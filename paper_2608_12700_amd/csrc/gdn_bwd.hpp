@@ -213,7 +213,7 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     const int len = min(CH, sp.len - c * CH);
     p.qg.load(KRow<OP, CH>{QgTg + tile * DK * CH});
     p.dob.load(KRow<OP, CH>{dOTg + tile * DV * CH + (long)v0 * CH});
-    p.gl = gcum[tile * CH + CH - 1];
+    p.gl = gcum[tile * CH + CH - 1 + opaque_zero()];  // vector load: see opaque_zero
     p.kf.load(KRowC<OP>{k + (row0 * H + h) * DK, (long)H * DK, len});  // rows past the end: masked in dU'
     p.len = len;
     if constexpr (DT_) p.wt.load(KRow<OP, CH>{WTg + tile * DK * CH});

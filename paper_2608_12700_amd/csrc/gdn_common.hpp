@@ -42,6 +42,39 @@ __device__ __forceinline__ bool finite_f(float x) {
   return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
 }
 
+// A zero the compiler cannot see through, held in a vector register.  Added to
+// an otherwise uniform index it keeps a prefetch on the vector memory path: a
+// uniform address becomes a scalar load, and copying its result into the
+// prefetch registers makes the wave wait for it on the spot.
+__device__ __forceinline__ int opaque_zero() {
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return z;
+}
+
+// Layout of a pre-arranged MFMA operand of K columns (contraction index k) in
+// HBM.  bf16: fragment-major -- the 8 elements lane l contributes to k-step s
+// of 16-row tile mt are contiguous and the 64 lanes' pieces of one (mt, s)
+// form one 1 KiB block, so a wave's fragment load reads whole cache lines.
+// fp32: row-major.  Runs of 4 (or 8) consecutive k starting at a multiple of 4
+// (or 8) stay contiguous in both.
+template <typename OP, int K>
+__device__ __forceinline__ long op_off(int m, int k) {
+  if constexpr (sizeof(OP) == 2)
+    return ((long)((m >> 4) * (K / 32) + (k >> 5)) * 64 + (m & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
+  else
+    return (long)m * K + k;
+}
+
+// Layout of a 64 x D fp32 chunk operand read as accumulator tiles of
+// Tiles<64, BV, 4, 1> (one 16-row tile per wave, BV-column value tiles): the
+// four rows r..r+3 (r % 4 == 0) of column v that one lane holds are one float4,
+// and the 64 lanes' float4 of one 16 x 16 tile are one 1 KiB block.
+template <int BV>
+__device__ __forceinline__ long cfrag_off(int r, int v) {
+  return ((((long)(v / BV) * 4 + (r >> 4)) * (BV / 16) + ((v % BV) >> 4)) * 64 + (v & 15) + 16 * ((r & 15) >> 2)) * 4;
+}
+
 // Masked tile rows: rows r >= len of a chunk are read from row len - 1
 // (len >= 1 for every chunk) and zeroed with a select afterwards.  Keeping
 // the load itself unconditional matters: a branch around a load forces the

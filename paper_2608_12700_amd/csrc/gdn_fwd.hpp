@@ -14,6 +14,8 @@
 //          The carry splits over value columns with no communication.
 #pragma once
 
+#include <type_traits>
+
 #include "gdn_chunk.hpp"
 #include "gdn_exact.hpp"
 #include "gdn_launch.hpp"
@@ -26,7 +28,7 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
                                                   const float* __restrict__ g, const float* __restrict__ beta,
                                                   float* __restrict__ gcum, OP* __restrict__ Wg,
                                                   float* __restrict__ Ug, OP* __restrict__ KhTg,
-                                                  OP* __restrict__ Pg, int* __restrict__ flag) {
+                                                  OP* __restrict__ Pg, OP* __restrict__ Qgg, int* __restrict__ flag) {
   constexpr bool DT_ = VAR != VAR_DECAY;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
@@ -68,6 +70,18 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
     Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
   }
   __syncthreads();
+  // diag(e^G) Q, the scan's A operand for the output term
+  {
+    OP* Qg = Qgg + tile * CH * DK;
+    for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
+      const int r = idx / (DK / VE), d0 = (idx - r * (DK / VE)) * VE;
+      const uint4 qv = *reinterpret_cast<const uint4*>(Qs + r * LK + d0);
+      OP vals[VE];
+#pragma unroll
+      for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Gam[r] * to_f(elem16<OP>(qv, j)));
+      *reinterpret_cast<uint4*>(Qg + op_off<OP, DK>(r, d0)) = pack16<OP>(vals);
+    }
+  }
   // P[r][i] = (q_r . k_i) e^{G_r - G_i} (i <= r): computed as K Q^T so that a
   // lane's four accumulator rows are four consecutive i of one row r of P
   {
@@ -84,7 +98,7 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
         const int i = i0 + j;
         v4[j] = from_f<OP>(i <= r ? s.acc[0][b][j] * __expf(Gs[r] - Gs[i]) : 0.f);
       }
-      *reinterpret_cast<V4*>(Pt + r * CH + i0) = pack4<OP>(v4);
+      *reinterpret_cast<V4*>(Pt + op_off<OP, CH>(r, i0)) = pack4<OP>(v4);
     }
   }
   if constexpr (DT_) {
@@ -111,7 +125,7 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
       OP vals[VE];
 #pragma unroll
       for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Dte[r0 + j] * to_f(Ks[(r0 + j) * LK + d]));
-      *reinterpret_cast<uint4*>(Kh + d * CH + r0) = pack16<OP>(vals);
+      *reinterpret_cast<uint4*>(Kh + op_off<OP, CH>(d, r0)) = pack16<OP>(vals);
     }
   }
   __syncthreads();  // Q and K are dead from here on
@@ -136,10 +150,11 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
           OP v4[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) v4[j] = from_f<OP>(wt.acc[a][b][j]);
-          *reinterpret_cast<V4*>(Wt + r * DK + d0) = pack4<OP>(v4);
+          *reinterpret_cast<V4*>(Wt + op_off<OP, DK>(r, d0)) = pack4<OP>(v4);
         }
     }
-    // U = T diag(beta) V, per slice of VS value columns, as U^T = (diag(beta) V)^T T^T
+    // U = T diag(beta) V, per slice of VS value columns, stored as the scan's
+    // accumulator tiles (four rows of one column per lane: one float4)
     float* Ut = Ug + tile * CH * DV;
     for (int c0 = 0; c0 < DV; c0 += VS) {
       for (int idx = threadIdx.x; idx < CH * VS / VE; idx += blockDim.x) {
@@ -151,14 +166,14 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
         for (int j = 0; j < VE; ++j) VbT[(v0 + j) * LT + i] = from_f<OP>(Bs[i] * to_f(elem16<OP>(vv, j)));
       }
       __syncthreads();
-      Tiles<VS, CH, 4, 2> ut;
-      ut.zero();
-      ut.template mma<OP, CH>(KRow<OP, LT>{VbT}, KRow<OP, LTT>{Tp});
+      Tiles<CH, VS, 4, 2> uu;
+      uu.zero();
+      uu.template mma<OP, CH>(KRow<OP, LTT>{Tp}, KRow<OP, LT>{VbT});
 #pragma unroll
-      for (int b = 0; b < ut.TN; ++b) {
-        const int r = ut.n0(b) + (l & 15), w0 = ut.m0(0) + (l >> 4) * 4;
-        *reinterpret_cast<float4*>(Ut + r * DV + c0 + w0) =
-            float4{ut.acc[0][b][0], ut.acc[0][b][1], ut.acc[0][b][2], ut.acc[0][b][3]};
+      for (int b = 0; b < uu.TN; ++b) {
+        const int r0 = uu.m0(0) + (l >> 4) * 4, vcol = c0 + uu.n0(b) + (l & 15);
+        *reinterpret_cast<float4*>(Ut + cfrag_off<SCAN_BV>(r0, vcol)) =
+            float4{uu.acc[0][b][0], uu.acc[0][b][1], uu.acc[0][b][2], uu.acc[0][b][3]};
       }
       __syncthreads();
     }
@@ -180,20 +195,23 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
 // into registers while chunk c is computed; only h and U' pass through LDS
 // (two barriers per chunk).
 template <int DK, int DV, int BV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __restrict__ q,
+__global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __restrict__ Qgg,
                                                   const OP* __restrict__ v, const float* __restrict__ S0,
                                                   const float* __restrict__ gcum, const OP* __restrict__ Wg,
                                                   const OP* __restrict__ KhTg, const OP* __restrict__ Pg,
                                                   const float* __restrict__ Ug, float* __restrict__ states,
                                                   float* __restrict__ ST, OP* __restrict__ o,
                                                   int* __restrict__ flag) {
+  static_assert(BV == SCAN_BV, "U is laid out for the scan's value tiles");
   constexpr int NVT = DV / BV;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LU = CH + pad_of<OP>();
+  constexpr int LF = BV + 4;            // row stride of the fp32 state staging
   constexpr bool PF = sizeof(OP) == 2;  // prefetch a chunk ahead (bf16 fragments are compact)
   typedef Tiles<DK, BV, 4, 1> HT;       // carried state slice h[:, v0:v0+BV]
   typedef Tiles<CH, BV, 4, 1> UT;       // U' and output slices
   __shared__ __align__(16) OP hT[BV * LK];
+  __shared__ __align__(16) float hF[DK * LF];  // h in fp32, row-major, for whole-line state stores
   __shared__ __align__(16) OP UsT[BV * LU];
 
   int s, vt;
@@ -208,20 +226,34 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     typename UT::template AFr<OP, CH> pf;
     typename HT::template AFr<OP, CH> kh;
     float u[UT::TN][4];
-    float gr[4];  // G of this lane's rows; exponentiated at use, so the prefetch never waits
-    float gl;     // G_last
+    float gl;  // G_last, exponentiated at use so the prefetch never waits
+  };
+  // A fragments of a pre-arranged operand (fragment-major for bf16, row-major for fp32)
+  auto frags = [&](auto& f, const OP* base, auto tiles_tag, auto k_tag) {
+    typedef decltype(tiles_tag) TT;
+    constexpr int K = decltype(k_tag)::value;
+    if constexpr (sizeof(OP) == 2) {
+#pragma unroll
+      for (int st = 0; st < K / 32; ++st)
+#pragma unroll
+        for (int a = 0; a < TT::TM; ++a)
+          f.f[st][a] = *reinterpret_cast<const bf16x8*>(base + ((long)((TT::m0(a) >> 4) * (K / 32) + st) * 64 + l) * 8);
+    } else {
+      f.load(KRow<OP, K>{base});
+    }
   };
   auto load_pre = [&](Pre& p, int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
     const long row0 = sp.row0 + (long)c * CH;
     const int len = min(CH, sp.len - c * CH);
     if constexpr (VAR != VAR_DECAY) {
-      p.w.load(KRow<OP, DK>{Wg + tile * CH * DK});
-      const float* Ut = Ug + tile * CH * DV + v0;
+      frags(p.w, Wg + tile * CH * DK, UT{}, std::integral_constant<int, DK>{});
+      const float* Ut = Ug + tile * CH * DV;
 #pragma unroll
-      for (int b = 0; b < UT::TN; ++b)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) p.u[b][j] = Ut[(UT::m0(0) + (l >> 4) * 4 + j) * DV + UT::n0(b) + (l & 15)];
+      for (int b = 0; b < UT::TN; ++b) {
+        const float4 x = *reinterpret_cast<const float4*>(Ut + cfrag_off<BV>(UT::m0(0) + (l >> 4) * 4, v0 + UT::n0(b) + (l & 15)));
+        p.u[b][0] = x.x; p.u[b][1] = x.y; p.u[b][2] = x.z; p.u[b][3] = x.w;
+      }
     } else {
       const OP* vp = v + (row0 * H + h) * DV + v0;
 #pragma unroll
@@ -234,13 +266,10 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
           p.u[b][j] = to_f(vp[(long)clamp_row(r, len) * H * DV + UT::n0(b) + (l & 15)]);
         }
     }
-    // q rows past the chunk's end only reach output rows that are not stored
-    p.qf.load(KRowC<OP>{q + (row0 * H + h) * DK, (long)H * DK, len});
-    p.pf.load(KRow<OP, CH>{Pg + tile * CH * CH});
-    p.kh.load(KRow<OP, CH>{KhTg + tile * DK * CH});
-#pragma unroll
-    for (int j = 0; j < 4; ++j) p.gr[j] = gcum[tile * CH + UT::m0(0) + (l >> 4) * 4 + j];
-    p.gl = gcum[tile * CH + CH - 1];
+    frags(p.qf, Qgg + tile * CH * DK, UT{}, std::integral_constant<int, DK>{});
+    frags(p.pf, Pg + tile * CH * CH, UT{}, std::integral_constant<int, CH>{});
+    frags(p.kh, KhTg + tile * DK * CH, HT{}, std::integral_constant<int, CH>{});
+    p.gl = gcum[tile * CH + CH - 1 + opaque_zero()];  // vector load: see opaque_zero
   };
 
   HT hs;
@@ -258,16 +287,35 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     const long tile = (long)(sp.c0 + c) * H + h;
     const long row0 = sp.row0 + (long)c * CH;
     const int len = min(CH, sp.len - c * CH);
-    float* hp = states + tile * DK * DV;
-    hs.each([&](int d, int vv, float& x) {
-      hp[d * DV + v0 + vv] = x;
-      hT[vv * LK + d] = from_f<OP>(x);
-    });
+    // h to LDS: operand copy (4 consecutive d per lane: one 8-byte write) and
+    // fp32 row-major copy for the state store
+#pragma unroll
+    for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+      for (int b = 0; b < HT::TN; ++b) {
+        const int d0 = HT::m0(a) + (l >> 4) * 4, vv = HT::n0(b) + (l & 15);
+        OP h4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          h4[j] = from_f<OP>(hs.acc[a][b][j]);
+          hF[(d0 + j) * LF + vv] = hs.acc[a][b][j];
+        }
+        *reinterpret_cast<typename vec4_of<OP>::type*>(hT + vv * LK + d0) = pack4<OP>(h4);
+      }
     __syncthreads();
     prefetch();
+    {
+      // the chunk state leaves as whole 128-byte rows (BV fp32 of one d)
+      float* hp = states + tile * DK * DV + v0;
+#pragma unroll
+      for (int t = 0; t < DK * BV / 4 / 256; ++t) {
+        const int idx = threadIdx.x + t * 256, d = idx / (BV / 4), c4 = (idx - d * (BV / 4)) * 4;
+        *reinterpret_cast<float4*>(hp + (long)d * DV + c4) = *reinterpret_cast<const float4*>(hF + d * LF + c4);
+      }
+    }
     UT up, ot;
     ot.zero();
-    ot.template mma<OP, DK>(cur.qf, KRow<OP, LK>{hT});  // Q h
+    ot.template mma<OP, DK>(cur.qf, KRow<OP, LK>{hT});  // diag(e^G) Q h
     if constexpr (VAR != VAR_DECAY) {
       up.zero();
       up.template mma<OP, DK>(cur.w, KRow<OP, LK>{hT});
@@ -281,18 +329,12 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
         for (int j = 0; j < 4; ++j) up.acc[0][b][j] = cur.u[b][j];
     }
-    float gam[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) gam[j] = __expf(cur.gr[j]);
 #pragma unroll
     for (int b = 0; b < UT::TN; ++b) {
       const int vv = UT::n0(b) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
       OP u4[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        u4[j] = from_f<OP>(up.acc[0][b][j]);
-        ot.acc[0][b][j] *= gam[j];
-      }
+      for (int j = 0; j < 4; ++j) u4[j] = from_f<OP>(up.acc[0][b][j]);
       *reinterpret_cast<typename vec4_of<OP>::type*>(UsT + vv * LU + r0) = pack4<OP>(u4);
     }
     __syncthreads();
@@ -311,11 +353,17 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
   };
   const int nch = sp.nch;
   if constexpr (PF) {
-    Pre p0, p1;
-    if (nch > 0) load_pre(p0, 0);
-    for (int c = 0; c < nch; c += 2) {
-      step(c, p0, [&] { if (c + 1 < nch) load_pre(p1, c + 1); });
-      if (c + 1 < nch) step(c + 1, p1, [&] { if (c + 2 < nch) load_pre(p0, c + 2); });
+    // The prefetch always issues (past the last chunk it re-reads that chunk):
+    // a conditional prefetch would leave one path with fewer memory operations
+    // in flight, and the wait counts, merged over both paths, would then wait
+    // for the loads just issued.
+    if (nch > 0) {
+      Pre p0, p1;
+      load_pre(p0, 0);
+      for (int c = 0; c < nch; c += 2) {
+        step(c, p0, [&] { load_pre(p1, min(c + 1, nch - 1)); });
+        if (c + 1 < nch) step(c + 1, p1, [&] { load_pre(p0, min(c + 2, nch - 1)); });
+      }
     }
   } else {
     Pre cur;
@@ -348,13 +396,13 @@ static hipError_t launch_fwd_t(const FwdArgs& a) {
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_prep_fwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, w.gcum,
-                       (OP*)w.W, w.U, (OP*)w.KhT, (OP*)w.P, w.flag_prep);
+                       (OP*)w.W, w.U, (OP*)w.KhT, (OP*)w.P, (OP*)w.Qg, w.flag_prep);
   }
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
-                       (const OP*)a.q, (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, (const OP*)w.KhT,
+                       (const OP*)w.Qg, (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, (const OP*)w.KhT,
                        (const OP*)w.P, w.U, a.states, a.ST, (OP*)a.o, w.flag_scan);
   }
   stage_mark(a.events, 2, a.stream);

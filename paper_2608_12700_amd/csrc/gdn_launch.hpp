@@ -18,6 +18,7 @@ struct FwdWs {
   float* U;        // [chunks*H*64*dv]
   void* KhT;       // [chunks*H*dk*64] operand dtype, (e^{G_last-G} K)^T
   void* P;         // [chunks*H*64*64] operand dtype, (Q K^T) * D
+  void* Qg;        // [chunks*H*64*dk] operand dtype, diag(e^G) Q
   float* exact;    // exact-path scratch
 };
 

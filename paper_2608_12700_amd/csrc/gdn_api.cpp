@@ -135,6 +135,7 @@ void layout_bwd(const Shape& s, char* base, BwdWs* w, size_t* total) {
   w->dOT = b.take<char>(tiles * kChunk * s.dv * s.es);
   w->PT = b.take<char>(tiles * kChunk * kChunk * s.es);
   w->T = b.take<char>(tiles * kChunk * kChunk * s.es);
+  w->Kh = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->dh = b.take<char>(tiles * (size_t)s.dk * s.dv * s.es);
   w->dUT = b.take<char>(tiles * kChunk * s.dv * s.es);
   w->grad_scratch = b.take<char>(s.es == 4 ? tiles * (size_t)grad_region_bytes((int)s.dk, 4) : 0);

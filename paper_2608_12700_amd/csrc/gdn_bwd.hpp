@@ -38,7 +38,7 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
                                                   float* __restrict__ gcum, OP* __restrict__ WTg,
                                                   OP* __restrict__ QgTg, OP* __restrict__ dOTg,
                                                   OP* __restrict__ PTg, OP* __restrict__ Tg,
-                                                  int* __restrict__ flag) {
+                                                  OP* __restrict__ Khg, int* __restrict__ flag) {
   constexpr bool DT_ = VAR != VAR_DECAY;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
@@ -58,7 +58,7 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   __shared__ __align__(16) char r2[R2];
   __shared__ __align__(16) OP KbT[DT_ ? DK * LT : 1];  // (diag(beta e^G) K)^T
   __shared__ __align__(16) char r4[R4];
-  __shared__ float Gs[CH], Bs[CH], Gam[CH];
+  __shared__ float Gs[CH], Bs[CH], Gam[CH], Dte[CH];
   OP* Qs = reinterpret_cast<OP*>(r1);
   float* Tf = reinterpret_cast<float*>(r1);
   OP* Ks = reinterpret_cast<OP*>(r2);
@@ -77,6 +77,7 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   if (threadIdx.x < CH) {
     gcum[tile * CH + threadIdx.x] = Gs[threadIdx.x];
     Gam[threadIdx.x] = __expf(Gs[threadIdx.x]);
+    Dte[threadIdx.x] = __expf(Gs[CH - 1] - Gs[threadIdx.x]);
   }
   __syncthreads();
   // P^T, written (i, r): the scan's A operand for P^T dO
@@ -94,7 +95,7 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
         const int r = r0 + j;
         v4[j] = from_f<OP>(i <= r ? p.acc[0][b][j] * __expf(Gs[r] - Gs[i]) : 0.f);
       }
-      *reinterpret_cast<V4*>(Pt + i * CH + r0) = pack4<OP>(v4);
+      *reinterpret_cast<V4*>(Pt + op_off<OP, CH>(i, r0)) = pack4<OP>(v4);
     }
   }
   // (diag(e^G) Q)^T for the scan's injection term
@@ -105,7 +106,19 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
       OP vals[VE];
 #pragma unroll
       for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Gam[r0 + j] * to_f(Qs[(r0 + j) * LK + d]));
-      *reinterpret_cast<uint4*>(Qg + d * CH + r0) = pack16<OP>(vals);
+      *reinterpret_cast<uint4*>(Qg + op_off<OP, CH>(d, r0)) = pack16<OP>(vals);
+    }
+  }
+  // Khat = diag(e^{G_last - G}) K, the scan's A operand for dU' (rows past the end stay zero)
+  {
+    OP* Kh = Khg + tile * CH * DK;
+    for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
+      const int r = idx / (DK / VE), d0 = (idx - r * (DK / VE)) * VE;
+      const uint4 kv = *reinterpret_cast<const uint4*>(Ks + r * LK + d0);
+      OP vals[VE];
+#pragma unroll
+      for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Dte[r] * to_f(elem16<OP>(kv, j)));
+      *reinterpret_cast<uint4*>(Kh + op_off<OP, DK>(r, d0)) = pack16<OP>(vals);
     }
   }
   if constexpr (DT_) {
@@ -144,7 +157,7 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
       OP v4[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) v4[j] = from_f<OP>(w.acc[0][b][j]);
-      *reinterpret_cast<V4*>(Wt + d * CH + r0) = pack4<OP>(v4);
+      *reinterpret_cast<V4*>(Wt + op_off<OP, CH>(d, r0)) = pack4<OP>(v4);
     }
   }
   // dO^T, in slices of VS value columns (dO slices reuse the A region)
@@ -153,13 +166,13 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   for (int c0 = 0; c0 < DV; c0 += VS) {
     ok &= load_rows<VS, LVS>(dop + c0, (long)H * DV, cp.len, dOs);
     __syncthreads();
-    OP* dOt = dOTg + tile * DV * CH + (long)c0 * CH;
+    OP* dOt = dOTg + tile * DV * CH;
     for (int idx = threadIdx.x; idx < VS * CH / VE; idx += blockDim.x) {
       const int vv = idx / (CH / VE), r0 = (idx - vv * (CH / VE)) * VE;
       OP vals[VE];
 #pragma unroll
       for (int j = 0; j < VE; ++j) vals[j] = dOs[(r0 + j) * LVS + vv];
-      *reinterpret_cast<uint4*>(dOt + vv * CH + r0) = pack16<OP>(vals);
+      *reinterpret_cast<uint4*>(dOt + op_off<OP, CH>(c0 + vv, r0)) = pack16<OP>(vals);
     }
     __syncthreads();
   }
@@ -175,7 +188,7 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
 //   dU' = P^T dO + diag(e^{G_last - G}) K dh
 //   dh <- e^{G_last} dh + (diag(e^G) Q)^T dO - W^T dU'
 template <int DK, int DV, int BV, typename OP, int VAR>
-__global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __restrict__ k,
+__global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __restrict__ Khg,
                                                   const float* __restrict__ dST, const float* __restrict__ gcum,
                                                   const OP* __restrict__ WTg, const OP* __restrict__ QgTg,
                                                   const OP* __restrict__ dOTg, const OP* __restrict__ PTg,
@@ -203,23 +216,19 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     typename HT::template AFr<OP, CH> qg;
     typename HT::template BFr<OP, CH> dob;
     typename UT::template AFr<OP, CH> pt;
-    float gr[4];  // G of this lane's rows; exponentiated at use, so the prefetch never waits
-    float gl;     // G_last
-    int len;      // valid rows of the chunk
+    float gl;  // G_last, exponentiated at use so the prefetch never waits
   };
   auto load_pre = [&](Pre& p, int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
-    const long row0 = sp.row0 + (long)c * CH;
-    const int len = min(CH, sp.len - c * CH);
-    p.qg.load(KRow<OP, CH>{QgTg + tile * DK * CH});
-    p.dob.load(KRow<OP, CH>{dOTg + tile * DV * CH + (long)v0 * CH});
+    load_op_frags<HT, OP, CH>(p.qg, QgTg + tile * DK * CH);
+    if constexpr (sizeof(OP) == 2)
+      load_op_frags_b<HT, OP, CH>(p.dob, dOTg + tile * DV * CH + op_off<OP, CH>(v0, 0));
+    else
+      p.dob.load(KRow<OP, CH>{dOTg + tile * DV * CH + (long)v0 * CH});
     p.gl = gcum[tile * CH + CH - 1 + opaque_zero()];  // vector load: see opaque_zero
-    p.kf.load(KRowC<OP>{k + (row0 * H + h) * DK, (long)H * DK, len});  // rows past the end: masked in dU'
-    p.len = len;
-    if constexpr (DT_) p.wt.load(KRow<OP, CH>{WTg + tile * DK * CH});
-    p.pt.load(KRow<OP, CH>{PTg + tile * CH * CH});
-#pragma unroll
-    for (int j = 0; j < 4; ++j) p.gr[j] = gcum[tile * CH + UT::m0(0) + (l >> 4) * 4 + j];
+    load_op_frags<UT, OP, DK>(p.kf, Khg + tile * CH * DK);
+    if constexpr (DT_) load_op_frags<HT, OP, CH>(p.wt, WTg + tile * DK * CH);
+    load_op_frags<UT, OP, CH>(p.pt, PTg + tile * CH * CH);
   };
 
   HT dh;
@@ -235,14 +244,32 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
   // fragment buffers alternate, so nothing is copied.
   auto step = [&](int c, const Pre& cur, auto&& prefetch) {
     const long tile = (long)(sp.c0 + c) * H + h;
-    OP* dhp = dhg + tile * DK * DV;
-    dh.each([&](int d, int vv, float& x) {
-      const OP xo = from_f<OP>(x);
-      dhp[d * DV + v0 + vv] = xo;
-      dhT[vv * LK + d] = xo;
-    });
+    // dh to LDS (4 consecutive d per lane: one vector write)
+#pragma unroll
+    for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+      for (int b = 0; b < HT::TN; ++b) {
+        const int d0 = HT::m0(a) + (l >> 4) * 4, vv = HT::n0(b) + (l & 15);
+        OP h4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) h4[j] = from_f<OP>(dh.acc[a][b][j]);
+        *reinterpret_cast<typename vec4_of<OP>::type*>(dhT + vv * LK + d0) = pack4<OP>(h4);
+      }
     __syncthreads();
     prefetch();
+    {
+      // dh entering this chunk, for the gradient kernel, in its fragment order
+      constexpr int VE = 16 / (int)sizeof(OP);
+      OP* dhp = dhg + tile * DK * DV;
+#pragma unroll
+      for (int t = 0; t < DK * BV / VE / 256; ++t) {
+        const int idx = threadIdx.x + t * 256, d = idx / (BV / VE), vq = (idx - d * (BV / VE)) * VE;
+        OP vals[VE];
+#pragma unroll
+        for (int j = 0; j < VE; ++j) vals[j] = dhT[(vq + j) * LK + d];
+        *reinterpret_cast<uint4*>(dhp + op_off<OP, DV>(d, v0 + vq)) = pack16<OP>(vals);
+      }
+    }
     HT inj;  // (diag(e^G) Q)^T dO, independent of the carry
     inj.zero();
     inj.template mma<OP, CH>(cur.qg, cur.dob);
@@ -251,17 +278,9 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
       // family member; only the delta rule feeds it back into the carry)
       UT du;
       du.zero();
-      du.template mma<OP, DK>(cur.kf, KRow<OP, LK>{dhT});
-#pragma unroll
-      for (int b = 0; b < UT::TN; ++b)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          // rows past the chunk's end (their k was read from the last valid row) are zero
-          const int r = UT::m0(0) + (l >> 4) * 4 + j;
-          du.acc[0][b][j] = r < cur.len ? du.acc[0][b][j] * __expf(cur.gl - cur.gr[j]) : 0.f;
-        }
+      du.template mma<OP, DK>(cur.kf, KRow<OP, LK>{dhT});  // Khat dh
       du.template mma_raw<OP, CH / Mma<OP>::KSTEP>(cur.pt.f, cur.dob.f);  // + P^T dO
-      OP* dUg = dUTg + tile * DV * CH + (long)v0 * CH;
+      OP* dUg = dUTg + tile * DV * CH;
 #pragma unroll
       for (int b = 0; b < UT::TN; ++b) {
         const int vv = UT::n0(b) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
@@ -273,8 +292,8 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
           u4[j] = from_f<OP>(u);
         }
         if (DT_) *reinterpret_cast<typename vec4_of<OP>::type*>(dUT + vv * LU + r0) = pack4<OP>(n4);
-        // dU' of this chunk for the gradient kernel, transposed (v, r)
-        *reinterpret_cast<typename vec4_of<OP>::type*>(dUg + vv * CH + r0) = pack4<OP>(u4);
+        // dU' of this chunk for the gradient kernel, transposed (v, r), in its fragment order
+        *reinterpret_cast<typename vec4_of<OP>::type*>(dUg + op_off<OP, CH>(v0 + vv, r0)) = pack4<OP>(u4);
       }
       __syncthreads();
     }
@@ -813,7 +832,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
     for (int s = 0; s < CH / 32; ++s)
 #pragma unroll
-      for (int a = 0; a < TY::TM; ++a) p.du[s][a] = M::load(KRow<bf16, CH>{dUp + (long)c0 * CH}, TY::m0(a), 32 * s);
+      for (int a = 0; a < TY::TM; ++a)
+        p.du[s][a] = *reinterpret_cast<const bf16x8*>(dUp + op_off<bf16, CH>(c0 + TY::m0(a), 32 * s) + l * 8);
     if constexpr (DT_) {
 #pragma unroll
       for (int s = 0; s < DK / 32; ++s)
@@ -840,7 +860,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
         const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
         p.hx[s][a][0] = x0.x; p.hx[s][a][1] = x0.y; p.hx[s][a][2] = x0.z; p.hx[s][a][3] = x0.w;
         p.hx[s][a][4] = x1.x; p.hx[s][a][5] = x1.y; p.hx[s][a][6] = x1.z; p.hx[s][a][7] = x1.w;
-        p.dh[s][a] = M::load(KRow<bf16, DV>{dhp + c0}, TD::m0(a), 32 * s);
+        p.dh[s][a] = *reinterpret_cast<const bf16x8*>(dhp + op_off<bf16, DV>(TD::m0(a), c0 + 32 * s) + l * 8);
       }
   };
 
@@ -1248,13 +1268,13 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_prep_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, a.g, a.beta, (const OP*)a.dO, w.gcum,
-                       (OP*)w.W, (OP*)w.QgT, (OP*)w.dOT, (OP*)w.PT, (OP*)w.T, w.flag_prep);
+                       (OP*)w.W, (OP*)w.QgT, (OP*)w.dOT, (OP*)w.PT, (OP*)w.T, (OP*)w.Kh, w.flag_prep);
   }
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
-                       (const OP*)a.k, a.dST, w.gcum, (const OP*)w.W, (const OP*)w.QgT, (const OP*)w.dOT,
+                       (const OP*)w.Kh, a.dST, w.gcum, (const OP*)w.W, (const OP*)w.QgT, (const OP*)w.dOT,
                        (const OP*)w.PT, (OP*)w.dh, (OP*)w.dUT, a.dS0, w.flag_scan);
   }
   stage_mark(a.events, 2, a.stream);

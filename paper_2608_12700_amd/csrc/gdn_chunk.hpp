@@ -259,6 +259,37 @@ __device__ __forceinline__ void unit_lower_inverse(const float* As, float* Tf, O
   __syncthreads();
 }
 
+// A fragments (for the rows this wave owns in Tiles TT) of a pre-arranged
+// operand with K contraction columns, laid out by op_off: one contiguous
+// 16-byte read per lane for bf16, the row-major view for fp32.
+template <class TT, typename OP, int K>
+__device__ __forceinline__ void load_op_frags(typename TT::template AFr<OP, K>& f, const OP* base) {
+  if constexpr (sizeof(OP) == 2) {
+    const int l = lane_id();
+#pragma unroll
+    for (int s = 0; s < K / 32; ++s)
+#pragma unroll
+      for (int a = 0; a < TT::TM; ++a)
+        f.f[s][a] = *reinterpret_cast<const bf16x8*>(base + ((long)((TT::m0(a) >> 4) * (K / 32) + s) * 64 + l) * 8);
+  } else {
+    f.load(KRow<OP, K>{base});
+  }
+}
+// The same for B fragments (the columns this wave owns), n playing the row.
+template <class TT, typename OP, int K>
+__device__ __forceinline__ void load_op_frags_b(typename TT::template BFr<OP, K>& f, const OP* base) {
+  if constexpr (sizeof(OP) == 2) {
+    const int l = lane_id();
+#pragma unroll
+    for (int s = 0; s < K / 32; ++s)
+#pragma unroll
+      for (int b = 0; b < TT::TN; ++b)
+        f.f[s][b] = *reinterpret_cast<const bf16x8*>(base + ((long)((TT::n0(b) >> 4) * (K / 32) + s) * 64 + l) * 8);
+  } else {
+    f.load(KRow<OP, K>{base});
+  }
+}
+
 // XCD-aware placement of the (stream, value-tile) blocks of a state scan:
 // blocks are dealt to the 8 XCDs round robin, so the value tiles of one
 // stream get block ids that are equal modulo 8 and share that XCD's L2.

@@ -46,6 +46,7 @@ struct BwdWs {
   void* dOT;       // [chunks*H*dv*64] operand dtype, dO^T
   void* PT;        // [chunks*H*64*64] operand dtype, P^T
   void* T;         // [chunks*H*64*64] operand dtype, T = (I + A)^{-1}
+  void* Kh;        // [chunks*H*64*dk] operand dtype, diag(e^{G_last - G}) K
   void* dh;        // [chunks*H*dk*dv] operand dtype: state gradient after each chunk
   void* dUT;       // [chunks*H*dv*64] operand dtype: dU' of each chunk, transposed
   void* grad_scratch;  // [chunks*H*grad_region_bytes] fp32 operands only

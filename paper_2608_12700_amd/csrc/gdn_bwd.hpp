@@ -827,7 +827,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
     for (int t = 0; t < NDO; ++t) {
       const int idx = threadIdx.x + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
-      p.dov[t] = keep16(r < len, *reinterpret_cast<const uint4*>(dop + clamp_row(r, len) * rsv + c0 + c));
+      p.dov[t] = *reinterpret_cast<const uint4*>(dop + clamp_row(r, len) * rsv + c0 + c);  // masked at use
     }
 #pragma unroll
     for (int s = 0; s < CH / 32; ++s)
@@ -846,7 +846,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
         for (int b = 0; b < TY::TN; ++b) {
           const int r = TY::n0(b) + lc;
-          p.vb[a][b] = keep8(r < len, *reinterpret_cast<const uint2*>(vp + clamp_row(r, len) * rsv + c0 + TY::m0(a) + 4 * lg));
+          // masked at use
+          p.vb[a][b] = *reinterpret_cast<const uint2*>(vp + clamp_row(r, len) * rsv + c0 + TY::m0(a) + 4 * lg);
         }
     }
   };
@@ -972,7 +973,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
           const int v0 = TY::m0(a) + 4 * lg;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const float vx = to_f(elem4<bf16>(pa.vb[a][b], j));
+            const float vx = r < len ? to_f(elem4<bf16>(pa.vb[a][b], j)) : 0.f;
             ok &= finite_f(vx);
             RT[(v0 + j) * LT + r] = from_f<bf16>(br * (vx - gr * kht.acc[a][b][j]));
           }
@@ -1008,7 +1009,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
             const float y = yt.acc[a][b][j];
             d4[j] = from_f<bf16>(br * y);
             y4[j] = from_f<bf16>(-y);
-            if (DT_) dbY[b] += to_f(elem4<bf16>(pa.vb[a][b], j)) * y;
+            if (DT_) dbY[b] += (r < len ? to_f(elem4<bf16>(pa.vb[a][b], j)) : 0.f) * y;
           }
           if (r < len) *reinterpret_cast<uint2*>(dvp + r * rsv + c0 + v0) = pack4<bf16>(d4);
           if (DT_) *reinterpret_cast<uint2*>(Ys + r * LV + v0) = pack4<bf16>(y4);
@@ -1018,7 +1019,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
     for (int t = 0; t < NDO; ++t) {
       const int idx = threadIdx.x + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
-      *reinterpret_cast<uint4*>(dOs + r * LV + c) = pa.dov[t];
+      *reinterpret_cast<uint4*>(dOs + r * LV + c) = keep16(r < len, pa.dov[t]);
     }
     if constexpr (!DT_) {
       // the scalar-decay member has U' = V

@@ -70,9 +70,24 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
   const int l = lane_id();
+  // every input row of the block is requested up front: q, k, then the dO
+  // slices (slice t of VS columns is piece t of each thread)
+  RowsIn<DK, 512, OP> qin, kin;
+  qin.load(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len);
+  kin.load(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len);
+  const OP* dop = dO + (cp.row0 * H + h) * DV;
+  constexpr int NSL = DV / VS, NPS = CH * VS / VE / 512;  // slices; pieces per thread and slice
+  uint4 din[NSL][NPS];
+#pragma unroll
+  for (int t = 0; t < NSL; ++t)
+#pragma unroll
+    for (int p = 0; p < NPS; ++p) {
+      const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), c = t * VS + (idx % (VS / VE)) * VE;
+      din[t][p] = *reinterpret_cast<const uint4*>(dop + (long)clamp_row(i, cp.len) * H * DV + c);
+    }
   bool ok = load_gates<VAR>(g, beta, cp.row0, H, h, cp.len, Gs, Bs);
-  ok &= load_rows<DK, LK>(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Qs);
-  ok &= load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
+  ok &= qin.template stage<LK>(Qs, cp.len);
+  ok &= kin.template stage<LK>(Ks, cp.len);
   __syncthreads();
   if (threadIdx.x < CH) {
     gcum[tile * CH + threadIdx.x] = Gs[threadIdx.x];
@@ -162,9 +177,16 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   }
   // dO^T, in slices of VS value columns (dO slices reuse the A region)
   __syncthreads();
-  const OP* dop = dO + (cp.row0 * H + h) * DV;
-  for (int c0 = 0; c0 < DV; c0 += VS) {
-    ok &= load_rows<VS, LVS>(dop + c0, (long)H * DV, cp.len, dOs);
+#pragma unroll
+  for (int t = 0; t < NSL; ++t) {
+    const int c0 = t * VS;
+#pragma unroll
+    for (int p = 0; p < NPS; ++p) {
+      const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
+      const uint4 x = keep16(i < cp.len, din[t][p]);
+      ok &= finite16B<OP>(x);
+      *reinterpret_cast<uint4*>(dOs + i * LVS + v0) = x;
+    }
     __syncthreads();
     OP* dOt = dOTg + tile * DV * CH;
     for (int idx = threadIdx.x; idx < VS * CH / VE; idx += blockDim.x) {

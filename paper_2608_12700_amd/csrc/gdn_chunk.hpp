@@ -104,6 +104,36 @@ __device__ __forceinline__ void load_dense(const T* __restrict__ src, T* dst) {
 
 // Write rows [0, len) of an LDS tile src[r * LD + d] (64 x D) to HBM rows `rs`
 // elements apart.
+// Rows [0, len) of a 64 x D chunk tile (rows rs elements apart in HBM), read
+// by a block of NT threads in one batch: load() puts every 16-byte piece in
+// flight at once (a load/wait/store loop would pay one memory round trip per
+// iteration), stage() masks the rows past the end and writes the tile to LDS.
+template <int D, int NT, typename T>
+struct RowsIn {
+  static constexpr int V = 16 / (int)sizeof(T), PER_ROW = D / V, N = CH * PER_ROW / NT;
+  static_assert(CH * PER_ROW % NT == 0, "whole pieces per thread");
+  uint4 u[N];
+  __device__ __forceinline__ void load(const T* __restrict__ src, long rs, int len) {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      const int idx = threadIdx.x + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
+      u[t] = *reinterpret_cast<const uint4*>(src + clamp_row(r, len) * rs + c);
+    }
+  }
+  template <int LD>
+  __device__ __forceinline__ bool stage(T* dst, int len) const {
+    bool ok = true;
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      const int idx = threadIdx.x + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
+      const uint4 x = keep16(r < len, u[t]);
+      ok &= finite16B<T>(x);
+      *reinterpret_cast<uint4*>(dst + r * LD + c) = x;
+    }
+    return ok;
+  }
+};
+
 template <int D, int LD, typename T>
 __device__ __forceinline__ void store_rows(T* __restrict__ dst, long rs, int len, const T* src) {
   constexpr int V = 16 / (int)sizeof(T);

@@ -59,9 +59,24 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
   const int l = lane_id();
+  // every input row of the block is requested up front: q, k, then the v
+  // slices of the U product (slice t of VS columns is piece t of each thread)
+  RowsIn<DK, 512, OP> qin, kin;
+  qin.load(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len);
+  kin.load(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len);
+  const OP* vp = v + (cp.row0 * H + h) * DV;
+  constexpr int NSL = DV / VS, NPS = CH * VS / VE / 512;  // slices; pieces per thread and slice
+  uint4 vin[NSL][NPS];
+#pragma unroll
+  for (int t = 0; t < NSL; ++t)
+#pragma unroll
+    for (int p = 0; p < NPS; ++p) {
+      const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), c = t * VS + (idx % (VS / VE)) * VE;
+      vin[t][p] = *reinterpret_cast<const uint4*>(vp + (long)clamp_row(i, cp.len) * H * DV + c);
+    }
   bool ok = load_gates<VAR>(g, beta, cp.row0, H, h, cp.len, Gs, Bs);
-  ok &= load_rows<DK, LK>(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Qs);
-  ok &= load_rows<DK, LK>(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len, Ks);
+  ok &= qin.template stage<LK>(Qs, cp.len);
+  ok &= kin.template stage<LK>(Ks, cp.len);
   __syncthreads();
   if (threadIdx.x < CH) {
     const int r = threadIdx.x;
@@ -129,7 +144,6 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
     }
   }
   __syncthreads();  // Q and K are dead from here on
-  const OP* vp = v + (cp.row0 * H + h) * DV;
   if constexpr (DT_) {
     unit_lower_inverse<OP, LC, LT, false>(As, Tf, Ts, (OP*)nullptr);
     const OP* Tp;
@@ -156,11 +170,13 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
     // U = T diag(beta) V, per slice of VS value columns, stored as the scan's
     // accumulator tiles (four rows of one column per lane: one float4)
     float* Ut = Ug + tile * CH * DV;
-    for (int c0 = 0; c0 < DV; c0 += VS) {
-      for (int idx = threadIdx.x; idx < CH * VS / VE; idx += blockDim.x) {
-        const int i = idx / (VS / VE), v0 = (idx - i * (VS / VE)) * VE;
-        const uint4 vv =
-            keep16(i < cp.len, *reinterpret_cast<const uint4*>(vp + (long)clamp_row(i, cp.len) * H * DV + c0 + v0));
+#pragma unroll
+    for (int t = 0; t < NSL; ++t) {
+      const int c0 = t * VS;
+#pragma unroll
+      for (int p = 0; p < NPS; ++p) {
+        const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
+        const uint4 vv = keep16(i < cp.len, vin[t][p]);
         ok &= finite16B<OP>(vv);
 #pragma unroll
         for (int j = 0; j < VE; ++j) VbT[(v0 + j) * LT + i] = from_f<OP>(Bs[i] * to_f(elem16<OP>(vv, j)));
@@ -179,11 +195,10 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
     }
   } else {
     // scalar-decay member: T = I, W = 0, U = V; only check v for non-finite values
-    for (int idx = threadIdx.x; idx < CH * DV / VE; idx += blockDim.x) {
-      const int i = idx / (DV / VE), c = (idx - i * (DV / VE)) * VE;
-      ok &= finite16B<OP>(
-          keep16(i < cp.len, *reinterpret_cast<const uint4*>(vp + (long)clamp_row(i, cp.len) * H * DV + c)));
-    }
+#pragma unroll
+    for (int t = 0; t < NSL; ++t)
+#pragma unroll
+      for (int p = 0; p < NPS; ++p) ok &= finite16B<OP>(keep16((threadIdx.x + p * 512) / (VS / VE) < cp.len, vin[t][p]));
   }
   const int bad = __syncthreads_or(!ok);
   if (threadIdx.x == 0) flag[tile] = bad;

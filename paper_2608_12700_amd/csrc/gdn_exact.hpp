@@ -50,6 +50,36 @@ __device__ __forceinline__ bool stream_flagged(const Geo& geo, int s, const int*
   return __syncthreads_or(any) != 0;
 }
 
+// Flags of the streams s0, s0 + step, ... (up to 8 of them, fewer past NS),
+// checked in one pass: the block's threads split into eight groups, one per
+// stream, and the group ORs its stream's chunk and value-tile flags into
+// bit i of the result.
+__device__ __forceinline__ unsigned streams_flagged8(const Geo& geo, int s0, int step, int NS, const int* fa,
+                                                     const int* fb, const int* fs, int nvt) {
+  __shared__ int fl[8];
+  const int per = blockDim.x / 8, i = threadIdx.x / per, li = threadIdx.x - i * per;
+  if (threadIdx.x < 8) fl[threadIdx.x] = 0;
+  __syncthreads();
+  const int s = s0 + i * step;
+  int any = 0;
+  if (s < NS) {
+    const int H = geo.H;
+    const int n = s / H, h = s - (s / H) * H;
+    const SeqPos sp = seq_pos(geo, n);
+    for (int c = li; c < sp.nch; c += per) {
+      const long t = (long)(sp.c0 + c) * H + h;
+      any |= fa[t] | fb[t];
+    }
+    for (int j = li; j < nvt; j += per) any |= fs[(long)s * nvt + j];
+  }
+  if (any) atomicOr(&fl[i], 1);  // integer OR: order-free
+  __syncthreads();
+  unsigned m = 0;
+  for (int j = 0; j < 8; ++j) m |= fl[j] ? 1u << j : 0u;
+  __syncthreads();
+  return m;
+}
+
 template <typename IO>
 __device__ __forceinline__ float ld(const IO* p, long i) { return to_f(p[i]); }
 
@@ -141,8 +171,10 @@ __global__ __launch_bounds__(256) void k_exact_bwd(Geo geo, const IO* __restrict
   const int col = threadIdx.x;
   float* slot = scratch + (long)blockIdx.x * (CH + 2) * DK * DV;
   float* park = slot + (long)(CH + 1) * DK * DV + (long)col * DK;  // dS while a chunk is replayed
-  for (int s = blockIdx.x; s < NS; s += EXACT_SLOTS) {
-    if (!stream_flagged(geo, s, fa, fb, fs, nvt)) continue;
+  unsigned mask = 0;
+  for (int s = blockIdx.x, i = 0; s < NS; s += EXACT_SLOTS, i = (i + 1) & 7) {
+    if (i == 0) mask = streams_flagged8(geo, s, EXACT_SLOTS, NS, fa, fb, fs, nvt);
+    if (!(mask >> i & 1u)) continue;
     const int n = s / H, h = s - (s / H) * H;
     const SeqPos sp = seq_pos(geo, n);
     float dS[DK];

@@ -40,36 +40,41 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
                                                   OP* __restrict__ PTg, OP* __restrict__ Tg,
                                                   OP* __restrict__ Khg, int* __restrict__ flag) {
   constexpr bool DT_ = VAR != VAR_DECAY;
+  // bf16 operands read transposed tiles straight from row-major LDS with the
+  // transposing load; fp32 operands go through explicit transposed copies
+  constexpr bool TR = sizeof(OP) == 2;
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
   constexpr int LT = CH + pad_of<OP>();
-  constexpr int VS = 64;
+  constexpr int VS = TR ? DV : 64;  // value columns per slice of dO
   constexpr int LVS = VS + pad_of<OP>();
   constexpr int VE = 16 / (int)sizeof(OP);
   typedef typename vec4_of<OP>::type V4;
   // LDS regions are reused by lifetime so that two blocks fit on a CU:
-  //   R1: Q, then T in fp32;  R2: K, then T in the operand dtype;
-  //   R3: (diag(beta e^G) K)^T;  R4: A in fp32, then dO slices.
+  //   R1: Q, then T in fp32;  R2: K (bf16: alive through W; fp32: then T);
+  //   R3: bf16: T in bf16; fp32: (diag(beta e^G) K)^T;  R4: A in fp32, then dO.
   constexpr int R1 = CH * LK * (int)sizeof(OP) > CH * LC * 4 ? CH * LK * (int)sizeof(OP) : CH * LC * 4;
   constexpr int R2 = CH * LK * (int)sizeof(OP);
+  constexpr int R3 = !DT_ ? 16 : (TR ? CH * LT * (int)sizeof(OP) : DK * LT * (int)sizeof(OP));
   constexpr int R4 = CH * LC * 4 > CH * LVS * (int)sizeof(OP) ? CH * LC * 4 : CH * LVS * (int)sizeof(OP);
-  static_assert(CH * LT * (int)sizeof(OP) <= R2, "T fits where K was");
+  static_assert(TR || CH * LT * (int)sizeof(OP) <= R2, "T fits where K was");
   __shared__ __align__(16) char r1[R1];
   __shared__ __align__(16) char r2[R2];
-  __shared__ __align__(16) OP KbT[DT_ ? DK * LT : 1];  // (diag(beta e^G) K)^T
+  __shared__ __align__(16) char r3[R3];
   __shared__ __align__(16) char r4[R4];
-  __shared__ float Gs[CH], Bs[CH], Gam[CH], Dte[CH];
+  __shared__ __align__(16) float Gs[CH], Bs[CH], Gam[CH], Dte[CH], BG[CH];
   OP* Qs = reinterpret_cast<OP*>(r1);
   float* Tf = reinterpret_cast<float*>(r1);
   OP* Ks = reinterpret_cast<OP*>(r2);
-  OP* Ts = reinterpret_cast<OP*>(r2);
+  OP* Ts = TR ? reinterpret_cast<OP*>(r3) : reinterpret_cast<OP*>(r2);
+  OP* KbT = reinterpret_cast<OP*>(r3);
   float* As = reinterpret_cast<float*>(r4);
   OP* dOs = reinterpret_cast<OP*>(r4);
 
   const int ci = blockIdx.x, h = blockIdx.y;
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
-  const int l = lane_id();
+  const int l = lane_id(), wv = wave_id();
   // every input row of the block is requested up front: q, k, then the dO
   // slices (slice t of VS columns is piece t of each thread)
   RowsIn<DK, 512, OP> qin, kin;
@@ -90,9 +95,12 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   ok &= kin.template stage<LK>(Ks, cp.len);
   __syncthreads();
   if (threadIdx.x < CH) {
-    gcum[tile * CH + threadIdx.x] = Gs[threadIdx.x];
-    Gam[threadIdx.x] = __expf(Gs[threadIdx.x]);
-    Dte[threadIdx.x] = __expf(Gs[CH - 1] - Gs[threadIdx.x]);
+    const int r = threadIdx.x;
+    gcum[tile * CH + r] = Gs[r];
+    const float gam = __expf(Gs[r]);
+    Gam[r] = gam;
+    BG[r] = Bs[r] * gam;
+    Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
   }
   __syncthreads();
   // P^T, written (i, r): the scan's A operand for P^T dO
@@ -116,19 +124,40 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   // (diag(e^G) Q)^T for the scan's injection term
   {
     OP* Qg = QgTg + tile * DK * CH;
-    for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
-      const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
-      OP vals[VE];
+    if constexpr (TR) {
+      // one transposed fragment (16 d x 32 r) of Q per wave and step, stored
+      // as one contiguous 1 KiB block
 #pragma unroll
-      for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Gam[r0 + j] * to_f(Qs[(r0 + j) * LK + d]));
-      *reinterpret_cast<uint4*>(Qg + op_off<OP, CH>(d, r0)) = pack16<OP>(vals);
+      for (int t = 0; t < DK * CH / (512 * 8); ++t) {
+        const int f = wv + 8 * t, mt = f / (CH / 32), s = f % (CH / 32);
+        const bf16x8 x = scale_frag(lds_frag_tr<LK>(Qs, 16 * mt, 32 * s), Gam, 32 * s);
+        *reinterpret_cast<bf16x8*>(Qg + ((long)f * 64 + l) * 8) = x;
+      }
+    } else {
+      for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
+        const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
+        OP vals[VE];
+#pragma unroll
+        for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Gam[r0 + j] * to_f(Qs[(r0 + j) * LK + d]));
+        *reinterpret_cast<uint4*>(Qg + op_off<OP, CH>(d, r0)) = pack16<OP>(vals);
+      }
     }
   }
-  // Khat = diag(e^{G_last - G}) K, the scan's A operand for dU' (rows past the end stay zero)
+  // Khat = diag(e^{G_last - G}) K, the scan's A operand for dU' (rows past the
+  // end stay zero); bf16 thread order follows the operand layout, so each
+  // wave writes whole 1 KiB fragments
   {
     OP* Kh = Khg + tile * CH * DK;
     for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
-      const int r = idx / (DK / VE), d0 = (idx - r * (DK / VE)) * VE;
+      int r, d0;
+      if constexpr (TR) {
+        const int f = idx >> 6, ll = idx & 63;
+        r = (f / (DK / 32)) * 16 + (ll & 15);
+        d0 = (f % (DK / 32)) * 32 + (ll >> 4) * 8;
+      } else {
+        r = idx / (DK / VE);
+        d0 = (idx - r * (DK / VE)) * VE;
+      }
       const uint4 kv = *reinterpret_cast<const uint4*>(Ks + r * LK + d0);
       OP vals[VE];
 #pragma unroll
@@ -143,28 +172,44 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
     bm.each([&](int r, int i, float& x) {
       As[r * LC + i] = (i < r) ? Bs[r] * x * __expf(Gs[r] - Gs[i]) : 0.f;
     });
-    // (diag(beta e^G) K)^T for the W product
-    for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
-      const int i = idx / (DK / VE), d0 = (idx - i * (DK / VE)) * VE;
-      const uint4 kv = *reinterpret_cast<const uint4*>(Ks + i * LK + d0);
-      const float sc = Bs[i] * Gam[i];
+    if constexpr (!TR) {
+      // (diag(beta e^G) K)^T for the W product
+      for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
+        const int i = idx / (DK / VE), d0 = (idx - i * (DK / VE)) * VE;
+        const uint4 kv = *reinterpret_cast<const uint4*>(Ks + i * LK + d0);
+        const float sc = BG[i];
 #pragma unroll
-      for (int j = 0; j < VE; ++j) KbT[(d0 + j) * LT + i] = from_f<OP>(sc * to_f(elem16<OP>(kv, j)));
+        for (int j = 0; j < VE; ++j) KbT[(d0 + j) * LT + i] = from_f<OP>(sc * to_f(elem16<OP>(kv, j)));
+      }
     }
     __syncthreads();
-    unit_lower_inverse<OP, LC, LT, false>(As, Tf, Ts, (OP*)nullptr);  // Tf over Q, Ts over K: both are dead here
+    // Tf over Q (dead here); Ts over K for fp32, in its own region for bf16
+    unit_lower_inverse<OP, LC, LT, false>(As, Tf, Ts, (OP*)nullptr);
     const OP* Tp;
-    if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
-    constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
+    if constexpr (TR) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
+    constexpr int LTT = TR ? LT : LC;
     // T itself, row-major, for the gradient kernel
     for (int idx = threadIdx.x; idx < CH * CH / VE; idx += blockDim.x) {
       const int r = idx / (CH / VE), c = (idx - r * (CH / VE)) * VE;
       *reinterpret_cast<uint4*>(Tg + tile * CH * CH + r * CH + c) = *reinterpret_cast<const uint4*>(Tp + r * LTT + c);
     }
+    if constexpr (TR) {
+      // A is dead: stage dO row-major for its transpose below
+#pragma unroll
+      for (int p = 0; p < NPS; ++p) {
+        const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
+        const uint4 x = keep16(i < cp.len, din[0][p]);
+        ok &= finite16B<OP>(x);
+        *reinterpret_cast<uint4*>(dOs + i * LVS + v0) = x;
+      }
+    }
     // W = T diag(beta e^G) K, written transposed (d, r)
     Tiles<CH, DK, 4, 2> w;
     w.zero();
-    w.template mma<OP, CH>(KRow<OP, LTT>{Tp}, KRow<OP, LT>{KbT});
+    if constexpr (TR)
+      w.template mma<OP, CH>(KRow<OP, LT>{Tp}, KColTr<LK, true>{Ks, BG});
+    else
+      w.template mma<OP, CH>(KRow<OP, LTT>{Tp}, KRow<OP, LT>{KbT});
     OP* Wt = WTg + tile * DK * CH;
 #pragma unroll
     for (int b = 0; b < w.TN; ++b) {
@@ -174,29 +219,47 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
       for (int j = 0; j < 4; ++j) v4[j] = from_f<OP>(w.acc[0][b][j]);
       *reinterpret_cast<V4*>(Wt + op_off<OP, CH>(d, r0)) = pack4<OP>(v4);
     }
-  }
-  // dO^T, in slices of VS value columns (dO slices reuse the A region)
-  __syncthreads();
-#pragma unroll
-  for (int t = 0; t < NSL; ++t) {
-    const int c0 = t * VS;
+  } else if constexpr (TR) {
+    // no A: dO goes straight into its region
 #pragma unroll
     for (int p = 0; p < NPS; ++p) {
       const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
-      const uint4 x = keep16(i < cp.len, din[t][p]);
+      const uint4 x = keep16(i < cp.len, din[0][p]);
       ok &= finite16B<OP>(x);
       *reinterpret_cast<uint4*>(dOs + i * LVS + v0) = x;
     }
-    __syncthreads();
-    OP* dOt = dOTg + tile * DV * CH;
-    for (int idx = threadIdx.x; idx < VS * CH / VE; idx += blockDim.x) {
-      const int vv = idx / (CH / VE), r0 = (idx - vv * (CH / VE)) * VE;
-      OP vals[VE];
+  }
+  // dO^T, the scan's A operand for the injection term
+  OP* dOt = dOTg + tile * DV * CH;
+  __syncthreads();
+  if constexpr (TR) {
 #pragma unroll
-      for (int j = 0; j < VE; ++j) vals[j] = dOs[(r0 + j) * LVS + vv];
-      *reinterpret_cast<uint4*>(dOt + op_off<OP, CH>(c0 + vv, r0)) = pack16<OP>(vals);
+    for (int t = 0; t < DV * CH / (512 * 8); ++t) {
+      const int f = wv + 8 * t, mt = f / (CH / 32), s = f % (CH / 32);
+      *reinterpret_cast<bf16x8*>(dOt + ((long)f * 64 + l) * 8) = lds_frag_tr<LVS>(dOs, 16 * mt, 32 * s);
     }
-    __syncthreads();
+  } else {
+    // in slices of VS value columns (dO slices reuse the A region)
+#pragma unroll
+    for (int t = 0; t < NSL; ++t) {
+      const int c0 = t * VS;
+#pragma unroll
+      for (int p = 0; p < NPS; ++p) {
+        const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
+        const uint4 x = keep16(i < cp.len, din[t][p]);
+        ok &= finite16B<OP>(x);
+        *reinterpret_cast<uint4*>(dOs + i * LVS + v0) = x;
+      }
+      __syncthreads();
+      for (int idx = threadIdx.x; idx < VS * CH / VE; idx += blockDim.x) {
+        const int vv = idx / (CH / VE), r0 = (idx - vv * (CH / VE)) * VE;
+        OP vals[VE];
+#pragma unroll
+        for (int j = 0; j < VE; ++j) vals[j] = dOs[(r0 + j) * LVS + vv];
+        *reinterpret_cast<uint4*>(dOt + op_off<OP, CH>(c0 + vv, r0)) = pack16<OP>(vals);
+      }
+      __syncthreads();
+    }
   }
   const int bad = __syncthreads_or(!ok);
   if (threadIdx.x == 0) flag[tile] = bad;
@@ -774,8 +837,8 @@ struct GradBF {
   typedef Tiles<DK, CH, WMd, WNr> TD;  // X^T, dQ^T, dK^T: d x 64
   typedef Tiles<VS, CH, WNv, WMv> TY;  // Y^T, U'^T, (K h)^T: VS x 64
   typedef Tiles<CH, CH, 4, 2> TC;      // P, A, dP, dA
-  static constexpr int PH1 = (VS * LT + 3 * CH * LV) * 2;
-  static constexpr int PH2 = 3 * CH * LT * 2 > 2 * CH * LK * 2 ? 3 * CH * LT * 2 : 2 * CH * LK * 2;
+  static constexpr int PH1 = 4 * CH * LV * 2;
+  static constexpr int PH2 = 2 * CH * LT * 2 > 2 * CH * LK * 2 ? 2 * CH * LT * 2 : 2 * CH * LK * 2;
   static constexpr int UB = PH1 > PH2 ? PH1 : PH2;
 };
 
@@ -807,8 +870,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 
   __shared__ __align__(16) bf16 Qs[CH * LK];
   __shared__ __align__(16) bf16 Ks[CH * LK];
-  __shared__ __align__(16) bf16 Ts[DT_ ? CH * LT : 1];
-  __shared__ __align__(16) bf16 TT[CH * LT];  // T^T (the identity for the scalar-decay member)
+  __shared__ __align__(16) bf16 Ts[CH * LT];  // T (the identity for the scalar-decay member)
   __shared__ __align__(16) float Gs[CH];
   __shared__ __align__(16) float Gam[CH];
   __shared__ __align__(16) float Bs[CH];
@@ -907,16 +969,15 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     *reinterpret_cast<uint4*>(Qs + r * LK + c) = qk[0][t];
     *reinterpret_cast<uint4*>(Ks + r * LK + c) = qk[1][t];
   }
-  if constexpr (DT_) {
+  {
     const int r = threadIdx.x >> 3, c = (threadIdx.x & 7) * 8;
-    *reinterpret_cast<uint4*>(Ts + r * LT + c) = tq;
+    if constexpr (!DT_) {
+      bf16 e[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) TT[(c + j) * LT + r] = elem16<bf16>(tq, j);
-  } else {
-    for (int idx = threadIdx.x; idx < CH * CH; idx += blockDim.x) {
-      const int r = idx >> 6, c = idx & 63;
-      TT[r * LT + c] = from_f<bf16>(r == c ? 1.f : 0.f);
+      for (int j = 0; j < 8; ++j) e[j] = from_f<bf16>(c + j == r ? 1.f : 0.f);
+      tq = pack16<bf16>(e);
     }
+    *reinterpret_cast<uint4*>(Ts + r * LT + c) = tq;
   }
   __syncthreads();
   if (threadIdx.x < CH) {
@@ -949,8 +1010,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   }
 
   // ================= phase 1: value slices
-  bf16* RT = reinterpret_cast<bf16*>(ub);
-  bf16* Ys = RT + VS * LT;
+  bf16* Rs = reinterpret_cast<bf16*>(ub);  // R, row-major
+  bf16* Ys = Rs + CH * LV;
   bf16* Ups = Ys + CH * LV;
   bf16* dOs = Ups + CH * LV;
   TC dA, dP;
@@ -970,7 +1031,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     if constexpr (DT_) {
       // R = diag(beta) (V - diag(e^G) K h), computed transposed, (K h)^T = h^T K^T,
       // so that a lane needs v[r][v0..v0+3] as one 8-byte piece (the same
-      // piece the dbeta term uses) and writes R^T rows directly
+      // piece the dbeta term uses) and writes four values of a row of R
       TY kht;
       kht.zero();
 #pragma unroll
@@ -993,12 +1054,14 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
         for (int a = 0; a < TY::TM; ++a) {
           const int v0 = TY::m0(a) + 4 * lg;
+          bf16 r4[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const float vx = r < len ? to_f(elem4<bf16>(pa.vb[a][b], j)) : 0.f;
             ok &= finite_f(vx);
-            RT[(v0 + j) * LT + r] = from_f<bf16>(br * (vx - gr * kht.acc[a][b][j]));
+            r4[j] = from_f<bf16>(br * (vx - gr * kht.acc[a][b][j]));
           }
+          *reinterpret_cast<uint2*>(Rs + r * LV + v0) = pack4<bf16>(r4);
         }
       }
     } else {
@@ -1012,7 +1075,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
       for (int s = 0; s < CH / 32; ++s) {
         bf16x8 fb[TY::TN];
 #pragma unroll
-        for (int b = 0; b < TY::TN; ++b) fb[b] = M::load(KRow<bf16, LT>{TT}, TY::n0(b), 32 * s);
+        for (int b = 0; b < TY::TN; ++b) fb[b] = M::load(KColTr<LT>{Ts, nullptr}, TY::n0(b), 32 * s);
 #pragma unroll
         for (int a = 0; a < TY::TM; ++a)
 #pragma unroll
@@ -1057,7 +1120,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
       // U'^T = R^T T^T
       TY ut;
       ut.zero();
-      ut.template mma<bf16, CH>(KRow<bf16, LT>{RT}, KRow<bf16, LT>{Ts});
+      ut.template mma<bf16, CH>(KColTr<LV>{Rs, nullptr}, KRow<bf16, LT>{Ts});
 #pragma unroll
       for (int a = 0; a < TY::TM; ++a)
 #pragma unroll
@@ -1115,39 +1178,32 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   __syncthreads();  // phase-1 LDS operands are consumed
 
   // ================= phase 2: the chunk-level gradients
-  bf16* dPs = reinterpret_cast<bf16*>(ub);
-  bf16* dPmT = dPs + CH * LT;
-  bf16* SdT = dPmT + CH * LT;  // dB + dB^T, dB = dA * beta_r * E
+  bf16* dPmT = reinterpret_cast<bf16*>(ub);  // (dP * D)^T
+  bf16* dBT = dPmT + CH * LT;                 // dB^T, dB = dA * beta_r * E (strict lower)
   TC zs;  // Z = dA * A + dP * P
   float rowA_l[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int b = 0; b < TC::TN; ++b) {
     const int i = TC::n0(b) + lc, r0 = TC::m0(0) + 4 * lg;
-    bf16 pt4[4];
+    bf16 pt4[4], bt4[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = r0 + j;
       const float dpm = dP.acc[0][b][j] * dd[b][j];
-      dPs[r * LT + i] = from_f<bf16>(dpm);
       pt4[j] = from_f<bf16>(dpm);
       float z = dP.acc[0][b][j] * pm.acc[0][b][j];
       if constexpr (DT_) {
-        // dB = dA * beta_r * E (strict lower); SdT = dB + dB^T, each entry
-        // written by exactly one lane: the owner of the lower-triangle element
         const float da = i < r ? dA.acc[0][b][j] : 0.f;
         z += da * Bs[r] * ae.acc[0][b][j];
         rowA_l[j] += da * ae.acc[0][b][j];
-        if (i < r) {
-          const bf16 sd = from_f<bf16>(da * Bs[r] * dd[b][j]);
-          SdT[r * LT + i] = sd;
-          SdT[i * LT + r] = sd;
-        } else if (i == r) {
-          SdT[r * LT + r] = from_f<bf16>(0.f);
-        }
+        bt4[j] = from_f<bf16>(da * Bs[r] * dd[b][j]);
       }
       zs.acc[0][b][j] = z;
     }
+    // both written transposed, four consecutive r per lane; every entry of
+    // the 64 x 64 tiles is written by exactly one lane
     *reinterpret_cast<uint2*>(dPmT + i * LT + r0) = pack4<bf16>(pt4);
+    if constexpr (DT_) *reinterpret_cast<uint2*>(dBT + i * LT + r0) = pack4<bf16>(bt4);
   }
   {
     const int wm = w / 2, wn = w % 2;
@@ -1213,12 +1269,16 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   __syncthreads();
   {
     // dQ^T += K^T (dP * D)^T,  dK^T += Q^T (dP * D) + K^T (dB + dB^T); the K^T and
-    // Q^T fragments are read down the columns of the row-major tiles
+    // Q^T fragments are read down the columns of the row-major tiles, and the
+    // transposed tiles are read both ways (rows, or columns by the transposing load)
     typename TD::template AFr<bf16, CH> kt;
-    kt.load(KCol<bf16, LK>{Ks});
-    dQt.template mma<bf16, CH>(kt, KRow<bf16, LT>{dPs});
-    if constexpr (DT_) dKt.template mma<bf16, CH>(kt, KRow<bf16, LT>{SdT});
-    dKt.template mma<bf16, CH>(KCol<bf16, LK>{Qs}, KRow<bf16, LT>{dPmT});
+    kt.load(KColTr<LK>{Ks, nullptr});
+    dQt.template mma<bf16, CH>(kt, KColTr<LT>{dPmT, nullptr});
+    if constexpr (DT_) {
+      dKt.template mma<bf16, CH>(kt, KRow<bf16, LT>{dBT});
+      dKt.template mma<bf16, CH>(kt, KColTr<LT>{dBT, nullptr});
+    }
+    dKt.template mma<bf16, CH>(KColTr<LK>{Qs, nullptr}, KRow<bf16, LT>{dPmT});
   }
   __syncthreads();
   bf16* dqst = reinterpret_cast<bf16*>(ub);

@@ -136,6 +136,51 @@ struct KCol {
   __device__ __forceinline__ T get(int o, int k) const { return p[k * LD + o]; }
 };
 
+// Element (o, k) at p[k * LD + o] of a 16-bit LDS array (o contiguous), read
+// with gfx950's transposing LDS load: a fragment takes two ds_read_b64_tr_b16
+// instead of eight 2-byte gathers.  With SCALED, element (o, k) is multiplied
+// by sc[k] (fp32, 16-byte aligned) before it is rounded back to bf16.
+template <int LD, bool SCALED = false>
+struct KColTr {
+  const bf16* p;
+  const float* sc;
+  static constexpr bool kVec = false;
+  static constexpr bool kTr = true;
+};
+
+// ds_read_b64_tr_b16: in each 16-lane group, lane s points at four
+// consecutive 16-bit elements (row s >> 2 of a 4 x 16 block, columns
+// 4 (s & 3) .. 4 (s & 3) + 3); lane i of the group receives column i of the
+// block, rows 0..3, as four 16-bit values.
+typedef __attribute__((ext_vector_type(4))) short i16x4;
+__device__ __forceinline__ uint2 lds_read_tr16(const bf16* p) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+  return __builtin_bit_cast(uint2, r);
+}
+
+// MFMA fragment (rows o..o+15, contraction k0..k0+31) of a matrix stored
+// k-major in LDS, p[k * LD + o]: lane l receives o + (l & 15) and the eight
+// k = k0 + 8 (l >> 4) + j, j = 0..7, the same placement a row-major read gives.
+template <int LD>
+__device__ __forceinline__ bf16x8 lds_frag_tr(const bf16* p, int o, int k0) {
+  static_assert(LD % 4 == 0, "8-byte aligned rows");
+  const int l = lane_id(), s = l & 15;
+  const bf16* a = p + (k0 + 8 * (l >> 4) + (s >> 2)) * LD + o + 4 * (s & 3);
+  const uint2 lo = lds_read_tr16(a), hi = lds_read_tr16(a + 4 * LD);
+  return __builtin_bit_cast(bf16x8, uint4{lo.x, lo.y, hi.x, hi.y});
+}
+
+// Scale the eight k-values of a fragment by sc[k0 + 8 (l >> 4) + j].
+__device__ __forceinline__ bf16x8 scale_frag(bf16x8 f, const float* sc, int k0) {
+  const float* s8 = sc + k0 + 8 * (lane_id() >> 4);
+  const float4 a = *reinterpret_cast<const float4*>(s8), b = *reinterpret_cast<const float4*>(s8 + 4);
+  const float m[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = static_cast<bf16>(static_cast<float>(f[j]) * m[j]);
+  return f;
+}
+
 // Element computed by a functor f(o, k) -> T.
 template <typename T, class F>
 struct KFun {
@@ -148,6 +193,13 @@ __device__ __forceinline__ KFun<T, F> kfun(F f) { return KFun<T, F>{f}; }
 
 template <class V, class = void> struct is_masked { static constexpr bool value = false; };
 template <class V> struct is_masked<V, decltype((void)V::kMasked)> { static constexpr bool value = true; };
+template <class V, class = void> struct is_tr { static constexpr bool value = false; };
+template <class V> struct is_tr<V, decltype((void)V::kTr)> { static constexpr bool value = true; };
+template <int LD, bool S>
+__device__ __forceinline__ bf16x8 tr_load(const KColTr<LD, S>& v, int o, int k0) {
+  const bf16x8 f = lds_frag_tr<LD>(v.p, o, k0);
+  if constexpr (S) return scale_frag(f, v.sc, k0); else return f;
+}
 
 template <typename OP> struct Mma;
 
@@ -161,6 +213,8 @@ struct Mma<bf16> {
     const int oo = o + (l & 15), kk = k0 + (l >> 4) * 8;
     if constexpr (V::kVec) {
       return *reinterpret_cast<const bf16x8*>(v.ptr(oo, kk));
+    } else if constexpr (is_tr<V>::value) {
+      return tr_load(v, o, k0);
     } else if constexpr (is_masked<V>::value) {
       const uint4 u = *reinterpret_cast<const uint4*>(v.ptr(clamp_row(oo, v.rows), kk));
       return __builtin_bit_cast(frag, keep16(oo < v.rows, u));

@@ -30,35 +30,43 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
                                                   float* __restrict__ Ug, OP* __restrict__ KhTg,
                                                   OP* __restrict__ Pg, OP* __restrict__ Qgg, int* __restrict__ flag) {
   constexpr bool DT_ = VAR != VAR_DECAY;
+  // bf16 operands read transposed tiles straight from row-major LDS with the
+  // transposing load; fp32 operands go through explicit transposed copies
+  constexpr bool TR = sizeof(OP) == 2;
   constexpr int LK = DK + pad_of<OP>();
+  constexpr int LV = DV + pad_of<OP>();
   constexpr int LC = CH + 4;
   constexpr int LT = CH + pad_of<OP>();
-  constexpr int VS = 64;  // value columns per slice of U
+  constexpr int VS = TR ? DV : 64;  // value columns per slice of U
   constexpr int VE = 16 / (int)sizeof(OP);
   typedef typename vec4_of<OP>::type V4;
   // LDS regions reused by lifetime (two blocks per CU):
-  //   R1: Q, then T in fp32;  R2: K, then T in the operand dtype;
-  //   R3: (diag(beta e^G) K)^T;  R4: A in fp32, then (diag(beta) V)^T slices.
+  //   R1: Q, then T in fp32;  R2: K (bf16: alive through W; fp32: then T);
+  //   R3: bf16: T in bf16; fp32: (diag(beta e^G) K)^T;
+  //   R4: A in fp32, then diag(beta) V (bf16: row-major; fp32: transposed slices).
   constexpr int R1 = CH * LK * (int)sizeof(OP) > CH * LC * 4 ? CH * LK * (int)sizeof(OP) : CH * LC * 4;
   constexpr int R2 = CH * LK * (int)sizeof(OP);
-  constexpr int R4 = CH * LC * 4 > VS * LT * (int)sizeof(OP) ? CH * LC * 4 : VS * LT * (int)sizeof(OP);
-  static_assert(CH * LT * (int)sizeof(OP) <= R2, "T fits where K was");
+  constexpr int R3 = !DT_ ? 16 : (TR ? CH * LT * (int)sizeof(OP) : DK * LT * (int)sizeof(OP));
+  constexpr int VB = TR ? CH * LV * (int)sizeof(OP) : VS * LT * (int)sizeof(OP);
+  constexpr int R4 = CH * LC * 4 > VB ? CH * LC * 4 : VB;
+  static_assert(TR || CH * LT * (int)sizeof(OP) <= R2, "T fits where K was");
   __shared__ __align__(16) char r1[R1];
   __shared__ __align__(16) char r2[R2];
-  __shared__ __align__(16) OP KbT[DT_ ? DK * LT : 1];
+  __shared__ __align__(16) char r3[R3];
   __shared__ __align__(16) char r4[R4];
-  __shared__ float Gs[CH], Bs[CH], Gam[CH], Dte[CH];
+  __shared__ __align__(16) float Gs[CH], Bs[CH], Gam[CH], Dte[CH], BG[CH];
   OP* Qs = reinterpret_cast<OP*>(r1);
   float* Tf = reinterpret_cast<float*>(r1);
   OP* Ks = reinterpret_cast<OP*>(r2);
-  OP* Ts = reinterpret_cast<OP*>(r2);
+  OP* Ts = TR ? reinterpret_cast<OP*>(r3) : reinterpret_cast<OP*>(r2);
+  OP* KbT = reinterpret_cast<OP*>(r3);
   float* As = reinterpret_cast<float*>(r4);
-  OP* VbT = reinterpret_cast<OP*>(r4);
+  OP* Vb = reinterpret_cast<OP*>(r4);
 
   const int ci = blockIdx.x, h = blockIdx.y;
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
-  const int l = lane_id();
+  const int l = lane_id(), w = wave_id();
   // every input row of the block is requested up front: q, k, then the v
   // slices of the U product (slice t of VS columns is piece t of each thread)
   RowsIn<DK, 512, OP> qin, kin;
@@ -81,15 +89,26 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
   if (threadIdx.x < CH) {
     const int r = threadIdx.x;
     gcum[tile * CH + r] = Gs[r];
-    Gam[r] = __expf(Gs[r]);
+    const float gam = __expf(Gs[r]);
+    Gam[r] = gam;
+    BG[r] = Bs[r] * gam;
     Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
   }
   __syncthreads();
-  // diag(e^G) Q, the scan's A operand for the output term
+  // diag(e^G) Q, the scan's A operand for the output term: thread order
+  // follows the operand layout, so each wave writes whole 1 KiB fragments
   {
     OP* Qg = Qgg + tile * CH * DK;
     for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
-      const int r = idx / (DK / VE), d0 = (idx - r * (DK / VE)) * VE;
+      int r, d0;
+      if constexpr (TR) {
+        const int f = idx >> 6, ll = idx & 63;
+        r = (f / (DK / 32)) * 16 + (ll & 15);
+        d0 = (f % (DK / 32)) * 32 + (ll >> 4) * 8;
+      } else {
+        r = idx / (DK / VE);
+        d0 = (idx - r * (DK / VE)) * VE;
+      }
       const uint4 qv = *reinterpret_cast<const uint4*>(Qs + r * LK + d0);
       OP vals[VE];
 #pragma unroll
@@ -123,38 +142,67 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
     bm.each([&](int r, int i, float& x) {
       As[r * LC + i] = (i < r) ? Bs[r] * x * __expf(Gs[r] - Gs[i]) : 0.f;
     });
-    // (diag(beta e^G) K)^T for the W product
-    for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
-      const int i = idx / (DK / VE), d0 = (idx - i * (DK / VE)) * VE;
-      const uint4 kv = *reinterpret_cast<const uint4*>(Ks + i * LK + d0);
-      const float sc = Bs[i] * Gam[i];
+    if constexpr (!TR) {
+      // (diag(beta e^G) K)^T for the W product
+      for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
+        const int i = idx / (DK / VE), d0 = (idx - i * (DK / VE)) * VE;
+        const uint4 kv = *reinterpret_cast<const uint4*>(Ks + i * LK + d0);
+        const float sc = BG[i];
 #pragma unroll
-      for (int j = 0; j < VE; ++j) KbT[(d0 + j) * LT + i] = from_f<OP>(sc * to_f(elem16<OP>(kv, j)));
+        for (int j = 0; j < VE; ++j) KbT[(d0 + j) * LT + i] = from_f<OP>(sc * to_f(elem16<OP>(kv, j)));
+      }
     }
   }
   // Khat^T[d][r] = e^{G_last - G_r} k_r[d], the scan's A operand for the carry
   {
     OP* Kh = KhTg + tile * DK * CH;
-    for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
-      const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
-      OP vals[VE];
+    if constexpr (TR) {
+      // one transposed fragment (16 d x 32 r) of K per wave and step, stored
+      // as one contiguous 1 KiB block
 #pragma unroll
-      for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Dte[r0 + j] * to_f(Ks[(r0 + j) * LK + d]));
-      *reinterpret_cast<uint4*>(Kh + op_off<OP, CH>(d, r0)) = pack16<OP>(vals);
+      for (int t = 0; t < DK * CH / (512 * 8); ++t) {
+        const int f = w + 8 * t, mt = f / (CH / 32), s = f % (CH / 32);
+        const bf16x8 x = scale_frag(lds_frag_tr<LK>(Ks, 16 * mt, 32 * s), Dte, 32 * s);
+        *reinterpret_cast<bf16x8*>(Kh + ((long)f * 64 + l) * 8) = x;
+      }
+    } else {
+      for (int idx = threadIdx.x; idx < DK * CH / VE; idx += blockDim.x) {
+        const int d = idx / (CH / VE), r0 = (idx - d * (CH / VE)) * VE;
+        OP vals[VE];
+#pragma unroll
+        for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Dte[r0 + j] * to_f(Ks[(r0 + j) * LK + d]));
+        *reinterpret_cast<uint4*>(Kh + op_off<OP, CH>(d, r0)) = pack16<OP>(vals);
+      }
     }
   }
-  __syncthreads();  // Q and K are dead from here on
+  __syncthreads();  // Q (and for fp32 K) is dead from here on
   if constexpr (DT_) {
     unit_lower_inverse<OP, LC, LT, false>(As, Tf, Ts, (OP*)nullptr);
     const OP* Tp;
-    if constexpr (sizeof(OP) == 2) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
-    constexpr int LTT = sizeof(OP) == 2 ? LT : LC;
+    if constexpr (TR) Tp = Ts; else Tp = reinterpret_cast<const OP*>(Tf);
+    constexpr int LTT = TR ? LT : LC;
+    if constexpr (TR) {
+      // A is dead: stage diag(beta) V row-major for the U product
+#pragma unroll
+      for (int p = 0; p < NPS; ++p) {
+        const int idx = threadIdx.x + p * 512, i = idx / (DV / VE), c = (idx % (DV / VE)) * VE;
+        const uint4 vv = keep16(i < cp.len, vin[0][p]);
+        ok &= finite16B<OP>(vv);
+        OP vals[VE];
+#pragma unroll
+        for (int j = 0; j < VE; ++j) vals[j] = from_f<OP>(Bs[i] * to_f(elem16<OP>(vv, j)));
+        *reinterpret_cast<uint4*>(Vb + i * LV + c) = pack16<OP>(vals);
+      }
+    }
     // W = T diag(beta e^G) K, computed as W^T = Kb^T T^T so a lane holds four
     // consecutive d of one row r of W
     {
       Tiles<DK, CH, 4, 2> wt;
       wt.zero();
-      wt.template mma<OP, CH>(KRow<OP, LT>{KbT}, KRow<OP, LTT>{Tp});
+      if constexpr (TR)
+        wt.template mma<OP, CH>(KColTr<LK, true>{Ks, BG}, KRow<OP, LT>{Tp});
+      else
+        wt.template mma<OP, CH>(KRow<OP, LT>{KbT}, KRow<OP, LTT>{Tp});
       OP* Wt = Wg + tile * CH * DK;
 #pragma unroll
       for (int a = 0; a < wt.TM; ++a)
@@ -173,25 +221,30 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
     for (int t = 0; t < NSL; ++t) {
       const int c0 = t * VS;
+      if constexpr (!TR) {
 #pragma unroll
-      for (int p = 0; p < NPS; ++p) {
-        const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
-        const uint4 vv = keep16(i < cp.len, vin[t][p]);
-        ok &= finite16B<OP>(vv);
+        for (int p = 0; p < NPS; ++p) {
+          const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
+          const uint4 vv = keep16(i < cp.len, vin[t][p]);
+          ok &= finite16B<OP>(vv);
 #pragma unroll
-        for (int j = 0; j < VE; ++j) VbT[(v0 + j) * LT + i] = from_f<OP>(Bs[i] * to_f(elem16<OP>(vv, j)));
+          for (int j = 0; j < VE; ++j) Vb[(v0 + j) * LT + i] = from_f<OP>(Bs[i] * to_f(elem16<OP>(vv, j)));
+        }
       }
       __syncthreads();
       Tiles<CH, VS, 4, 2> uu;
       uu.zero();
-      uu.template mma<OP, CH>(KRow<OP, LTT>{Tp}, KRow<OP, LT>{VbT});
+      if constexpr (TR)
+        uu.template mma<OP, CH>(KRow<OP, LT>{Tp}, KColTr<LV>{Vb, nullptr});
+      else
+        uu.template mma<OP, CH>(KRow<OP, LTT>{Tp}, KRow<OP, LT>{Vb});
 #pragma unroll
       for (int b = 0; b < uu.TN; ++b) {
         const int r0 = uu.m0(0) + (l >> 4) * 4, vcol = c0 + uu.n0(b) + (l & 15);
         *reinterpret_cast<float4*>(Ut + cfrag_off<SCAN_BV>(r0, vcol)) =
             float4{uu.acc[0][b][0], uu.acc[0][b][1], uu.acc[0][b][2], uu.acc[0][b][3]};
       }
-      __syncthreads();
+      if (t + 1 < NSL) __syncthreads();
     }
   } else {
     // scalar-decay member: T = I, W = 0, U = V; only check v for non-finite values

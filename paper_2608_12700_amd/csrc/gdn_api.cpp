@@ -309,6 +309,12 @@ gdn_status gdn_bwd_ex(const gdn_problem* p, const void* q, const void* k, const 
       for (int i = 0; i <= NUM_STAGES; ++i) stage_mark(a.events, i, a.stream);
       return GDN_OK;
     }
+    int dev = 0;
+    a.num_cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&a.num_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        a.num_cus < 1)
+      return GDN_ERR_HIP;
     hipError_t e;
     const bool bf = p->io_dtype == GDN_BF16;
     switch (p->variant) {

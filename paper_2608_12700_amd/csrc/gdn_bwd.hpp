@@ -438,16 +438,16 @@ struct GradRegion {
 
 // Sum over the 16 lanes that share a k-group (lanes l with equal l >> 4).
 __device__ __forceinline__ float sum16(float x) {
-  x += __shfl_xor(x, 1, WAVE);
-  x += __shfl_xor(x, 2, WAVE);
-  x += __shfl_xor(x, 4, WAVE);
-  x += __shfl_xor(x, 8, WAVE);
+  x += shfl_xor(x, 1);
+  x += shfl_xor(x, 2);
+  x += shfl_xor(x, 4);
+  x += shfl_xor(x, 8);
   return x;
 }
 // Sum over the 4 k-groups (lanes l, l^16, l^32, l^48).
 __device__ __forceinline__ float sum_groups(float x) {
-  x += __shfl_xor(x, 16, WAVE);
-  x += __shfl_xor(x, 32, WAVE);
+  x += shfl_xor(x, 16);
+  x += shfl_xor(x, 32);
   return x;
 }
 
@@ -795,9 +795,9 @@ __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __re
 #pragma unroll
     for (int i = 0; i < 8; ++i) hd += hdh_w[i];
     if (l == CH - 1) x += Gam[CH - 1] * hd + kk;
-    const float rev = __shfl(x, CH - 1 - l, WAVE);
+    const float rev = shfl_idx(x, CH - 1 - l);
     const float sc = wave_incl_scan(rev);
-    const float dgv = __shfl(sc, CH - 1 - l, WAVE);
+    const float dgv = shfl_idx(sc, CH - 1 - l);
     if (l < cp.len) {
       const long o = (cp.row0 + l) * H + h;
       if (VAR != VAR_DELTA) dg[o] = dgv;
@@ -849,8 +849,9 @@ __device__ __forceinline__ bf16x8 cvt8(const float (&x)[8]) {
   return r;
 }
 
+#ifdef GDN_TILE_LOOP
 template <int DK, int DV, int VAR>
-__global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __restrict__ q,
+__global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, const bf16* __restrict__ q,
                                                  const bf16* __restrict__ k, const bf16* __restrict__ v,
                                                  const float* __restrict__ g, const float* __restrict__ beta,
                                                  const float* __restrict__ states, const bf16* __restrict__ dO,
@@ -880,22 +881,34 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   __shared__ float hdh_w[8];
   __shared__ __align__(16) char ub[C::UB];
 
-  const int ci = blockIdx.x, h = blockIdx.y;
-  const ChunkPos cp = chunk_pos(geo, ci);
-  const long tile = (long)ci * H + h;
-  const int w = wave_id(), l = lane_id(), lg = l >> 4, lc = l & 15;
-  const int len = cp.len;
-  const bf16* qp = q + (cp.row0 * H + h) * DK;
-  const bf16* kp = k + (cp.row0 * H + h) * DK;
-  const bf16* vp = v + (cp.row0 * H + h) * DV;
-  const bf16* dop = dO + (cp.row0 * H + h) * DV;
-  bf16* dvp = dvo + (cp.row0 * H + h) * DV;
-  const float* hp = states + tile * DK * DV;
-  const bf16* dhp = dhg + tile * DK * DV;
-  const bf16* dUp = dUTg + tile * DV * CH;
+  // the loop-safe thread index reads this word: it is stored before any use
+  if (threadIdx.x == 0) gdn_tid_bias = 0;
+  __syncthreads();
   const long rsv = (long)H * DV;
 
-  // ---- operands of one value slice, loaded ahead of their use
+  // one (chunk, head) tile
+  struct Tile {
+    ChunkPos cp;
+    int h;
+    long t;
+  };
+  auto tile_at = [&](int t) {
+    Tile x;
+    const int ci = t / H;
+    x.h = t - ci * H;
+    x.t = t;
+    x.cp = chunk_pos(geo, ci);
+    return x;
+  };
+
+  // ---- operands loaded ahead of their use: a tile's q, k, T and raw gates
+  // (during the previous tile's last phase), and the value-slice operands
+  // (at the start of the tile, or a slice ahead)
+  struct Pre0 {
+    uint4 qk[2][NQK];  // q and k rows, masked at use
+    uint4 tq;          // 8 entries of T: row (thread index) / 8
+    float gv, bv;      // gate and beta of row l (wave 0 uses them), masked at use
+  };
   struct PreA {
     uint4 dov[NDO];                      // dO slice, staged to LDS
     bf16x8 du[CH / 32][TY::TM];          // dU'^T rows: A fragments of Y^T
@@ -906,11 +919,34 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     float hx[VS / 32][TD::TM][8];        // h: A fragments of X^T and dQ^T
     bf16x8 dh[VS / 32][TD::TM];          // dh: A fragments of dK^T
   };
-  bool ok = true;
-  auto load_a = [&](PreA& p, int c0) {
+  auto load_0 = [&](Pre0& p, const Tile& x) {
+    const int l = lane_id(), len = x.cp.len;
+    const bf16* qp = q + (x.cp.row0 * H + x.h) * DK;
+    const bf16* kp = k + (x.cp.row0 * H + x.h) * DK;
+#pragma unroll
+    for (int t = 0; t < NQK; ++t) {
+      const int idx = thread_x() + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
+      const long ro = clamp_row(r, len) * (long)H * DK + c;
+      p.qk[0][t] = *reinterpret_cast<const uint4*>(qp + ro);
+      p.qk[1][t] = *reinterpret_cast<const uint4*>(kp + ro);
+    }
+    p.tq = uint4{0u, 0u, 0u, 0u};
+    if constexpr (DT_) p.tq = *reinterpret_cast<const uint4*>(Tg + x.t * CH * CH + thread_x() * 8);
+    const long o = (x.cp.row0 + clamp_row(l, len)) * H + x.h;
+    p.gv = 0.f;
+    p.bv = 0.f;
+    if constexpr (VAR != VAR_DELTA) p.gv = g[o];
+    if constexpr (VAR != VAR_DECAY) p.bv = beta[o];
+  };
+  auto load_a = [&](PreA& p, const Tile& x, int c0) {
+    const int l = lane_id(), lg = l >> 4, lc = l & 15, len = x.cp.len;
+    const bf16* dop = dO + (x.cp.row0 * H + x.h) * DV;
+    const bf16* dUp = dUTg + x.t * DV * CH;
+    const float* hp = states + x.t * DK * DV;
+    const bf16* vp = v + (x.cp.row0 * H + x.h) * DV;
 #pragma unroll
     for (int t = 0; t < NDO; ++t) {
-      const int idx = threadIdx.x + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
+      const int idx = thread_x() + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
       p.dov[t] = *reinterpret_cast<const uint4*>(dop + clamp_row(r, len) * rsv + c0 + c);  // masked at use
     }
 #pragma unroll
@@ -935,7 +971,10 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
         }
     }
   };
-  auto load_b = [&](PreB& p, int c0) {
+  auto load_b = [&](PreB& p, const Tile& x, int c0) {
+    const int l = lane_id(), lg = l >> 4, lc = l & 15;
+    const float* hp = states + x.t * DK * DV;
+    const bf16* dhp = dhg + x.t * DK * DV;
 #pragma unroll
     for (int s = 0; s < VS / 32; ++s)
 #pragma unroll
@@ -949,28 +988,33 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
       }
   };
 
-  // ================= phase 0: gates, P, A; T comes from the prep kernel
-  uint4 qk[2][NQK];
-#pragma unroll
-  for (int t = 0; t < NQK; ++t) {
-    const int idx = threadIdx.x + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
-    const long ro = clamp_row(r, len) * (long)H * DK + c;
-    qk[0][t] = keep16(r < len, *reinterpret_cast<const uint4*>(qp + ro));
-    qk[1][t] = keep16(r < len, *reinterpret_cast<const uint4*>(kp + ro));
-  }
-  uint4 tq = {0u, 0u, 0u, 0u};  // 8 entries of T: row threadIdx.x / 8
-  if constexpr (DT_) tq = *reinterpret_cast<const uint4*>(Tg + tile * CH * CH + threadIdx.x * 8);
-  ok &= load_gates<VAR>(g, beta, cp.row0, H, h, len, Gs, Bs);
+  // Persistent: the block walks the tiles t = blockIdx.x, blockIdx.x + gridDim.x,
+  // ... (the grid never exceeds the tile count), so the next tile's operands
+  // load while this one's last phase runs.
+  Tile cur = tile_at(blockIdx.x);
+  Pre0 p0;
+  load_0(p0, cur);
+  for (int tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
+  const int w = wave_id(), l = lane_id(), lg = l >> 4, lc = l & 15;
+  const ChunkPos cp = cur.cp;
+  const int h = cur.h, len = cp.len;
+  const long tile = cur.t;
+  const bf16* vp = v + (cp.row0 * H + h) * DV;
+  bf16* dvp = dvo + (cp.row0 * H + h) * DV;
+  bool ok = true;
   PreA pa;
-  load_a(pa, 0);
+  load_a(pa, cur, 0);
+
+  // ================= phase 0: gates, P, A; T comes from the prep kernel
 #pragma unroll
   for (int t = 0; t < NQK; ++t) {
-    const int idx = threadIdx.x + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
-    *reinterpret_cast<uint4*>(Qs + r * LK + c) = qk[0][t];
-    *reinterpret_cast<uint4*>(Ks + r * LK + c) = qk[1][t];
+    const int idx = thread_x() + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
+    *reinterpret_cast<uint4*>(Qs + r * LK + c) = keep16(r < len, p0.qk[0][t]);
+    *reinterpret_cast<uint4*>(Ks + r * LK + c) = keep16(r < len, p0.qk[1][t]);
   }
   {
-    const int r = threadIdx.x >> 3, c = (threadIdx.x & 7) * 8;
+    const int r = thread_x() >> 3, c = (thread_x() & 7) * 8;
+    uint4 tq = p0.tq;
     if constexpr (!DT_) {
       bf16 e[8];
 #pragma unroll
@@ -979,9 +1023,16 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     }
     *reinterpret_cast<uint4*>(Ts + r * LT + c) = tq;
   }
+  if (w == 0) {
+    // in-chunk gates: G = inclusive cumsum of g (0 past the end), beta (0 past the end)
+    const float gv = l < len ? p0.gv : 0.f, bv = l < len ? p0.bv : 0.f;
+    ok = finite_f(gv) && finite_f(bv);
+    Gs[l] = wave_incl_scan(gv);
+    Bs[l] = bv;
+  }
   __syncthreads();
-  if (threadIdx.x < CH) {
-    const int r = threadIdx.x;
+  if (thread_x() < CH) {
+    const int r = thread_x();
     Gam[r] = __expf(Gs[r]);
     Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
   }
@@ -1025,7 +1076,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   for (int c0 = 0; c0 < DV; c0 += VS) {
     if (c0 > 0) {
       __syncthreads();  // the previous slice's LDS operands are consumed
-      load_a(pa, c0);
+      load_a(pa, cur, c0);
     }
     PreB pb;
     if constexpr (DT_) {
@@ -1046,7 +1097,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
           for (int a = 0; a < TY::TM; ++a) kht.acc[a][b] = M::mma(fa[a], fb, kht.acc[a][b]);
         }
       }
-      load_b(pb, c0);
+      load_b(pb, cur, c0);
 #pragma unroll
       for (int b = 0; b < TY::TN; ++b) {
         const int r = TY::n0(b) + lc;
@@ -1065,7 +1116,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
         }
       }
     } else {
-      load_b(pb, c0);
+      load_b(pb, cur, c0);
     }
     // Y^T = dU'^T T, so Y = T^T dU'.  dV = diag(beta) Y; keep -Y for dA and X
     {
@@ -1103,12 +1154,12 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     }
 #pragma unroll
     for (int t = 0; t < NDO; ++t) {
-      const int idx = threadIdx.x + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
+      const int idx = thread_x() + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
       *reinterpret_cast<uint4*>(dOs + r * LV + c) = keep16(r < len, pa.dov[t]);
     }
     if constexpr (!DT_) {
       // the scalar-decay member has U' = V
-      for (int idx = threadIdx.x; idx < CH * VS / 8; idx += blockDim.x) {
+      for (int idx = thread_x(); idx < CH * VS / 8; idx += blockDim.x) {
         const int r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
         const uint4 u = keep16(r < len, *reinterpret_cast<const uint4*>(vp + clamp_row(r, len) * rsv + c0 + c));
         ok &= finite16B<bf16>(u);
@@ -1176,6 +1227,10 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
     }
   }
   __syncthreads();  // phase-1 LDS operands are consumed
+  // the next tile's operands (this tile's again on the last pass: a clamped,
+  // unconditional prefetch keeps the registers loop-carried without copies)
+  const Tile nxt = tile_at(tt + (int)gridDim.x < ntiles ? tt + (int)gridDim.x : tt);
+  load_0(p0, nxt);
 
   // ================= phase 2: the chunk-level gradients
   bf16* dPmT = reinterpret_cast<bf16*>(ub);  // (dP * D)^T
@@ -1319,9 +1374,9 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
 #pragma unroll
     for (int i = 0; i < 8; ++i) hd += hdh_w[i];
     if (l == CH - 1) x += Gam[CH - 1] * hd + kk;
-    const float rev = __shfl(x, CH - 1 - l, WAVE);
+    const float rev = shfl_idx(x, CH - 1 - l);
     const float sc = wave_incl_scan(rev);
-    const float dgv = __shfl(sc, CH - 1 - l, WAVE);
+    const float dgv = shfl_idx(sc, CH - 1 - l);
     if (l < len) {
       const long o = (cp.row0 + l) * H + h;
       if (VAR != VAR_DELTA) dg[o] = dgv;
@@ -1331,11 +1386,35 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, const bf16* __r
   __syncthreads();
   store_rows<DK, LK>(dq + (cp.row0 * H + h) * DK, (long)H * DK, len, dqst);
   store_rows<DK, LK>(dk + (cp.row0 * H + h) * DK, (long)H * DK, len, dkst);
+  if (threadIdx.x == 0) gdn_tid_bias = 0;  // a new pass: index arithmetic is recomputed
   const int bad = __syncthreads_or(!ok);
   if (threadIdx.x == 0) flag[tile] = bad;
+  cur = nxt;
+  }
 }
 
+// Persistent launch: one block per compute unit (never more than the tiles).
+template <int DK, int DV, int VAR>
+hipError_t launch_grad_bf(const BwdArgs& a) {
+  const Geo& geo = a.geo;
+  const int H = geo.H;
+  const BwdWs& w = a.ws;
+  const int ntiles = geo.total_chunks * H;
+  const int grid = ntiles < a.num_cus ? ntiles : a.num_cus;
+  hipLaunchKernelGGL((k_grad_bf<DK, DV, VAR>), dim3(grid), dim3(512), 0, a.stream, geo, H, ntiles,
+                     (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, a.g, a.beta, a.states,
+                     (const bf16*)a.dO, (const bf16*)w.dh, (const bf16*)w.dUT, (const bf16*)w.T, (bf16*)a.dq,
+                     (bf16*)a.dk_, (bf16*)a.dv_, a.dg, a.dbeta, w.flag_grad);
+  return hipGetLastError();
+}
+#endif  // GDN_TILE_LOOP
+
 // ---------------------------------------------------------------------------
+// Launches the bf16 chunk-gradient kernel; instantiated in the translation
+// units compiled with GDN_TILE_LOOP.
+template <int DK, int DV, int VAR>
+hipError_t launch_grad_bf(const BwdArgs& a);
+
 template <int DK, int DV, typename OP, int VAR>
 static hipError_t launch_bwd_t(const BwdArgs& a) {
   constexpr int BV = SCAN_BV;
@@ -1362,11 +1441,8 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
   }
   stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0 && sizeof(OP) == 2) {
-    hipLaunchKernelGGL((k_grad_bf<DK, DV, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
-                       (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, a.g, a.beta, a.states,
-                       (const bf16*)a.dO, (const bf16*)w.dh, (const bf16*)w.dUT, (const bf16*)w.T, (bf16*)a.dq,
-                       (bf16*)a.dk_,
-                       (bf16*)a.dv_, a.dg, a.dbeta, w.flag_grad);
+    const hipError_t e = launch_grad_bf<DK, DV, VAR>(a);
+    if (e != hipSuccess) return e;
   } else if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_grad_bwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, a.states,

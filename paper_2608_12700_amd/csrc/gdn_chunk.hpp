@@ -82,7 +82,7 @@ __device__ __forceinline__ bool load_rows(const T* __restrict__ src, long rs, in
   constexpr int V = 16 / (int)sizeof(T);  // elements per 16-byte vector
   constexpr int PER_ROW = D / V;
   bool ok = true;
-  for (int idx = threadIdx.x; idx < CH * PER_ROW; idx += blockDim.x) {
+  for (int idx = thread_x(); idx < CH * PER_ROW; idx += blockDim.x) {
     const int r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
     const uint4 u = keep16(r < len, *reinterpret_cast<const uint4*>(src + clamp_row(r, len) * rs + c));
     ok &= finite16B<T>(u);
@@ -96,7 +96,7 @@ template <int R, int D, int LD, typename T>
 __device__ __forceinline__ void load_dense(const T* __restrict__ src, T* dst) {
   constexpr int V = 16 / (int)sizeof(T);
   constexpr int PER_ROW = D / V;
-  for (int idx = threadIdx.x; idx < R * PER_ROW; idx += blockDim.x) {
+  for (int idx = thread_x(); idx < R * PER_ROW; idx += blockDim.x) {
     const int r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
     *reinterpret_cast<uint4*>(dst + r * LD + c) = *reinterpret_cast<const uint4*>(src + (long)r * D + c);
   }
@@ -116,7 +116,7 @@ struct RowsIn {
   __device__ __forceinline__ void load(const T* __restrict__ src, long rs, int len) {
 #pragma unroll
     for (int t = 0; t < N; ++t) {
-      const int idx = threadIdx.x + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
+      const int idx = thread_x() + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
       u[t] = *reinterpret_cast<const uint4*>(src + clamp_row(r, len) * rs + c);
     }
   }
@@ -125,7 +125,7 @@ struct RowsIn {
     bool ok = true;
 #pragma unroll
     for (int t = 0; t < N; ++t) {
-      const int idx = threadIdx.x + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
+      const int idx = thread_x() + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
       const uint4 x = keep16(r < len, u[t]);
       ok &= finite16B<T>(x);
       *reinterpret_cast<uint4*>(dst + r * LD + c) = x;
@@ -138,7 +138,7 @@ template <int D, int LD, typename T>
 __device__ __forceinline__ void store_rows(T* __restrict__ dst, long rs, int len, const T* src) {
   constexpr int V = 16 / (int)sizeof(T);
   constexpr int PER_ROW = D / V;
-  for (int idx = threadIdx.x; idx < CH * PER_ROW; idx += blockDim.x) {
+  for (int idx = thread_x(); idx < CH * PER_ROW; idx += blockDim.x) {
     const int r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
     if (r < len)
       *reinterpret_cast<uint4*>(dst + r * rs + c) = *reinterpret_cast<const uint4*>(src + r * LD + c);
@@ -190,7 +190,7 @@ __device__ __forceinline__ void unit_lower_inverse(const float* As, float* Tf, O
   constexpr bool BF = sizeof(OP) == 2;
   const int w = wave_id(), l = lane_id(), g = l >> 4, c = l & 15;
   // the six blocks above the diagonal are zero (T^T: below it)
-  for (int idx = threadIdx.x; idx < 6 * 256; idx += blockDim.x) {
+  for (int idx = thread_x(); idx < 6 * 256; idx += blockDim.x) {
     const int blk = idx >> 8, rr = (idx >> 4) & 15, cc = idx & 15;
     const int bi = blk < 3 ? 0 : (blk < 5 ? 1 : 2);
     const int bj = blk < 3 ? blk + 1 : (blk < 5 ? blk - 1 : 3);

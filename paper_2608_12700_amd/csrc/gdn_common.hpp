@@ -35,8 +35,28 @@ template <> struct op_of<DT_BF16> { typedef bf16 type; };
 template <> __device__ __forceinline__ float from_f<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f<bf16>(float x) { return static_cast<bf16>(x); }
 
-__device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
-__device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
+// Thread index within the block.  A translation unit whose kernel walks
+// several tiles in one launch defines GDN_TILE_LOOP: the index then reads
+// gdn_tid_bias, an LDS word that is always 0 and that the kernel stores again
+// on every pass of its tile loop.  Index arithmetic derived from it can be
+// neither hoisted out of the loop (where it would sit in registers through
+// every phase) nor carried across a barrier; it is recomputed next to its
+// uses.  Such a kernel stores the word before its first barrier.
+#ifdef GDN_TILE_LOOP
+__shared__ int gdn_tid_bias;
+__device__ __forceinline__ int thread_x() { return (int)threadIdx.x + gdn_tid_bias; }
+#else
+__device__ __forceinline__ int thread_x() { return (int)threadIdx.x; }
+#endif
+__device__ __forceinline__ int lane_id() { return (int)((unsigned)thread_x() & (WAVE - 1)); }
+__device__ __forceinline__ int wave_id() { return (int)((unsigned)thread_x() / WAVE); }
+
+// Value of x held by lane src (0..63) of the wave; addresses outside the
+// wave wrap around.
+__device__ __forceinline__ float shfl_idx(float x, int src) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src << 2, __builtin_bit_cast(int, x)));
+}
+__device__ __forceinline__ float shfl_xor(float x, int m) { return shfl_idx(x, lane_id() ^ m); }
 
 __device__ __forceinline__ bool finite_f(float x) {
   return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
@@ -427,7 +447,7 @@ __device__ __forceinline__ float wave_incl_scan(float x) {
   const int l = lane_id();
 #pragma unroll
   for (int off = 1; off < WAVE; off <<= 1) {
-    const float y = __shfl_up(x, off, WAVE);
+    const float y = shfl_idx(x, l - off);  // unused where l < off
     if (l >= off) x += y;
   }
   return x;
@@ -436,7 +456,7 @@ __device__ __forceinline__ float wave_incl_scan(float x) {
 // Fixed-order wave reduction (butterfly).
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
-  for (int off = WAVE / 2; off > 0; off >>= 1) x += __shfl_xor(x, off, WAVE);
+  for (int off = WAVE / 2; off > 0; off >>= 1) x += shfl_xor(x, off);
   return x;
 }
 

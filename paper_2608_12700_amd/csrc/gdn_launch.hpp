@@ -65,6 +65,7 @@ struct BwdArgs {
   BwdWs ws;
   hipStream_t stream;
   hipEvent_t const* events;
+  int num_cus;  // compute units of the device (grid of the persistent gradient kernel)
 };
 
 constexpr int NUM_STAGES = 4;

@@ -436,21 +436,6 @@ struct GradRegion {
   static_assert(bytes == grad_region_bytes(DK, (int)sizeof(OP)), "host and device disagree");
 };
 
-// Sum over the 16 lanes that share a k-group (lanes l with equal l >> 4).
-__device__ __forceinline__ float sum16(float x) {
-  x += shfl_xor(x, 1);
-  x += shfl_xor(x, 2);
-  x += shfl_xor(x, 4);
-  x += shfl_xor(x, 8);
-  return x;
-}
-// Sum over the 4 k-groups (lanes l, l^16, l^32, l^48).
-__device__ __forceinline__ float sum_groups(float x) {
-  x += shfl_xor(x, 16);
-  x += shfl_xor(x, 32);
-  return x;
-}
-
 template <int DK, int DV, typename OP, int VAR>
 __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __restrict__ q,
                                                   const OP* __restrict__ k, const OP* __restrict__ v,
@@ -938,11 +923,11 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     if constexpr (VAR != VAR_DELTA) p.gv = g[o];
     if constexpr (VAR != VAR_DECAY) p.bv = beta[o];
   };
-  auto load_a = [&](PreA& p, const Tile& x, int c0) {
+  // dO, dU'^T and v of a value slice
+  auto load_a1 = [&](PreA& p, const Tile& x, int c0) {
     const int l = lane_id(), lg = l >> 4, lc = l & 15, len = x.cp.len;
     const bf16* dop = dO + (x.cp.row0 * H + x.h) * DV;
     const bf16* dUp = dUTg + x.t * DV * CH;
-    const float* hp = states + x.t * DK * DV;
     const bf16* vp = v + (x.cp.row0 * H + x.h) * DV;
 #pragma unroll
     for (int t = 0; t < NDO; ++t) {
@@ -956,12 +941,6 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
         p.du[s][a] = *reinterpret_cast<const bf16x8*>(dUp + op_off<bf16, CH>(c0 + TY::m0(a), 32 * s) + l * 8);
     if constexpr (DT_) {
 #pragma unroll
-      for (int s = 0; s < DK / 32; ++s)
-#pragma unroll
-        for (int a = 0; a < TY::TM; ++a)
-#pragma unroll
-          for (int j = 0; j < 8; ++j) p.hk[s][a][j] = hp[(32 * s + 8 * lg + j) * DV + c0 + TY::m0(a) + lc];
-#pragma unroll
       for (int a = 0; a < TY::TM; ++a)
 #pragma unroll
         for (int b = 0; b < TY::TN; ++b) {
@@ -969,6 +948,19 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
           // masked at use
           p.vb[a][b] = *reinterpret_cast<const uint2*>(vp + clamp_row(r, len) * rsv + c0 + TY::m0(a) + 4 * lg);
         }
+    }
+  };
+  // h^T of a value slice
+  auto load_a2 = [&](PreA& p, const Tile& x, int c0) {
+    const int l = lane_id(), lg = l >> 4, lc = l & 15;
+    const float* hp = states + x.t * DK * DV;
+    if constexpr (DT_) {
+#pragma unroll
+      for (int s = 0; s < DK / 32; ++s)
+#pragma unroll
+        for (int a = 0; a < TY::TM; ++a)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) p.hk[s][a][j] = hp[(32 * s + 8 * lg + j) * DV + c0 + TY::m0(a) + lc];
     }
   };
   auto load_b = [&](PreB& p, const Tile& x, int c0) {
@@ -993,7 +985,10 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   // load while this one's last phase runs.
   Tile cur = tile_at(blockIdx.x);
   Pre0 p0;
+  PreA pa;
   load_0(p0, cur);
+  load_a1(pa, cur, 0);
+  load_a2(pa, cur, 0);
   for (int tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
   const int w = wave_id(), l = lane_id(), lg = l >> 4, lc = l & 15;
   const ChunkPos cp = cur.cp;
@@ -1002,8 +997,6 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   const bf16* vp = v + (cp.row0 * H + h) * DV;
   bf16* dvp = dvo + (cp.row0 * H + h) * DV;
   bool ok = true;
-  PreA pa;
-  load_a(pa, cur, 0);
 
   // ================= phase 0: gates, P, A; T comes from the prep kernel
 #pragma unroll
@@ -1076,7 +1069,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   for (int c0 = 0; c0 < DV; c0 += VS) {
     if (c0 > 0) {
       __syncthreads();  // the previous slice's LDS operands are consumed
-      load_a(pa, cur, c0);
+      load_a1(pa, cur, c0);
+      load_a2(pa, cur, c0);
     }
     PreB pb;
     if constexpr (DT_) {
@@ -1231,6 +1225,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   // unconditional prefetch keeps the registers loop-carried without copies)
   const Tile nxt = tile_at(tt + (int)gridDim.x < ntiles ? tt + (int)gridDim.x : tt);
   load_0(p0, nxt);
+  load_a1(pa, nxt, 0);
 
   // ================= phase 2: the chunk-level gradients
   bf16* dPmT = reinterpret_cast<bf16*>(ub);  // (dP * D)^T
@@ -1352,6 +1347,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
       *reinterpret_cast<uint2*>(dqst + r * LK + d0) = pack4<bf16>(q4);
       *reinterpret_cast<uint2*>(dkst + r * LK + d0) = pack4<bf16>(k4);
     }
+  load_a2(pa, nxt, 0);  // the accumulators are free: the next tile's h^T
   if (w == 0) {
     const int r = l;
     float rq = 0.f, rx = 0.f, rk = 0.f;

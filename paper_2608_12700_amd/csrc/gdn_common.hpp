@@ -453,11 +453,33 @@ __device__ __forceinline__ float wave_incl_scan(float x) {
   return x;
 }
 
-// Fixed-order wave reduction (butterfly).
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int off = WAVE / 2; off > 0; off >>= 1) x += shfl_xor(x, off);
+// Cross-lane sums on the VALU (no LDS traffic).  Every lane of a group ends
+// with the same bits: each step adds a pair of partial sums that the two lanes
+// of the pair hold in the same order.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+// Sum over the 16 lanes of a row (lanes with equal l >> 4): quad xor 1, quad
+// xor 2, half-row mirror, row mirror.
+__device__ __forceinline__ float sum16(float x) {
+  x += dpp<0xB1>(x);
+  x += dpp<0x4E>(x);
+  x += dpp<0x141>(x);
+  x += dpp<0x140>(x);
   return x;
 }
+// Sum over the 4 rows (lanes l, l^16, l^32, l^48): swap the wave halves, then
+// the odd and even rows (gfx950 v_permlane32_swap / v_permlane16_swap).
+__device__ __forceinline__ float sum_groups(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  x = __builtin_bit_cast(float, (unsigned)a[0]) + __builtin_bit_cast(float, (unsigned)a[1]);
+  const unsigned v = __builtin_bit_cast(unsigned, x);
+  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return __builtin_bit_cast(float, (unsigned)b[0]) + __builtin_bit_cast(float, (unsigned)b[1]);
+}
+// Fixed-order wave reduction.
+__device__ __forceinline__ float wave_sum(float x) { return sum_groups(sum16(x)); }
 
 }  // namespace gdn

@@ -27,7 +27,7 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
                                                   const OP* __restrict__ k, const OP* __restrict__ v,
                                                   const float* __restrict__ g, const float* __restrict__ beta,
                                                   float* __restrict__ gcum, OP* __restrict__ Wg,
-                                                  float* __restrict__ Ug, OP* __restrict__ KhTg,
+                                                  OP* __restrict__ Ug, OP* __restrict__ KhTg,
                                                   OP* __restrict__ Pg, OP* __restrict__ Qgg, int* __restrict__ flag) {
   constexpr bool DT_ = VAR != VAR_DECAY;
   // bf16 operands read transposed tiles straight from row-major LDS with the
@@ -215,9 +215,9 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
           *reinterpret_cast<V4*>(Wt + op_off<OP, DK>(r, d0)) = pack4<OP>(v4);
         }
     }
-    // U = T diag(beta) V, per slice of VS value columns, stored as the scan's
-    // accumulator tiles (four rows of one column per lane: one float4)
-    float* Ut = Ug + tile * CH * DV;
+    // U = T diag(beta) V, per slice of VS value columns, stored in the operand
+    // dtype as the scan's accumulator tiles (four rows of one column per lane)
+    OP* Ut = Ug + tile * CH * DV;
 #pragma unroll
     for (int t = 0; t < NSL; ++t) {
       const int c0 = t * VS;
@@ -241,8 +241,10 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
       for (int b = 0; b < uu.TN; ++b) {
         const int r0 = uu.m0(0) + (l >> 4) * 4, vcol = c0 + uu.n0(b) + (l & 15);
-        *reinterpret_cast<float4*>(Ut + cfrag_off<SCAN_BV>(r0, vcol)) =
-            float4{uu.acc[0][b][0], uu.acc[0][b][1], uu.acc[0][b][2], uu.acc[0][b][3]};
+        OP u4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) u4[j] = from_f<OP>(uu.acc[0][b][j]);
+        *reinterpret_cast<V4*>(Ut + cfrag_off<SCAN_BV>(r0, vcol)) = pack4<OP>(u4);
       }
       if (t + 1 < NSL) __syncthreads();
     }
@@ -267,7 +269,7 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
                                                   const OP* __restrict__ v, const float* __restrict__ S0,
                                                   const float* __restrict__ gcum, const OP* __restrict__ Wg,
                                                   const OP* __restrict__ KhTg, const OP* __restrict__ Pg,
-                                                  const float* __restrict__ Ug, float* __restrict__ states,
+                                                  const OP* __restrict__ Ug, float* __restrict__ states,
                                                   float* __restrict__ ST, OP* __restrict__ o,
                                                   int* __restrict__ flag) {
   static_assert(BV == SCAN_BV, "U is laid out for the scan's value tiles");
@@ -293,7 +295,7 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     typename UT::template AFr<OP, DK> qf;
     typename UT::template AFr<OP, CH> pf;
     typename HT::template AFr<OP, CH> kh;
-    float u[UT::TN][4];
+    typename vec4_of<OP>::type u[UT::TN];  // U (or V): four rows of one column per lane
     float gl;  // G_last, exponentiated at use so the prefetch never waits
   };
   // A fragments of a pre-arranged operand (fragment-major for bf16, row-major for fp32)
@@ -316,23 +318,25 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     const int len = min(CH, sp.len - c * CH);
     if constexpr (VAR != VAR_DECAY) {
       frags(p.w, Wg + tile * CH * DK, UT{}, std::integral_constant<int, DK>{});
-      const float* Ut = Ug + tile * CH * DV;
+      const OP* Ut = Ug + tile * CH * DV;
 #pragma unroll
-      for (int b = 0; b < UT::TN; ++b) {
-        const float4 x = *reinterpret_cast<const float4*>(Ut + cfrag_off<BV>(UT::m0(0) + (l >> 4) * 4, v0 + UT::n0(b) + (l & 15)));
-        p.u[b][0] = x.x; p.u[b][1] = x.y; p.u[b][2] = x.z; p.u[b][3] = x.w;
-      }
+      for (int b = 0; b < UT::TN; ++b)
+        p.u[b] = *reinterpret_cast<const typename vec4_of<OP>::type*>(
+            Ut + cfrag_off<BV>(UT::m0(0) + (l >> 4) * 4, v0 + UT::n0(b) + (l & 15)));
     } else {
       const OP* vp = v + (row0 * H + h) * DV + v0;
 #pragma unroll
-      for (int b = 0; b < UT::TN; ++b)
+      for (int b = 0; b < UT::TN; ++b) {
+        OP x4[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int r = UT::m0(0) + (l >> 4) * 4 + j;
           // U' = V here; its rows past the chunk's end meet only zero columns of
           // Khat^T and P, so the last valid row may stand in for them
-          p.u[b][j] = to_f(vp[(long)clamp_row(r, len) * H * DV + UT::n0(b) + (l & 15)]);
+          x4[j] = vp[(long)clamp_row(r, len) * H * DV + UT::n0(b) + (l & 15)];
         }
+        p.u[b] = pack4<OP>(x4);
+      }
     }
     frags(p.qf, Qgg + tile * CH * DK, UT{}, std::integral_constant<int, DK>{});
     frags(p.pf, Pg + tile * CH * CH, UT{}, std::integral_constant<int, CH>{});
@@ -390,12 +394,12 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 #pragma unroll
       for (int b = 0; b < UT::TN; ++b)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) up.acc[0][b][j] = cur.u[b][j] - up.acc[0][b][j];
+        for (int j = 0; j < 4; ++j) up.acc[0][b][j] = to_f(elem4<OP>(cur.u[b], j)) - up.acc[0][b][j];
     } else {
 #pragma unroll
       for (int b = 0; b < UT::TN; ++b)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) up.acc[0][b][j] = cur.u[b][j];
+        for (int j = 0; j < 4; ++j) up.acc[0][b][j] = to_f(elem4<OP>(cur.u[b], j));
     }
 #pragma unroll
     for (int b = 0; b < UT::TN; ++b) {
@@ -464,14 +468,14 @@ static hipError_t launch_fwd_t(const FwdArgs& a) {
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_prep_fwd<DK, DV, OP, VAR>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream,
                        geo, H, (const OP*)a.q, (const OP*)a.k, (const OP*)a.v, a.g, a.beta, w.gcum,
-                       (OP*)w.W, w.U, (OP*)w.KhT, (OP*)w.P, (OP*)w.Qg, w.flag_prep);
+                       (OP*)w.W, (OP*)w.U, (OP*)w.KhT, (OP*)w.P, (OP*)w.Qg, w.flag_prep);
   }
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
     hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
                        (const OP*)w.Qg, (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, (const OP*)w.KhT,
-                       (const OP*)w.P, w.U, a.states, a.ST, (OP*)a.o, w.flag_scan);
+                       (const OP*)w.P, (const OP*)w.U, a.states, a.ST, (OP*)a.o, w.flag_scan);
   }
   stage_mark(a.events, 2, a.stream);
   if (NS > 0) {

@@ -15,7 +15,7 @@ struct FwdWs {
   int* flag_scan;  // [N*H*NVT]    non-finite S0 slice
   float* gcum;     // [chunks*H*64] in-chunk cumulative log-decay
   void* W;         // [chunks*H*64*dk] operand dtype
-  float* U;        // [chunks*H*64*dv]
+  float* U;        // [chunks*H*64*dv] in the operand dtype (sized for fp32)
   void* KhT;       // [chunks*H*dk*64] operand dtype, (e^{G_last-G} K)^T
   void* P;         // [chunks*H*64*64] operand dtype, (Q K^T) * D
   void* Qg;        // [chunks*H*64*dk] operand dtype, diag(e^G) Q

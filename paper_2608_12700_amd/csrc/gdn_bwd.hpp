@@ -346,13 +346,25 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
       // dh entering this chunk, for the gradient kernel, in its fragment order
       constexpr int VE = 16 / (int)sizeof(OP);
       OP* dhp = dhg + tile * DK * DV;
+      if constexpr (sizeof(OP) == 2) {
+        // one (16 d x 32 v) fragment per wave and step, read down the columns
+        // of dh^T by the transposing load and stored as one 1 KiB block
+        static_assert(BV % 32 == 0 && (DK / 16) * (BV / 32) % 4 == 0, "whole fragments per wave");
 #pragma unroll
-      for (int t = 0; t < DK * BV / VE / 256; ++t) {
-        const int idx = threadIdx.x + t * 256, d = idx / (BV / VE), vq = (idx - d * (BV / VE)) * VE;
-        OP vals[VE];
+        for (int t = 0; t < (DK / 16) * (BV / 32) / 4; ++t) {
+          const int f = wave_id() + 4 * t, mt = f / (BV / 32), kb = f - mt * (BV / 32);
+          const bf16x8 x = lds_frag_tr<LK>(dhT, 16 * mt, 32 * kb);
+          *reinterpret_cast<bf16x8*>(dhp + op_off<OP, DV>(16 * mt, v0 + 32 * kb) + l * 8) = x;
+        }
+      } else {
 #pragma unroll
-        for (int j = 0; j < VE; ++j) vals[j] = dhT[(vq + j) * LK + d];
-        *reinterpret_cast<uint4*>(dhp + op_off<OP, DV>(d, v0 + vq)) = pack16<OP>(vals);
+        for (int t = 0; t < DK * BV / VE / 256; ++t) {
+          const int idx = threadIdx.x + t * 256, d = idx / (BV / VE), vq = (idx - d * (BV / VE)) * VE;
+          OP vals[VE];
+#pragma unroll
+          for (int j = 0; j < VE; ++j) vals[j] = dhT[(vq + j) * LK + d];
+          *reinterpret_cast<uint4*>(dhp + op_off<OP, DV>(d, v0 + vq)) = pack16<OP>(vals);
+        }
       }
     }
     HT inj;  // (diag(e^G) Q)^T dO, independent of the carry

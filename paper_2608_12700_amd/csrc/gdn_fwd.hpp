@@ -450,6 +450,223 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
   if (threadIdx.x == 0) flag[(long)s * NVT + vt] = bad;
 }
 
+// The forward scan for bf16 operands of the delta-rule members, split into
+// four chain waves and four copy waves.  Everything the chain reads per chunk
+// except the carry (W, diag(e^G) Q, P, Khat^T, this block's slice of U and
+// the chunk's G) is stored in HBM as contiguous 1 KiB fragment blocks; the
+// copy waves move the next chunk's 60 KiB straight into one of two LDS
+// buffers with global_load_lds_dwordx4 and write the chunk state out of LDS,
+// so the chain waves never queue behind the address unit.  Per chunk:
+//   chain: h -> LDS | barrier | U' = U - W h, O = diag(e^G) Q h | barrier |
+//          h <- e^{G_last} h + Khat^T U', O += P U', store O
+//   copy:             | next chunk's operands -> LDS, state -> HBM | | wait
+template <int DK, int DV, int BV, int VAR>
+__global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16* __restrict__ Qgg,
+                                                     const float* __restrict__ S0, const float* __restrict__ gcum,
+                                                     const bf16* __restrict__ Wg, const bf16* __restrict__ KhTg,
+                                                     const bf16* __restrict__ Pg, const bf16* __restrict__ Ug,
+                                                     float* __restrict__ states, float* __restrict__ ST,
+                                                     bf16* __restrict__ o, int* __restrict__ flag) {
+  static_assert(BV == SCAN_BV && VAR != VAR_DECAY, "U is laid out for the scan's value tiles");
+  constexpr int NVT = DV / BV;
+  constexpr int LK = DK + 8, LU = CH + 8, LF = BV + 4;
+  typedef Tiles<DK, BV, 4, 1> HT;  // carried state slice h[:, v0:v0+BV] (chain waves)
+  typedef Tiles<CH, BV, 4, 1> UT;  // U' and output slices (chain waves)
+  // one operand buffer: fragment blocks of 1 KiB (64 lanes x 16 B) in HBM order
+  constexpr int NW = (CH / 16) * (DK / 32), NP = (CH / 16) * (CH / 32), NK = (DK / 16) * (CH / 32);
+  constexpr int NU = CH * BV * 2 / 1024;
+  constexpr int OW = 0, OQ = OW + NW, OP_ = OQ + NW, OK = OP_ + NP, OU = OK + NK, NB = OU + NU;
+  constexpr int BUF = NB * 1024 + CH * 4;  // + the chunk's G (64 fp32)
+  __shared__ __align__(1024) char buf[2][BUF];
+  __shared__ __align__(16) bf16 hT[BV * LK];
+  __shared__ __align__(16) float hF[DK * LF];  // h in fp32, row-major, for whole-line state stores
+  __shared__ __align__(16) bf16 UsT[BV * LU];
+  __shared__ __align__(16) char sink[1024];  // target of the L2 warm-up loads (never read)
+
+  int s, vt;
+  scan_block_coords(blockIdx.x, geo.N * H, NVT, s, vt);
+  const int n = s / H, h = s - (s / H) * H, v0 = vt * BV;
+  const SeqPos sp = seq_pos(geo, n);
+  const int w = wave_id(), l = lane_id();
+  const bool chain = w < 4;  // waves 0-3: the carry; waves 4-7: copies
+  const int nch = sp.nch;
+
+  // copy waves: chunk c's operands into buffer b (block j of the list goes to
+  // buf[b] + j KiB; the copy wave w - 4 takes every fourth block)
+  typedef __attribute__((address_space(1))) void gvoid;
+  typedef __attribute__((address_space(3))) void lvoid;
+  auto fill = [&](int c, int b) {
+    const long tile = (long)(sp.c0 + c) * H + h;
+#pragma unroll
+    for (int j0 = 0; j0 < NB; j0 += 4) {
+      const int j = j0 + (w - 4);
+      if (j < NB) {
+        const bf16* src;
+        if (j < OQ) src = Wg + tile * CH * DK + (j - OW) * 512;
+        else if (j < OP_) src = Qgg + tile * CH * DK + (j - OQ) * 512;
+        else if (j < OK) src = Pg + tile * CH * CH + (j - OP_) * 512;
+        else if (j < OU) src = KhTg + tile * DK * CH + (j - OK) * 512;
+        else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512;
+        __builtin_amdgcn_global_load_lds((gvoid*)(src + l * 8), (lvoid*)(buf[b] + j * 1024), 16, 0, 0);
+      }
+    }
+    if (w == 4) __builtin_amdgcn_global_load_lds((gvoid*)(gcum + tile * CH + l), (lvoid*)(buf[b] + NB * 1024), 4, 0, 0);
+  };
+  // the copy waves' loads landed: their state stores, issued after them, may
+  // stay in flight (vmcnt counts in issue order on gfx9)
+  constexpr int NST = DK * BV / 4 / 256;  // state stores per copy-wave lane and chunk
+  static_assert(NST < 16, "vmcnt field");
+  // L2 warm-up two chunks ahead: the NVT blocks of a stream share the
+  // chunk's W, Q, P and Khat^T blocks (one in NVT each) and each warms its
+  // own U slice; every copy wave issues exactly NWARM loads.
+  constexpr int NSH = (OU + NVT - 1) / NVT;  // shared blocks warmed per block
+  constexpr int NWARM = (NSH + NU + 3) / 4;
+  auto warm = [&](int c) {
+    const long tile = (long)(sp.c0 + c) * H + h;
+#pragma unroll
+    for (int t = 0; t < NWARM; ++t) {
+      int e = (w - 4) + 4 * t;
+      e = e < NSH + NU ? e : NSH + NU - 1;
+      int j = e < NSH ? e * NVT + vt : OU + (e - NSH);
+      j = j < NB ? j : NB - 1;
+      const bf16* src;
+      if (j < OQ) src = Wg + tile * CH * DK + (j - OW) * 512;
+      else if (j < OP_) src = Qgg + tile * CH * DK + (j - OQ) * 512;
+      else if (j < OK) src = Pg + tile * CH * CH + (j - OP_) * 512;
+      else if (j < OU) src = KhTg + tile * DK * CH + (j - OK) * 512;
+      else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512;
+      __builtin_amdgcn_global_load_lds((gvoid*)(src + l * 8), (lvoid*)sink, 16, 0, 0);
+    }
+  };
+  static_assert(NWARM + NST < 16, "vmcnt field");
+  auto copies_done = [] { __builtin_amdgcn_s_waitcnt(0x0F70 | (NWARM + NST)); };  // vmcnt(NWARM + NST)
+  // A workgroup barrier that waits for this wave's LDS operations only.  Each
+  // wave's global loads into LDS are waited for by that wave (copies_done);
+  // a full __syncthreads would also wait for every store still in flight.
+  auto lds_barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+
+  HT hs;
+  bool ok = true;
+  if (chain) {
+    const float* S0p = S0 ? S0 + ((long)n * H + h) * DK * DV : nullptr;
+    hs.each([&](int d, int vv, float& x) {
+      x = S0p ? S0p[d * DV + v0 + vv] : 0.f;
+      ok &= finite_f(x);
+    });
+    lds_barrier();
+    // The chain and the copy waves run separate loops with the same barrier
+    // sequence (two per chunk), so neither waits for the other's memory
+    // operations at a barrier.
+    for (int c = 0; c < nch; ++c) {
+      const char* B = buf[c & 1];
+      // h to LDS: operand copy (4 consecutive d per lane: one 8-byte write) and
+      // fp32 row-major copy for the state store
+#pragma unroll
+      for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+        for (int bb = 0; bb < HT::TN; ++bb) {
+          const int d0 = HT::m0(a) + (l >> 4) * 4, vv = HT::n0(bb) + (l & 15);
+          bf16 h4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            h4[j] = from_f<bf16>(hs.acc[a][bb][j]);
+            hF[(d0 + j) * LF + vv] = hs.acc[a][bb][j];
+          }
+          *reinterpret_cast<uint2*>(hT + vv * LK + d0) = pack4<bf16>(h4);
+        }
+      lds_barrier();  // A: h in LDS, this chunk's operands in buffer c & 1
+      // U' = U - W h and O = diag(e^G) Q h; A fragments of wave w are 16-row tile w
+      UT up, ot;
+      const bf16x8* Wf = reinterpret_cast<const bf16x8*>(B + OW * 1024);
+      const bf16x8* Qf = reinterpret_cast<const bf16x8*>(B + OQ * 1024);
+      ot.zero();
+      up.zero();
+#pragma unroll
+      for (int st = 0; st < DK / 32; ++st) {
+        const bf16x8 fq = Qf[(w * (DK / 32) + st) * 64 + l];
+        const bf16x8 fw = Wf[(w * (DK / 32) + st) * 64 + l];
+#pragma unroll
+        for (int bb = 0; bb < UT::TN; ++bb) {
+          const bf16x8 fh = Mma<bf16>::load(KRow<bf16, LK>{hT}, UT::n0(bb), 32 * st);
+          ot.acc[0][bb] = Mma<bf16>::mma(fq, fh, ot.acc[0][bb]);
+          up.acc[0][bb] = Mma<bf16>::mma(fw, fh, up.acc[0][bb]);
+        }
+      }
+      const uint2* Uf = reinterpret_cast<const uint2*>(B + OU * 1024);
+#pragma unroll
+      for (int bb = 0; bb < UT::TN; ++bb) {
+        const uint2 u = Uf[(w * UT::TN + bb) * 64 + l];
+        const int vv = UT::n0(bb) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
+        bf16 u4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          up.acc[0][bb][j] = to_f(elem4<bf16>(u, j)) - up.acc[0][bb][j];
+          u4[j] = from_f<bf16>(up.acc[0][bb][j]);
+        }
+        *reinterpret_cast<uint2*>(UsT + vv * LU + r0) = pack4<bf16>(u4);
+      }
+      lds_barrier();  // B: U' in LDS
+      const float gl = __expf(reinterpret_cast<const float*>(B + NB * 1024)[CH - 1]);
+      hs.each([&](int, int, float& x) { x *= gl; });
+      const bf16x8* Kf = reinterpret_cast<const bf16x8*>(B + OK * 1024);
+      const bf16x8* Pf = reinterpret_cast<const bf16x8*>(B + OP_ * 1024);
+#pragma unroll
+      for (int st = 0; st < CH / 32; ++st) {
+        bf16x8 fk[HT::TM];
+#pragma unroll
+        for (int a = 0; a < HT::TM; ++a) fk[a] = Kf[((HT::m0(a) >> 4) * (CH / 32) + st) * 64 + l];
+        const bf16x8 fp = Pf[(w * (CH / 32) + st) * 64 + l];
+#pragma unroll
+        for (int bb = 0; bb < UT::TN; ++bb) {
+          const bf16x8 fu = Mma<bf16>::load(KRow<bf16, LU>{UsT}, UT::n0(bb), 32 * st);
+#pragma unroll
+          for (int a = 0; a < HT::TM; ++a) hs.acc[a][bb] = Mma<bf16>::mma(fk[a], fu, hs.acc[a][bb]);
+          ot.acc[0][bb] = Mma<bf16>::mma(fp, fu, ot.acc[0][bb]);
+        }
+      }
+      const long row0 = sp.row0 + (long)c * CH;
+      const int len = min(CH, sp.len - c * CH);
+      bf16* op = o + (row0 * H + h) * DV + v0;
+#pragma unroll
+      for (int bb = 0; bb < UT::TN; ++bb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = UT::m0(0) + (l >> 4) * 4 + j;
+          if (r < len) op[(long)r * H * DV + UT::n0(bb) + (l & 15)] = from_f<bf16>(ot.acc[0][bb][j]);
+        }
+    }
+    float* STp = ST + ((long)n * H + h) * DK * DV;
+    hs.each([&](int d, int vv, float& x) { STp[d * DV + v0 + vv] = x; });
+  } else {
+    if (nch > 0) {
+      fill(0, 0);
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    }
+    lds_barrier();
+    for (int c = 0; c < nch; ++c) {
+      const long tile = (long)(sp.c0 + c) * H + h;
+      lds_barrier();  // A: h of this chunk in LDS; buffer (c + 1) & 1 is free
+      // issue order fills, warm-ups, stores (kept by the empty asm statements):
+      // copies_done counts on it
+      if (c + 1 < nch) fill(c + 1, (c + 1) & 1);
+      asm volatile("" ::: "memory");
+      warm(c + 2 < nch ? c + 2 : nch - 1);
+      asm volatile("" ::: "memory");
+      // the chunk state leaves as whole 128-byte rows (BV fp32 of one d)
+      float* hp = states + tile * DK * DV + v0;
+#pragma unroll
+      for (int t = 0; t < NST; ++t) {
+        const int idx = (thread_x() - 256) + t * 256, d = idx / (BV / 4), c4 = (idx - d * (BV / 4)) * 4;
+        *reinterpret_cast<float4*>(hp + (long)d * DV + c4) = *reinterpret_cast<const float4*>(hF + d * LF + c4);
+      }
+      lds_barrier();  // B: hF read
+      copies_done();  // the next chunk's operands are in LDS before barrier A
+    }
+  }
+  const int bad = __syncthreads_or(!ok);
+  if (threadIdx.x == 0) flag[(long)s * NVT + vt] = bad;
+}
+
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
@@ -473,9 +690,15 @@ static hipError_t launch_fwd_t(const FwdArgs& a) {
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
-    hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
-                       (const OP*)w.Qg, (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, (const OP*)w.KhT,
-                       (const OP*)w.P, (const OP*)w.U, a.states, a.ST, (OP*)a.o, w.flag_scan);
+    if constexpr (sizeof(OP) == 2 && VAR != VAR_DECAY) {
+      hipLaunchKernelGGL((k_scan_fwd_ws<DK, DV, BV, VAR>), dim3(NS * NVT), dim3(512), 0, a.stream, geo, H,
+                         (const bf16*)w.Qg, a.S0, w.gcum, (const bf16*)w.W, (const bf16*)w.KhT,
+                         (const bf16*)w.P, (const bf16*)w.U, a.states, a.ST, (bf16*)a.o, w.flag_scan);
+    } else {
+      hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
+                         (const OP*)w.Qg, (const OP*)a.v, a.S0, w.gcum, (const OP*)w.W, (const OP*)w.KhT,
+                         (const OP*)w.P, (const OP*)w.U, a.states, a.ST, (OP*)a.o, w.flag_scan);
+    }
   }
   stage_mark(a.events, 2, a.stream);
   if (NS > 0) {

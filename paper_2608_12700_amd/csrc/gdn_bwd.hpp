@@ -430,6 +430,226 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
   if (threadIdx.x == 0) flag[(long)s * NVT + vt] = bad;
 }
 
+// The reverse scan for bf16 operands, split into four chain waves and four
+// copy waves (the layout of the forward scan's split): every per-chunk
+// operand of the carry (Khat, (diag(e^G) Q)^T, W^T, this block's slice of
+// dO^T, P^T and the chunk's G) is stored in HBM as contiguous 1 KiB fragment
+// blocks, which the copy waves move into one of two LDS buffers with
+// global_load_lds_dwordx4 a chunk ahead (warming L2 two chunks ahead); they
+// also write the dh entering each chunk out of LDS.  Per chunk:
+//   chain: dh -> LDS | barrier | inj = Qg^T dO, dU' = P^T dO + Khat dh,
+//          store dU'^T | barrier | dh <- e^{G_last} dh + inj - W^T dU'
+//   copy:             | operands of the chunk before -> LDS, dh -> HBM | | wait
+template <int DK, int DV, int BV, int VAR>
+__global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16* __restrict__ Khg,
+                                                     const float* __restrict__ dST, const float* __restrict__ gcum,
+                                                     const bf16* __restrict__ WTg, const bf16* __restrict__ QgTg,
+                                                     const bf16* __restrict__ dOTg, const bf16* __restrict__ PTg,
+                                                     bf16* __restrict__ dhg, bf16* __restrict__ dUTg,
+                                                     float* __restrict__ dS0, int* __restrict__ flag) {
+  static_assert(BV == SCAN_BV, "value tiles");
+  constexpr int NVT = DV / BV;
+  constexpr bool DT_ = VAR != VAR_DECAY;  // delta term present
+  constexpr int LK = DK + 8, LU = CH + 8;
+  typedef Tiles<DK, BV, 4, 1> HT;  // dh slice (chain waves)
+  typedef Tiles<CH, BV, 4, 1> UT;  // dU' slice (chain waves)
+  constexpr int NKh = (CH / 16) * (DK / 32), NQ = (DK / 16) * (CH / 32), NWT = DT_ ? NQ : 0;
+  constexpr int ND = (BV / 16) * (CH / 32), NP = (CH / 16) * (CH / 32);
+  constexpr int OKh = 0, OQ = OKh + NKh, OW = OQ + NQ, OD = OW + NWT, OP_ = OD + ND, NB = OP_ + NP;
+  constexpr int BUF = NB * 1024 + CH * 4;  // + the chunk's G (64 fp32)
+  __shared__ __align__(1024) char buf[2][BUF];
+  __shared__ __align__(16) bf16 dhT[BV * LK];
+  __shared__ __align__(16) bf16 dUT[DT_ ? BV * LU : 8];
+  __shared__ __align__(16) char sink[1024];  // target of the L2 warm-up loads (never read)
+
+  int s, vt;
+  scan_block_coords(blockIdx.x, geo.N * H, NVT, s, vt);
+  const int n = s / H, h = s - (s / H) * H, v0 = vt * BV;
+  const SeqPos sp = seq_pos(geo, n);
+  const int w = wave_id(), l = lane_id();
+  const bool chain = w < 4;
+  const int nch = sp.nch;
+
+  typedef __attribute__((address_space(1))) void gvoid;
+  typedef __attribute__((address_space(3))) void lvoid;
+  auto src_of = [&](long tile, int j) -> const bf16* {
+    if (j < OQ) return Khg + tile * CH * DK + (j - OKh) * 512;
+    if (j < OW) return QgTg + tile * DK * CH + (j - OQ) * 512;
+    if (j < OD) return WTg + tile * DK * CH + (j - OW) * 512;
+    if (j < OP_) return dOTg + tile * DV * CH + op_off<bf16, CH>(v0, 0) + (j - OD) * 512;
+    return PTg + tile * CH * CH + (j - OP_) * 512;
+  };
+  // copy waves: chunk c's operands into buffer b (wave w - 4 takes every fourth block)
+  auto fill = [&](int c, int b) {
+    const long tile = (long)(sp.c0 + c) * H + h;
+#pragma unroll
+    for (int j0 = 0; j0 < NB; j0 += 4) {
+      const int j = j0 + (w - 4);
+      if (j < NB) __builtin_amdgcn_global_load_lds((gvoid*)(src_of(tile, j) + l * 8), (lvoid*)(buf[b] + j * 1024), 16, 0, 0);
+    }
+    if (w == 4) __builtin_amdgcn_global_load_lds((gvoid*)(gcum + tile * CH + l), (lvoid*)(buf[b] + NB * 1024), 4, 0, 0);
+  };
+  // L2 warm-up: the NVT blocks of a stream split the shared blocks (all but
+  // the dO^T slice) and each warms its own dO^T slice; NWARM loads per wave
+  constexpr int NSHB = NB - ND;
+  constexpr int NSH = (NSHB + NVT - 1) / NVT;
+  constexpr int NWARM = (NSH + ND + 3) / 4;
+  auto warm = [&](int c) {
+    const long tile = (long)(sp.c0 + c) * H + h;
+#pragma unroll
+    for (int t = 0; t < NWARM; ++t) {
+      int e = (w - 4) + 4 * t;
+      e = e < NSH + ND ? e : NSH + ND - 1;
+      int j;
+      if (e < NSH) {
+        j = e * NVT + vt;                 // index among the shared blocks
+        j = j < NSHB ? j : NSHB - 1;
+        j = j < OD ? j : j + ND;          // skip the dO^T slice
+      } else {
+        j = OD + (e - NSH);
+      }
+      __builtin_amdgcn_global_load_lds((gvoid*)(src_of(tile, j) + l * 8), (lvoid*)sink, 16, 0, 0);
+    }
+  };
+  constexpr int NST = (DK / 16) * (BV / 32) / 4;  // dh fragment stores per copy-wave lane and chunk
+  static_assert((DK / 16) * (BV / 32) % 4 == 0 && NWARM + NST < 16, "whole fragments; vmcnt field");
+  auto copies_done = [] { __builtin_amdgcn_s_waitcnt(0x0F70 | (NWARM + NST)); };  // vmcnt(NWARM + NST)
+  auto lds_barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+
+  bool ok = true;
+  if (chain) {
+    HT dh;
+    const float* dSTp = dST ? dST + ((long)n * H + h) * DK * DV : nullptr;
+    dh.each([&](int d, int vv, float& x) {
+      x = dSTp ? dSTp[d * DV + v0 + vv] : 0.f;
+      ok &= finite_f(x);
+    });
+    lds_barrier();
+    for (int i = 0; i < nch; ++i) {
+      const int c = nch - 1 - i;
+      const char* B = buf[i & 1];
+      const long tile = (long)(sp.c0 + c) * H + h;
+      // dh to LDS (4 consecutive d per lane: one 8-byte write)
+#pragma unroll
+      for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+        for (int bb = 0; bb < HT::TN; ++bb) {
+          const int d0 = HT::m0(a) + (l >> 4) * 4, vv = HT::n0(bb) + (l & 15);
+          bf16 h4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) h4[j] = from_f<bf16>(dh.acc[a][bb][j]);
+          *reinterpret_cast<uint2*>(dhT + vv * LK + d0) = pack4<bf16>(h4);
+        }
+      lds_barrier();  // A: dh in LDS, this chunk's operands in buffer i & 1
+      const bf16x8* Kf = reinterpret_cast<const bf16x8*>(B + OKh * 1024);
+      const bf16x8* Qf = reinterpret_cast<const bf16x8*>(B + OQ * 1024);
+      const bf16x8* Df = reinterpret_cast<const bf16x8*>(B + OD * 1024);
+      const bf16x8* Pf = reinterpret_cast<const bf16x8*>(B + OP_ * 1024);
+      bf16x8 fd[CH / 32][HT::TN];  // dO^T slice: B fragments of both products
+#pragma unroll
+      for (int st = 0; st < CH / 32; ++st)
+#pragma unroll
+        for (int bb = 0; bb < HT::TN; ++bb) fd[st][bb] = Df[((HT::n0(bb) >> 4) * (CH / 32) + st) * 64 + l];
+      HT inj;  // (diag(e^G) Q)^T dO, independent of the carry
+      inj.zero();
+#pragma unroll
+      for (int st = 0; st < CH / 32; ++st)
+#pragma unroll
+        for (int a = 0; a < HT::TM; ++a) {
+          const bf16x8 fq = Qf[((HT::m0(a) >> 4) * (CH / 32) + st) * 64 + l];
+#pragma unroll
+          for (int bb = 0; bb < HT::TN; ++bb) inj.acc[a][bb] = Mma<bf16>::mma(fq, fd[st][bb], inj.acc[a][bb]);
+        }
+      {
+        // dU' = P^T dO + Khat dh (written for the gradient kernel for every
+        // family member; only the delta rule feeds it back into the carry)
+        UT du;
+        du.zero();
+#pragma unroll
+        for (int st = 0; st < DK / 32; ++st) {
+          const bf16x8 fk = Kf[(w * (DK / 32) + st) * 64 + l];
+#pragma unroll
+          for (int bb = 0; bb < UT::TN; ++bb)
+            du.acc[0][bb] = Mma<bf16>::mma(fk, Mma<bf16>::load(KRow<bf16, LK>{dhT}, UT::n0(bb), 32 * st), du.acc[0][bb]);
+        }
+#pragma unroll
+        for (int st = 0; st < CH / 32; ++st) {
+          const bf16x8 fp = Pf[(w * (CH / 32) + st) * 64 + l];
+#pragma unroll
+          for (int bb = 0; bb < UT::TN; ++bb) du.acc[0][bb] = Mma<bf16>::mma(fp, fd[st][bb], du.acc[0][bb]);
+        }
+        bf16* dUg = dUTg + tile * DV * CH;
+#pragma unroll
+        for (int bb = 0; bb < UT::TN; ++bb) {
+          const int vv = UT::n0(bb) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
+          bf16 u4[4], n4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float u = du.acc[0][bb][j];
+            n4[j] = from_f<bf16>(-u);
+            u4[j] = from_f<bf16>(u);
+          }
+          if constexpr (DT_) *reinterpret_cast<uint2*>(dUT + vv * LU + r0) = pack4<bf16>(n4);
+          // dU' of this chunk for the gradient kernel, transposed (v, r), in its fragment order
+          *reinterpret_cast<uint2*>(dUg + op_off<bf16, CH>(v0 + vv, r0)) = pack4<bf16>(u4);
+        }
+      }
+      lds_barrier();  // B: -dU' in LDS; dh read by the copy waves
+      const float gl = __expf(reinterpret_cast<const float*>(B + NB * 1024)[CH - 1]);
+#pragma unroll
+      for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+        for (int bb = 0; bb < HT::TN; ++bb)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dh.acc[a][bb][j] = gl * dh.acc[a][bb][j] + inj.acc[a][bb][j];
+      if constexpr (DT_) {
+        const bf16x8* Wf = reinterpret_cast<const bf16x8*>(B + OW * 1024);
+#pragma unroll
+        for (int st = 0; st < CH / 32; ++st)
+#pragma unroll
+          for (int a = 0; a < HT::TM; ++a) {
+            const bf16x8 fw = Wf[((HT::m0(a) >> 4) * (CH / 32) + st) * 64 + l];
+#pragma unroll
+            for (int bb = 0; bb < HT::TN; ++bb)
+              dh.acc[a][bb] = Mma<bf16>::mma(fw, Mma<bf16>::load(KRow<bf16, LU>{dUT}, HT::n0(bb), 32 * st), dh.acc[a][bb]);
+          }
+      }
+    }
+    float* dS0p = dS0 + ((long)n * H + h) * DK * DV;
+    dh.each([&](int d, int vv, float& x) { dS0p[d * DV + v0 + vv] = x; });
+  } else {
+    if (nch > 0) {
+      fill(nch - 1, 0);
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    }
+    lds_barrier();
+    for (int i = 0; i < nch; ++i) {
+      const int c = nch - 1 - i;
+      const long tile = (long)(sp.c0 + c) * H + h;
+      lds_barrier();  // A: dh entering this chunk in LDS; buffer (i + 1) & 1 is free
+      // issue order fills, warm-ups, stores (kept by the empty asm statements):
+      // copies_done counts on it
+      if (c > 0) fill(c - 1, (i + 1) & 1);
+      asm volatile("" ::: "memory");
+      warm(c > 1 ? c - 2 : 0);
+      asm volatile("" ::: "memory");
+      // dh entering this chunk, for the gradient kernel: (16 d x 32 v) fragments
+      // read down the columns of dh^T by the transposing load, 1 KiB per store
+      bf16* dhp = dhg + tile * DK * DV;
+#pragma unroll
+      for (int t = 0; t < NST; ++t) {
+        const int f = (w - 4) + 4 * t, mt = f / (BV / 32), kb = f - mt * (BV / 32);
+        const bf16x8 x = lds_frag_tr<LK>(dhT, 16 * mt, 32 * kb);
+        *reinterpret_cast<bf16x8*>(dhp + op_off<bf16, DV>(16 * mt, v0 + 32 * kb) + l * 8) = x;
+      }
+      lds_barrier();  // B: dh read
+      copies_done();  // the chunk before's operands are in LDS before barrier A
+    }
+  }
+  const int bad = __syncthreads_or(!ok);
+  if (threadIdx.x == 0) flag[(long)s * NVT + vt] = bad;
+}
+
 // Bytes of the phase-dependent region of the grad kernel (LDS for bf16
 // operands, a per-block slice of the workspace for fp32 operands).
 template <int DK, typename OP>
@@ -1443,9 +1663,15 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0) {
-    hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
-                       (const OP*)w.Kh, a.dST, w.gcum, (const OP*)w.W, (const OP*)w.QgT, (const OP*)w.dOT,
-                       (const OP*)w.PT, (OP*)w.dh, (OP*)w.dUT, a.dS0, w.flag_scan);
+    if constexpr (sizeof(OP) == 2) {
+      hipLaunchKernelGGL((k_scan_bwd_ws<DK, DV, BV, VAR>), dim3(NS * NVT), dim3(512), 0, a.stream, geo, H,
+                         (const bf16*)w.Kh, a.dST, w.gcum, (const bf16*)w.W, (const bf16*)w.QgT,
+                         (const bf16*)w.dOT, (const bf16*)w.PT, (bf16*)w.dh, (bf16*)w.dUT, a.dS0, w.flag_scan);
+    } else {
+      hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
+                         (const OP*)w.Kh, a.dST, w.gcum, (const OP*)w.W, (const OP*)w.QgT, (const OP*)w.dOT,
+                         (const OP*)w.PT, (OP*)w.dh, (OP*)w.dUT, a.dS0, w.flag_scan);
+    }
   }
   stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0 && sizeof(OP) == 2) {

@@ -460,7 +460,7 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
   __shared__ __align__(1024) char buf[2][BUF];
   __shared__ __align__(16) bf16 dhT[BV * LK];
   __shared__ __align__(16) bf16 dUT[DT_ ? BV * LU : 8];
-  __shared__ __align__(16) char sink[1024];  // target of the L2 warm-up loads (never read)
+  __shared__ __align__(16) char sink[256];  // target of the L2 warm-up loads (never read)
 
   int s, vt;
   scan_block_coords(blockIdx.x, geo.N * H, NVT, s, vt);
@@ -490,16 +490,19 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
     if (w == 4) __builtin_amdgcn_global_load_lds((gvoid*)(gcum + tile * CH + l), (lvoid*)(buf[b] + NB * 1024), 4, 0, 0);
   };
   // L2 warm-up: the NVT blocks of a stream split the shared blocks (all but
-  // the dO^T slice) and each warms its own dO^T slice; NWARM loads per wave
+  // the dO^T slice) and each warms its own dO^T slice, touching every
+  // 128-byte line once: one 4-byte load per lane (64 lines per instruction)
   constexpr int NSHB = NB - ND;
   constexpr int NSH = (NSHB + NVT - 1) / NVT;
-  constexpr int NWARM = (NSH + ND + 3) / 4;
+  constexpr int NWL = (NSH + ND) * 8;
+  constexpr int NWARM = (NWL + 255) / 256;
   auto warm = [&](int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
 #pragma unroll
     for (int t = 0; t < NWARM; ++t) {
-      int e = (w - 4) + 4 * t;
-      e = e < NSH + ND ? e : NSH + ND - 1;
+      int L = ((w - 4) + 4 * t) * 64 + l;
+      L = L < NWL ? L : NWL - 1;
+      const int e = L >> 3;
       int j;
       if (e < NSH) {
         j = e * NVT + vt;                 // index among the shared blocks
@@ -508,7 +511,7 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
       } else {
         j = OD + (e - NSH);
       }
-      __builtin_amdgcn_global_load_lds((gvoid*)(src_of(tile, j) + l * 8), (lvoid*)sink, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((gvoid*)(src_of(tile, j) + (L & 7) * 64), (lvoid*)sink, 4, 0, 0);
     }
   };
   constexpr int NST = (DK / 16) * (BV / 32) / 4;  // dh fragment stores per copy-wave lane and chunk

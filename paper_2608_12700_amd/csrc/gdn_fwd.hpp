@@ -481,7 +481,7 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
   __shared__ __align__(16) bf16 hT[BV * LK];
   __shared__ __align__(16) float hF[DK * LF];  // h in fp32, row-major, for whole-line state stores
   __shared__ __align__(16) bf16 UsT[BV * LU];
-  __shared__ __align__(16) char sink[1024];  // target of the L2 warm-up loads (never read)
+  __shared__ __align__(16) char sink[256];  // target of the L2 warm-up loads (never read)
 
   int s, vt;
   scan_block_coords(blockIdx.x, geo.N * H, NVT, s, vt);
@@ -516,17 +516,20 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
   // stay in flight (vmcnt counts in issue order on gfx9)
   constexpr int NST = DK * BV / 4 / 256;  // state stores per copy-wave lane and chunk
   static_assert(NST < 16, "vmcnt field");
-  // L2 warm-up two chunks ahead: the NVT blocks of a stream share the
+  // L2 warm-up two chunks ahead: the NVT blocks of a stream split the
   // chunk's W, Q, P and Khat^T blocks (one in NVT each) and each warms its
-  // own U slice; every copy wave issues exactly NWARM loads.
-  constexpr int NSH = (OU + NVT - 1) / NVT;  // shared blocks warmed per block
-  constexpr int NWARM = (NSH + NU + 3) / 4;
+  // own U slice, touching every 128-byte line once: one 4-byte load per lane
+  // (64 lines per instruction), so the warm-up costs the address unit little.
+  constexpr int NSH = (OU + NVT - 1) / NVT;          // shared blocks warmed per block
+  constexpr int NWL = (NSH + NU) * 8;                 // lines warmed per block
+  constexpr int NWARM = (NWL + 255) / 256;            // loads per copy-wave lane
   auto warm = [&](int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
 #pragma unroll
     for (int t = 0; t < NWARM; ++t) {
-      int e = (w - 4) + 4 * t;
-      e = e < NSH + NU ? e : NSH + NU - 1;
+      int L = ((w - 4) + 4 * t) * 64 + l;
+      L = L < NWL ? L : NWL - 1;
+      const int e = L >> 3;
       int j = e < NSH ? e * NVT + vt : OU + (e - NSH);
       j = j < NB ? j : NB - 1;
       const bf16* src;
@@ -535,7 +538,7 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
       else if (j < OK) src = Pg + tile * CH * CH + (j - OP_) * 512;
       else if (j < OU) src = KhTg + tile * DK * CH + (j - OK) * 512;
       else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512;
-      __builtin_amdgcn_global_load_lds((gvoid*)(src + l * 8), (lvoid*)sink, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((gvoid*)(src + (L & 7) * 64), (lvoid*)sink, 4, 0, 0);
     }
   };
   static_assert(NWARM + NST < 16, "vmcnt field");

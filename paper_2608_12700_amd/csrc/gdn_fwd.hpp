@@ -481,6 +481,7 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
   __shared__ __align__(16) bf16 hT[BV * LK];
   __shared__ __align__(16) float hF[DK * LF];  // h in fp32, row-major, for whole-line state stores
   __shared__ __align__(16) bf16 UsT[BV * LU];
+  __shared__ __align__(16) bf16 OsT[BV * LU];  // the chunk output, transposed (v, r), for the copy waves
   __shared__ __align__(16) char sink[256];  // target of the L2 warm-up loads (never read)
 
   int s, vt;
@@ -627,20 +628,31 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
           ot.acc[0][bb] = Mma<bf16>::mma(fp, fu, ot.acc[0][bb]);
         }
       }
-      const long row0 = sp.row0 + (long)c * CH;
-      const int len = min(CH, sp.len - c * CH);
-      bf16* op = o + (row0 * H + h) * DV + v0;
+      // the output goes to LDS (4 consecutive rows per lane: one 8-byte write);
+      // the copy waves store it after the next barrier
 #pragma unroll
-      for (int bb = 0; bb < UT::TN; ++bb)
+      for (int bb = 0; bb < UT::TN; ++bb) {
+        const int vv = UT::n0(bb) + (l & 15), r0 = UT::m0(0) + (l >> 4) * 4;
+        bf16 o4[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int r = UT::m0(0) + (l >> 4) * 4 + j;
-          if (r < len) op[(long)r * H * DV + UT::n0(bb) + (l & 15)] = from_f<bf16>(ot.acc[0][bb][j]);
-        }
+        for (int j = 0; j < 4; ++j) o4[j] = from_f<bf16>(ot.acc[0][bb][j]);
+        *reinterpret_cast<uint2*>(OsT + vv * LU + r0) = pack4<bf16>(o4);
+      }
     }
+    lds_barrier();  // the last chunk's output is in LDS
     float* STp = ST + ((long)n * H + h) * DK * DV;
     hs.each([&](int d, int vv, float& x) { STp[d * DV + v0 + vv] = x; });
   } else {
+    // chunk c's output, read down the columns of O^T by the transposing load
+    // (16 rows x 32 columns per wave: 64 bytes of each row per 16 lanes)
+    static_assert(BV == 32, "one output fragment per copy wave");
+    auto store_o = [&](int c) {
+      const long row0 = sp.row0 + (long)c * CH;
+      const int len = min(CH, sp.len - c * CH);
+      const bf16x8 x = lds_frag_tr<LU>(OsT, 16 * (w - 4), 0);
+      const int r = 16 * (w - 4) + (l & 15);
+      if (r < len) *reinterpret_cast<bf16x8*>(o + ((row0 + r) * H + h) * DV + v0 + 8 * (l >> 4)) = x;
+    };
     if (nch > 0) {
       fill(0, 0);
       __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
@@ -662,9 +674,12 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
         const int idx = (thread_x() - 256) + t * 256, d = idx / (BV / 4), c4 = (idx - d * (BV / 4)) * 4;
         *reinterpret_cast<float4*>(hp + (long)d * DV + c4) = *reinterpret_cast<const float4*>(hF + d * LF + c4);
       }
-      lds_barrier();  // B: hF read
+      if (c > 0) store_o(c - 1);
+      lds_barrier();  // B: hF and the previous output read
       copies_done();  // the next chunk's operands are in LDS before barrier A
     }
+    lds_barrier();
+    if (nch > 0) store_o(nch - 1);
   }
   const int bad = __syncthreads_or(!ok);
   if (threadIdx.x == 0) flag[(long)s * NVT + vt] = bad;

@@ -1264,6 +1264,12 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     Gam[r] = __expf(Gs[r]);
     Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
   }
+  // h and dh of the value slice: with one slice they are issued before the
+  // first products, so the second read of the chunk state follows the first
+  // closely (and is an L2 hit more often); with two, a slice ahead
+  constexpr bool EARLY_B = DV <= VS;
+  PreB pb;
+  if constexpr (EARLY_B) load_b(pb, cur, 0);
   TC pm, ae;  // P = (Q K^T) * D and (K K^T) * E, kept for phase 2
   float dd[TC::TN][4];  // D_ri = e^{G_r - G_i} for i <= r, else 0
   pm.zero();
@@ -1307,7 +1313,6 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
       load_a1(pa, cur, c0);
       load_a2(pa, cur, c0);
     }
-    PreB pb;
     if constexpr (DT_) {
       // R = diag(beta) (V - diag(e^G) K h), computed transposed, (K h)^T = h^T K^T,
       // so that a lane needs v[r][v0..v0+3] as one 8-byte piece (the same
@@ -1326,7 +1331,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
           for (int a = 0; a < TY::TM; ++a) kht.acc[a][b] = M::mma(fa[a], fb, kht.acc[a][b]);
         }
       }
-      load_b(pb, cur, c0);
+      if (!EARLY_B) load_b(pb, cur, c0);
 #pragma unroll
       for (int b = 0; b < TY::TN; ++b) {
         const int r = TY::n0(b) + lc;
@@ -1345,7 +1350,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
         }
       }
     } else {
-      load_b(pb, cur, c0);
+      if (!EARLY_B) load_b(pb, cur, c0);
     }
     // Y^T = dU'^T T, so Y = T^T dU'.  dV = diag(beta) Y; keep -Y for dA and X
     {

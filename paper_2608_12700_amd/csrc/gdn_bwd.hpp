@@ -143,10 +143,9 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
       }
     }
   }
-  // Khat = diag(e^{G_last - G}) K, the scan's A operand for dU' (rows past the
-  // end stay zero); bf16 thread order follows the operand layout, so each
-  // wave writes whole 1 KiB fragments
-  {
+  // Khat = diag(e^{G_last - G}) K, the A operand of dU' in the generic scan
+  // (rows past the end stay zero; the split bf16 scan reads k itself)
+  if constexpr (!TR) {
     OP* Kh = Khg + tile * CH * DK;
     for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
       int r, d0;
@@ -432,16 +431,20 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
 
 // The reverse scan for bf16 operands, split into four chain waves and four
 // copy waves (the layout of the forward scan's split): every per-chunk
-// operand of the carry (Khat, (diag(e^G) Q)^T, W^T, this block's slice of
-// dO^T, P^T and the chunk's G) is stored in HBM as contiguous 1 KiB fragment
-// blocks, which the copy waves move into one of two LDS buffers with
-// global_load_lds_dwordx4 a chunk ahead (warming L2 two chunks ahead); they
-// also write the dh entering each chunk out of LDS.  Per chunk:
-//   chain: dh -> LDS | barrier | inj = Qg^T dO, dU' = P^T dO + Khat dh,
-//          store dU'^T | barrier | dh <- e^{G_last} dh + inj - W^T dU'
+// operand of the carry (K, (diag(e^G) Q)^T, W^T, this block's slice of dO^T,
+// P^T and the chunk's G) goes through LDS in 1 KiB blocks, which the copy
+// waves move into one of two LDS buffers with global_load_lds_dwordx4 a chunk
+// ahead (warming L2 two chunks ahead): the prep kernel's outputs are stored
+// as MFMA fragment blocks in HBM, and k's token-major rows (the contraction
+// index d_k is contiguous there) are gathered a line at a time (RowLines).
+// The copy waves also write the dh
+// entering each chunk out of LDS.  Per chunk:
+//   chain: dh -> LDS | barrier | inj = Qg^T dO,
+//          dU' = diag(e^{G_last - G}) (K dh) + P^T dO, store dU'^T | barrier |
+//          dh <- e^{G_last} dh + inj - W^T dU'
 //   copy:             | operands of the chunk before -> LDS, dh -> HBM | | wait
 template <int DK, int DV, int BV, int VAR>
-__global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16* __restrict__ Khg,
+__global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16* __restrict__ k,
                                                      const float* __restrict__ dST, const float* __restrict__ gcum,
                                                      const bf16* __restrict__ WTg, const bf16* __restrict__ QgTg,
                                                      const bf16* __restrict__ dOTg, const bf16* __restrict__ PTg,
@@ -450,6 +453,8 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
   static_assert(BV == SCAN_BV, "value tiles");
   constexpr int NVT = DV / BV;
   constexpr bool DT_ = VAR != VAR_DECAY;  // delta term present
+  typedef RowLines<DK> KL;
+  static_assert(KL::NBLK == (CH / 16) * (DK / 32), "k takes the blocks of a 64 x DK fragment operand");
   constexpr int LK = DK + 8, LU = CH + 8;
   typedef Tiles<DK, BV, 4, 1> HT;  // dh slice (chain waves)
   typedef Tiles<CH, BV, 4, 1> UT;  // dU' slice (chain waves)
@@ -472,8 +477,14 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
 
   typedef __attribute__((address_space(1))) void gvoid;
   typedef __attribute__((address_space(3))) void lvoid;
+  // row r of k in chunk c (rows past the chunk's end repeat its last row;
+  // their products are masked)
+  auto k_row = [&](int c, int r) -> const bf16* {
+    const int len = min(CH, sp.len - c * CH);
+    return k + ((sp.row0 + (long)c * CH + clamp_row(r, len)) * H + h) * DK;
+  };
+  // start of prep-written block j (j >= OQ)
   auto src_of = [&](long tile, int j) -> const bf16* {
-    if (j < OQ) return Khg + tile * CH * DK + (j - OKh) * 512;
     if (j < OW) return QgTg + tile * DK * CH + (j - OQ) * 512;
     if (j < OD) return WTg + tile * DK * CH + (j - OW) * 512;
     if (j < OP_) return dOTg + tile * DV * CH + op_off<bf16, CH>(v0, 0) + (j - OD) * 512;
@@ -485,7 +496,17 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
 #pragma unroll
     for (int j0 = 0; j0 < NB; j0 += 4) {
       const int j = j0 + (w - 4);
-      if (j < NB) __builtin_amdgcn_global_load_lds((gvoid*)(src_of(tile, j) + l * 8), (lvoid*)(buf[b] + j * 1024), 16, 0, 0);
+      if (j < NB) {
+        const bf16* src;
+        if (j < OQ) {
+          int r, e;
+          KL::src(j - OKh, l, r, e);
+          src = k_row(c, r) + e;
+        } else {
+          src = src_of(tile, j) + l * 8;
+        }
+        __builtin_amdgcn_global_load_lds((gvoid*)src, (lvoid*)(buf[b] + j * 1024), 16, 0, 0);
+      }
     }
     if (w == 4) __builtin_amdgcn_global_load_lds((gvoid*)(gcum + tile * CH + l), (lvoid*)(buf[b] + NB * 1024), 4, 0, 0);
   };
@@ -511,7 +532,16 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
       } else {
         j = OD + (e - NSH);
       }
-      __builtin_amdgcn_global_load_lds((gvoid*)(src_of(tile, j) + (L & 7) * 64), (lvoid*)sink, 4, 0, 0);
+      const bf16* src;
+      if (j < OQ) {
+        // line (L & 7) of k block j - OKh
+        int r, e;
+        KL::src(j - OKh, (L & 7) << 3, r, e);
+        src = k_row(c, r) + (e & ~63);
+      } else {
+        src = src_of(tile, j) + (L & 7) * 64;
+      }
+      __builtin_amdgcn_global_load_lds((gvoid*)src, (lvoid*)sink, 4, 0, 0);
     }
   };
   constexpr int NST = (DK / 16) * (BV / 32) / 4;  // dh fragment stores per copy-wave lane and chunk
@@ -546,6 +576,18 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
       lds_barrier();  // A: dh in LDS, this chunk's operands in buffer i & 1
       const bf16x8* Kf = reinterpret_cast<const bf16x8*>(B + OKh * 1024);
       const bf16x8* Qf = reinterpret_cast<const bf16x8*>(B + OQ * 1024);
+      // row scales e^{G_last - G_r} of K dh (0 past the chunk's end), formed
+      // here under the products
+      float er[4];
+      {
+        const float* Gc = reinterpret_cast<const float*>(B + NB * 1024);
+        const int len = min(CH, sp.len - c * CH);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = UT::m0(0) + (l >> 4) * 4 + j;
+          er[j] = r < len ? __expf(Gc[CH - 1] - Gc[r]) : 0.f;
+        }
+      }
       const bf16x8* Df = reinterpret_cast<const bf16x8*>(B + OD * 1024);
       const bf16x8* Pf = reinterpret_cast<const bf16x8*>(B + OP_ * 1024);
       bf16x8 fd[CH / 32][HT::TN];  // dO^T slice: B fragments of both products
@@ -564,17 +606,23 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
           for (int bb = 0; bb < HT::TN; ++bb) inj.acc[a][bb] = Mma<bf16>::mma(fq, fd[st][bb], inj.acc[a][bb]);
         }
       {
-        // dU' = P^T dO + Khat dh (written for the gradient kernel for every
-        // family member; only the delta rule feeds it back into the carry)
+        // dU' = diag(e^{G_last - G}) (K dh) + P^T dO (written for the gradient
+        // kernel for every family member; only the delta rule feeds it back
+        // into the carry).  The row scale goes on the fp32 products; rows past
+        // the chunk's end are zero.
         UT du;
         du.zero();
 #pragma unroll
         for (int st = 0; st < DK / 32; ++st) {
-          const bf16x8 fk = Kf[(w * (DK / 32) + st) * 64 + l];
+          const bf16x8 fk = Kf[KL::frag_slot(w, st, l)];
 #pragma unroll
           for (int bb = 0; bb < UT::TN; ++bb)
             du.acc[0][bb] = Mma<bf16>::mma(fk, Mma<bf16>::load(KRow<bf16, LK>{dhT}, UT::n0(bb), 32 * st), du.acc[0][bb]);
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int bb = 0; bb < UT::TN; ++bb) du.acc[0][bb][j] *= er[j];
 #pragma unroll
         for (int st = 0; st < CH / 32; ++st) {
           const bf16x8 fp = Pf[(w * (CH / 32) + st) * 64 + l];
@@ -1088,6 +1136,12 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   constexpr int VS = C::VS, LK = C::LK, LT = C::LT, LC = C::LC, LV = C::LV;
   constexpr int NDO = CH * VS / 8 / 512;  // 16-byte pieces of a dO slice per thread
   constexpr int NQK = CH * DK / 8 / 512;  // 16-byte pieces of q (or k) per thread
+  // With one value slice the chunk state h is read from HBM once, a tile
+  // ahead, in the row-fragment layout of X^T and dQ^T; phase 0 stores it in
+  // LDS as bf16, and (K h)^T takes its h^T fragments from there with
+  // transposing reads.  With two slices both layouts are loaded per slice.
+  constexpr bool HL = DV <= VS;
+  constexpr int LH = VS + 8;
 
   __shared__ __align__(16) bf16 Qs[CH * LK];
   __shared__ __align__(16) bf16 Ks[CH * LK];
@@ -1100,6 +1154,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   __shared__ float rqp[C::WMd][CH], rxp[C::WMd][CH], rkp[C::WMd][CH], dbYp[C::WNv][CH];
   __shared__ float hdh_w[8];
   __shared__ __align__(16) char ub[C::UB];
+  __shared__ __align__(16) bf16 Hs[HL ? DK * LH : 8];
 
   // the loop-safe thread index reads this word: it is stored before any use
   if (threadIdx.x == 0) gdn_tid_bias = 0;
@@ -1198,10 +1253,9 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
           for (int j = 0; j < 8; ++j) p.hk[s][a][j] = hp[(32 * s + 8 * lg + j) * DV + c0 + TY::m0(a) + lc];
     }
   };
-  auto load_b = [&](PreB& p, const Tile& x, int c0) {
+  auto load_h = [&](PreB& p, const Tile& x, int c0) {
     const int l = lane_id(), lg = l >> 4, lc = l & 15;
     const float* hp = states + x.t * DK * DV;
-    const bf16* dhp = dhg + x.t * DK * DV;
 #pragma unroll
     for (int s = 0; s < VS / 32; ++s)
 #pragma unroll
@@ -1211,8 +1265,20 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
         const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
         p.hx[s][a][0] = x0.x; p.hx[s][a][1] = x0.y; p.hx[s][a][2] = x0.z; p.hx[s][a][3] = x0.w;
         p.hx[s][a][4] = x1.x; p.hx[s][a][5] = x1.y; p.hx[s][a][6] = x1.z; p.hx[s][a][7] = x1.w;
-        p.dh[s][a] = *reinterpret_cast<const bf16x8*>(dhp + op_off<bf16, DV>(TD::m0(a), c0 + 32 * s) + l * 8);
       }
+  };
+  auto load_dh = [&](PreB& p, const Tile& x, int c0) {
+    const int l = lane_id();
+    const bf16* dhp = dhg + x.t * DK * DV;
+#pragma unroll
+    for (int s = 0; s < VS / 32; ++s)
+#pragma unroll
+      for (int a = 0; a < TD::TM; ++a)
+        p.dh[s][a] = *reinterpret_cast<const bf16x8*>(dhp + op_off<bf16, DV>(TD::m0(a), c0 + 32 * s) + l * 8);
+  };
+  auto load_b = [&](PreB& p, const Tile& x, int c0) {
+    load_h(p, x, c0);
+    load_dh(p, x, c0);
   };
 
   // Persistent: the block walks the tiles t = blockIdx.x, blockIdx.x + gridDim.x,
@@ -1221,9 +1287,10 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   Tile cur = tile_at(blockIdx.x);
   Pre0 p0;
   PreA pa;
+  PreB pb;
   load_0(p0, cur);
   load_a1(pa, cur, 0);
-  load_a2(pa, cur, 0);
+  if constexpr (HL) load_b(pb, cur, 0); else load_a2(pa, cur, 0);
   for (int tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
   const int w = wave_id(), l = lane_id(), lg = l >> 4, lc = l & 15;
   const ChunkPos cp = cur.cp;
@@ -1232,6 +1299,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   const bf16* vp = v + (cp.row0 * H + h) * DV;
   bf16* dvp = dvo + (cp.row0 * H + h) * DV;
   bool ok = true;
+  float hdh = 0.f;  // <h, dh> over this wave's part of the state
 
   // ================= phase 0: gates, P, A; T comes from the prep kernel
 #pragma unroll
@@ -1251,6 +1319,23 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     }
     *reinterpret_cast<uint4*>(Ts + r * LT + c) = tq;
   }
+  if constexpr (HL) {
+    // h -> LDS in bf16; <h, dh> and the finiteness check take the fp32 values.
+    // Where two waves hold the same rows (d_k = 64) one of them does this.
+    if (TD::n0(0) == 0) {
+#pragma unroll
+      for (int s = 0; s < VS / 32; ++s)
+#pragma unroll
+        for (int a = 0; a < TD::TM; ++a) {
+          *reinterpret_cast<bf16x8*>(Hs + (TD::m0(a) + lc) * LH + 32 * s + 8 * lg) = cvt8(pb.hx[s][a]);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            ok &= finite_f(pb.hx[s][a][j]);
+            hdh += pb.hx[s][a][j] * to_f(pb.dh[s][a][j]);
+          }
+        }
+    }
+  }
   if (w == 0) {
     // in-chunk gates: G = inclusive cumsum of g (0 past the end), beta (0 past the end)
     const float gv = l < len ? p0.gv : 0.f, bv = l < len ? p0.bv : 0.f;
@@ -1259,17 +1344,16 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     Bs[l] = bv;
   }
   __syncthreads();
+  // the next tile (this one again on the last pass: a clamped, unconditional
+  // prefetch keeps the registers loop-carried).  With one slice, q, k, T and
+  // the gates are in LDS now, and their next copies load from here on.
+  const Tile nxt = tile_at(tt + (int)gridDim.x < ntiles ? tt + (int)gridDim.x : tt);
+  if constexpr (HL) load_0(p0, nxt);
   if (thread_x() < CH) {
     const int r = thread_x();
     Gam[r] = __expf(Gs[r]);
     Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
   }
-  // h and dh of the value slice: with one slice they are issued before the
-  // first products, so the second read of the chunk state follows the first
-  // closely (and is an L2 hit more often); with two, a slice ahead
-  constexpr bool EARLY_B = DV <= VS;
-  PreB pb;
-  if constexpr (EARLY_B) load_b(pb, cur, 0);
   TC pm, ae;  // P = (Q K^T) * D and (K K^T) * E, kept for phase 2
   float dd[TC::TN][4];  // D_ri = e^{G_r - G_i} for i <= r, else 0
   pm.zero();
@@ -1305,7 +1389,6 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   float dbY[TY::TN];
 #pragma unroll
   for (int b = 0; b < TY::TN; ++b) dbY[b] = 0.f;
-  float hdh = 0.f;
 
   for (int c0 = 0; c0 < DV; c0 += VS) {
     if (c0 > 0) {
@@ -1323,7 +1406,10 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
       for (int s = 0; s < DK / 32; ++s) {
         bf16x8 fa[TY::TM];
 #pragma unroll
-        for (int a = 0; a < TY::TM; ++a) fa[a] = cvt8(pa.hk[s][a]);
+        for (int a = 0; a < TY::TM; ++a) {
+          if constexpr (HL) fa[a] = lds_frag_tr<LH>(Hs, TY::m0(a), 32 * s);
+          else fa[a] = cvt8(pa.hk[s][a]);
+        }
 #pragma unroll
         for (int b = 0; b < TY::TN; ++b) {
           const bf16x8 fb = M::load(KRow<bf16, LK>{Ks}, TY::n0(b), 32 * s);
@@ -1331,7 +1417,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
           for (int a = 0; a < TY::TM; ++a) kht.acc[a][b] = M::mma(fa[a], fb, kht.acc[a][b]);
         }
       }
-      if (!EARLY_B) load_b(pb, cur, c0);
+      if constexpr (!HL) load_b(pb, cur, c0);
 #pragma unroll
       for (int b = 0; b < TY::TN; ++b) {
         const int r = TY::n0(b) + lc;
@@ -1350,7 +1436,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
         }
       }
     } else {
-      if (!EARLY_B) load_b(pb, cur, c0);
+      if constexpr (!HL) load_b(pb, cur, c0);
     }
     // Y^T = dU'^T T, so Y = T^T dU'.  dV = diag(beta) Y; keep -Y for dA and X
     {
@@ -1424,12 +1510,16 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
       bf16x8 fh[TD::TM];
 #pragma unroll
       for (int a = 0; a < TD::TM; ++a) {
-        fh[a] = cvt8(pb.hx[s][a]);
+        if constexpr (HL) {
+          fh[a] = M::load(KRow<bf16, LH>{Hs}, TD::m0(a), 32 * s);
+        } else {
+          fh[a] = cvt8(pb.hx[s][a]);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) ok &= finite_f(pb.hx[s][a][j]);
-        if (TD::n0(0) == 0) {  // one wave column adds <h, dh> for its rows
+          for (int j = 0; j < 8; ++j) ok &= finite_f(pb.hx[s][a][j]);
+          if (TD::n0(0) == 0) {  // one wave column adds <h, dh> for its rows
 #pragma unroll
-          for (int j = 0; j < 8; ++j) hdh += pb.hx[s][a][j] * to_f(pb.dh[s][a][j]);
+            for (int j = 0; j < 8; ++j) hdh += pb.hx[s][a][j] * to_f(pb.dh[s][a][j]);
+          }
         }
       }
 #pragma unroll
@@ -1461,10 +1551,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     }
   }
   __syncthreads();  // phase-1 LDS operands are consumed
-  // the next tile's operands (this tile's again on the last pass: a clamped,
-  // unconditional prefetch keeps the registers loop-carried without copies)
-  const Tile nxt = tile_at(tt + (int)gridDim.x < ntiles ? tt + (int)gridDim.x : tt);
-  load_0(p0, nxt);
+  // the next tile's value-slice operands (and, with two slices, q, k, T, gates)
+  if constexpr (!HL) load_0(p0, nxt);
   load_a1(pa, nxt, 0);
 
   // ================= phase 2: the chunk-level gradients
@@ -1587,7 +1675,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
       *reinterpret_cast<uint2*>(dqst + r * LK + d0) = pack4<bf16>(q4);
       *reinterpret_cast<uint2*>(dkst + r * LK + d0) = pack4<bf16>(k4);
     }
-  load_a2(pa, nxt, 0);  // the accumulators are free: the next tile's h^T
+  // the accumulators are free: the next tile's h and dh (or h^T with two slices)
+  if constexpr (HL) load_b(pb, nxt, 0); else load_a2(pa, nxt, 0);
   if (w == 0) {
     const int r = l;
     float rq = 0.f, rx = 0.f, rk = 0.f;
@@ -1673,7 +1762,7 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
   if (NS > 0) {
     if constexpr (sizeof(OP) == 2) {
       hipLaunchKernelGGL((k_scan_bwd_ws<DK, DV, BV, VAR>), dim3(NS * NVT), dim3(512), 0, a.stream, geo, H,
-                         (const bf16*)w.Kh, a.dST, w.gcum, (const bf16*)w.W, (const bf16*)w.QgT,
+                         (const bf16*)a.k, a.dST, w.gcum, (const bf16*)w.W, (const bf16*)w.QgT,
                          (const bf16*)w.dOT, (const bf16*)w.PT, (bf16*)w.dh, (bf16*)w.dUT, a.dS0, w.flag_scan);
     } else {
       hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,

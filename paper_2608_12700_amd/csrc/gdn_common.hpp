@@ -86,6 +86,33 @@ __device__ __forceinline__ long op_off(int m, int k) {
     return (long)m * K + k;
 }
 
+// Token-major rows of a chunk operand (64 rows of DK 16-bit values, the
+// contraction index contiguous) gathered into LDS for MFMA fragment reads by
+// 1 KiB copies: block I holds 8 rows x one 128-byte line of each (DK / 64
+// lines per row), so every copy instruction reads whole lines.  Within a row
+// the eight 16-byte pieces of a line are permuted by (row >> 1) & 7: the 16
+// rows of one fragment read then fall on distinct LDS banks.
+template <int DK>
+struct RowLines {
+  static constexpr int LPR = DK / 64;         // 128-byte lines per row
+  static constexpr int NBLK = CH * LPR / 8;   // 1 KiB blocks per chunk
+  // lane l of block I copies row `row`, elements e .. e + 7
+  __device__ __forceinline__ static void src(int I, int l, int& row, int& e) {
+    const int rg = I / LPR, hl = I - rg * LPR;
+    row = 8 * rg + (l >> 3);
+    e = hl * 64 + (((l & 7) ^ ((row >> 1) & 7)) << 3);
+  }
+  // 16-byte slot, from the first block, of row r, elements k0 .. k0 + 7 (k0 % 8 == 0)
+  __device__ __forceinline__ static int slot(int r, int k0) {
+    const int p = k0 >> 3, hl = p >> 3;
+    return ((r >> 3) * LPR + hl) * 64 + 8 * (r & 7) + ((p & 7) ^ ((r >> 1) & 7));
+  }
+  // lane l's slot of the A fragment (rows 16 mt .. 16 mt + 15, k-step st of 32)
+  __device__ __forceinline__ static int frag_slot(int mt, int st, int l) {
+    return slot(16 * mt + (l & 15), 32 * st + 8 * (l >> 4));
+  }
+};
+
 // Layout of a 64 x D fp32 chunk operand read as accumulator tiles of
 // Tiles<64, BV, 4, 1> (one 16-row tile per wave, BV-column value tiles): the
 // four rows r..r+3 (r % 4 == 0) of column v that one lane holds are one float4,

@@ -95,9 +95,10 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
     Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
   }
   __syncthreads();
-  // diag(e^G) Q, the scan's A operand for the output term: thread order
-  // follows the operand layout, so each wave writes whole 1 KiB fragments
-  {
+  // diag(e^G) Q, the A operand of the output term of the generic scan (the
+  // split bf16 scan reads q itself): thread order follows the operand layout,
+  // so each wave writes whole 1 KiB fragments
+  if constexpr (!(TR && DT_)) {
     OP* Qg = Qgg + tile * CH * DK;
     for (int idx = threadIdx.x; idx < CH * DK / VE; idx += blockDim.x) {
       int r, d0;
@@ -452,22 +453,27 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
 
 // The forward scan for bf16 operands of the delta-rule members, split into
 // four chain waves and four copy waves.  Everything the chain reads per chunk
-// except the carry (W, diag(e^G) Q, P, Khat^T, this block's slice of U and
-// the chunk's G) is stored in HBM as contiguous 1 KiB fragment blocks; the
-// copy waves move the next chunk's 60 KiB straight into one of two LDS
-// buffers with global_load_lds_dwordx4 and write the chunk state out of LDS,
-// so the chain waves never queue behind the address unit.  Per chunk:
-//   chain: h -> LDS | barrier | U' = U - W h, O = diag(e^G) Q h | barrier |
-//          h <- e^{G_last} h + Khat^T U', O += P U', store O
+// except the carry (W, Q, P, Khat^T, this block's slice of U and the chunk's
+// G) goes through LDS in 1 KiB blocks: the prep kernel's outputs are stored
+// as MFMA fragment blocks in HBM, and q's token-major rows (the contraction
+// index d_k is contiguous there) are gathered a line at a time (RowLines).
+// The copy waves move the
+// next chunk's 60 KiB straight into one of two LDS buffers with
+// global_load_lds_dwordx4 and write the chunk state out of LDS, so the chain
+// waves never queue behind the address unit.  Per chunk:
+//   chain: h -> LDS | barrier | U' = U - W h, O = Q h | barrier |
+//          O <- diag(e^G) O, h <- e^{G_last} h + Khat^T U', O += P U', store O
 //   copy:             | next chunk's operands -> LDS, state -> HBM | | wait
 template <int DK, int DV, int BV, int VAR>
-__global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16* __restrict__ Qgg,
+__global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16* __restrict__ q,
                                                      const float* __restrict__ S0, const float* __restrict__ gcum,
                                                      const bf16* __restrict__ Wg, const bf16* __restrict__ KhTg,
                                                      const bf16* __restrict__ Pg, const bf16* __restrict__ Ug,
                                                      float* __restrict__ states, float* __restrict__ ST,
                                                      bf16* __restrict__ o, int* __restrict__ flag) {
   static_assert(BV == SCAN_BV && VAR != VAR_DECAY, "U is laid out for the scan's value tiles");
+  typedef RowLines<DK> QL;
+  static_assert(QL::NBLK == (CH / 16) * (DK / 32), "q takes the blocks of a 64 x DK fragment operand");
   constexpr int NVT = DV / BV;
   constexpr int LK = DK + 8, LU = CH + 8, LF = BV + 4;
   typedef Tiles<DK, BV, 4, 1> HT;  // carried state slice h[:, v0:v0+BV] (chain waves)
@@ -496,6 +502,12 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
   // buf[b] + j KiB; the copy wave w - 4 takes every fourth block)
   typedef __attribute__((address_space(1))) void gvoid;
   typedef __attribute__((address_space(3))) void lvoid;
+  // row r of q in chunk c (rows past the chunk's end repeat its last row:
+  // they reach only output rows that are never stored)
+  auto q_row = [&](int c, int r) -> const bf16* {
+    const int len = min(CH, sp.len - c * CH);
+    return q + ((sp.row0 + (long)c * CH + clamp_row(r, len)) * H + h) * DK;
+  };
   auto fill = [&](int c, int b) {
     const long tile = (long)(sp.c0 + c) * H + h;
 #pragma unroll
@@ -503,12 +515,16 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
       const int j = j0 + (w - 4);
       if (j < NB) {
         const bf16* src;
-        if (j < OQ) src = Wg + tile * CH * DK + (j - OW) * 512;
-        else if (j < OP_) src = Qgg + tile * CH * DK + (j - OQ) * 512;
-        else if (j < OK) src = Pg + tile * CH * CH + (j - OP_) * 512;
-        else if (j < OU) src = KhTg + tile * DK * CH + (j - OK) * 512;
-        else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512;
-        __builtin_amdgcn_global_load_lds((gvoid*)(src + l * 8), (lvoid*)(buf[b] + j * 1024), 16, 0, 0);
+        if (j < OQ) src = Wg + tile * CH * DK + (j - OW) * 512 + l * 8;
+        else if (j < OP_) {
+          int r, e;
+          QL::src(j - OQ, l, r, e);
+          src = q_row(c, r) + e;
+        }
+        else if (j < OK) src = Pg + tile * CH * CH + (j - OP_) * 512 + l * 8;
+        else if (j < OU) src = KhTg + tile * DK * CH + (j - OK) * 512 + l * 8;
+        else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512 + l * 8;
+        __builtin_amdgcn_global_load_lds((gvoid*)src, (lvoid*)(buf[b] + j * 1024), 16, 0, 0);
       }
     }
     if (w == 4) __builtin_amdgcn_global_load_lds((gvoid*)(gcum + tile * CH + l), (lvoid*)(buf[b] + NB * 1024), 4, 0, 0);
@@ -534,12 +550,17 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
       int j = e < NSH ? e * NVT + vt : OU + (e - NSH);
       j = j < NB ? j : NB - 1;
       const bf16* src;
-      if (j < OQ) src = Wg + tile * CH * DK + (j - OW) * 512;
-      else if (j < OP_) src = Qgg + tile * CH * DK + (j - OQ) * 512;
-      else if (j < OK) src = Pg + tile * CH * CH + (j - OP_) * 512;
-      else if (j < OU) src = KhTg + tile * DK * CH + (j - OK) * 512;
-      else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512;
-      __builtin_amdgcn_global_load_lds((gvoid*)(src + (L & 7) * 64), (lvoid*)sink, 4, 0, 0);
+      if (j < OQ) src = Wg + tile * CH * DK + (j - OW) * 512 + (L & 7) * 64;
+      else if (j < OP_) {
+        // line (L & 7) of q block j - OQ
+        int r, e;
+        QL::src(j - OQ, (L & 7) << 3, r, e);
+        src = q_row(c, r) + (e & ~63);
+      }
+      else if (j < OK) src = Pg + tile * CH * CH + (j - OP_) * 512 + (L & 7) * 64;
+      else if (j < OU) src = KhTg + tile * DK * CH + (j - OK) * 512 + (L & 7) * 64;
+      else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512 + (L & 7) * 64;
+      __builtin_amdgcn_global_load_lds((gvoid*)src, (lvoid*)sink, 4, 0, 0);
     }
   };
   static_assert(NWARM + NST < 16, "vmcnt field");
@@ -579,7 +600,12 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
           *reinterpret_cast<uint2*>(hT + vv * LK + d0) = pack4<bf16>(h4);
         }
       lds_barrier();  // A: h in LDS, this chunk's operands in buffer c & 1
-      // U' = U - W h and O = diag(e^G) Q h; A fragments of wave w are 16-row tile w
+      // U' = U - W h and O = Q h; A fragments of wave w are 16-row tile w.
+      // The row scales e^{G_r} of O are formed here, under the products.
+      const float* Gc = reinterpret_cast<const float*>(B + NB * 1024);
+      float gam[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) gam[j] = __expf(Gc[UT::m0(0) + (l >> 4) * 4 + j]);
       UT up, ot;
       const bf16x8* Wf = reinterpret_cast<const bf16x8*>(B + OW * 1024);
       const bf16x8* Qf = reinterpret_cast<const bf16x8*>(B + OQ * 1024);
@@ -587,7 +613,7 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
       up.zero();
 #pragma unroll
       for (int st = 0; st < DK / 32; ++st) {
-        const bf16x8 fq = Qf[(w * (DK / 32) + st) * 64 + l];
+        const bf16x8 fq = Qf[QL::frag_slot(w, st, l)];
         const bf16x8 fw = Wf[(w * (DK / 32) + st) * 64 + l];
 #pragma unroll
         for (int bb = 0; bb < UT::TN; ++bb) {
@@ -610,8 +636,13 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
         *reinterpret_cast<uint2*>(UsT + vv * LU + r0) = pack4<bf16>(u4);
       }
       lds_barrier();  // B: U' in LDS
-      const float gl = __expf(reinterpret_cast<const float*>(B + NB * 1024)[CH - 1]);
+      const float gl = __expf(Gc[CH - 1]);
       hs.each([&](int, int, float& x) { x *= gl; });
+      // O = diag(e^G) Q h: the row scale applied to the fp32 products
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int bb = 0; bb < UT::TN; ++bb) ot.acc[0][bb][j] *= gam[j];
       const bf16x8* Kf = reinterpret_cast<const bf16x8*>(B + OK * 1024);
       const bf16x8* Pf = reinterpret_cast<const bf16x8*>(B + OP_ * 1024);
 #pragma unroll
@@ -710,7 +741,7 @@ static hipError_t launch_fwd_t(const FwdArgs& a) {
   if (NS > 0) {
     if constexpr (sizeof(OP) == 2 && VAR != VAR_DECAY) {
       hipLaunchKernelGGL((k_scan_fwd_ws<DK, DV, BV, VAR>), dim3(NS * NVT), dim3(512), 0, a.stream, geo, H,
-                         (const bf16*)w.Qg, a.S0, w.gcum, (const bf16*)w.W, (const bf16*)w.KhT,
+                         (const bf16*)a.q, a.S0, w.gcum, (const bf16*)w.W, (const bf16*)w.KhT,
                          (const bf16*)w.P, (const bf16*)w.U, a.states, a.ST, (bf16*)a.o, w.flag_scan);
     } else {
       hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,

@@ -29,6 +29,7 @@ struct Shape {
   int64_t B, T, H, dk, dv, N, chunks, NT;
   bool packed;
   int es;  // bytes per activation element
+  int variant;
 };
 
 // Validates the problem description (sizes, variant, dtype, packed offsets).
@@ -43,6 +44,7 @@ gdn_status check_problem(const gdn_problem* p, Shape* s) {
   s->B = p->B; s->T = p->T; s->H = p->H; s->dk = p->dk; s->dv = p->dv;
   s->packed = packed;
   s->es = p->io_dtype == GDN_BF16 ? 2 : 4;
+  s->variant = p->variant;
   if (packed) {
     if (!p->cu_seqlens_host || !p->cu_seqlens_dev) return GDN_ERR_NULL;
     if (p->B != 1 || p->num_seqs < 0) return GDN_ERR_VARLEN;
@@ -117,7 +119,10 @@ void layout_fwd(const Shape& s, char* base, FwdWs* w, size_t* total) {
   w->U = b.take<float>(tiles * kChunk * s.dv);
   w->KhT = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->P = b.take<char>(tiles * kChunk * kChunk * s.es);
-  w->Qg = b.take<char>(tiles * kChunk * s.dk * s.es);
+  // diag(e^G) Q: only the generic scan reads it (the split bf16 scan of the
+  // delta-rule members reads q)
+  const bool split = s.es == 2 && s.variant != GDN_DECAY_ONLY;
+  w->Qg = b.take<char>(split ? 0 : tiles * kChunk * s.dk * s.es);
   w->exact = nullptr;  // the exact forward needs no scratch
   *total = b.off;
 }
@@ -135,7 +140,7 @@ void layout_bwd(const Shape& s, char* base, BwdWs* w, size_t* total) {
   w->dOT = b.take<char>(tiles * kChunk * s.dv * s.es);
   w->PT = b.take<char>(tiles * kChunk * kChunk * s.es);
   w->T = b.take<char>(tiles * kChunk * kChunk * s.es);
-  w->Kh = b.take<char>(tiles * kChunk * s.dk * s.es);
+  w->Kh = b.take<char>(s.es == 2 ? 0 : tiles * kChunk * s.dk * s.es);  // the bf16 scan reads k
   w->dh = b.take<char>(tiles * (size_t)s.dk * s.dv * s.es);
   w->dUT = b.take<char>(tiles * kChunk * s.dv * s.es);
   w->grad_scratch = b.take<char>(s.es == 4 ? tiles * (size_t)grad_region_bytes((int)s.dk, 4) : 0);

@@ -1063,9 +1063,7 @@ __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __re
 #pragma unroll
     for (int i = 0; i < 8; ++i) hd += hdh_w[i];
     if (l == CH - 1) x += Gam[CH - 1] * hd + kk;
-    const float rev = shfl_idx(x, CH - 1 - l);
-    const float sc = wave_incl_scan(rev);
-    const float dgv = shfl_idx(sc, CH - 1 - l);
+    const float dgv = wave_reverse(wave_incl_scan(wave_reverse(x)));
     if (l < cp.len) {
       const long o = (cp.row0 + l) * H + h;
       if (VAR != VAR_DELTA) dg[o] = dgv;
@@ -1337,11 +1335,15 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     }
   }
   if (w == 0) {
-    // in-chunk gates: G = inclusive cumsum of g (0 past the end), beta (0 past the end)
+    // in-chunk gates: G = inclusive cumsum of g (0 past the end), beta (0 past
+    // the end), e^{G_r} and e^{G_last - G_r}
     const float gv = l < len ? p0.gv : 0.f, bv = l < len ? p0.bv : 0.f;
-    ok = finite_f(gv) && finite_f(bv);
-    Gs[l] = wave_incl_scan(gv);
+    ok &= finite_f(gv) && finite_f(bv);
+    const float gc = wave_incl_scan(gv);
+    Gs[l] = gc;
     Bs[l] = bv;
+    Gam[l] = __expf(gc);
+    Dte[l] = __expf(shfl_idx(gc, CH - 1) - gc);
   }
   __syncthreads();
   // the next tile (this one again on the last pass: a clamped, unconditional
@@ -1349,11 +1351,6 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   // the gates are in LDS now, and their next copies load from here on.
   const Tile nxt = tile_at(tt + (int)gridDim.x < ntiles ? tt + (int)gridDim.x : tt);
   if constexpr (HL) load_0(p0, nxt);
-  if (thread_x() < CH) {
-    const int r = thread_x();
-    Gam[r] = __expf(Gs[r]);
-    Dte[r] = __expf(Gs[CH - 1] - Gs[r]);
-  }
   TC pm, ae;  // P = (Q K^T) * D and (K K^T) * E, kept for phase 2
   float dd[TC::TN][4];  // D_ri = e^{G_r - G_i} for i <= r, else 0
   pm.zero();
@@ -1677,7 +1674,9 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     }
   // the accumulators are free: the next tile's h and dh (or h^T with two slices)
   if constexpr (HL) load_b(pb, nxt, 0); else load_a2(pa, nxt, 0);
+  __syncthreads();
   if (w == 0) {
+    // dg (reverse cumsum of dG) and dbeta, while the other waves store dq, dk
     const int r = l;
     float rq = 0.f, rx = 0.f, rk = 0.f;
 #pragma unroll
@@ -1699,16 +1698,13 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
 #pragma unroll
     for (int i = 0; i < 8; ++i) hd += hdh_w[i];
     if (l == CH - 1) x += Gam[CH - 1] * hd + kk;
-    const float rev = shfl_idx(x, CH - 1 - l);
-    const float sc = wave_incl_scan(rev);
-    const float dgv = shfl_idx(sc, CH - 1 - l);
+    const float dgv = wave_reverse(wave_incl_scan(wave_reverse(x)));
     if (l < len) {
       const long o = (cp.row0 + l) * H + h;
       if (VAR != VAR_DELTA) dg[o] = dgv;
       if (DT_) dbeta[o] = db;
     }
   }
-  __syncthreads();
   store_rows<DK, LK>(dq + (cp.row0 * H + h) * DK, (long)H * DK, len, dqst);
   store_rows<DK, LK>(dk + (cp.row0 * H + h) * DK, (long)H * DK, len, dkst);
   if (threadIdx.x == 0) gdn_tid_bias = 0;  // a new pass: index arithmetic is recomputed

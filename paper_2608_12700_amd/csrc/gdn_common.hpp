@@ -468,18 +468,6 @@ __device__ __forceinline__ SeqPos seq_pos(const Geo& g, int n) {
   return s;
 }
 
-// Inclusive prefix sum of one value per lane over a wave (Hillis-Steele; the
-// order of additions is fixed, so the result is deterministic).
-__device__ __forceinline__ float wave_incl_scan(float x) {
-  const int l = lane_id();
-#pragma unroll
-  for (int off = 1; off < WAVE; off <<= 1) {
-    const float y = shfl_idx(x, l - off);  // unused where l < off
-    if (l >= off) x += y;
-  }
-  return x;
-}
-
 // Cross-lane sums on the VALU (no LDS traffic).  Every lane of a group ends
 // with the same bits: each step adds a pair of partial sums that the two lanes
 // of the pair hold in the same order.
@@ -508,5 +496,38 @@ __device__ __forceinline__ float sum_groups(float x) {
 }
 // Fixed-order wave reduction.
 __device__ __forceinline__ float wave_sum(float x) { return sum_groups(sum16(x)); }
+
+// DPP move with a row mask: rows outside the mask (and lanes without a
+// source) receive 0.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_rows(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROWS, 0xF, false));
+}
+
+// Inclusive prefix sum of one value per lane over a wave, on the VALU: a
+// Hillis-Steele scan inside each row of 16 (row shifts by 1, 2, 4, 8), then
+// the last lane of row 0 / row 2 added to rows 1 / 3 and the last lane of row
+// 1 to rows 2 and 3 (row broadcasts).  The order of additions is fixed, so
+// the result is deterministic.
+__device__ __forceinline__ float wave_incl_scan(float x) {
+  x += dpp_rows<0x111, 0xF>(x);  // row_shr:1
+  x += dpp_rows<0x112, 0xF>(x);  // row_shr:2
+  x += dpp_rows<0x114, 0xF>(x);  // row_shr:4
+  x += dpp_rows<0x118, 0xF>(x);  // row_shr:8
+  x += dpp_rows<0x142, 0xA>(x);  // row_bcast:15 into rows 1 and 3
+  x += dpp_rows<0x143, 0xC>(x);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
+// Lane l receives lane 63 - l: mirror inside each row of 16, then the row
+// order reversed (swap the wave halves, then adjacent rows).
+__device__ __forceinline__ float wave_reverse(float x) {
+  const int l = lane_id();
+  const unsigned u = __builtin_bit_cast(unsigned, dpp<0x140>(x));
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const unsigned v = (l < 32) ? (unsigned)a[1] : (unsigned)a[0];
+  const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return __builtin_bit_cast(float, ((l >> 4) & 1) ? (unsigned)b[0] : (unsigned)b[1]);
+}
 
 }  // namespace gdn

@@ -159,16 +159,16 @@ def kernel_model(B, T, H, dk, dv, es, N=None):
     vv = CH * dv * es  # one chunk of v, o, dO (or a 64 x dv operand)
     pp = CH * CH * es  # one 64 x 64 operand
     per = {
-        # q, k, v, g, beta -> gcum, W, U, Khat^T, P, diag(e^G) Q
-        "fwd_prep": (2 * qk + vv + 2 * g4 + g4 + 2 * qk + vv + pp + qk,
+        # q, k, v, g, beta -> gcum, W, U, Khat^T, P
+        "fwd_prep": (2 * qk + vv + 2 * g4 + g4 + 2 * qk + vv + pp,
                      3 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dk + 2 * CH * CH * dv),
         # q, W, Khat^T, P, U, gcum -> chunk states, o
         "fwd_scan": (3 * qk + pp + vv + g4 + st + vv,
                      3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
-        # q, k, g, beta, dO -> gcum, W^T, (diag(e^G) Q)^T, dO^T, P^T, T, Khat
-        "bwd_prep": (2 * qk + 2 * g4 + vv + g4 + 2 * qk + vv + 2 * pp + qk,
+        # q, k, g, beta, dO -> gcum, W^T, (diag(e^G) Q)^T, dO^T, P^T, T
+        "bwd_prep": (2 * qk + 2 * g4 + vv + g4 + 2 * qk + vv + 2 * pp,
                      3 * 2 * CH * CH * dk + CH ** 3 / 3),
-        # Khat, gcum, W^T, Qg^T, dO^T, P^T -> dh (I/O dtype), dU'^T
+        # k, gcum, W^T, Qg^T, dO^T, P^T -> dh (I/O dtype), dU'^T
         "bwd_scan": (3 * qk + g4 + vv + pp + dk * dv * es + vv,
                      3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
         # q, k, v, g, beta, T, states, dO, dh, dU'^T -> dq, dk, dv, dg, dbeta

@@ -46,7 +46,8 @@
  * GDN_F32 keeps every operand in fp32 (fp32 matrix cores).
  *
  * Supported: chunk == 64, d_k in {64, 128}, d_v in {64, 128, 256}, T >= 0,
- * sequence lengths >= 0.  Anything else returns GDN_ERR_UNSUPPORTED.
+ * sequence lengths >= 0, H * d_v < 2^24 (the kernels form in-chunk row
+ * offsets with 24-bit multiplies).  Anything else returns GDN_ERR_UNSUPPORTED.
  *
  * Non-finite inputs: a (sequence, head) stream whose inputs hold a NaN or Inf
  * is recomputed token by token in fp32 in the operation order written above,
@@ -84,7 +85,7 @@ typedef enum {
   GDN_OK = 0,
   GDN_ERR_NULL = -1,        /* a required pointer is NULL */
   GDN_ERR_SHAPE = -2,       /* negative or inconsistent sizes */
-  GDN_ERR_UNSUPPORTED = -3, /* chunk, d_k or d_v outside the supported set */
+  GDN_ERR_UNSUPPORTED = -3, /* chunk, d_k, d_v or H * d_v outside the supported set */
   GDN_ERR_DTYPE = -4,       /* unknown io_dtype */
   GDN_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required */
   GDN_ERR_ALIAS = -6,       /* an output overlaps an input or another output */

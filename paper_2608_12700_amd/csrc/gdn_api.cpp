@@ -37,6 +37,8 @@ gdn_status check_problem(const gdn_problem* p, Shape* s) {
   if (!p) return GDN_ERR_NULL;
   if (p->B < 0 || p->T < 0 || p->H < 0 || p->dk <= 0 || p->dv <= 0) return GDN_ERR_SHAPE;
   if (p->chunk != kChunk || !dims_supported(p->dk, p->dv)) return GDN_ERR_UNSUPPORTED;
+  // row strides H * d (elements) must fit the kernels' 24-bit in-chunk offsets
+  if ((int64_t)p->H * (p->dk > p->dv ? p->dk : p->dv) >= (int64_t)1 << 24) return GDN_ERR_UNSUPPORTED;
   if (p->io_dtype != GDN_F32 && p->io_dtype != GDN_BF16) return GDN_ERR_DTYPE;
   if (p->variant != GDN_GATED_DELTA && p->variant != GDN_DELTA && p->variant != GDN_DECAY_ONLY)
     return GDN_ERR_VARIANT;

@@ -1157,7 +1157,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   // the loop-safe thread index reads this word: it is stored before any use
   if (threadIdx.x == 0) gdn_tid_bias = 0;
   __syncthreads();
-  const long rsv = (long)H * DV;
+  const int rsv = H * DV;  // row strides (elements) of v, dO, dv and of q, k, dq, dk
+  const int rsk = H * DK;
 
   // one (chunk, head) tile
   struct Tile {
@@ -1199,13 +1200,13 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
 #pragma unroll
     for (int t = 0; t < NQK; ++t) {
       const int idx = thread_x() + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
-      const long ro = clamp_row(r, len) * (long)H * DK + c;
+      const unsigned ro = row_off(clamp_row(r, len), rsk) + c;
       p.qk[0][t] = *reinterpret_cast<const uint4*>(qp + ro);
       p.qk[1][t] = *reinterpret_cast<const uint4*>(kp + ro);
     }
     p.tq = uint4{0u, 0u, 0u, 0u};
     if constexpr (DT_) p.tq = *reinterpret_cast<const uint4*>(Tg + x.t * CH * CH + thread_x() * 8);
-    const long o = (x.cp.row0 + clamp_row(l, len)) * H + x.h;
+    const long o = (x.cp.row0 * H + x.h) + row_off(clamp_row(l, len), H);
     p.gv = 0.f;
     p.bv = 0.f;
     if constexpr (VAR != VAR_DELTA) p.gv = g[o];
@@ -1220,7 +1221,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
 #pragma unroll
     for (int t = 0; t < NDO; ++t) {
       const int idx = thread_x() + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
-      p.dov[t] = *reinterpret_cast<const uint4*>(dop + clamp_row(r, len) * rsv + c0 + c);  // masked at use
+      p.dov[t] = *reinterpret_cast<const uint4*>(dop + row_off(clamp_row(r, len), rsv) + c0 + c);  // masked at use
     }
 #pragma unroll
     for (int s = 0; s < CH / 32; ++s)
@@ -1234,7 +1235,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
         for (int b = 0; b < TY::TN; ++b) {
           const int r = TY::n0(b) + lc;
           // masked at use
-          p.vb[a][b] = *reinterpret_cast<const uint2*>(vp + clamp_row(r, len) * rsv + c0 + TY::m0(a) + 4 * lg);
+          p.vb[a][b] = *reinterpret_cast<const uint2*>(vp + row_off(clamp_row(r, len), rsv) + c0 + TY::m0(a) + 4 * lg);
         }
     }
   };
@@ -1464,7 +1465,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
             y4[j] = from_f<bf16>(-y);
             if (DT_) dbY[b] += (r < len ? to_f(elem4<bf16>(pa.vb[a][b], j)) : 0.f) * y;
           }
-          if (r < len) *reinterpret_cast<uint2*>(dvp + r * rsv + c0 + v0) = pack4<bf16>(d4);
+          if (r < len) *reinterpret_cast<uint2*>(dvp + row_off(r, rsv) + c0 + v0) = pack4<bf16>(d4);
           if (DT_) *reinterpret_cast<uint2*>(Ys + r * LV + v0) = pack4<bf16>(y4);
         }
       }
@@ -1478,7 +1479,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
       // the scalar-decay member has U' = V
       for (int idx = thread_x(); idx < CH * VS / 8; idx += blockDim.x) {
         const int r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
-        const uint4 u = keep16(r < len, *reinterpret_cast<const uint4*>(vp + clamp_row(r, len) * rsv + c0 + c));
+        const uint4 u = keep16(r < len, *reinterpret_cast<const uint4*>(vp + row_off(clamp_row(r, len), rsv) + c0 + c));
         ok &= finite16B<bf16>(u);
         *reinterpret_cast<uint4*>(Ups + r * LV + c) = u;
       }
@@ -1700,13 +1701,13 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     if (l == CH - 1) x += Gam[CH - 1] * hd + kk;
     const float dgv = wave_reverse(wave_incl_scan(wave_reverse(x)));
     if (l < len) {
-      const long o = (cp.row0 + l) * H + h;
+      const long o = (cp.row0 * H + h) + row_off(l, H);
       if (VAR != VAR_DELTA) dg[o] = dgv;
       if (DT_) dbeta[o] = db;
     }
   }
-  store_rows<DK, LK>(dq + (cp.row0 * H + h) * DK, (long)H * DK, len, dqst);
-  store_rows<DK, LK>(dk + (cp.row0 * H + h) * DK, (long)H * DK, len, dkst);
+  store_rows<DK, LK>(dq + (cp.row0 * H + h) * DK, rsk, len, dqst);
+  store_rows<DK, LK>(dk + (cp.row0 * H + h) * DK, rsk, len, dkst);
   if (threadIdx.x == 0) gdn_tid_bias = 0;  // a new pass: index arithmetic is recomputed
   const int bad = __syncthreads_or(!ok);
   if (threadIdx.x == 0) flag[tile] = bad;

@@ -141,7 +141,7 @@ __device__ __forceinline__ void store_rows(T* __restrict__ dst, long rs, int len
   for (int idx = thread_x(); idx < CH * PER_ROW; idx += blockDim.x) {
     const int r = idx / PER_ROW, c = (idx - r * PER_ROW) * V;
     if (r < len)
-      *reinterpret_cast<uint4*>(dst + r * rs + c) = *reinterpret_cast<const uint4*>(src + r * LD + c);
+      *reinterpret_cast<uint4*>(dst + row_off(r, (int)rs) + c) = *reinterpret_cast<const uint4*>(src + r * LD + c);
   }
 }
 

@@ -122,6 +122,13 @@ __device__ __forceinline__ long cfrag_off(int r, int v) {
   return ((((long)(v / BV) * 4 + (r >> 4)) * (BV / 16) + ((v % BV) >> 4)) * 64 + (v & 15) + 16 * ((r & 15) >> 2)) * 4;
 }
 
+// Offset of row `row` (0 <= row < 64) of a token-major tile with row stride
+// `stride` elements (stride < 2^24, which the C ABI checks): one full-rate
+// 24-bit multiply.  The chunk's own base offset is formed separately in 64 bits.
+__device__ __forceinline__ unsigned row_off(int row, int stride) {
+  return __umul24((unsigned)row, (unsigned)stride);
+}
+
 // Masked tile rows: rows r >= len of a chunk are read from row len - 1
 // (len >= 1 for every chunk) and zeroed with a select afterwards.  Keeping
 // the load itself unconditional matters: a branch around a load forces the

@@ -76,6 +76,15 @@ def test_unsupported_dims_and_chunk():
     assert call_fwd(p) == -3
 
 
+def test_head_stride_limit():
+    # row strides H * max(d_k, d_v) must stay below 2^24 elements
+    p = gdn.make_problem(1, 64, (1 << 24) // 256, 64, 256)
+    assert call_fwd(p) == -3 and call_bwd(p) == -3
+    assert gdn.gdn_fwd_workspace_size(p) == 0
+    p = gdn.make_problem(1, 64, (1 << 24) // 256 - 1, 64, 256)
+    assert gdn.gdn_fwd_workspace_size(p) > 0
+
+
 def test_bad_shape_dtype_variant():
     assert call_fwd(gdn.make_problem(-1, 64, 1, 64, 64)) == -2
     assert call_fwd(gdn.make_problem(1, 64, 1, 64, 64, io_dtype=7)) == -4

@@ -1319,8 +1319,9 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     *reinterpret_cast<uint4*>(Ts + r * LT + c) = tq;
   }
   if constexpr (HL) {
-    // h -> LDS in bf16; <h, dh> and the finiteness check take the fp32 values.
-    // Where two waves hold the same rows (d_k = 64) one of them does this.
+    // h -> LDS in bf16; <h, dh> takes the fp32 values (and checks them: a
+    // non-finite element of h makes the sum non-finite).  Where two waves hold
+    // the same rows (d_k = 64) one of them does this.
     if (TD::n0(0) == 0) {
 #pragma unroll
       for (int s = 0; s < VS / 32; ++s)
@@ -1328,10 +1329,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
         for (int a = 0; a < TD::TM; ++a) {
           *reinterpret_cast<bf16x8*>(Hs + (TD::m0(a) + lc) * LH + 32 * s + 8 * lg) = cvt8(pb.hx[s][a]);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            ok &= finite_f(pb.hx[s][a][j]);
-            hdh += pb.hx[s][a][j] * to_f(pb.dh[s][a][j]);
-          }
+          for (int j = 0; j < 8; ++j) hdh += pb.hx[s][a][j] * to_f(pb.dh[s][a][j]);
         }
     }
   }
@@ -1426,8 +1424,8 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
           bf16 r4[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
+            // (v is checked through the dbeta partial sum v . Y below)
             const float vx = r < len ? to_f(elem4<bf16>(pa.vb[a][b], j)) : 0.f;
-            ok &= finite_f(vx);
             r4[j] = from_f<bf16>(br * (vx - gr * kht.acc[a][b][j]));
           }
           *reinterpret_cast<uint2*>(Rs + r * LV + v0) = pack4<bf16>(r4);
@@ -1540,11 +1538,16 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
 
   hdh = wave_sum(hdh);
   if (l == 0) hdh_w[w] = hdh;
+  // A non-finite element of h (or of dh) leaves <h, dh> non-finite; so does
+  // one of v in v . Y (Inf times 0 is NaN).  An overflow of the sums alone
+  // flags the stream as well, which only sends it to the exact path.
+  if constexpr (HL) ok &= finite_f(hdh);
   if constexpr (DT_) {
     // dbeta partial v_r . Y_r: over the 4 lane groups, then one partial per wave row of Y^T
 #pragma unroll
     for (int b = 0; b < TY::TN; ++b) {
       const float s = sum_groups(dbY[b]);
+      ok &= finite_f(s);
       if (lg == 0) dbYp[w / C::WMv][TY::n0(b) + lc] = s;
     }
   }

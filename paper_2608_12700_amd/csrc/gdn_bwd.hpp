@@ -1097,12 +1097,16 @@ __global__ __launch_bounds__(512) void k_grad_bwd(Geo geo, int H, const OP* __re
 template <int DK, int DV>
 struct GradBF {
   static constexpr int VS = DV > 128 ? 128 : DV;
+  // waves per block: 16 with one value slice (four per SIMD, to hide the
+  // phases' dependency chains), 8 with two (whose operands need more registers)
+  static constexpr int NW = DV <= 128 ? 16 : 8, NT = 64 * NW;
   static constexpr int LK = DK + 8, LT = CH + 8, LC = CH + 4, LV = VS + 8;
-  static constexpr int WMd = DK / 16, WNr = 8 / WMd;  // waves along d and along r of the d x 64 results
-  static constexpr int WNv = VS / 16, WMv = 8 / WNv;
+  static constexpr int WMd = DK / 16, WNr = NW / WMd;  // waves along d and along r of the d x 64 results
+  static constexpr int WNv = VS / 16, WMv = NW / WNv;
+  static constexpr int WMc = 4, WNc = NW / 4;          // waves along the rows and columns of 64 x 64 results
   typedef Tiles<DK, CH, WMd, WNr> TD;  // X^T, dQ^T, dK^T: d x 64
   typedef Tiles<VS, CH, WNv, WMv> TY;  // Y^T, U'^T, (K h)^T: VS x 64
-  typedef Tiles<CH, CH, 4, 2> TC;      // P, A, dP, dA
+  typedef Tiles<CH, CH, WMc, WNc> TC;  // P, A, dP, dA
   static constexpr int PH1 = 4 * CH * LV * 2;
   static constexpr int PH2 = 2 * CH * LT * 2 > 2 * CH * LK * 2 ? 2 * CH * LT * 2 : 2 * CH * LK * 2;
   static constexpr int UB = PH1 > PH2 ? PH1 : PH2;
@@ -1117,7 +1121,7 @@ __device__ __forceinline__ bf16x8 cvt8(const float (&x)[8]) {
 
 #ifdef GDN_TILE_LOOP
 template <int DK, int DV, int VAR>
-__global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, const bf16* __restrict__ q,
+__global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int H, int ntiles, const bf16* __restrict__ q,
                                                  const bf16* __restrict__ k, const bf16* __restrict__ v,
                                                  const float* __restrict__ g, const float* __restrict__ beta,
                                                  const float* __restrict__ states, const bf16* __restrict__ dO,
@@ -1132,14 +1136,22 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   typedef Mma<bf16> M;
   constexpr bool DT_ = VAR != VAR_DECAY;
   constexpr int VS = C::VS, LK = C::LK, LT = C::LT, LC = C::LC, LV = C::LV;
-  constexpr int NDO = CH * VS / 8 / 512;  // 16-byte pieces of a dO slice per thread
-  constexpr int NQK = CH * DK / 8 / 512;  // 16-byte pieces of q (or k) per thread
+  constexpr int NW = C::NW, NT = C::NT;
+  static_assert(NT == (DV <= 128 ? 1024 : 512), "launch bounds");
+  // 16-byte pieces of a dO slice, of q (or k) and of T; each thread takes
+  // every NT-th (threads past the end repeat the last piece: same value, same place)
+  constexpr int PDO = CH * VS / 8, PQK = CH * DK / 8, PT = CH * CH / 8;
+  constexpr int NDO = (PDO + NT - 1) / NT, NQK = (PQK + NT - 1) / NT;
+  static_assert(PT <= NT, "one piece of T per thread");
   // With one value slice the chunk state h is read from HBM once, a tile
   // ahead, in the row-fragment layout of X^T and dQ^T; phase 0 stores it in
   // LDS as bf16, and (K h)^T takes its h^T fragments from there with
   // transposing reads.  With two slices both layouts are loaded per slice.
   constexpr bool HL = DV <= VS;
   constexpr int LH = VS + 8;
+  // with one slice, the waves that share a block of d rows split its 32-column
+  // steps s = wr, wr + WNr, ... (wr = the wave's column index) for the load of h
+  constexpr int SH = HL ? (VS / 32 + C::WNr - 1) / C::WNr : VS / 32;
 
   __shared__ __align__(16) bf16 Qs[CH * LK];
   __shared__ __align__(16) bf16 Ks[CH * LK];
@@ -1148,9 +1160,9 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   __shared__ __align__(16) float Gam[CH];
   __shared__ __align__(16) float Bs[CH];
   __shared__ __align__(16) float Dte[CH];
-  __shared__ float rowZ[2][CH], colZ[4][CH], rowA[2][CH];
+  __shared__ float rowZ[C::WNc][CH], colZ[C::WMc][CH], rowA[C::WNc][CH];
   __shared__ float rqp[C::WMd][CH], rxp[C::WMd][CH], rkp[C::WMd][CH], dbYp[C::WNv][CH];
-  __shared__ float hdh_w[8];
+  __shared__ float hdh_w[NW];
   __shared__ __align__(16) char ub[C::UB];
   __shared__ __align__(16) bf16 Hs[HL ? DK * LH : 8];
 
@@ -1190,7 +1202,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     uint2 vb[TY::TM][TY::TN];            // v[r][v0..v0+3] in the Y^T accumulator layout
   };
   struct PreB {
-    float hx[VS / 32][TD::TM][8];        // h: A fragments of X^T and dQ^T
+    float hx[SH][TD::TM][8];             // h (with one slice: this wave's steps only)
     bf16x8 dh[VS / 32][TD::TM];          // dh: A fragments of dK^T
   };
   auto load_0 = [&](Pre0& p, const Tile& x) {
@@ -1199,13 +1211,13 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     const bf16* kp = k + (x.cp.row0 * H + x.h) * DK;
 #pragma unroll
     for (int t = 0; t < NQK; ++t) {
-      const int idx = thread_x() + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
+      const int idx = min(thread_x() + t * NT, PQK - 1), r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
       const unsigned ro = row_off(clamp_row(r, len), rsk) + c;
       p.qk[0][t] = *reinterpret_cast<const uint4*>(qp + ro);
       p.qk[1][t] = *reinterpret_cast<const uint4*>(kp + ro);
     }
     p.tq = uint4{0u, 0u, 0u, 0u};
-    if constexpr (DT_) p.tq = *reinterpret_cast<const uint4*>(Tg + x.t * CH * CH + thread_x() * 8);
+    if constexpr (DT_) p.tq = *reinterpret_cast<const uint4*>(Tg + x.t * CH * CH + min(thread_x(), PT - 1) * 8);
     const long o = (x.cp.row0 * H + x.h) + row_off(clamp_row(l, len), H);
     p.gv = 0.f;
     p.bv = 0.f;
@@ -1220,7 +1232,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     const bf16* vp = v + (x.cp.row0 * H + x.h) * DV;
 #pragma unroll
     for (int t = 0; t < NDO; ++t) {
-      const int idx = thread_x() + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
+      const int idx = min(thread_x() + t * NT, PDO - 1), r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
       p.dov[t] = *reinterpret_cast<const uint4*>(dop + row_off(clamp_row(r, len), rsv) + c0 + c);  // masked at use
     }
 #pragma unroll
@@ -1266,6 +1278,24 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
         p.hx[s][a][4] = x1.x; p.hx[s][a][5] = x1.y; p.hx[s][a][6] = x1.z; p.hx[s][a][7] = x1.w;
       }
   };
+  // with one slice: step s = wr + WNr i of this wave's rows (clamped: a wave
+  // without an i-th step repeats its last one and skips it at use)
+  auto load_hs = [&](PreB& p, const Tile& x) {
+    const int l = lane_id(), lg = l >> 4, lc = l & 15, wr = wave_id() % C::WNr;
+    const float* hp = states + x.t * DK * DV;
+#pragma unroll
+    for (int i = 0; i < SH; ++i) {
+      const int st = min(wr + C::WNr * i, VS / 32 - 1);
+#pragma unroll
+      for (int a = 0; a < TD::TM; ++a) {
+        const float* src = hp + (TD::m0(a) + lc) * DV + 32 * st + 8 * lg;
+        const float4 x0 = *reinterpret_cast<const float4*>(src);
+        const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
+        p.hx[i][a][0] = x0.x; p.hx[i][a][1] = x0.y; p.hx[i][a][2] = x0.z; p.hx[i][a][3] = x0.w;
+        p.hx[i][a][4] = x1.x; p.hx[i][a][5] = x1.y; p.hx[i][a][6] = x1.z; p.hx[i][a][7] = x1.w;
+      }
+    }
+  };
   auto load_dh = [&](PreB& p, const Tile& x, int c0) {
     const int l = lane_id();
     const bf16* dhp = dhg + x.t * DK * DV;
@@ -1276,7 +1306,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
         p.dh[s][a] = *reinterpret_cast<const bf16x8*>(dhp + op_off<bf16, DV>(TD::m0(a), c0 + 32 * s) + l * 8);
   };
   auto load_b = [&](PreB& p, const Tile& x, int c0) {
-    load_h(p, x, c0);
+    if constexpr (HL) load_hs(p, x); else load_h(p, x, c0);
     load_dh(p, x, c0);
   };
 
@@ -1303,12 +1333,12 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   // ================= phase 0: gates, P, A; T comes from the prep kernel
 #pragma unroll
   for (int t = 0; t < NQK; ++t) {
-    const int idx = thread_x() + t * 512, r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
+    const int idx = min(thread_x() + t * NT, PQK - 1), r = idx / (DK / 8), c = (idx - r * (DK / 8)) * 8;
     *reinterpret_cast<uint4*>(Qs + r * LK + c) = keep16(r < len, p0.qk[0][t]);
     *reinterpret_cast<uint4*>(Ks + r * LK + c) = keep16(r < len, p0.qk[1][t]);
   }
   {
-    const int r = thread_x() >> 3, c = (thread_x() & 7) * 8;
+    const int pc = min(thread_x(), PT - 1), r = pc >> 3, c = (pc & 7) * 8;
     uint4 tq = p0.tq;
     if constexpr (!DT_) {
       bf16 e[8];
@@ -1320,18 +1350,22 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
   }
   if constexpr (HL) {
     // h -> LDS in bf16; <h, dh> takes the fp32 values (and checks them: a
-    // non-finite element of h makes the sum non-finite).  Where two waves hold
-    // the same rows (d_k = 64) one of them does this.
-    if (TD::n0(0) == 0) {
+    // non-finite element of h makes the sum non-finite).  Each wave does its
+    // own 32-column steps of its rows.
+    // (register arrays indexed by compile-time steps under a wave-uniform test)
+    const int wr = w % C::WNr;
 #pragma unroll
-      for (int s = 0; s < VS / 32; ++s)
+    for (int i = 0; i < SH; ++i)
+#pragma unroll
+      for (int st = 0; st < VS / 32; ++st) {
+        if (st != wr + C::WNr * i) continue;
 #pragma unroll
         for (int a = 0; a < TD::TM; ++a) {
-          *reinterpret_cast<bf16x8*>(Hs + (TD::m0(a) + lc) * LH + 32 * s + 8 * lg) = cvt8(pb.hx[s][a]);
+          *reinterpret_cast<bf16x8*>(Hs + (TD::m0(a) + lc) * LH + 32 * st + 8 * lg) = cvt8(pb.hx[i][a]);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) hdh += pb.hx[s][a][j] * to_f(pb.dh[s][a][j]);
+          for (int j = 0; j < 8; ++j) hdh += pb.hx[i][a][j] * to_f(pb.dh[st][a][j]);
         }
-    }
+      }
   }
   if (w == 0) {
     // in-chunk gates: G = inclusive cumsum of g (0 past the end), beta (0 past
@@ -1470,7 +1504,7 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     }
 #pragma unroll
     for (int t = 0; t < NDO; ++t) {
-      const int idx = thread_x() + t * 512, r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
+      const int idx = min(thread_x() + t * NT, PDO - 1), r = idx / (VS / 8), c = (idx - r * (VS / 8)) * 8;
       *reinterpret_cast<uint4*>(dOs + r * LV + c) = keep16(r < len, pa.dov[t]);
     }
     if constexpr (!DT_) {
@@ -1585,10 +1619,13 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
     if constexpr (DT_) *reinterpret_cast<uint2*>(dBT + i * LT + r0) = pack4<bf16>(bt4);
   }
   {
-    const int wm = w / 2, wn = w % 2;
+    const int wm = w / C::WNc, wn = w % C::WNc;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const float rs = sum16(zs.acc[0][0][j] + zs.acc[0][1][j]);
+      float zr = zs.acc[0][0][j];
+#pragma unroll
+      for (int b = 1; b < TC::TN; ++b) zr += zs.acc[0][b][j];
+      const float rs = sum16(zr);
       const float ra = sum16(rowA_l[j]);
       const int r = TC::m0(0) + 4 * lg + j;
       if (lc == 0) {
@@ -1693,14 +1730,22 @@ __global__ __launch_bounds__(512) void k_grad_bf(Geo geo, int H, int ntiles, con
 #pragma unroll
     for (int i = 0; i < C::WNv; ++i) dbv += dbYp[i][r];
     const float kk_r = Dte[r] * rk;  // khat_r . dkhat_r
-    float x = (rowZ[0][r] + rowZ[1][r]) - (((colZ[0][r] + colZ[1][r]) + colZ[2][r]) + colZ[3][r]);
+    float zr = rowZ[0][r], zc = colZ[0][r], ra = rowA[0][r];
+#pragma unroll
+    for (int i = 1; i < C::WNc; ++i) {
+      zr += rowZ[i][r];
+      ra += rowA[i][r];
+    }
+#pragma unroll
+    for (int i = 1; i < C::WMc; ++i) zc += colZ[i][r];
+    float x = zr - zc;
     x += Gam[r] * (rq + Bs[r] * rx);
     x -= kk_r;
-    const float db = (rowA[0][r] + rowA[1][r]) + Gam[r] * rx + dbv;
+    const float db = ra + Gam[r] * rx + dbv;
     const float kk = wave_sum(kk_r);
     float hd = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) hd += hdh_w[i];
+    for (int i = 0; i < NW; ++i) hd += hdh_w[i];
     if (l == CH - 1) x += Gam[CH - 1] * hd + kk;
     const float dgv = wave_reverse(wave_incl_scan(wave_reverse(x)));
     if (l < len) {
@@ -1726,7 +1771,7 @@ hipError_t launch_grad_bf(const BwdArgs& a) {
   const BwdWs& w = a.ws;
   const int ntiles = geo.total_chunks * H;
   const int grid = ntiles < a.num_cus ? ntiles : a.num_cus;
-  hipLaunchKernelGGL((k_grad_bf<DK, DV, VAR>), dim3(grid), dim3(512), 0, a.stream, geo, H, ntiles,
+  hipLaunchKernelGGL((k_grad_bf<DK, DV, VAR>), dim3(grid), dim3(GradBF<DK, DV>::NT), 0, a.stream, geo, H, ntiles,
                      (const bf16*)a.q, (const bf16*)a.k, (const bf16*)a.v, a.g, a.beta, a.states,
                      (const bf16*)a.dO, (const bf16*)w.dh, (const bf16*)w.dUT, (const bf16*)w.T, (bf16*)a.dq,
                      (bf16*)a.dk_, (bf16*)a.dv_, a.dg, a.dbeta, w.flag_grad);

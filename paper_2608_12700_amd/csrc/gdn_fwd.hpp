@@ -504,30 +504,48 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
   typedef __attribute__((address_space(3))) void lvoid;
   // row r of q in chunk c (rows past the chunk's end repeat its last row:
   // they reach only output rows that are never stored)
-  auto q_row = [&](int c, int r) -> const bf16* {
+  auto q_row = [&](int c, int r) __attribute__((always_inline)) -> const bf16* {
     const int len = min(CH, sp.len - c * CH);
     return q + ((sp.row0 + (long)c * CH + clamp_row(r, len)) * H + h) * DK;
   };
-  auto fill = [&](int c, int b) {
+  // block j0 + (w - 4): the region bounds are multiples of 4, so the unrolled
+  // j0 alone selects the region
+  static_assert(OQ % 4 == 0 && OP_ % 4 == 0 && OK % 4 == 0 && OU % 4 == 0 && NB % 4 == 0, "region bounds");
+  auto copy_block = [&](int c, int j0, int b) __attribute__((always_inline)) {
     const long tile = (long)(sp.c0 + c) * H + h;
-#pragma unroll
-    for (int j0 = 0; j0 < NB; j0 += 4) {
-      const int j = j0 + (w - 4);
-      if (j < NB) {
-        const bf16* src;
-        if (j < OQ) src = Wg + tile * CH * DK + (j - OW) * 512 + l * 8;
-        else if (j < OP_) {
-          int r, e;
-          QL::src(j - OQ, l, r, e);
-          src = q_row(c, r) + e;
-        }
-        else if (j < OK) src = Pg + tile * CH * CH + (j - OP_) * 512 + l * 8;
-        else if (j < OU) src = KhTg + tile * DK * CH + (j - OK) * 512 + l * 8;
-        else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512 + l * 8;
-        __builtin_amdgcn_global_load_lds((gvoid*)src, (lvoid*)(buf[b] + j * 1024), 16, 0, 0);
-      }
+    const int j = j0 + (w - 4);
+    const bf16* src;
+    if (j0 < OQ) src = Wg + tile * CH * DK + (j - OW) * 512 + l * 8;
+    else if (j0 < OP_) {
+      int r, e;
+      QL::src(j - OQ, l, r, e);
+      src = q_row(c, r) + e;
     }
-    if (w == 4) __builtin_amdgcn_global_load_lds((gvoid*)(gcum + tile * CH + l), (lvoid*)(buf[b] + NB * 1024), 4, 0, 0);
+    else if (j0 < OK) src = Pg + tile * CH * CH + (j - OP_) * 512 + l * 8;
+    else if (j0 < OU) src = KhTg + tile * DK * CH + (j - OK) * 512 + l * 8;
+    else src = Ug + tile * CH * DV + (long)vt * CH * BV + (j - OU) * 512 + l * 8;
+    __builtin_amdgcn_global_load_lds((gvoid*)src, (lvoid*)(buf[b] + j * 1024), 16, 0, 0);
+  };
+  // The chain reads W, Q and U only before its second barrier and P, Khat^T
+  // and G after it, so a buffer's W/Q/U region is free half a chunk before
+  // the rest: "early" fills (W, Q, U) of chunk c + 2 go out right after the
+  // chain's second barrier of chunk c, "late" fills (P, Khat^T, G) of chunk
+  // c + 1 after its first barrier of chunk c.  Every copy wave issues the same
+  // number of each (static: the waits below count them).
+  static_assert(NU == 4, "one U block per copy wave");
+  constexpr int NE = OP_ / 4 + 1;  // early fills per copy wave
+  auto fill_early = [&](int c, int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j0 = 0; j0 < OP_; j0 += 4) copy_block(c, j0, b);
+    copy_block(c, OU, b);
+  };
+  auto fill_late = [&](int c, int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j0 = OP_; j0 < OU; j0 += 4) copy_block(c, j0, b);
+    if (w == 4) {
+      const long tile = (long)(sp.c0 + c) * H + h;
+      __builtin_amdgcn_global_load_lds((gvoid*)(gcum + tile * CH + l), (lvoid*)(buf[b] + NB * 1024), 4, 0, 0);
+    }
   };
   // the copy waves' loads landed: their state stores, issued after them, may
   // stay in flight (vmcnt counts in issue order on gfx9)
@@ -563,8 +581,9 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
       __builtin_amdgcn_global_load_lds((gvoid*)src, (lvoid*)sink, 4, 0, 0);
     }
   };
-  static_assert(NWARM + NST < 16, "vmcnt field");
-  auto copies_done = [] { __builtin_amdgcn_s_waitcnt(0x0F70 | (NWARM + NST)); };  // vmcnt(NWARM + NST)
+  static_assert(NWARM + NST + NE < 16, "vmcnt field");
+  // vmcnt(NWARM + NST + NE): everything up to the late fills of the next chunk landed
+  auto copies_done = [] { __builtin_amdgcn_s_waitcnt(0x0F70 | (NWARM + NST + NE)); };
   // A workgroup barrier that waits for this wave's LDS operations only.  Each
   // wave's global loads into LDS are waited for by that wave (copies_done);
   // a full __syncthreads would also wait for every store still in flight.
@@ -684,19 +703,27 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
       const int r = 16 * (w - 4) + (l & 15);
       if (r < len) *reinterpret_cast<bf16x8*>(o + ((row0 + r) * H + h) * DV + v0 + 8 * (l >> 4)) = x;
     };
+    // chunks past the end are clamped to the last one (a redundant copy into
+    // a buffer no chunk reads again), so the fill counts are always the same
+    auto cl = [&](int c) { return c < nch ? c : nch - 1; };
     if (nch > 0) {
-      fill(0, 0);
-      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+      fill_early(0, 0);
+      fill_late(0, 0);
+      fill_early(cl(1), 1);
+      __builtin_amdgcn_s_waitcnt(0x0F70 | NE);  // chunk 0 landed
     }
     lds_barrier();
     for (int c = 0; c < nch; ++c) {
       const long tile = (long)(sp.c0 + c) * H + h;
       lds_barrier();  // A: h of this chunk in LDS; buffer (c + 1) & 1 is free
-      // issue order fills, warm-ups, stores (kept by the empty asm statements):
-      // copies_done counts on it
-      if (c + 1 < nch) fill(c + 1, (c + 1) & 1);
+      // issue order (kept by the empty asm statements; copies_done counts on
+      // it): the previous output (conditional, so before the counted
+      // operations), late fills, warm-ups, state stores, early fills
+      if (c > 0) store_o(c - 1);
       asm volatile("" ::: "memory");
-      warm(c + 2 < nch ? c + 2 : nch - 1);
+      fill_late(cl(c + 1), (c + 1) & 1);
+      asm volatile("" ::: "memory");
+      warm(cl(c + 2));
       asm volatile("" ::: "memory");
       // the chunk state leaves as whole 128-byte rows (BV fp32 of one d)
       float* hp = states + tile * DK * DV + v0;
@@ -705,12 +732,14 @@ __global__ __launch_bounds__(512) void k_scan_fwd_ws(Geo geo, int H, const bf16*
         const int idx = (thread_x() - 256) + t * 256, d = idx / (BV / 4), c4 = (idx - d * (BV / 4)) * 4;
         *reinterpret_cast<float4*>(hp + (long)d * DV + c4) = *reinterpret_cast<const float4*>(hF + d * LF + c4);
       }
-      if (c > 0) store_o(c - 1);
-      lds_barrier();  // B: hF and the previous output read
+      lds_barrier();  // B: hF read; the chain is done with this buffer's W, Q, U
+      asm volatile("" ::: "memory");
+      fill_early(cl(c + 2), c & 1);
       copies_done();  // the next chunk's operands are in LDS before barrier A
     }
     lds_barrier();
     if (nch > 0) store_o(nch - 1);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // no copy into LDS outlives the block
   }
   const int bad = __syncthreads_or(!ok);
   if (threadIdx.x == 0) flag[(long)s * NVT + vt] = bad;

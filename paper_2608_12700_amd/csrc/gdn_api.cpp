@@ -157,6 +157,53 @@ size_t exact_scratch_floats(const Shape& s) {
   return (size_t)kExactSlots * (kChunk + 2) * s.dk * s.dv;
 }
 
+void layout_cw_fwd(const Shape& s, char* base, CwFwdWs* w, size_t* total) {
+  Bump b{base};
+  const size_t tiles = (size_t)s.chunks * s.H;
+  w->chunk_off = b.take<int>(s.packed ? s.N + 1 : 0);
+  w->flag_scan = b.take<int>((size_t)s.N * s.H * (s.dv / SCAN_BV));
+  w->gC = b.take<float>(tiles * s.dk);
+  w->W = b.take<float>(tiles * kChunk * s.dk);
+  w->U = b.take<float>(tiles * kChunk * s.dv);
+  w->KhT = b.take<float>(tiles * kChunk * s.dk);
+  w->P = b.take<float>(tiles * kChunk * kChunk);
+  w->Qg = b.take<float>(tiles * kChunk * s.dk);
+  *total = b.off;
+}
+
+void layout_cw_bwd(const Shape& s, char* base, CwBwdWs* w, size_t* total) {
+  Bump b{base};
+  const size_t tiles = (size_t)s.chunks * s.H;
+  const size_t ck = tiles * kChunk * s.dk, cv = tiles * kChunk * s.dv, cc = tiles * kChunk * kChunk;
+  w->chunk_off = b.take<int>(s.packed ? s.N + 1 : 0);
+  w->flag_scan = b.take<int>((size_t)s.N * s.H * (s.dv / SCAN_BV));
+  w->gC = b.take<float>(tiles * s.dk);
+  w->WT = b.take<float>(ck);
+  w->QgT = b.take<float>(ck);
+  w->dOT = b.take<float>(cv);
+  w->PT = b.take<float>(cc);
+  w->T = b.take<float>(cc);
+  w->Kh = b.take<float>(ck);
+  w->KbG = b.take<float>(ck);
+  w->dh = b.take<float>(tiles * (size_t)s.dk * s.dv);
+  w->dUT = b.take<float>(cv);
+  w->dP = b.take<float>(cc);
+  w->dA = b.take<float>(cc);
+  w->X = b.take<float>(ck);
+  w->dQg = b.take<float>(ck);
+  w->dKh = b.take<float>(ck);
+  w->hdh = b.take<float>(tiles * s.dk);
+  *total = b.off;
+}
+
+// The channel-wise entry points take fp32 activations only; the problem's
+// variant is not read (the gate pointers select the member).
+gdn_status check_cw_problem(const gdn_problem* p, Shape* s) {
+  const gdn_status st = check_problem(p, s);
+  if (st != GDN_OK) return st;
+  return p->io_dtype == GDN_F32 ? GDN_OK : GDN_ERR_UNSUPPORTED;
+}
+
 Geo make_geo(const Shape& s, const gdn_problem* p, const int* chunk_off) {
   Geo g;
   g.B = (int)s.B; g.T = (int)s.T; g.H = (int)s.H; g.N = (int)s.N;
@@ -330,6 +377,135 @@ gdn_status gdn_bwd_ex(const gdn_problem* p, const void* q, const void* k, const 
       default: e = bf ? launch_bwd_var<DT_BF16, VAR_DECAY>(a) : launch_bwd_var<DT_F32, VAR_DECAY>(a); break;
     }
     return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+  } catch (...) {
+    return GDN_ERR_HIP;
+  }
+}
+
+size_t gdn_cw_fwd_workspace_size(const gdn_problem* p) {
+  Shape s;
+  if (check_cw_problem(p, &s) != GDN_OK) return 0;
+  CwFwdWs w;
+  size_t total = 0;
+  layout_cw_fwd(s, nullptr, &w, &total);
+  return total;
+}
+
+size_t gdn_cw_bwd_workspace_size(const gdn_problem* p) {
+  Shape s;
+  if (check_cw_problem(p, &s) != GDN_OK) return 0;
+  CwBwdWs w;
+  size_t total = 0;
+  layout_cw_bwd(s, nullptr, &w, &total);
+  return total;
+}
+
+gdn_status gdn_cw_fwd(const gdn_problem* p, const float* q, const float* k, const float* v, const float* g,
+                      const float* b, const float* w, const float* S0, float* o, float* S_T,
+                      float* chunk_states, void* workspace, size_t workspace_bytes, void* stream) {
+  return gdn_cw_fwd_ex(p, q, k, v, g, b, w, S0, o, S_T, chunk_states, workspace, workspace_bytes, stream,
+                       nullptr);
+}
+
+gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const float* q, const float* k, const float* v,
+                         const float* g, const float* b, const float* w, const float* S0, float* o,
+                         float* S_T, float* chunk_states, void* workspace, size_t workspace_bytes,
+                         void* stream, void* const* events) {
+  try {
+    Shape s;
+    gdn_status st = check_cw_problem(p, &s);
+    if (st != GDN_OK) return st;
+    const size_t tok = (size_t)s.B * s.T * s.H;
+    const size_t qk_b = tok * s.dk * 4, v_b = tok * s.dv * 4;
+    const size_t state_b = (size_t)s.N * s.H * s.dk * s.dv * sizeof(float);
+    const size_t states_b = (size_t)s.chunks * s.H * s.dk * s.dv * sizeof(float);
+    if (!need(q, qk_b) || !need(k, qk_b) || !need(v, v_b) || !need(o, v_b) || !need(S_T, state_b) ||
+        !need(chunk_states, states_b))
+      return GDN_ERR_NULL;
+    size_t ws_need = 0;
+    CwFwdWs ws;
+    layout_cw_fwd(s, nullptr, &ws, &ws_need);
+    if (!workspace || workspace_bytes < ws_need || ((uintptr_t)workspace & (kAlign - 1)))
+      return GDN_ERR_WORKSPACE;
+    const Region in[] = {{q, qk_b}, {k, qk_b}, {v, v_b}, {g, g ? qk_b : 0}, {b, b ? qk_b : 0},
+                         {w, w ? v_b : 0}, {S0, S0 ? state_b : 0},
+                         {s.packed ? p->cu_seqlens_dev : nullptr, s.packed ? (size_t)(s.N + 1) * 4 : 0}};
+    const Region out[] = {{o, v_b}, {S_T, state_b}, {chunk_states, states_b}, {workspace, ws_need}};
+    st = check_alias(in, 8, out, 4);
+    if (st != GDN_OK) return st;
+
+    layout_cw_fwd(s, static_cast<char*>(workspace), &ws, &ws_need);
+    CwFwdArgs a;
+    a.geo = make_geo(s, p, ws.chunk_off);
+    a.dk = (int)s.dk; a.dv = (int)s.dv;
+    a.q = q; a.k = k; a.v = v; a.g = g; a.b = b; a.w = w; a.S0 = S0;
+    a.o = o; a.ST = S_T; a.states = chunk_states; a.ws = ws;
+    a.stream = static_cast<hipStream_t>(stream);
+    a.events = reinterpret_cast<hipEvent_t const*>(events);
+    if (s.N * s.H == 0) {
+      for (int i = 0; i <= NUM_STAGES; ++i) stage_mark(a.events, i, a.stream);
+      return GDN_OK;
+    }
+    return launch_cw_fwd(a) == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+  } catch (...) {
+    return GDN_ERR_HIP;
+  }
+}
+
+gdn_status gdn_cw_bwd(const gdn_problem* p, const float* q, const float* k, const float* v, const float* g,
+                      const float* b, const float* w, const float* chunk_states, const float* dO,
+                      const float* dS_T, float* dq, float* dk, float* dv, float* dg, float* db, float* dw,
+                      float* dS0, void* workspace, size_t workspace_bytes, void* stream) {
+  return gdn_cw_bwd_ex(p, q, k, v, g, b, w, chunk_states, dO, dS_T, dq, dk, dv, dg, db, dw, dS0, workspace,
+                       workspace_bytes, stream, nullptr);
+}
+
+gdn_status gdn_cw_bwd_ex(const gdn_problem* p, const float* q, const float* k, const float* v,
+                         const float* g, const float* b, const float* w, const float* chunk_states,
+                         const float* dO, const float* dS_T, float* dq, float* dk, float* dv, float* dg,
+                         float* db, float* dw, float* dS0, void* workspace, size_t workspace_bytes,
+                         void* stream, void* const* events) {
+  try {
+    Shape s;
+    gdn_status st = check_cw_problem(p, &s);
+    if (st != GDN_OK) return st;
+    const size_t tok = (size_t)s.B * s.T * s.H;
+    const size_t qk_b = tok * s.dk * 4, v_b = tok * s.dv * 4;
+    const size_t state_b = (size_t)s.N * s.H * s.dk * s.dv * sizeof(float);
+    const size_t states_b = (size_t)s.chunks * s.H * s.dk * s.dv * sizeof(float);
+    // a gradient is written exactly for the gates that are given
+    if ((g == nullptr) != (dg == nullptr) || (b == nullptr) != (db == nullptr) || (w == nullptr) != (dw == nullptr))
+      return GDN_ERR_VARIANT;
+    if (!need(q, qk_b) || !need(k, qk_b) || !need(v, v_b) || !need(dO, v_b) ||
+        !need(chunk_states, states_b) || !need(dq, qk_b) || !need(dk, qk_b) || !need(dv, v_b) ||
+        !need(dS0, state_b))
+      return GDN_ERR_NULL;
+    size_t ws_need = 0;
+    CwBwdWs ws;
+    layout_cw_bwd(s, nullptr, &ws, &ws_need);
+    if (!workspace || workspace_bytes < ws_need || ((uintptr_t)workspace & (kAlign - 1)))
+      return GDN_ERR_WORKSPACE;
+    const Region in[] = {{q, qk_b}, {k, qk_b}, {v, v_b}, {g, g ? qk_b : 0}, {b, b ? qk_b : 0},
+                         {w, w ? v_b : 0}, {chunk_states, states_b}, {dO, v_b}, {dS_T, dS_T ? state_b : 0},
+                         {s.packed ? p->cu_seqlens_dev : nullptr, s.packed ? (size_t)(s.N + 1) * 4 : 0}};
+    const Region out[] = {{dq, qk_b}, {dk, qk_b}, {dv, v_b}, {dg, dg ? qk_b : 0}, {db, db ? qk_b : 0},
+                          {dw, dw ? v_b : 0}, {dS0, state_b}, {workspace, ws_need}};
+    st = check_alias(in, 10, out, 8);
+    if (st != GDN_OK) return st;
+
+    layout_cw_bwd(s, static_cast<char*>(workspace), &ws, &ws_need);
+    CwBwdArgs a;
+    a.geo = make_geo(s, p, ws.chunk_off);
+    a.dk = (int)s.dk; a.dv = (int)s.dv;
+    a.q = q; a.k = k; a.v = v; a.g = g; a.b = b; a.w = w; a.states = chunk_states; a.dO = dO; a.dST = dS_T;
+    a.dq = dq; a.dk_ = dk; a.dv_ = dv; a.dg = dg; a.db = db; a.dw = dw; a.dS0 = dS0; a.ws = ws;
+    a.stream = static_cast<hipStream_t>(stream);
+    a.events = reinterpret_cast<hipEvent_t const*>(events);
+    if (s.N * s.H == 0) {
+      for (int i = 0; i <= NUM_STAGES; ++i) stage_mark(a.events, i, a.stream);
+      return GDN_OK;
+    }
+    return launch_cw_bwd(a) == hipSuccess ? GDN_OK : GDN_ERR_HIP;
   } catch (...) {
     return GDN_ERR_HIP;
   }

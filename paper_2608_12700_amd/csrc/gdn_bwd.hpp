@@ -271,7 +271,9 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
 // into registers while chunk c is processed:
 //   dU' = P^T dO + diag(e^{G_last - G}) K dh
 //   dh <- e^{G_last} dh + (diag(e^G) Q)^T dO - W^T dU'
-template <int DK, int DV, int BV, typename OP, int VAR>
+// CWD (channel-wise decay): dh decays row by row, dh[d, :] *= e^{G_last[d]}, with
+// gcum holding each chunk's d_k values of G_last.
+template <int DK, int DV, int BV, typename OP, int VAR, bool CWD = false>
 __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __restrict__ Khg,
                                                   const float* __restrict__ dST, const float* __restrict__ gcum,
                                                   const OP* __restrict__ WTg, const OP* __restrict__ QgTg,
@@ -301,6 +303,7 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
     typename HT::template BFr<OP, CH> dob;
     typename UT::template AFr<OP, CH> pt;
     float gl;  // G_last, exponentiated at use so the prefetch never waits
+    float gd[CWD ? HT::TM : 1][4];  // CWD: G_last of this lane's rows of dh
   };
   auto load_pre = [&](Pre& p, int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
@@ -309,7 +312,14 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
       load_op_frags_b<HT, OP, CH>(p.dob, dOTg + tile * DV * CH + op_off<OP, CH>(v0, 0));
     else
       p.dob.load(KRow<OP, CH>{dOTg + tile * DV * CH + (long)v0 * CH});
-    p.gl = gcum[tile * CH + CH - 1 + opaque_zero()];  // vector load: see opaque_zero
+    if constexpr (CWD) {
+#pragma unroll
+      for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p.gd[a][j] = gcum[tile * DK + HT::m0(a) + (l >> 4) * 4 + j];
+    } else {
+      p.gl = gcum[tile * CH + CH - 1 + opaque_zero()];  // vector load: see opaque_zero
+    }
     load_op_frags<UT, OP, DK>(p.kf, Khg + tile * CH * DK);
     if constexpr (DT_) load_op_frags<HT, OP, CH>(p.wt, WTg + tile * DK * CH);
     load_op_frags<UT, OP, CH>(p.pt, PTg + tile * CH * CH);
@@ -393,13 +403,14 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
       }
       __syncthreads();
     }
-    const float gl = expf(cur.gl);
 #pragma unroll
     for (int a = 0; a < HT::TM; ++a)
 #pragma unroll
-      for (int b = 0; b < HT::TN; ++b)
+      for (int j = 0; j < 4; ++j) {
+        const float gd = CWD ? expf(cur.gd[a][CWD ? j : 0]) : expf(cur.gl);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) dh.acc[a][b][j] = gl * dh.acc[a][b][j] + inj.acc[a][b][j];
+        for (int b = 0; b < HT::TN; ++b) dh.acc[a][b][j] = gd * dh.acc[a][b][j] + inj.acc[a][b][j];
+      }
     if constexpr (DT_) dh.template mma<OP, CH>(cur.wt, KRow<OP, LU>{dUT});
   };
   const int nch = sp.nch;

@@ -1,0 +1,521 @@
+// Channel-wise members of the recurrence family on gfx950 (paper Sec. 4.1,
+// Eq. (gdn) with its gates per channel; table "One recurrence, five models":
+// full GDN, KDA, GLA and LA are gate settings of it):
+//
+//   S_t = (I - k_t (b_t * k_t)^T) Diag(e^{g_t}) S_{t-1} + k_t (w_t * v_t)^T,  o_t = S_t^T q_t
+//
+// with g_t, b_t in R^{d_k} and w_t in R^{d_v}; a NULL gate is neutral (g = 0,
+// b = 0, w = 1).  fp32 operands throughout (fp32 matrix cores).
+//
+// Chunked form (Sec. 4.2), per chunk of 64 tokens with G_r = sum_{s<=r} g_s (a
+// d_k-vector per row), Gamma = e^G, Kb = b * K, Khat_r = e^{G_last - G_r} * k_r:
+//   A_ri = sum_d Kb_rd K_id e^{G_rd - G_id}  (i < r),   T = (I + A)^{-1}
+//   P_ri = sum_d Q_rd  K_id e^{G_rd - G_id}  (i <= r)
+//   W = T (Gamma * Kb),   U = T (w * V),   U' = U - W h
+//   O = (Gamma * Q) h + P U',   h <- Diag(e^{G_last}) h + Khat^T U'
+// The carry and the output reuse the generic scans with a per-row decay.
+//
+// Decay-weighted contractions.  Every product above and in the backward
+// that carries e^{G_r - G_i} inside its sum over channels is split by 16-row
+// blocks.  Pairs (r, i) in different blocks go to the matrix cores with the
+// exponent split at a reference row between them: for output rows in block R
+// the row just before the block (the chunk's entry, G = 0, for R = 0), so both
+// e^{G_r - G_ref} and e^{G_ref - G_i} are <= 1 for a decay (g <= 0) and nothing
+// can overflow; the operand is zeroed (before the exponential) outside those
+// blocks.  Contractions down the columns (the transposed gradients) use the
+// last row of the block instead.  Pairs inside one block are summed exactly
+// on the vector ALUs with e^{G_r - G_i} formed per term.
+#pragma once
+
+#include "gdn_bwd.hpp"
+#include "gdn_fwd.hpp"
+
+namespace gdn {
+
+// G (cumulative log-decay per channel) in place down each column of a 64 x D
+// LDS tile with row stride LD: one wave per column, rows on lanes.
+template <int D, int LD>
+__device__ __forceinline__ void cw_cumsum_columns(float* Gs) {
+  const int nw = (int)blockDim.x / WAVE, l = lane_id();
+  for (int d = wave_id(); d < D; d += nw) Gs[l * LD + d] = wave_incl_scan(Gs[l * LD + d]);
+}
+
+// The reference log-decay of 16-row block R (row 16R - 1; 0 for R = 0).
+template <int LD>
+__device__ __forceinline__ float cw_ref(const float* Gs, int R, int d) {
+  return R > 0 ? Gs[(16 * R - 1) * LD + d] : 0.f;
+}
+
+// One block per (chunk, head).  Forward mode writes the operands of the
+// generic forward scan (P, diag-scaled Q, Khat^T, W, U); backward mode writes
+// those of the reverse scan and the gradient kernels (P^T, (Gamma Q)^T,
+// Khat, W^T, T, Gamma * Kb, dO^T).  Both write G_last per channel.
+template <int DK, int DV, bool BWD>
+__global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __restrict__ q,
+                                                 const float* __restrict__ k, const float* __restrict__ v,
+                                                 const float* __restrict__ g, const float* __restrict__ b,
+                                                 const float* __restrict__ w, const float* __restrict__ dO,
+                                                 float* __restrict__ gC, float* __restrict__ Pg,
+                                                 float* __restrict__ Qgg, float* __restrict__ Khg,
+                                                 float* __restrict__ Wg, float* __restrict__ Ug,
+                                                 float* __restrict__ Tg, float* __restrict__ KbGg,
+                                                 float* __restrict__ dOTg) {
+  constexpr int LK = DK + 4, LC = CH + 4, VS = 64, LV = VS + 4;
+  static_assert(CH * LC <= CH * LK && CH * LV <= CH * LK, "T and the w * V slices reuse Q's and K's tiles");
+  __shared__ __align__(16) float Qs[CH * LK];  // Q, then T (stride LC)
+  __shared__ __align__(16) float Ks[CH * LK];  // K, then slices of w * V (stride LV)
+  __shared__ __align__(16) float Gs[CH * LK];  // G
+  __shared__ __align__(16) float Bk[CH * LK];  // b * K, then Gamma * b * K
+  __shared__ __align__(16) float As[CH * LC];  // A
+  float* Tf = Qs;
+  float* Vw = Ks;
+
+  const int ci = blockIdx.x, h = blockIdx.y;
+  const ChunkPos cp = chunk_pos(geo, ci);
+  const long tile = (long)ci * H + h;
+  const long rsk = (long)H * DK, bk = (cp.row0 * H + h) * DK;
+  const long rsv = (long)H * DV, bv = (cp.row0 * H + h) * DV;
+  load_rows<DK, LK>(q + bk, rsk, cp.len, Qs);
+  load_rows<DK, LK>(k + bk, rsk, cp.len, Ks);
+  if (g) load_rows<DK, LK>(g + bk, rsk, cp.len, Gs);
+  else
+    for (int i = thread_x(); i < CH * LK; i += blockDim.x) Gs[i] = 0.f;
+  if (b) load_rows<DK, LK>(b + bk, rsk, cp.len, Bk);
+  __syncthreads();
+  if (g) cw_cumsum_columns<DK, LK>(Gs);
+  if (b)
+    for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
+      const int r = i / DK, d = i - r * DK;
+      Bk[r * LK + d] *= Ks[r * LK + d];
+    }
+  __syncthreads();
+
+  // P and A: wave (R, ·) of Tiles<64, 64, 4, 2> owns 16-row block R
+  const int R = wave_id() / 2;
+  auto ref = [&](int d) { return cw_ref<LK>(Gs, R, d); };
+  auto kcol = kfun<float>([&](int i, int d) {
+    return i < 16 * R ? Ks[i * LK + d] * __expf(ref(d) - Gs[i * LK + d]) : 0.f;
+  });
+  // the diagonal 16 x 16 tile of row block R, summed exactly: the rows of X
+  // against the rows of K (i <= r, or i < r when strict)
+  auto diag = [&](Tiles<CH, CH, 4, 2>& t, const float* X, bool strict) {
+    const int l = lane_id();
+#pragma unroll
+    for (int bb = 0; bb < t.TN; ++bb) {
+      if (t.n0(bb) != 16 * R) continue;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = t.m0(0) + (l >> 4) * 4 + j, i = t.n0(bb) + (l & 15);
+        float sum = 0.f;
+        if (strict ? i < r : i <= r)
+          for (int d = 0; d < DK; ++d)
+            sum += X[r * LK + d] * Ks[i * LK + d] * __expf(Gs[r * LK + d] - Gs[i * LK + d]);
+        t.acc[0][bb][j] += sum;
+      }
+    }
+  };
+  {
+    Tiles<CH, CH, 4, 2> p;
+    p.zero();
+    p.template mma<float, DK>(kfun<float>([&](int r, int d) { return Qs[r * LK + d] * __expf(Gs[r * LK + d] - ref(d)); }),
+                              kcol);
+    diag(p, Qs, false);
+    float* Pt = Pg + tile * CH * CH;
+    p.each([&](int r, int i, float& x) {
+      const float val = i <= r ? x : 0.f;
+      if (BWD) Pt[i * CH + r] = val;
+      else Pt[r * CH + i] = val;
+    });
+  }
+  if (b) {
+    Tiles<CH, CH, 4, 2> a;
+    a.zero();
+    a.template mma<float, DK>(kfun<float>([&](int r, int d) { return Bk[r * LK + d] * __expf(Gs[r * LK + d] - ref(d)); }),
+                              kcol);
+    diag(a, Bk, true);
+    a.each([&](int r, int i, float& x) { As[r * LC + i] = i < r ? x : 0.f; });
+  }
+  // Gamma * Q and Khat = e^{G_last - G} * K, each in the layout its scan reads
+  {
+    float* Qt = Qgg + tile * CH * DK;
+    float* Kt = Khg + tile * CH * DK;
+    for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
+      // row-major [r][d] outputs walk d fastest, transposed [d][r] ones r fastest
+      const int r1 = i / DK, d1 = i - r1 * DK, d2 = i / CH, r2 = i - d2 * CH;
+      const float G1 = Gs[r1 * LK + d1], G2 = Gs[r2 * LK + d2];
+      if (BWD) {
+        Qt[d2 * CH + r2] = __expf(G2) * Qs[r2 * LK + d2];
+        Kt[r1 * DK + d1] = __expf(Gs[(CH - 1) * LK + d1] - G1) * Ks[r1 * LK + d1];
+      } else {
+        Qt[r1 * DK + d1] = __expf(G1) * Qs[r1 * LK + d1];
+        Kt[d2 * CH + r2] = __expf(Gs[(CH - 1) * LK + d2] - G2) * Ks[r2 * LK + d2];
+      }
+    }
+    for (int d = thread_x(); d < DK; d += blockDim.x) gC[tile * DK + d] = Gs[(CH - 1) * LK + d];
+  }
+  __syncthreads();  // Q is dead: T takes its tile
+  if (b) {
+    unit_lower_inverse<float, LC, LC, false>(As, Tf, (float*)nullptr, (float*)nullptr);
+  } else {
+    for (int i = thread_x(); i < CH * CH; i += blockDim.x) {
+      const int r = i / CH, c = i - r * CH;
+      Tf[r * LC + c] = r == c ? 1.f : 0.f;
+    }
+    __syncthreads();
+  }
+  // Gamma * Kb (A has been formed from b * K above)
+  if (b)
+    for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
+      const int r = i / DK, d = i - r * DK;
+      Bk[r * LK + d] *= __expf(Gs[r * LK + d]);
+    }
+  if (BWD) {
+    float* Tt = Tg + tile * CH * CH;
+    for (int i = thread_x(); i < CH * CH; i += blockDim.x) Tt[i] = Tf[(i / CH) * LC + (i % CH)];
+    float* Kb = KbGg + tile * CH * DK;
+    for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
+      const int r = i / DK, d = i - r * DK;
+      Kb[i] = b ? Bk[r * LK + d] : 0.f;
+    }
+    // dO^T [v][r]
+    float* Dt = dOTg + tile * DV * CH;
+    for (int i = thread_x(); i < DV * CH; i += blockDim.x) {
+      const int vv = i / CH, r = i - vv * CH;
+      const float x = dO[bv + (long)clamp_row(r, cp.len) * rsv + vv];
+      Dt[i] = r < cp.len ? x : 0.f;
+    }
+  }
+  __syncthreads();
+  // W = T (Gamma * Kb)
+  {
+    float* Wt = Wg + tile * CH * DK;
+    if (b) {
+      Tiles<CH, DK, 4, 2> wt;
+      wt.zero();
+      wt.template mma<float, CH>(KRow<float, LC>{Tf}, KCol<float, LK>{Bk});
+      wt.each([&](int r, int d, float& x) {
+        if (BWD) Wt[d * CH + r] = x;
+        else Wt[r * DK + d] = x;
+      });
+    } else {
+      for (int i = thread_x(); i < CH * DK; i += blockDim.x) Wt[i] = 0.f;
+    }
+  }
+  // U = T (w * V) in the forward scan's accumulator-tile layout
+  if (!BWD) {
+    float* Ut = Ug + tile * CH * DV;
+    for (int c0 = 0; c0 < DV; c0 += VS) {
+      __syncthreads();  // K (first pass) or the previous slice is no longer read
+      for (int i = thread_x(); i < CH * VS; i += blockDim.x) {
+        const int r = i / VS, c = i - r * VS;
+        const long o = bv + (long)clamp_row(r, cp.len) * rsv + c0 + c;
+        const float x = v[o] * (w ? w[o] : 1.f);
+        Vw[r * LV + c] = r < cp.len ? x : 0.f;
+      }
+      __syncthreads();
+      Tiles<CH, VS, 4, 2> uu;
+      uu.zero();
+      uu.template mma<float, CH>(KRow<float, LC>{Tf}, KCol<float, LV>{Vw});
+      const int l = lane_id();
+#pragma unroll
+      for (int bb = 0; bb < uu.TN; ++bb) {
+        const int r0 = uu.m0(0) + (l >> 4) * 4, vcol = c0 + uu.n0(bb) + (l & 15);
+        const float u4[4] = {uu.acc[0][bb][0], uu.acc[0][bb][1], uu.acc[0][bb][2], uu.acc[0][bb][3]};
+        *reinterpret_cast<uint4*>(Ut + cfrag_off<SCAN_BV>(r0, vcol)) = pack4<float>(u4);
+      }
+    }
+  }
+}
+
+// Gradient kernel, value part: one block per (chunk, head), value slices of 32
+// columns.  With h the chunk's entry state, dh the state gradient after it and
+// dU' from the reverse scan:
+//   R = w * V - (Gamma * Kb) h,  U' = T R,  Y = T^T dU'  ->  dv = w * Y, dw = v * Y
+// and, summed over the slices,
+//   dP = dO U'^T (i <= r),  dA = -Y U'^T (i < r: the solve's VJP in its short
+//   form, -T^T (dU' R^T) T^T = -Y U'^T),  X = -Y h^T,  dQg = dO h^T,
+//   dKhat = U' dh^T,  <h, dh> per row d.
+template <int DK, int DV>
+__global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* __restrict__ v,
+                                                   const float* __restrict__ w, const float* __restrict__ dO,
+                                                   const float* __restrict__ states, const float* __restrict__ Tg,
+                                                   const float* __restrict__ KbGg, const float* __restrict__ dhg,
+                                                   const float* __restrict__ dUTg, float* __restrict__ dvo,
+                                                   float* __restrict__ dwo, float* __restrict__ dPg,
+                                                   float* __restrict__ dAg, float* __restrict__ Xg,
+                                                   float* __restrict__ dQgg, float* __restrict__ dKhg,
+                                                   float* __restrict__ hdhg) {
+  constexpr int LK = DK + 4, LC = CH + 4, VS = 32, LV = VS + 4;
+  __shared__ __align__(16) float Ts[CH * LC];
+  __shared__ __align__(16) float KbG[CH * LK];
+  __shared__ __align__(16) float Vs[CH * LV], Ws[CH * LV], dOs[CH * LV], Rs[CH * LV], Ups[CH * LV], Ys[CH * LV];
+  __shared__ __align__(16) float dUT[VS * LC];
+  __shared__ __align__(16) float hs[DK * LV], dhs[DK * LV];
+
+  const int ci = blockIdx.x, h = blockIdx.y;
+  const ChunkPos cp = chunk_pos(geo, ci);
+  const long tile = (long)ci * H + h;
+  const long rsv = (long)H * DV, bv = (cp.row0 * H + h) * DV;
+  load_dense<CH, CH, LC>(Tg + tile * CH * CH, Ts);
+  load_dense<CH, DK, LK>(KbGg + tile * CH * DK, KbG);
+  Tiles<CH, CH, 4, 2> dP, dA;
+  Tiles<CH, DK, 4, 2> X, dQg, dKh;
+  dP.zero(); dA.zero(); X.zero(); dQg.zero(); dKh.zero();
+  float hdh = 0.f;  // thread d < DK: sum over v of h[d][v] dh[d][v]
+  const float* hp = states + tile * DK * DV;
+  const float* dhp = dhg + tile * DK * DV;
+  const float* dUp = dUTg + tile * DV * CH;
+  for (int c0 = 0; c0 < DV; c0 += VS) {
+    load_rows<VS, LV>(v + bv + c0, rsv, cp.len, Vs);
+    if (w) load_rows<VS, LV>(w + bv + c0, rsv, cp.len, Ws);
+    load_rows<VS, LV>(dO + bv + c0, rsv, cp.len, dOs);
+    for (int i = thread_x(); i < DK * VS / 4; i += blockDim.x) {
+      const int d = i / (VS / 4), c = (i - d * (VS / 4)) * 4;
+      *reinterpret_cast<float4*>(hs + d * LV + c) = *reinterpret_cast<const float4*>(hp + (long)d * DV + c0 + c);
+      *reinterpret_cast<float4*>(dhs + d * LV + c) = *reinterpret_cast<const float4*>(dhp + (long)d * DV + c0 + c);
+    }
+    for (int i = thread_x(); i < VS * CH / 4; i += blockDim.x) {
+      const int vv = i / (CH / 4), r = (i - vv * (CH / 4)) * 4;
+      *reinterpret_cast<float4*>(dUT + vv * LC + r) = *reinterpret_cast<const float4*>(dUp + (long)(c0 + vv) * CH + r);
+    }
+    __syncthreads();
+    if (thread_x() < DK) {
+      const int d = thread_x();
+#pragma unroll 8
+      for (int c = 0; c < VS; ++c) hdh += hs[d * LV + c] * dhs[d * LV + c];
+    }
+    {
+      Tiles<CH, VS, 4, 2> rr;
+      rr.zero();
+      rr.template mma<float, DK>(KRow<float, LK>{KbG}, KCol<float, LV>{hs});
+      rr.each([&](int r, int vv, float& x) {
+        const float wv = w ? Ws[r * LV + vv] : 1.f;
+        Rs[r * LV + vv] = wv * Vs[r * LV + vv] - x;
+      });
+    }
+    {
+      Tiles<CH, VS, 4, 2> y;
+      y.zero();
+      y.template mma<float, CH>(KCol<float, LC>{Ts}, KRow<float, LC>{dUT});
+      y.each([&](int r, int vv, float& x) {
+        Ys[r * LV + vv] = x;
+        if (r < cp.len) {
+          const long o = bv + (long)r * rsv + c0 + vv;
+          dvo[o] = (w ? Ws[r * LV + vv] : 1.f) * x;
+          if (w) dwo[o] = Vs[r * LV + vv] * x;
+        }
+      });
+    }
+    __syncthreads();
+    {
+      Tiles<CH, VS, 4, 2> up;
+      up.zero();
+      up.template mma<float, CH>(KRow<float, LC>{Ts}, KCol<float, LV>{Rs});
+      up.each([&](int r, int vv, float& x) { Ups[r * LV + vv] = x; });
+    }
+    __syncthreads();
+    dP.template mma<float, VS>(KRow<float, LV>{dOs}, KRow<float, LV>{Ups});
+    dA.template mma<float, VS>(KRow<float, LV>{Ys}, KRow<float, LV>{Ups});
+    X.template mma<float, VS>(KRow<float, LV>{Ys}, KRow<float, LV>{hs});
+    dQg.template mma<float, VS>(KRow<float, LV>{dOs}, KRow<float, LV>{hs});
+    dKh.template mma<float, VS>(KRow<float, LV>{Ups}, KRow<float, LV>{dhs});
+    __syncthreads();
+  }
+  float* dPt = dPg + tile * CH * CH;
+  float* dAt = dAg + tile * CH * CH;
+  dP.each([&](int r, int i, float& x) { dPt[r * CH + i] = i <= r ? x : 0.f; });
+  dA.each([&](int r, int i, float& x) { dAt[r * CH + i] = i < r ? -x : 0.f; });
+  float* Xt = Xg + tile * CH * DK;
+  float* Qt = dQgg + tile * CH * DK;
+  float* Kt = dKhg + tile * CH * DK;
+  X.each([&](int r, int d, float& x) { Xt[r * DK + d] = -x; });
+  dQg.each([&](int r, int d, float& x) { Qt[r * DK + d] = x; });
+  dKh.each([&](int r, int d, float& x) { Kt[r * DK + d] = x; });
+  if (thread_x() < DK) hdhg[tile * DK + thread_x()] = hdh;
+}
+
+// Gradient kernel, channel part: one block per (chunk, head, 32 channels).
+// The four decay-weighted contractions (split by blocks as in the header):
+//   dQ^P_rd  = sum_{i<=r} dP_ri K_id  e^{G_rd - G_id}     dK^P_id = sum_{r>=i} dP_ri Q_rd  e^{G_rd - G_id}
+//   dKb^A_rd = sum_{i<r}  dA_ri K_id  e^{G_rd - G_id}     dK^A_id = sum_{r>i}  dA_ri Kb_rd e^{G_rd - G_id}
+// then dKb = Gamma * X + dKb^A, db = K * dKb, dq = Gamma * dQg + dQ^P,
+// dk = e^{G_last - G} * dKhat + dK^P + dK^A + b * dKb, and
+//   dG = Gamma Q dQg + Q dQ^P - K dK^P + Kb dKb^A - K dK^A + Gamma Kb X - Khat dKhat
+// (elementwise), with e^{G_last} <h, dh>_d + sum_r Khat_rd dKhat_rd added on the
+// last row; dg is its reverse cumulative sum down each channel (one wave per
+// channel, fixed order).
+template <int DK>
+__global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* __restrict__ q,
+                                                   const float* __restrict__ k, const float* __restrict__ g,
+                                                   const float* __restrict__ b, const float* __restrict__ dPg,
+                                                   const float* __restrict__ dAg, const float* __restrict__ Xg,
+                                                   const float* __restrict__ dQgg, const float* __restrict__ dKhg,
+                                                   const float* __restrict__ hdhg, float* __restrict__ dq,
+                                                   float* __restrict__ dk, float* __restrict__ dg,
+                                                   float* __restrict__ db) {
+  constexpr int DS = 32, LS = DS + 4, LC = CH + 4;
+  __shared__ __align__(16) float dPs[CH * LC], dAs[CH * LC];
+  __shared__ __align__(16) float Qs[CH * LS], Ks[CH * LS], Bs[CH * LS], Gs[CH * LS], dGs[CH * LS], Zs[CH * LS];
+  const int ci = blockIdx.x, h = blockIdx.y, d0 = blockIdx.z * DS;
+  const ChunkPos cp = chunk_pos(geo, ci);
+  const long tile = (long)ci * H + h;
+  const long rsk = (long)H * DK, bk = (cp.row0 * H + h) * DK + d0;
+  load_rows<DS, LS>(q + bk, rsk, cp.len, Qs);
+  load_rows<DS, LS>(k + bk, rsk, cp.len, Ks);
+  if (g) load_rows<DS, LS>(g + bk, rsk, cp.len, Gs);
+  else
+    for (int i = thread_x(); i < CH * LS; i += blockDim.x) Gs[i] = 0.f;
+  if (b) load_rows<DS, LS>(b + bk, rsk, cp.len, Bs);
+  else
+    for (int i = thread_x(); i < CH * LS; i += blockDim.x) Bs[i] = 0.f;
+  load_dense<CH, CH, LC>(dPg + tile * CH * CH, dPs);
+  load_dense<CH, CH, LC>(dAg + tile * CH * CH, dAs);
+  __syncthreads();
+  if (g) {
+    cw_cumsum_columns<DS, LS>(Gs);
+    __syncthreads();
+  }
+
+  typedef Tiles<CH, DS, 4, 2> TD;  // one 16 x 16 output tile per wave
+  static_assert(TD::TM == 1 && TD::TN == 1, "one tile per wave");
+  const int R = wave_id() / 2;     // the wave's 16-row block
+  auto ref = [&](int d) { return cw_ref<LS>(Gs, R, d); };
+  auto last = [&](int d) { return Gs[(16 * R + 15) * LS + d]; };
+  // K rows of earlier blocks, scaled to the reference before block R
+  auto kdown = kfun<float>([&](int d, int i) {
+    return i < 16 * R ? Ks[i * LS + d] * __expf(ref(d) - Gs[i * LS + d]) : 0.f;
+  });
+  TD aP, aA, bP, bA;
+  aP.zero(); aA.zero(); bP.zero(); bA.zero();
+  aP.template mma<float, CH>(KRow<float, LC>{dPs}, kdown);
+  bP.template mma<float, CH>(KCol<float, LC>{dPs}, kfun<float>([&](int d, int r) {
+    return r >= 16 * (R + 1) ? Qs[r * LS + d] * __expf(Gs[r * LS + d] - last(d)) : 0.f;
+  }));
+  if (b) {
+    aA.template mma<float, CH>(KRow<float, LC>{dAs}, kdown);
+    bA.template mma<float, CH>(KCol<float, LC>{dAs}, kfun<float>([&](int d, int r) {
+      return r >= 16 * (R + 1) ? Bs[r * LS + d] * Ks[r * LS + d] * __expf(Gs[r * LS + d] - last(d)) : 0.f;
+    }));
+  }
+  // the pairs inside block R, exactly: row sums over i in [16R, r] (a) and
+  // column sums over r in [i, 16R + 15] (b), e^{G_r - G_i} per term
+  auto diag_a = [&](const float* M, const float* Y, int r, int dl, bool strict) {
+    float sum = 0.f;
+    const int hi = strict ? r - 1 : r;
+    for (int i = 16 * R; i <= hi; ++i)
+      sum += M[r * LC + i] * Y[i * LS + dl] * __expf(Gs[r * LS + dl] - Gs[i * LS + dl]);
+    return sum;
+  };
+  {
+    const int l = lane_id();
+    const float* Xt = Xg + tile * CH * DK + d0;
+    const float* Qgt = dQgg + tile * CH * DK + d0;
+    const float* Kht = dKhg + tile * CH * DK + d0;
+    const int dl = TD::n0(0) + (l & 15);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = TD::m0(0) + (l >> 4) * 4 + j;
+      const float G = Gs[r * LS + dl], GL = Gs[(CH - 1) * LS + dl];
+      const float gam = __expf(G), dte = __expf(GL - G);
+      const float qv = Qs[r * LS + dl], kv = Ks[r * LS + dl], bv = Bs[r * LS + dl], kb = bv * kv;
+      const float xv = Xt[r * DK + dl], dqg = Qgt[r * DK + dl], dkh = Kht[r * DK + dl];
+      float dkP = 0.f, dkA = 0.f;  // column sums inside the block (row r plays i)
+      for (int rr = r; rr <= 16 * R + 15; ++rr) {
+        const float e = __expf(Gs[rr * LS + dl] - G);
+        dkP += dPs[rr * LC + r] * Qs[rr * LS + dl] * e;
+        if (rr > r) dkA += dAs[rr * LC + r] * Bs[rr * LS + dl] * Ks[rr * LS + dl] * e;
+      }
+      const float dqP = aP.acc[0][0][j] * __expf(G - ref(dl)) + diag_a(dPs, Ks, r, dl, false);
+      dkP += bP.acc[0][0][j] * __expf(last(dl) - G);
+      const float dkbA = b ? aA.acc[0][0][j] * __expf(G - ref(dl)) + diag_a(dAs, Ks, r, dl, true) : 0.f;
+      dkA = b ? dkA + bA.acc[0][0][j] * __expf(last(dl) - G) : 0.f;
+      const float dkb = gam * xv + dkbA;
+      const float khdkh = dte * kv * dkh;
+      dGs[r * LS + dl] = gam * qv * dqg + qv * dqP - kv * dkP + kb * dkbA - kv * dkA + gam * kb * xv - khdkh;
+      Zs[r * LS + dl] = khdkh;
+      if (r < cp.len) {
+        const long o = bk + (long)r * rsk + dl;
+        dq[o] = gam * dqg + dqP;
+        dk[o] = dte * dkh + dkP + dkA + bv * dkb;
+        if (b) db[o] = kv * dkb;
+      }
+    }
+  }
+  if (g) {
+    __syncthreads();
+    const int r = lane_id(), nw = (int)blockDim.x / WAVE;
+    for (int dl = wave_id(); dl < DS; dl += nw) {
+      const float tot = wave_sum(Zs[r * LS + dl]);
+      float x = dGs[r * LS + dl];
+      if (r == CH - 1) x += __expf(Gs[(CH - 1) * LS + dl]) * hdhg[tile * DK + d0 + dl] + tot;
+      const float dgv = wave_reverse(wave_incl_scan(wave_reverse(x)));
+      if (r < cp.len) dg[bk + (long)r * rsk + dl] = dgv;
+    }
+  }
+}
+
+template <int DK, int DV>
+static hipError_t launch_cw_fwd_t(const CwFwdArgs& a) {
+  constexpr int BV = SCAN_BV, NVT = DV / BV;
+  const Geo& geo = a.geo;
+  const int H = geo.H;
+  const CwFwdWs& w = a.ws;
+  stage_mark(a.events, 0, a.stream);
+  if (geo.cu != nullptr) {
+    const hipError_t e = launch_chunk_offsets(geo.cu, geo.N, const_cast<int*>(geo.chunk_off), a.stream);
+    if (e != hipSuccess) return e;
+  }
+  if (geo.total_chunks > 0)
+    hipLaunchKernelGGL((k_cw_prep<DK, DV, false>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
+                       a.q, a.k, a.v, a.g, a.b, a.w, (const float*)nullptr, w.gC, w.P, w.Qg, w.KhT, w.W, w.U,
+                       (float*)nullptr, (float*)nullptr, (float*)nullptr);
+  stage_mark(a.events, 1, a.stream);
+  const int NS = geo.N * H;
+  if (NS > 0)
+    hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, float, VAR_GATED, true>), dim3(NS * NVT), dim3(256), 0, a.stream,
+                       geo, H, (const float*)w.Qg, a.v, a.S0, w.gC, (const float*)w.W, (const float*)w.KhT,
+                       (const float*)w.P, (const float*)w.U, a.states, a.ST, a.o, w.flag_scan);
+  stage_mark(a.events, 2, a.stream);
+  stage_mark(a.events, 3, a.stream);
+  stage_mark(a.events, 4, a.stream);
+  return hipGetLastError();
+}
+
+template <int DK, int DV>
+static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
+  constexpr int BV = SCAN_BV, NVT = DV / BV;
+  const Geo& geo = a.geo;
+  const int H = geo.H;
+  const CwBwdWs& w = a.ws;
+  stage_mark(a.events, 0, a.stream);
+  if (geo.cu != nullptr) {
+    const hipError_t e = launch_chunk_offsets(geo.cu, geo.N, const_cast<int*>(geo.chunk_off), a.stream);
+    if (e != hipSuccess) return e;
+  }
+  if (geo.total_chunks > 0)
+    hipLaunchKernelGGL((k_cw_prep<DK, DV, true>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
+                       a.q, a.k, a.v, a.g, a.b, a.w, a.dO, w.gC, w.PT, w.QgT, w.Kh, w.WT, (float*)nullptr, w.T,
+                       w.KbG, w.dOT);
+  stage_mark(a.events, 1, a.stream);
+  const int NS = geo.N * H;
+  if (NS > 0)
+    hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, float, VAR_GATED, true>), dim3(NS * NVT), dim3(256), 0, a.stream,
+                       geo, H, (const float*)w.Kh, a.dST, w.gC, (const float*)w.WT, (const float*)w.QgT,
+                       (const float*)w.dOT, (const float*)w.PT, w.dh, w.dUT, a.dS0, w.flag_scan);
+  stage_mark(a.events, 2, a.stream);
+  if (geo.total_chunks > 0) {
+    hipLaunchKernelGGL((k_cw_grad_v<DK, DV>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H, a.v, a.w,
+                       a.dO, a.states, (const float*)w.T, (const float*)w.KbG, (const float*)w.dh,
+                       (const float*)w.dUT, a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg, w.dKh, w.hdh);
+    stage_mark(a.events, 3, a.stream);
+    hipLaunchKernelGGL((k_cw_grad_d<DK>), dim3(geo.total_chunks, H, DK / 32), dim3(512), 0, a.stream, geo, H, a.q,
+                       a.k, a.g, a.b, (const float*)w.dP, (const float*)w.dA, (const float*)w.X,
+                       (const float*)w.dQg, (const float*)w.dKh, (const float*)w.hdh, a.dq, a.dk_, a.dg, a.db);
+  } else {
+    stage_mark(a.events, 3, a.stream);
+  }
+  stage_mark(a.events, 4, a.stream);
+  return hipGetLastError();
+}
+
+}  // namespace gdn

@@ -265,7 +265,10 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
 // straight from the input), so the A fragments of chunk c+1 load from HBM/L2
 // into registers while chunk c is computed; only h and U' pass through LDS
 // (two barriers per chunk).
-template <int DK, int DV, int BV, typename OP, int VAR>
+// CWD (channel-wise decay): the carry decays row by row, h[d, :] *= e^{G_last[d]},
+// with gcum holding each chunk's d_k values of G_last instead of the 64 in-chunk
+// values of a scalar G.
+template <int DK, int DV, int BV, typename OP, int VAR, bool CWD = false>
 __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __restrict__ Qgg,
                                                   const OP* __restrict__ v, const float* __restrict__ S0,
                                                   const float* __restrict__ gcum, const OP* __restrict__ Wg,
@@ -298,6 +301,7 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     typename HT::template AFr<OP, CH> kh;
     typename vec4_of<OP>::type u[UT::TN];  // U (or V): four rows of one column per lane
     float gl;  // G_last, exponentiated at use so the prefetch never waits
+    float gd[CWD ? HT::TM : 1][4];  // CWD: G_last of this lane's state rows
   };
   // A fragments of a pre-arranged operand (fragment-major for bf16, row-major for fp32)
   auto frags = [&](auto& f, const OP* base, auto tiles_tag, auto k_tag) {
@@ -342,7 +346,14 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     frags(p.qf, Qgg + tile * CH * DK, UT{}, std::integral_constant<int, DK>{});
     frags(p.pf, Pg + tile * CH * CH, UT{}, std::integral_constant<int, CH>{});
     frags(p.kh, KhTg + tile * DK * CH, HT{}, std::integral_constant<int, CH>{});
-    p.gl = gcum[tile * CH + CH - 1 + opaque_zero()];  // vector load: see opaque_zero
+    if constexpr (CWD) {
+#pragma unroll
+      for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p.gd[a][j] = gcum[tile * DK + HT::m0(a) + (l >> 4) * 4 + j];
+    } else {
+      p.gl = gcum[tile * CH + CH - 1 + opaque_zero()];  // vector load: see opaque_zero
+    }
   };
 
   HT hs;
@@ -411,8 +422,19 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
       *reinterpret_cast<typename vec4_of<OP>::type*>(UsT + vv * LU + r0) = pack4<OP>(u4);
     }
     __syncthreads();
-    const float gl = __expf(cur.gl);
-    hs.each([&](int, int, float& x) { x *= gl; });
+    if constexpr (CWD) {
+#pragma unroll
+      for (int a = 0; a < HT::TM; ++a)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float gd = __expf(cur.gd[a][j]);
+#pragma unroll
+          for (int b = 0; b < HT::TN; ++b) hs.acc[a][b][j] *= gd;
+        }
+    } else {
+      const float gl = __expf(cur.gl);
+      hs.each([&](int, int, float& x) { x *= gl; });
+    }
     hs.template mma<OP, CH>(cur.kh, KRow<OP, LU>{UsT});
     ot.template mma<OP, CH>(cur.pf, KRow<OP, LU>{UsT});  // + P U'
     OP* op = o + (row0 * H + h) * DV + v0;

@@ -91,6 +91,63 @@ constexpr int grad_region_bytes(int dk, int es) {
   return (m + 255) / 256 * 256;
 }
 
+// Channel-wise members (per-channel g, b, w; fp32 operands).  A NULL gate is
+// neutral: g = 0, b = 0 (no erase), w = 1.
+struct CwFwdWs {
+  int* chunk_off;
+  int* flag_scan;  // [N*H*NVT] written by the generic scan, not read
+  float* gC;       // [chunks*H*dk]    G of each chunk's last row, per channel
+  float* W;        // [chunks*H*64*dk] T (Gamma * b * K)
+  float* U;        // [chunks*H*64*dv] T (w * V), accumulator-tile layout
+  float* KhT;      // [chunks*H*dk*64] (e^{G_last - G} * K)^T
+  float* P;        // [chunks*H*64*64] decay-weighted Q K^T, i <= r
+  float* Qg;       // [chunks*H*64*dk] e^G * Q
+};
+
+struct CwFwdArgs {
+  Geo geo;
+  int dk, dv;
+  const float *q, *k, *v, *g, *b, *w, *S0;
+  float *o, *ST, *states;
+  CwFwdWs ws;
+  hipStream_t stream;
+  hipEvent_t const* events;
+};
+
+struct CwBwdWs {
+  int* chunk_off;
+  int* flag_scan;
+  float* gC;   // [chunks*H*dk]
+  float* WT;   // [chunks*H*dk*64]
+  float* QgT;  // [chunks*H*dk*64]
+  float* dOT;  // [chunks*H*dv*64]
+  float* PT;   // [chunks*H*64*64]
+  float* T;    // [chunks*H*64*64]
+  float* Kh;   // [chunks*H*64*dk]
+  float* KbG;  // [chunks*H*64*dk] Gamma * b * K
+  float* dh;   // [chunks*H*dk*dv]
+  float* dUT;  // [chunks*H*dv*64]
+  float* dP;   // [chunks*H*64*64]
+  float* dA;   // [chunks*H*64*64]
+  float* X;    // [chunks*H*64*dk]
+  float* dQg;  // [chunks*H*64*dk]
+  float* dKh;  // [chunks*H*64*dk]
+  float* hdh;  // [chunks*H*dk]
+};
+
+struct CwBwdArgs {
+  Geo geo;
+  int dk, dv;
+  const float *q, *k, *v, *g, *b, *w, *states, *dO, *dST;
+  float *dq, *dk_, *dv_, *dg, *db, *dw, *dS0;
+  CwBwdWs ws;
+  hipStream_t stream;
+  hipEvent_t const* events;
+};
+
+hipError_t launch_cw_fwd(const CwFwdArgs& a);
+hipError_t launch_cw_bwd(const CwBwdArgs& a);
+
 template <int DT, int VAR> hipError_t launch_fwd_var(const FwdArgs& a);
 template <int DT, int VAR> hipError_t launch_bwd_var(const BwdArgs& a);
 

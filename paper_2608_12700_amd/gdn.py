@@ -8,6 +8,8 @@ been built, every entry point raises: there is no fallback.
 Names mirror the C ABI in include/gdn.h:
   gdn_fwd(...) / gdn_bwd(...)       raw calls on pointers (ctypes)
   fwd(...) / bwd(...)               torch-tensor conveniences built on them
+  gdn_cw_fwd / gdn_cw_bwd,          the channel-wise members (per-channel g, b, w)
+  cw_fwd(...) / cw_bwd(...)
 """
 from __future__ import annotations
 
@@ -47,7 +49,10 @@ class Problem(ctypes.Structure):
 
 
 EXPORTED = ("gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_fwd",
-            "gdn_bwd", "gdn_fwd_ex", "gdn_bwd_ex", "gdn_status_str", "gdn_version")
+            "gdn_bwd", "gdn_fwd_ex", "gdn_bwd_ex", "gdn_cw_fwd_workspace_size",
+            "gdn_cw_bwd_workspace_size", "gdn_cw_fwd", "gdn_cw_bwd", "gdn_cw_fwd_ex", "gdn_cw_bwd_ex",
+            "gdn_status_str", "gdn_version")
+CW_BWD_STAGES = ("cw_bwd_prep", "cw_bwd_scan", "cw_bwd_grad_v", "cw_bwd_grad_d")
 NUM_STAGES = 4
 FWD_STAGES = ("fwd_prep", "fwd_scan", "fwd_exact", None)  # the output is fused into the scan
 BWD_STAGES = ("bwd_prep", "bwd_scan", "bwd_grad", "bwd_exact")
@@ -79,6 +84,18 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gdn_fwd_ex.restype = ctypes.c_int
     lib.gdn_bwd_ex.argtypes = [P] + [vp] * 14 + [vp, sz, vp, vp]
     lib.gdn_bwd_ex.restype = ctypes.c_int
+    lib.gdn_cw_fwd_workspace_size.argtypes = [P]
+    lib.gdn_cw_fwd_workspace_size.restype = sz
+    lib.gdn_cw_bwd_workspace_size.argtypes = [P]
+    lib.gdn_cw_bwd_workspace_size.restype = sz
+    lib.gdn_cw_fwd.argtypes = [P] + [vp] * 10 + [vp, sz, vp]
+    lib.gdn_cw_fwd.restype = ctypes.c_int
+    lib.gdn_cw_bwd.argtypes = [P] + [vp] * 16 + [vp, sz, vp]
+    lib.gdn_cw_bwd.restype = ctypes.c_int
+    lib.gdn_cw_fwd_ex.argtypes = [P] + [vp] * 10 + [vp, sz, vp, vp]
+    lib.gdn_cw_fwd_ex.restype = ctypes.c_int
+    lib.gdn_cw_bwd_ex.argtypes = [P] + [vp] * 16 + [vp, sz, vp, vp]
+    lib.gdn_cw_bwd_ex.restype = ctypes.c_int
     lib.gdn_status_str.argtypes = [ctypes.c_int]
     lib.gdn_status_str.restype = ctypes.c_char_p
     lib.gdn_version.argtypes = []
@@ -139,6 +156,35 @@ def gdn_bwd_ex(p, q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg, dbeta, dS0
                stream, events) -> int:
     return int(load().gdn_bwd_ex(ctypes.byref(p), q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg,
                                  dbeta, dS0, ws, ws_bytes, stream, events))
+
+
+def gdn_cw_fwd_workspace_size(p: Problem) -> int:
+    return int(load().gdn_cw_fwd_workspace_size(ctypes.byref(p)))
+
+
+def gdn_cw_bwd_workspace_size(p: Problem) -> int:
+    return int(load().gdn_cw_bwd_workspace_size(ctypes.byref(p)))
+
+
+def gdn_cw_fwd(p, q, k, v, g, b, w, S0, o, S_T, states, ws, ws_bytes, stream) -> int:
+    return int(load().gdn_cw_fwd(ctypes.byref(p), q, k, v, g, b, w, S0, o, S_T, states, ws, ws_bytes, stream))
+
+
+def gdn_cw_bwd(p, q, k, v, g, b, w, states, dO, dS_T, dq, dk, dv, dg, db, dw, dS0, ws, ws_bytes,
+               stream) -> int:
+    return int(load().gdn_cw_bwd(ctypes.byref(p), q, k, v, g, b, w, states, dO, dS_T, dq, dk, dv, dg, db, dw,
+                                 dS0, ws, ws_bytes, stream))
+
+
+def gdn_cw_fwd_ex(p, q, k, v, g, b, w, S0, o, S_T, states, ws, ws_bytes, stream, events) -> int:
+    return int(load().gdn_cw_fwd_ex(ctypes.byref(p), q, k, v, g, b, w, S0, o, S_T, states, ws, ws_bytes,
+                                    stream, events))
+
+
+def gdn_cw_bwd_ex(p, q, k, v, g, b, w, states, dO, dS_T, dq, dk, dv, dg, db, dw, dS0, ws, ws_bytes,
+                  stream, events) -> int:
+    return int(load().gdn_cw_bwd_ex(ctypes.byref(p), q, k, v, g, b, w, states, dO, dS_T, dq, dk, dv, dg, db,
+                                    dw, dS0, ws, ws_bytes, stream, events))
 
 
 def gdn_status_str(code: int) -> str:
@@ -255,7 +301,67 @@ def bwd(q, k, v, g, beta, chunk_states, dO, dS_T=None, *, variant="gated_delta",
     return dq, dk_, dvv, dg, db, dS0
 
 
+def _packed_of(cu_seqlens, dev):
+    if cu_seqlens is None:
+        return None
+    return cu_seqlens if isinstance(cu_seqlens, Packed) else Packed(cu_seqlens, dev)
+
+
+def cw_fwd(q, k, v, g=None, b=None, w=None, S0=None, *, cu_seqlens=None, workspace=None):
+    """Channel-wise forward (fp32): returns (o, S_T, chunk_states).  g, b [B,T,H,d_k] and
+    w [B,T,H,d_v] may each be None (neutral gate).  See include/gdn.h."""
+    dev = q.device
+    packed = _packed_of(cu_seqlens, dev)
+    p = _problem_for(q, v, "gated_delta", packed)
+    for name, t in (("q", q), ("k", k), ("v", v), ("g", g), ("b", b), ("w", w), ("S0", S0)):
+        if t is not None:
+            _check(t, name, torch.float32, dev)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    nch = gdn_num_chunks(p)
+    if nch < 0:
+        raise GdnError(nch, "gdn_num_chunks")
+    o = torch.empty((B, T, H, dv), dtype=torch.float32, device=dev)
+    S_T = torch.empty((p.num_seqs, H, dk, dv), dtype=torch.float32, device=dev)
+    states = torch.empty((nch, H, dk, dv), dtype=torch.float32, device=dev)
+    wsb = gdn_cw_fwd_workspace_size(p)
+    ws = workspace if workspace is not None else torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    rc = gdn_cw_fwd(p, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(b), _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T),
+                    _ptr(states), _ptr(ws), ws.numel(), ctypes.c_void_p(_stream_handle(dev)))
+    if rc != GDN_OK:
+        raise GdnError(rc, "gdn_cw_fwd")
+    return o, S_T, states
+
+
+def cw_bwd(q, k, v, g, b, w, chunk_states, dO, dS_T=None, *, cu_seqlens=None, workspace=None):
+    """Channel-wise backward (fp32): returns (dq, dk, dv, dg, db, dw, dS0); a gate's gradient
+    is None when the gate is None."""
+    dev = q.device
+    packed = _packed_of(cu_seqlens, dev)
+    p = _problem_for(q, v, "gated_delta", packed)
+    for name, t in (("q", q), ("k", k), ("v", v), ("dO", dO), ("g", g), ("b", b), ("w", w),
+                    ("chunk_states", chunk_states), ("dS_T", dS_T)):
+        if t is not None:
+            _check(t, name, torch.float32, dev)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    like = lambda t: None if t is None else torch.empty_like(t)
+    dq, dk_, dvv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    dg, db, dw = like(g), like(b), like(w)
+    dS0 = torch.empty((p.num_seqs, H, dk, dv), dtype=torch.float32, device=dev)
+    wsb = gdn_cw_bwd_workspace_size(p)
+    ws = workspace if workspace is not None else torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    rc = gdn_cw_bwd(p, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(b), _ptr(w), _ptr(chunk_states), _ptr(dO),
+                    _ptr(dS_T), _ptr(dq), _ptr(dk_), _ptr(dvv), _ptr(dg), _ptr(db), _ptr(dw), _ptr(dS0),
+                    _ptr(ws), ws.numel(), ctypes.c_void_p(_stream_handle(dev)))
+    if rc != GDN_OK:
+        raise GdnError(rc, "gdn_cw_bwd")
+    return dq, dk_, dvv, dg, db, dw, dS0
+
+
 __all__ = ["load", "make_problem", "Problem", "Packed", "GdnError", "fwd", "bwd", "gdn_fwd", "gdn_bwd",
            "gdn_fwd_ex", "gdn_bwd_ex", "NUM_STAGES", "FWD_STAGES", "BWD_STAGES",
            "gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_status_str",
-           "gdn_version", "EXPORTED", "LIB_PATH", "VARIANTS"]
+           "gdn_version", "EXPORTED", "LIB_PATH", "VARIANTS", "cw_fwd", "cw_bwd", "gdn_cw_fwd", "gdn_cw_bwd",
+           "gdn_cw_fwd_ex", "gdn_cw_bwd_ex", "gdn_cw_fwd_workspace_size", "gdn_cw_bwd_workspace_size",
+           "CW_BWD_STAGES"]

@@ -262,7 +262,77 @@ def describe(case: Case) -> str:
             f"H={case.H} dk={case.dk} dv={case.dv} N={case.N}")
 
 
+# ---------------------------------------------------------------------------
+# Channel-wise members: per-channel gates g, b [B,T,H,dk] and w [B,T,H,dv].
+# Draw order (one PCG64(seed) per case): q, k, v, g_raw, b_logit, w_logit, S0,
+# dO, dS_T.  g = -decay * softplus(g_raw) (a log-decay per channel, mean about
+# -0.8 * decay), b = sigmoid(b_logit), w = 1.5 * sigmoid(w_logit); q, k are
+# L2-normalised per (token, head).  Everything is rounded once to float32.
+# ``gates`` names the gates present: "gbw" (full GDN), "kda" (b = w = a scalar
+# beta per token broadcast over the channels, g per channel), "g" (GLA), ""
+# (LA).  Absent gates are None.
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class CwCase:
+    name: str
+    B: int
+    T: int
+    H: int
+    dk: int
+    dv: int
+    gates: str
+    q: np.ndarray
+    k: np.ndarray
+    v: np.ndarray
+    g: Optional[np.ndarray]
+    b: Optional[np.ndarray]
+    w: Optional[np.ndarray]
+    S0: np.ndarray
+    dO: np.ndarray
+    dS_T: np.ndarray
+    cu_seqlens: Optional[np.ndarray] = None
+
+    @property
+    def N(self) -> int:
+        return self.B if self.cu_seqlens is None else len(self.cu_seqlens) - 1
+
+
+def make_cw_case(name, B, T, H, dk, dv, *, gates="gbw", seed=0, decay=1.0, cu_seqlens=None,
+                 S0_std=0.1, dST_std=1.0) -> CwCase:
+    if cu_seqlens is not None:
+        assert B == 1 and int(cu_seqlens[-1]) == T
+    rng = np.random.Generator(np.random.PCG64(seed))
+    N = B if cu_seqlens is None else len(cu_seqlens) - 1
+    f32 = lambda x: np.ascontiguousarray(x, dtype=np.float32)
+
+    def normed(x):
+        return x / np.linalg.norm(x, axis=-1, keepdims=True)
+
+    q = f32(normed(rng.standard_normal((B, T, H, dk))))
+    k = f32(normed(rng.standard_normal((B, T, H, dk))))
+    v = f32(rng.standard_normal((B, T, H, dv)))
+    g_raw = rng.standard_normal((B, T, H, dk))
+    b_logit = rng.standard_normal((B, T, H, dk))
+    w_logit = rng.standard_normal((B, T, H, dv))
+    S0 = f32(S0_std * rng.standard_normal((N, H, dk, dv)))
+    dO = f32(rng.standard_normal((B, T, H, dv)))
+    dS_T = f32(dST_std * rng.standard_normal((N, H, dk, dv)))
+    g = f32(-decay * _softplus(g_raw)) if gates in ("gbw", "kda", "g") else None
+    b = w = None
+    if gates == "gbw":
+        b = f32(_sigmoid(b_logit))
+        w = f32(1.5 * _sigmoid(w_logit))
+    elif gates == "kda":
+        beta = f32(_sigmoid(b_logit[..., 0]))
+        b = f32(np.repeat(beta[..., None], dk, axis=-1))
+        w = f32(np.repeat(beta[..., None], dv, axis=-1))
+    return CwCase(name, B, T, H, dk, dv, gates, q, k, v, g, b, w, S0, dO, dS_T,
+                  None if cu_seqlens is None else np.asarray(cu_seqlens, dtype=np.int32))
+
+
 __all__ = [
+    "CwCase", "make_cw_case",
     "VARIANTS", "Case", "make_case", "round_bf16", "bf16_bits", "varlen_lengths",
     "config0", "config1", "config2", "config3", "config4", "config4_cu_seqlens",
     "total_chunks_for", "describe",

@@ -108,7 +108,7 @@ def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, c
             "kernels": kern}
 
 
-def summarize_trace(trace_dir, command):
+def summarize_trace(trace_dir, command, title="gated delta rule fwd+bwd, bf16 I/O, B=4 T=4096 H=16 dk=dv=128"):
     """Markdown table of a `rocprofv3 --kernel-trace --stats --output-format csv` run."""
     import csv
     import glob
@@ -118,12 +118,21 @@ def summarize_trace(trace_dir, command):
         rows = list(csv.DictReader(fh))
 
     def short(n):
+        d = re.search(r"gdn::(k_\w+)<([^>]*)>", n)  # demangled name
+        if d:
+            args = [x.strip() for x in d.group(2).split(",")]
+            nums = [x for x in args if x.isdigit()][:2]
+            mode = " (bwd)" if d.group(1) == "k_cw_prep" and args[-1] == "true" else ""
+            bf = " bf16" if "bf16" in args or "__hip_bfloat16" in d.group(2) else ""
+            return f"{d.group(1)}<{','.join(nums)}>" + bf + mode
         m = re.search(r"gdn\d*(k_\w+?)I(.*?)EE", n)
         if not m:
             return n[:60]
         nums = re.findall(r"Li(\d+)E", m.group(2))
-        return f"{m.group(1)}<{','.join(nums)}>" + (" bf16" if "DF16b" in m.group(2) else "")
-    out = ["# Kernel trace: gated delta rule fwd+bwd, bf16 I/O, B=4 T=4096 H=16 dk=dv=128", "",
+        flags = re.findall(r"Lb([01])E", m.group(2))
+        mode = " (bwd)" if m.group(1) == "k_cw_prep" and flags == ["1"] else ""
+        return f"{m.group(1)}<{','.join(nums)}>" + (" bf16" if "DF16b" in m.group(2) else "") + mode
+    out = [f"# Kernel trace: {title}", "",
            "Command (from the repository root, one MI355X):", "", "```", command, "```", "",
            "| kernel | calls | average (us) | total (us) | % |", "|---|---:|---:|---:|---:|"]
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
@@ -181,6 +190,138 @@ def kernel_model(B, T, H, dk, dv, es, N=None):
     out["fwd_scan"] = (out["fwd_scan"][0] + sio, out["fwd_scan"][1])
     out["bwd_scan"] = (out["bwd_scan"][0] + sio, out["bwd_scan"][1])
     return out
+
+
+def cw_kernel_model(B, T, H, dk, dv, N=None):
+    """Algorithmic bytes and flops per launch of the channel-wise stages (fp32:
+    each kernel's own inputs and outputs moved once)."""
+    N = B if N is None else N
+    tiles = B * (-(-T // CH)) * H
+    ck, cv, cc, st, vk = CH * dk * 4, CH * dv * 4, CH * CH * 4, dk * dv * 4, dk * 4
+    per = {
+        # q, k, g, b, v, w -> G_last, P, e^G Q, Khat^T, W, U
+        "cw_fwd_prep": (4 * ck + 2 * cv + vk + cc + 3 * ck + cv,
+                        2 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dk + 2 * CH * CH * dv),
+        # e^G Q, W, Khat^T, P, U, G_last -> chunk states, o
+        "cw_fwd_scan": (3 * ck + cc + cv + vk + st + cv, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
+        # q, k, g, b, dO -> G_last, P^T, (e^G Q)^T, Khat, W^T, T, Gamma*b*k, dO^T
+        "cw_bwd_prep": (4 * ck + cv + vk + 2 * cc + 4 * ck + cv,
+                        2 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dk),
+        # Khat, W^T, (e^G Q)^T, dO^T, P^T, G_last -> dh, dU'^T
+        "cw_bwd_scan": (3 * ck + cv + cc + vk + st + cv, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
+        # v, w, dO, state, T, Gamma*b*k, dh, dU'^T -> dv, dw, dP, dA, X, dQg, dKhat, <h, dh>
+        "cw_bwd_grad_v": (3 * cv + st + cc + ck + st + cv + 2 * cv + 2 * cc + 3 * ck + vk,
+                          2 * CH * dk * dv + 3 * 2 * CH * CH * dv + 3 * 2 * CH * dk * dv),
+        # q, k, g, b, dP, dA, X, dQg, dKhat, <h, dh> -> dq, dk, dg, db
+        "cw_bwd_grad_d": (4 * ck + 2 * cc + 3 * ck + vk + 4 * ck, 4 * 2 * CH * CH * dk),
+    }
+    out = {k: (b * tiles, f * tiles) for k, (b, f) in per.items()}
+    sio = 2 * N * H * dk * dv * 4
+    out["cw_fwd_scan"] = (out["cw_fwd_scan"][0] + sio, out["cw_fwd_scan"][1])
+    out["cw_bwd_scan"] = (out["cw_bwd_scan"][0] + sio, out["cw_bwd_scan"][1])
+    return out
+
+
+def bench_cw(a):
+    """The channel-wise path (per-channel g, b, w; fp32) on B4 T4096 H16 d128: one JSON line."""
+    import time
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2608_12700_amd import gdn
+
+    B, T, H, dk, dv = 4, 4096, 16, 128, 128
+    case = W.make_cw_case("cw_B4_T4096_H16_d128", B, T, H, dk, dv, gates="gbw", seed=6)
+    cpu = None
+    if not a.no_cpu_baseline:
+        # the oracle on one (b, h) stream of the same inputs, one core
+        from oracle import cw_oracle as CWO
+        f64 = lambda x: np.ascontiguousarray(x[:1, :, :1], dtype=np.float64)
+        args = [f64(getattr(case, n)) for n in ("q", "k", "v", "g", "b", "w")]
+        t0 = time.perf_counter()
+        CWO.cw_oracle_bwd(*args, case.S0[:1, :1].astype(np.float64), f64(case.dO),
+                          case.dS_T[:1, :1].astype(np.float64))  # recomputes the forward inside
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(T / H / dt, 1), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+               "sample": f"1 of 64 (b,h) streams, full T={T}, float64 token-serial fwd+bwd on one core "
+                         f"({dt:.1f} s); tokens/s counts all 16 heads"}
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t = {n: (None if getattr(case, n) is None else torch.from_numpy(getattr(case, n)).to(dev))
+         for n in ("q", "k", "v", "g", "b", "w", "S0", "dO", "dS_T")}
+    p = gdn.make_problem(B, T, H, dk, dv, io_dtype=gdn.GDN_F32)
+    nch = gdn.gdn_num_chunks(p)
+    o = torch.empty_like(t["v"])
+    S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
+    states = torch.empty((nch, H, dk, dv), dtype=torch.float32, device=dev)
+    grads = [torch.empty_like(t[n]) for n in ("q", "k", "v", "g", "b", "w", "S0")]
+    wsf = torch.empty(gdn.gdn_cw_fwd_workspace_size(p), dtype=torch.uint8, device=dev)
+    wsb = torch.empty(gdn.gdn_cw_bwd_workspace_size(p), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    P = lambda x: ctypes.c_void_p(x.data_ptr())
+    hip = Hip()
+    ns = gdn.NUM_STAGES + 1
+
+    def step(evf=None, evb=None):
+        rc = gdn.gdn_cw_fwd_ex(p, P(t["q"]), P(t["k"]), P(t["v"]), P(t["g"]), P(t["b"]), P(t["w"]), P(t["S0"]),
+                               P(o), P(S_T), P(states), P(wsf), wsf.numel(), ctypes.c_void_p(stream), evf)
+        assert rc == 0, rc
+        rc = gdn.gdn_cw_bwd_ex(p, P(t["q"]), P(t["k"]), P(t["v"]), P(t["g"]), P(t["b"]), P(t["w"]), P(states),
+                               P(t["dO"]), P(t["dS_T"]), *[P(x) for x in grads], P(wsb), wsb.numel(),
+                               ctypes.c_void_p(stream), evb)
+        assert rc == 0, rc
+
+    for _ in range(a.warmup):
+        step()
+    flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+    evs = [((ctypes.c_void_p * ns)(*[hip.event() for _ in range(ns)]),
+            (ctypes.c_void_p * ns)(*[hip.event() for _ in range(ns)])) for _ in range(a.steps)]
+    torch.cuda.synchronize()
+    for i in range(a.steps):
+        flush.fill_(float(i))
+        step(*evs[i])
+    torch.cuda.synchronize()
+    ms_step = sum(hip.ms(ef[0], eb[ns - 1]) for ef, eb in evs) / a.steps
+    fwd_names = ("cw_fwd_prep", "cw_fwd_scan", None, None)
+    stage_ms = {}
+    for ef, eb in evs:
+        for j in range(gdn.NUM_STAGES):
+            for nm, e in ((fwd_names[j], ef), (gdn.CW_BWD_STAGES[j], eb)):
+                if nm is not None:
+                    stage_ms[nm] = stage_ms.get(nm, 0.0) + hip.ms(e[j], e[j + 1]) / a.steps
+    ok = all(bool(torch.isfinite(x).all()) for x in [o, S_T] + grads)
+    km = cw_kernel_model(B, T, H, dk, dv)
+    dom = max(km, key=lambda n: stage_ms[n])
+    dom_s = stage_ms[dom] / 1e3
+    ach = km[dom][0] / dom_s / 1e9
+    res = {
+        "metric": "GDN channel-wise (per-channel g, b, w) fwd+bwd tokens/s at B4 T4096 H16 d128 fp32",
+        "value": round(B * T / (ms_step / 1e3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded: q,k L2-normalised N(0,1); v,dO N(0,1); g=-softplus(N) per channel; "
+                "b=sigmoid(N) per channel; w=1.5*sigmoid(N) per channel; S0 N(0,0.1^2); dS_T N(0,1))",
+        "config": {"workload": "channel-wise gated delta rule fwd+bwd (full GDN gates), fp32 I/O and state, "
+                               "B=4 T=4096 H=16 dk=dv=128 chunk=64", "B": B, "T": T, "H": H, "dk": dk, "dv": dv},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": int(km[dom][0]), "avg_launch_ms": round(stage_ms[dom], 4),
+                     "mfma_tflops": round(km[dom][1] / dom_s / 1e12, 1)},
+        "timing": {"cold_caches": True, "note": "mean of per-step HIP event intervals, each step after a "
+                                                "512 MiB scratch write"},
+        "path": {"stage_ms": {k_: round(x, 4) for k_, x in stage_ms.items()}, "outputs_finite": ok},
+    }
+    if a.stages:
+        for nm, x in stage_ms.items():
+            b_, f_ = km[nm]
+            print(f"{nm:14s} {x*1e3:9.1f} us  {b_/(x/1e3)/1e9:8.1f} GB/s  {f_/(x/1e3)/1e12:7.1f} TFLOP/s",
+                  file=sys.stderr)
+    if cpu is not None:
+        res["cpu_baseline"] = cpu
+    print(json.dumps(res), flush=True)
+    return 0
 
 
 def path_model(B, T, H, dk, dv, es, N=None):
@@ -278,13 +419,19 @@ def main(argv=None):
     ap.add_argument("--summarize-trace", metavar="TRACE", help="write the kernel-trace summary of a "
                     "rocprofv3 --kernel-trace --stats --output-format csv folder")
     ap.add_argument("--command", default="", help="the profiling command recorded in the summary")
+    ap.add_argument("--cw", action="store_true",
+                    help="measure the channel-wise path (per-channel g, b, w; fp32) instead")
+    ap.add_argument("--trace-out", default="kernel_trace_bf16_B4_T4096_H16_d128.md",
+                    help="file name under profiles/ for --summarize-trace")
     a = ap.parse_args(argv)
     if a.copy_kernel:
         copy_kernel()
         return 0
     if a.summarize_trace:
-        md = summarize_trace(a.summarize_trace, a.command)
-        with open(os.path.join(ROOT, "profiles", "kernel_trace_bf16_B4_T4096_H16_d128.md"), "w") as fh:
+        md = summarize_trace(a.summarize_trace, a.command, *(
+            ["channel-wise gated delta rule fwd+bwd (per-channel g, b, w), fp32, B=4 T=4096 H=16 dk=dv=128"]
+            if a.cw else []))
+        with open(os.path.join(ROOT, "profiles", a.trace_out), "w") as fh:
             fh.write(md)
         print(md)
         return 0
@@ -299,6 +446,8 @@ def main(argv=None):
               f"(sequence, head) streams with no communication, so N GPUs run N independent copies.",
               file=sys.stderr)
         return 2
+    if a.cw:
+        return bench_cw(a)
 
     import numpy as np
     import torch

@@ -12,4 +12,5 @@ Modules:
   chunked_ref  chunkwise reference, checked against the token-serial oracle
   dense_ref    closed forms used only to pin the oracle (brute-force unroll,
                dense masked decayed attention)
+  cw_oracle    the channel-wise recurrence (per-channel g, b, w) and its adjoint
 """

@@ -151,3 +151,52 @@ def test_chunk_count_and_workspace_grow_with_size():
     assert gdn.gdn_fwd_workspace_size(big) > gdn.gdn_fwd_workspace_size(small)
     assert gdn.gdn_bwd_workspace_size(big) > gdn.gdn_bwd_workspace_size(small)
     assert gdn.gdn_num_chunks(gdn.make_problem(1, 0, 2, 64, 64)) == 0
+
+
+# ---------------------------------------------------------------- channel-wise entry points
+
+def call_cw_fwd(p, ws_bytes=None, **over):
+    args = dict(q=fake(1), k=fake(2), v=fake(3), g=fake(4), b=fake(5), w=fake(16), S0=None, o=fake(6),
+                S_T=fake(7), states=fake(8))
+    args.update(over)
+    wsb = gdn.gdn_cw_fwd_workspace_size(p) if ws_bytes is None else ws_bytes
+    return gdn.gdn_cw_fwd(p, args["q"], args["k"], args["v"], args["g"], args["b"], args["w"], args["S0"],
+                          args["o"], args["S_T"], args["states"], fake(9), wsb, None)
+
+
+def call_cw_bwd(p, **over):
+    args = dict(q=fake(1), k=fake(2), v=fake(3), g=fake(4), b=fake(5), w=fake(16), st=fake(6), dO=fake(7),
+                dST=None, dq=fake(10), dk=fake(11), dv=fake(12), dg=fake(13), db=fake(14), dw=fake(17),
+                dS0=fake(15))
+    args.update(over)
+    return gdn.gdn_cw_bwd(p, args["q"], args["k"], args["v"], args["g"], args["b"], args["w"], args["st"],
+                          args["dO"], args["dST"], args["dq"], args["dk"], args["dv"], args["dg"], args["db"],
+                          args["dw"], args["dS0"], fake(20), gdn.gdn_cw_bwd_workspace_size(p), None)
+
+
+def test_channelwise_needs_fp32_io():
+    p = gdn.make_problem(1, 64, 2, 64, 64, io_dtype=gdn.GDN_BF16)
+    assert gdn.gdn_cw_fwd_workspace_size(p) == 0
+    assert call_cw_fwd(p, ws_bytes=1 << 30) == -3
+
+
+def test_channelwise_gradients_follow_the_gates():
+    p = gdn.make_problem(1, 64, 2, 64, 64, io_dtype=gdn.GDN_F32)
+    assert call_cw_bwd(p, dg=None) == -9
+    assert call_cw_bwd(p, b=None) == -9
+    assert call_cw_bwd(p, dw=None) == -9
+
+
+def test_channelwise_null_alias_and_workspace():
+    p = gdn.make_problem(1, 64, 2, 64, 64, io_dtype=gdn.GDN_F32)
+    need = gdn.gdn_cw_fwd_workspace_size(p)
+    assert need > 0 and need % 256 == 0
+    assert call_cw_fwd(p, q=None) == -1
+    assert call_cw_fwd(p, ws_bytes=need - 1) == -5
+    assert call_cw_fwd(p, o=fake(4)) == -6           # o on top of g
+    assert call_cw_bwd(p, dw=fake(16)) == -6         # dw on top of w
+    assert call_cw_bwd(p, dS0=None) == -1
+    # a larger problem needs more workspace, the backward more than the forward
+    big = gdn.make_problem(2, 640, 4, 128, 128, io_dtype=gdn.GDN_F32)
+    assert gdn.gdn_cw_fwd_workspace_size(big) > need
+    assert gdn.gdn_cw_bwd_workspace_size(big) > gdn.gdn_cw_fwd_workspace_size(big)

@@ -67,6 +67,7 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
   __shared__ __align__(16) float Gs[CH * LK];  // G
   __shared__ __align__(16) float Bk[CH * LK];  // b * K, then Gamma * b * K
   __shared__ __align__(16) float As[CH * LC];  // A
+  __shared__ __align__(16) float Pd[4 * 16 * 16];  // P inside the four diagonal 16 x 16 blocks
   float* Tf = Qs;
   float* Vw = Ks;
 
@@ -90,39 +91,51 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
     }
   __syncthreads();
 
+  // Pairs inside one 16-row block, exactly, spread over the whole block: pair
+  // q of block RB is (rl, il) with il <= rl; one exponential per term serves P
+  // and A.  A's sums land in As at their own positions (the A product's owner
+  // lane adds its part there), P's in Pd.
+  for (int pi = thread_x(); pi < 4 * 136; pi += blockDim.x) {
+    const int RB = pi / 136, q = pi - RB * 136;
+    int rl = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
+    while ((rl + 1) * (rl + 2) / 2 <= q) ++rl;
+    while (rl * (rl + 1) / 2 > q) --rl;
+    const int il = q - rl * (rl + 1) / 2, r = 16 * RB + rl, i = 16 * RB + il;
+    float sp = 0.f, sa = 0.f;
+#pragma unroll 4
+    for (int d = 0; d < DK; d += 4) {
+      const float4 qr = *reinterpret_cast<const float4*>(Qs + r * LK + d);
+      const float4 ki = *reinterpret_cast<const float4*>(Ks + i * LK + d);
+      const float4 gr = *reinterpret_cast<const float4*>(Gs + r * LK + d);
+      const float4 gi = *reinterpret_cast<const float4*>(Gs + i * LK + d);
+      const float e0 = __expf(gr.x - gi.x), e1 = __expf(gr.y - gi.y), e2 = __expf(gr.z - gi.z), e3 = __expf(gr.w - gi.w);
+      const float k0 = ki.x * e0, k1 = ki.y * e1, k2 = ki.z * e2, k3 = ki.w * e3;
+      sp += qr.x * k0 + qr.y * k1 + qr.z * k2 + qr.w * k3;
+      if (b) {
+        const float4 br = *reinterpret_cast<const float4*>(Bk + r * LK + d);
+        sa += br.x * k0 + br.y * k1 + br.z * k2 + br.w * k3;
+      }
+    }
+    Pd[(RB * 16 + rl) * 16 + il] = sp;
+    if (b && il < rl) As[r * LC + i] = sa;
+  }
+  __syncthreads();
+
   // P and A: wave (R, ·) of Tiles<64, 64, 4, 2> owns 16-row block R
   const int R = wave_id() / 2;
   auto ref = [&](int d) { return cw_ref<LK>(Gs, R, d); };
   auto kcol = kfun<float>([&](int i, int d) {
     return i < 16 * R ? Ks[i * LK + d] * __expf(ref(d) - Gs[i * LK + d]) : 0.f;
   });
-  // the diagonal 16 x 16 tile of row block R, summed exactly: the rows of X
-  // against the rows of K (i <= r, or i < r when strict)
-  auto diag = [&](Tiles<CH, CH, 4, 2>& t, const float* X, bool strict) {
-    const int l = lane_id();
-#pragma unroll
-    for (int bb = 0; bb < t.TN; ++bb) {
-      if (t.n0(bb) != 16 * R) continue;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = t.m0(0) + (l >> 4) * 4 + j, i = t.n0(bb) + (l & 15);
-        float sum = 0.f;
-        if (strict ? i < r : i <= r)
-          for (int d = 0; d < DK; ++d)
-            sum += X[r * LK + d] * Ks[i * LK + d] * __expf(Gs[r * LK + d] - Gs[i * LK + d]);
-        t.acc[0][bb][j] += sum;
-      }
-    }
-  };
   {
     Tiles<CH, CH, 4, 2> p;
     p.zero();
     p.template mma<float, DK>(kfun<float>([&](int r, int d) { return Qs[r * LK + d] * __expf(Gs[r * LK + d] - ref(d)); }),
                               kcol);
-    diag(p, Qs, false);
     float* Pt = Pg + tile * CH * CH;
     p.each([&](int r, int i, float& x) {
-      const float val = i <= r ? x : 0.f;
+      const float dg = (r >> 4) == (i >> 4) ? Pd[(r * 16) + (i & 15)] : 0.f;
+      const float val = i <= r ? x + dg : 0.f;
       if (BWD) Pt[i * CH + r] = val;
       else Pt[r * CH + i] = val;
     });
@@ -132,8 +145,10 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
     a.zero();
     a.template mma<float, DK>(kfun<float>([&](int r, int d) { return Bk[r * LK + d] * __expf(Gs[r * LK + d] - ref(d)); }),
                               kcol);
-    diag(a, Bk, true);
-    a.each([&](int r, int i, float& x) { As[r * LC + i] = i < r ? x : 0.f; });
+    a.each([&](int r, int i, float& x) {
+      const float dg = (r >> 4) == (i >> 4) && i < r ? As[r * LC + i] : 0.f;
+      As[r * LC + i] = i < r ? x + dg : 0.f;
+    });
   }
   // Gamma * Q and Khat = e^{G_last - G} * K, each in the layout its scan reads
   {
@@ -355,7 +370,9 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
                                                    float* __restrict__ db) {
   constexpr int DS = 32, LS = DS + 4, LC = CH + 4;
   __shared__ __align__(16) float dPs[CH * LC], dAs[CH * LC];
-  __shared__ __align__(16) float Qs[CH * LS], Ks[CH * LS], Bs[CH * LS], Gs[CH * LS], dGs[CH * LS], Zs[CH * LS];
+  __shared__ __align__(16) float Qs[CH * LS], Ks[CH * LS], Bs[CH * LS], Gs[CH * LS];
+  float* dGs = Qs;  // dG and Khat * dKhat take Q's and K's tiles once every wave is done with them
+  float* Zs = Ks;
   const int ci = blockIdx.x, h = blockIdx.y, d0 = blockIdx.z * DS;
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
@@ -385,6 +402,19 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
   auto kdown = kfun<float>([&](int d, int i) {
     return i < 16 * R ? Ks[i * LS + d] * __expf(ref(d) - Gs[i * LS + d]) : 0.f;
   });
+  // this lane's X, dQg, dKhat (issued ahead of the products)
+  float xin[4], qgin[4], khin[4];
+  {
+    const int l = lane_id(), dl = TD::n0(0) + (l & 15);
+    const long base = tile * CH * DK + d0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = TD::m0(0) + (l >> 4) * 4 + j;
+      xin[j] = Xg[base + r * DK + dl];
+      qgin[j] = dQgg[base + r * DK + dl];
+      khin[j] = dKhg[base + r * DK + dl];
+    }
+  }
   TD aP, aA, bP, bA;
   aP.zero(); aA.zero(); bP.zero(); bA.zero();
   aP.template mma<float, CH>(KRow<float, LC>{dPs}, kdown);
@@ -397,20 +427,12 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
       return r >= 16 * (R + 1) ? Bs[r * LS + d] * Ks[r * LS + d] * __expf(Gs[r * LS + d] - last(d)) : 0.f;
     }));
   }
-  // the pairs inside block R, exactly: row sums over i in [16R, r] (a) and
-  // column sums over r in [i, 16R + 15] (b), e^{G_r - G_i} per term
-  auto diag_a = [&](const float* M, const float* Y, int r, int dl, bool strict) {
-    float sum = 0.f;
-    const int hi = strict ? r - 1 : r;
-    for (int i = 16 * R; i <= hi; ++i)
-      sum += M[r * LC + i] * Y[i * LS + dl] * __expf(Gs[r * LS + dl] - Gs[i * LS + dl]);
-    return sum;
-  };
+  // the pairs inside block R are summed exactly below: row sums over
+  // i in [16R, r] (a) and column sums over r in [i, 16R + 15] (b), one
+  // exponential e^{G_r - G_i} per term shared by the dP and dA sums
+  float dGv[4], Zv[4];
   {
     const int l = lane_id();
-    const float* Xt = Xg + tile * CH * DK + d0;
-    const float* Qgt = dQgg + tile * CH * DK + d0;
-    const float* Kht = dKhg + tile * CH * DK + d0;
     const int dl = TD::n0(0) + (l & 15);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -418,21 +440,27 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
       const float G = Gs[r * LS + dl], GL = Gs[(CH - 1) * LS + dl];
       const float gam = __expf(G), dte = __expf(GL - G);
       const float qv = Qs[r * LS + dl], kv = Ks[r * LS + dl], bv = Bs[r * LS + dl], kb = bv * kv;
-      const float xv = Xt[r * DK + dl], dqg = Qgt[r * DK + dl], dkh = Kht[r * DK + dl];
+      const float xv = xin[j], dqg = qgin[j], dkh = khin[j];
+      float dqP = 0.f, dkbA = 0.f;  // row sums inside the block
+      for (int i = 16 * R; i <= r; ++i) {
+        const float ke = Ks[i * LS + dl] * __expf(G - Gs[i * LS + dl]);
+        dqP += dPs[r * LC + i] * ke;
+        dkbA += dAs[r * LC + i] * ke;  // dA is zero on the diagonal
+      }
       float dkP = 0.f, dkA = 0.f;  // column sums inside the block (row r plays i)
       for (int rr = r; rr <= 16 * R + 15; ++rr) {
         const float e = __expf(Gs[rr * LS + dl] - G);
         dkP += dPs[rr * LC + r] * Qs[rr * LS + dl] * e;
-        if (rr > r) dkA += dAs[rr * LC + r] * Bs[rr * LS + dl] * Ks[rr * LS + dl] * e;
+        dkA += dAs[rr * LC + r] * Bs[rr * LS + dl] * Ks[rr * LS + dl] * e;  // zero at rr == r
       }
-      const float dqP = aP.acc[0][0][j] * __expf(G - ref(dl)) + diag_a(dPs, Ks, r, dl, false);
+      dqP += aP.acc[0][0][j] * __expf(G - ref(dl));
       dkP += bP.acc[0][0][j] * __expf(last(dl) - G);
-      const float dkbA = b ? aA.acc[0][0][j] * __expf(G - ref(dl)) + diag_a(dAs, Ks, r, dl, true) : 0.f;
+      dkbA = b ? dkbA + aA.acc[0][0][j] * __expf(G - ref(dl)) : 0.f;
       dkA = b ? dkA + bA.acc[0][0][j] * __expf(last(dl) - G) : 0.f;
       const float dkb = gam * xv + dkbA;
       const float khdkh = dte * kv * dkh;
-      dGs[r * LS + dl] = gam * qv * dqg + qv * dqP - kv * dkP + kb * dkbA - kv * dkA + gam * kb * xv - khdkh;
-      Zs[r * LS + dl] = khdkh;
+      dGv[j] = gam * qv * dqg + qv * dqP - kv * dkP + kb * dkbA - kv * dkA + gam * kb * xv - khdkh;
+      Zv[j] = khdkh;
       if (r < cp.len) {
         const long o = bk + (long)r * rsk + dl;
         dq[o] = gam * dqg + dqP;
@@ -442,6 +470,16 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
     }
   }
   if (g) {
+    __syncthreads();  // every wave is done with Q and K
+    {
+      const int l = lane_id(), dl = TD::n0(0) + (l & 15);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = TD::m0(0) + (l >> 4) * 4 + j;
+        dGs[r * LS + dl] = dGv[j];
+        Zs[r * LS + dl] = Zv[j];
+      }
+    }
     __syncthreads();
     const int r = lane_id(), nw = (int)blockDim.x / WAVE;
     for (int dl = wave_id(); dl < DS; dl += nw) {

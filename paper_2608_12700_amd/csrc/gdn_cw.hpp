@@ -40,6 +40,31 @@ __device__ __forceinline__ void cw_cumsum_columns(float* Gs) {
   for (int d = wave_id(); d < D; d += nw) Gs[l * LD + d] = wave_incl_scan(Gs[l * LD + d]);
 }
 
+// A ROWS x D fp32 tile (rows rs floats apart in HBM), read by NT threads in
+// one batch: every load is in flight before the first LDS store (a load /
+// store loop would pay one memory round trip per iteration).
+template <int ROWS, int D, int NT>
+struct TileIn {
+  static constexpr int PER_ROW = D / 4, N = ROWS * PER_ROW / NT;
+  static_assert(ROWS * PER_ROW % NT == 0, "whole pieces per thread");
+  float4 u[N];
+  __device__ __forceinline__ void load(const float* __restrict__ src, long rs) {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      const int idx = thread_x() + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * 4;
+      u[t] = *reinterpret_cast<const float4*>(src + r * rs + c);
+    }
+  }
+  template <int LD>
+  __device__ __forceinline__ void stage(float* dst) const {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      const int idx = thread_x() + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * 4;
+      *reinterpret_cast<float4*>(dst + r * LD + c) = u[t];
+    }
+  }
+};
+
 // The reference log-decay of 16-row block R (row 16R - 1; 0 for R = 0).
 template <int LD>
 __device__ __forceinline__ float cw_ref(const float* Gs, int R, int d) {
@@ -76,12 +101,31 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
   const long tile = (long)ci * H + h;
   const long rsk = (long)H * DK, bk = (cp.row0 * H + h) * DK;
   const long rsv = (long)H * DV, bv = (cp.row0 * H + h) * DV;
-  load_rows<DK, LK>(q + bk, rsk, cp.len, Qs);
-  load_rows<DK, LK>(k + bk, rsk, cp.len, Ks);
-  if (g) load_rows<DK, LK>(g + bk, rsk, cp.len, Gs);
+  // every input row of the block is requested up front: q, k, g, b, then the
+  // forward's v and w slices (or the backward's dO)
+  constexpr int NSL = BWD ? 1 : DV / VS;
+  RowsIn<DK, 512, float> qin, kin, gin, bin;
+  RowsIn<VS, 512, float> vin[NSL], win[NSL];
+  RowsIn<DV, 512, float> doin;
+  qin.load(q + bk, rsk, cp.len);
+  kin.load(k + bk, rsk, cp.len);
+  if (g) gin.load(g + bk, rsk, cp.len);
+  if (b) bin.load(b + bk, rsk, cp.len);
+  if constexpr (!BWD) {
+#pragma unroll
+    for (int t = 0; t < NSL; ++t) {
+      vin[t].load(v + bv + t * VS, rsv, cp.len);
+      if (w) win[t].load(w + bv + t * VS, rsv, cp.len);
+    }
+  } else {
+    doin.load(dO + bv, rsv, cp.len);
+  }
+  qin.template stage<LK>(Qs, cp.len);
+  kin.template stage<LK>(Ks, cp.len);
+  if (g) gin.template stage<LK>(Gs, cp.len);
   else
     for (int i = thread_x(); i < CH * LK; i += blockDim.x) Gs[i] = 0.f;
-  if (b) load_rows<DK, LK>(b + bk, rsk, cp.len, Bk);
+  if (b) bin.template stage<LK>(Bk, cp.len);
   __syncthreads();
   if (g) cw_cumsum_columns<DK, LK>(Gs);
   if (b)
@@ -192,13 +236,6 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
       const int r = i / DK, d = i - r * DK;
       Kb[i] = b ? Bk[r * LK + d] : 0.f;
     }
-    // dO^T [v][r]
-    float* Dt = dOTg + tile * DV * CH;
-    for (int i = thread_x(); i < DV * CH; i += blockDim.x) {
-      const int vv = i / CH, r = i - vv * CH;
-      const float x = dO[bv + (long)clamp_row(r, cp.len) * rsv + vv];
-      Dt[i] = r < cp.len ? x : 0.f;
-    }
   }
   __syncthreads();
   // W = T (Gamma * Kb)
@@ -216,16 +253,45 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
       for (int i = thread_x(); i < CH * DK; i += blockDim.x) Wt[i] = 0.f;
     }
   }
+  // dO^T [v][r]: 64 columns of dO at a time staged row-major in K's tile (free
+  // once W is formed), then written down its columns so each store instruction
+  // covers whole rows of dO^T
+  if constexpr (BWD) {
+    constexpr int PW = 64, PR = DV / 4;
+    static_assert(PW <= LK && DV % PW == 0, "a pass fits K's tile");
+    float* Dt = dOTg + tile * DV * CH;
+#pragma unroll
+    for (int ps = 0; ps < DV / PW; ++ps) {
+      __syncthreads();
+#pragma unroll
+      for (int pc = 0; pc < doin.N; ++pc) {
+        const int idx = thread_x() + pc * 512, r = idx / PR, c = (idx - r * PR) * 4;
+        if (c / PW == ps) *reinterpret_cast<uint4*>(Ks + r * LK + (c - ps * PW)) = keep16(r < cp.len, doin.u[pc]);
+      }
+      __syncthreads();
+      for (int i = thread_x(); i < PW * CH; i += blockDim.x) {
+        const int vv = i / CH, r = i - vv * CH;
+        Dt[(long)(ps * PW + vv) * CH + r] = Ks[r * LK + vv];
+      }
+    }
+  }
   // U = T (w * V) in the forward scan's accumulator-tile layout
-  if (!BWD) {
+  if constexpr (!BWD) {
     float* Ut = Ug + tile * CH * DV;
-    for (int c0 = 0; c0 < DV; c0 += VS) {
+#pragma unroll
+    for (int t = 0; t < NSL; ++t) {
+      const int c0 = t * VS;
       __syncthreads();  // K (first pass) or the previous slice is no longer read
-      for (int i = thread_x(); i < CH * VS; i += blockDim.x) {
-        const int r = i / VS, c = i - r * VS;
-        const long o = bv + (long)clamp_row(r, cp.len) * rsv + c0 + c;
-        const float x = v[o] * (w ? w[o] : 1.f);
-        Vw[r * LV + c] = r < cp.len ? x : 0.f;
+#pragma unroll
+      for (int pc = 0; pc < vin[t].N; ++pc) {
+        constexpr int PR = VS / 4;
+        const int idx = thread_x() + pc * 512, r = idx / PR, c = (idx - r * PR) * 4;
+        float4 x = __builtin_bit_cast(float4, keep16(r < cp.len, vin[t].u[pc]));
+        if (w) {
+          const float4 y = __builtin_bit_cast(float4, win[t].u[pc]);
+          x.x *= y.x; x.y *= y.y; x.z *= y.z; x.w *= y.w;
+        }
+        *reinterpret_cast<float4*>(Vw + r * LV + c) = x;
       }
       __syncthreads();
       Tiles<CH, VS, 4, 2> uu;
@@ -271,28 +337,48 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
   const long rsv = (long)H * DV, bv = (cp.row0 * H + h) * DV;
-  load_dense<CH, CH, LC>(Tg + tile * CH * CH, Ts);
-  load_dense<CH, DK, LK>(KbGg + tile * CH * DK, KbG);
+  // the tiles of one value slice, requested in one batch
+  struct Slice {
+    RowsIn<VS, 512, float> v, w, dO;
+    TileIn<DK, VS, 512> h, dh;
+    TileIn<VS, CH, 512> dut;
+  };
+  const float* hp = states + tile * DK * DV;
+  const float* dhp = dhg + tile * DK * DV;
+  const float* dUp = dUTg + tile * DV * CH;
+  auto load_slice = [&](Slice& sl, int c0) {
+    sl.v.load(v + bv + c0, rsv, cp.len);
+    if (w) sl.w.load(w + bv + c0, rsv, cp.len);
+    sl.dO.load(dO + bv + c0, rsv, cp.len);
+    sl.h.load(hp + c0, DV);
+    sl.dh.load(dhp + c0, DV);
+    sl.dut.load(dUp + (long)c0 * CH, CH);
+  };
+  {
+    TileIn<CH, CH, 512> tin;
+    TileIn<CH, DK, 512> kin;
+    tin.load(Tg + tile * CH * CH, CH);
+    kin.load(KbGg + tile * CH * DK, DK);
+    tin.template stage<LC>(Ts);
+    kin.template stage<LK>(KbG);
+  }
+  Slice cur, nxt;
+  load_slice(cur, 0);
   Tiles<CH, CH, 4, 2> dP, dA;
   Tiles<CH, DK, 4, 2> X, dQg, dKh;
   dP.zero(); dA.zero(); X.zero(); dQg.zero(); dKh.zero();
   float hdh = 0.f;  // thread d < DK: sum over v of h[d][v] dh[d][v]
-  const float* hp = states + tile * DK * DV;
-  const float* dhp = dhg + tile * DK * DV;
-  const float* dUp = dUTg + tile * DV * CH;
+#pragma unroll
   for (int c0 = 0; c0 < DV; c0 += VS) {
-    load_rows<VS, LV>(v + bv + c0, rsv, cp.len, Vs);
-    if (w) load_rows<VS, LV>(w + bv + c0, rsv, cp.len, Ws);
-    load_rows<VS, LV>(dO + bv + c0, rsv, cp.len, dOs);
-    for (int i = thread_x(); i < DK * VS / 4; i += blockDim.x) {
-      const int d = i / (VS / 4), c = (i - d * (VS / 4)) * 4;
-      *reinterpret_cast<float4*>(hs + d * LV + c) = *reinterpret_cast<const float4*>(hp + (long)d * DV + c0 + c);
-      *reinterpret_cast<float4*>(dhs + d * LV + c) = *reinterpret_cast<const float4*>(dhp + (long)d * DV + c0 + c);
-    }
-    for (int i = thread_x(); i < VS * CH / 4; i += blockDim.x) {
-      const int vv = i / (CH / 4), r = (i - vv * (CH / 4)) * 4;
-      *reinterpret_cast<float4*>(dUT + vv * LC + r) = *reinterpret_cast<const float4*>(dUp + (long)(c0 + vv) * CH + r);
-    }
+    cur.v.template stage<LV>(Vs, cp.len);
+    if (w) cur.w.template stage<LV>(Ws, cp.len);
+    cur.dO.template stage<LV>(dOs, cp.len);
+    cur.h.template stage<LV>(hs);
+    cur.dh.template stage<LV>(dhs);
+    cur.dut.template stage<LC>(dUT);
+    // the next slice's tiles load under this slice's products (the last slice
+    // re-reads itself, so the count of loads in flight never changes)
+    load_slice(nxt, c0 + VS < DV ? c0 + VS : c0);
     __syncthreads();
     if (thread_x() < DK) {
       const int d = thread_x();
@@ -335,6 +421,7 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
     dQg.template mma<float, VS>(KRow<float, LV>{dOs}, KRow<float, LV>{hs});
     dKh.template mma<float, VS>(KRow<float, LV>{Ups}, KRow<float, LV>{dhs});
     __syncthreads();
+    cur = nxt;
   }
   float* dPt = dPg + tile * CH * CH;
   float* dAt = dAg + tile * CH * CH;
@@ -377,16 +464,26 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
   const long rsk = (long)H * DK, bk = (cp.row0 * H + h) * DK + d0;
-  load_rows<DS, LS>(q + bk, rsk, cp.len, Qs);
-  load_rows<DS, LS>(k + bk, rsk, cp.len, Ks);
-  if (g) load_rows<DS, LS>(g + bk, rsk, cp.len, Gs);
-  else
-    for (int i = thread_x(); i < CH * LS; i += blockDim.x) Gs[i] = 0.f;
-  if (b) load_rows<DS, LS>(b + bk, rsk, cp.len, Bs);
-  else
-    for (int i = thread_x(); i < CH * LS; i += blockDim.x) Bs[i] = 0.f;
-  load_dense<CH, CH, LC>(dPg + tile * CH * CH, dPs);
-  load_dense<CH, CH, LC>(dAg + tile * CH * CH, dAs);
+  {
+    RowsIn<DS, 512, float> qin, kin, gin, bin;
+    TileIn<CH, CH, 512> pin, ain;
+    qin.load(q + bk, rsk, cp.len);
+    kin.load(k + bk, rsk, cp.len);
+    if (g) gin.load(g + bk, rsk, cp.len);
+    if (b) bin.load(b + bk, rsk, cp.len);
+    pin.load(dPg + tile * CH * CH, CH);
+    ain.load(dAg + tile * CH * CH, CH);
+    qin.template stage<LS>(Qs, cp.len);
+    kin.template stage<LS>(Ks, cp.len);
+    if (g) gin.template stage<LS>(Gs, cp.len);
+    else
+      for (int i = thread_x(); i < CH * LS; i += blockDim.x) Gs[i] = 0.f;
+    if (b) bin.template stage<LS>(Bs, cp.len);
+    else
+      for (int i = thread_x(); i < CH * LS; i += blockDim.x) Bs[i] = 0.f;
+    pin.template stage<LC>(dPs);
+    ain.template stage<LC>(dAs);
+  }
   __syncthreads();
   if (g) {
     cw_cumsum_columns<DS, LS>(Gs);

@@ -284,6 +284,11 @@ struct Mma<bf16> {
   }
 };
 
+// fp32: the contraction is enumerated in groups of 16 -- in group G, lane l
+// supplies k = 16 G + 4 (l >> 4) + t at sub-step t (k-step k0 = 16 G + 4 t) --
+// so a lane's four operands of a group are contiguous on both sides of every
+// product: one 16-byte load (load4) serves four k-steps.  Every fp32 fragment
+// goes through load or load4, so A and B always agree on the enumeration.
 template <>
 struct Mma<float> {
   static constexpr int KSTEP = 4;
@@ -291,7 +296,13 @@ struct Mma<float> {
   template <class V>
   __device__ __forceinline__ static frag load(const V& v, int o, int k0) {
     const int l = lane_id();
-    return v.get(o + (l & 15), k0 + (l >> 4));
+    return v.get(o + (l & 15), (k0 & ~15) + 4 * (l >> 4) + ((k0 & 15) >> 2));
+  }
+  // the four sub-steps of group k16 / 16 (k16 % 16 == 0), for views with ptr()
+  template <class V>
+  __device__ __forceinline__ static f32x4 load4(const V& v, int o, int k16) {
+    const int l = lane_id();
+    return *reinterpret_cast<const f32x4*>(v.ptr(o + (l & 15), k16 + 4 * (l >> 4)));
   }
   __device__ __forceinline__ static f32x4 mma(frag a, frag b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -321,6 +332,26 @@ struct Tiles {
   template <typename OP, int K, class VA, class VB>
   __device__ __forceinline__ void mma(const VA& A, const VB& B) {
     typedef Mma<OP> X;
+    if constexpr (sizeof(OP) == 4 && VA::kVec && VB::kVec) {
+      static_assert(K % 16 == 0, "whole groups of the fp32 enumeration");
+      // one group (4 x TM x TN products) per iteration is ILP enough; a second
+      // one in flight would double the live fragments
+#pragma unroll 1
+      for (int k16 = 0; k16 < K; k16 += 16) {
+        f32x4 fa[TM], fb[TN];
+#pragma unroll
+        for (int a = 0; a < TM; ++a) fa[a] = X::load4(A, m0(a), k16);
+#pragma unroll
+        for (int b = 0; b < TN; ++b) fb[b] = X::load4(B, n0(b), k16);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int a = 0; a < TM; ++a)
+#pragma unroll
+            for (int b = 0; b < TN; ++b) acc[a][b] = X::mma(fa[a][t], fb[b][t], acc[a][b]);
+      }
+      return;
+    }
 #pragma unroll 2
     for (int k0 = 0; k0 < K; k0 += X::KSTEP) {
       typename X::frag fa[TM], fb[TN];
@@ -342,10 +373,21 @@ struct Tiles {
     typename Mma<OP>::frag f[K / Mma<OP>::KSTEP][TM];
     template <class V>
     __device__ __forceinline__ void load(const V& A) {
+      if constexpr (sizeof(OP) == 4 && V::kVec) {
 #pragma unroll
-      for (int s = 0; s < K / Mma<OP>::KSTEP; ++s)
+        for (int g = 0; g < K / 16; ++g)
 #pragma unroll
-        for (int a = 0; a < TM; ++a) f[s][a] = Mma<OP>::load(A, m0(a), s * Mma<OP>::KSTEP);
+          for (int a = 0; a < TM; ++a) {
+            const f32x4 x = Mma<float>::load4(A, m0(a), 16 * g);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) f[4 * g + t][a] = x[t];
+          }
+      } else {
+#pragma unroll
+        for (int s = 0; s < K / Mma<OP>::KSTEP; ++s)
+#pragma unroll
+          for (int a = 0; a < TM; ++a) f[s][a] = Mma<OP>::load(A, m0(a), s * Mma<OP>::KSTEP);
+      }
     }
   };
   template <typename OP, int K>
@@ -353,10 +395,21 @@ struct Tiles {
     typename Mma<OP>::frag f[K / Mma<OP>::KSTEP][TN];
     template <class V>
     __device__ __forceinline__ void load(const V& B) {
+      if constexpr (sizeof(OP) == 4 && V::kVec) {
 #pragma unroll
-      for (int s = 0; s < K / Mma<OP>::KSTEP; ++s)
+        for (int g = 0; g < K / 16; ++g)
 #pragma unroll
-        for (int b = 0; b < TN; ++b) f[s][b] = Mma<OP>::load(B, n0(b), s * Mma<OP>::KSTEP);
+          for (int b = 0; b < TN; ++b) {
+            const f32x4 x = Mma<float>::load4(B, n0(b), 16 * g);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) f[4 * g + t][b] = x[t];
+          }
+      } else {
+#pragma unroll
+        for (int s = 0; s < K / Mma<OP>::KSTEP; ++s)
+#pragma unroll
+          for (int b = 0; b < TN; ++b) f[s][b] = Mma<OP>::load(B, n0(b), s * Mma<OP>::KSTEP);
+      }
     }
   };
 
@@ -364,6 +417,21 @@ struct Tiles {
   template <typename OP, int K, class VB>
   __device__ __forceinline__ void mma(const AFr<OP, K>& fa, const VB& B) {
     typedef Mma<OP> X;
+    if constexpr (sizeof(OP) == 4 && VB::kVec) {
+#pragma unroll
+      for (int g = 0; g < K / 16; ++g) {
+        f32x4 fb[TN];
+#pragma unroll
+        for (int b = 0; b < TN; ++b) fb[b] = X::load4(B, n0(b), 16 * g);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int a = 0; a < TM; ++a)
+#pragma unroll
+            for (int b = 0; b < TN; ++b) acc[a][b] = X::mma(fa.f[4 * g + t][a], fb[b][t], acc[a][b]);
+      }
+      return;
+    }
 #pragma unroll
     for (int s = 0; s < K / X::KSTEP; ++s) {
       typename X::frag fb[TN];

@@ -334,10 +334,10 @@ struct Tiles {
     typedef Mma<OP> X;
     if constexpr (sizeof(OP) == 4 && VA::kVec && VB::kVec) {
       static_assert(K % 16 == 0, "whole groups of the fp32 enumeration");
-      // one group (4 x TM x TN products) per iteration is ILP enough; a second
-      // one in flight would double the live fragments
-#pragma unroll 1
-      for (int k16 = 0; k16 < K; k16 += 16) {
+      // one group (4 x TM x TN products) per iteration; with few output tiles a
+      // second group in flight hides the loads, with more it would only double
+      // the live fragments
+      auto group = [&](int k16) __attribute__((always_inline)) {
         f32x4 fa[TM], fb[TN];
 #pragma unroll
         for (int a = 0; a < TM; ++a) fa[a] = X::load4(A, m0(a), k16);
@@ -349,6 +349,13 @@ struct Tiles {
           for (int a = 0; a < TM; ++a)
 #pragma unroll
             for (int b = 0; b < TN; ++b) acc[a][b] = X::mma(fa[a][t], fb[b][t], acc[a][b]);
+      };
+      if constexpr (TM * TN <= 2) {
+#pragma unroll 2
+        for (int k16 = 0; k16 < K; k16 += 16) group(k16);
+      } else {
+#pragma unroll 1
+        for (int k16 = 0; k16 < K; k16 += 16) group(k16);
       }
       return;
     }

@@ -75,8 +75,9 @@ __device__ __forceinline__ float cw_ref(const float* Gs, int R, int d) {
 // generic forward scan (P, diag-scaled Q, Khat^T, W, U); backward mode writes
 // those of the reverse scan and the gradient kernels (P^T, (Gamma Q)^T,
 // Khat, W^T, T, Gamma * Kb, dO^T).  Both write G_last per channel.
+constexpr int CW_PREP_THREADS = 1024;  // 16 waves: one block per CU (LDS), so all its latency hiding is in-block
 template <int DK, int DV, bool BWD>
-__global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __restrict__ q,
+__global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, const float* __restrict__ q,
                                                  const float* __restrict__ k, const float* __restrict__ v,
                                                  const float* __restrict__ g, const float* __restrict__ b,
                                                  const float* __restrict__ w, const float* __restrict__ dO,
@@ -104,9 +105,10 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
   // every input row of the block is requested up front: q, k, g, b, then the
   // forward's v and w slices (or the backward's dO)
   constexpr int NSL = BWD ? 1 : DV / VS;
-  RowsIn<DK, 512, float> qin, kin, gin, bin;
-  RowsIn<VS, 512, float> vin[NSL], win[NSL];
-  RowsIn<DV, 512, float> doin;
+  constexpr int NT = CW_PREP_THREADS, WN = NT / 256;  // wave columns of the 64-row products
+  RowsIn<DK, NT, float> qin, kin, gin, bin;
+  RowsIn<VS, NT, float> vin[NSL], win[NSL];
+  RowsIn<DV, NT, float> doin;
   qin.load(q + bk, rsk, cp.len);
   kin.load(k + bk, rsk, cp.len);
   if (g) gin.load(g + bk, rsk, cp.len);
@@ -165,14 +167,14 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
   }
   __syncthreads();
 
-  // P and A: wave (R, ·) of Tiles<64, 64, 4, 2> owns 16-row block R
-  const int R = wave_id() / 2;
+  // P and A: wave (R, ·) of Tiles<64, 64, 4, WN> owns 16-row block R
+  const int R = wave_id() / WN;
   auto ref = [&](int d) { return cw_ref<LK>(Gs, R, d); };
   auto kcol = kfun<float>([&](int i, int d) {
     return i < 16 * R ? Ks[i * LK + d] * __expf(ref(d) - Gs[i * LK + d]) : 0.f;
   });
   {
-    Tiles<CH, CH, 4, 2> p;
+    Tiles<CH, CH, 4, WN> p;
     p.zero();
     p.template mma<float, DK>(kfun<float>([&](int r, int d) { return Qs[r * LK + d] * __expf(Gs[r * LK + d] - ref(d)); }),
                               kcol);
@@ -185,7 +187,7 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
     });
   }
   if (b) {
-    Tiles<CH, CH, 4, 2> a;
+    Tiles<CH, CH, 4, WN> a;
     a.zero();
     a.template mma<float, DK>(kfun<float>([&](int r, int d) { return Bk[r * LK + d] * __expf(Gs[r * LK + d] - ref(d)); }),
                               kcol);
@@ -242,7 +244,7 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
   {
     float* Wt = Wg + tile * CH * DK;
     if (b) {
-      Tiles<CH, DK, 4, 2> wt;
+      Tiles<CH, DK, 4, WN> wt;
       wt.zero();
       wt.template mma<float, CH>(KRow<float, LC>{Tf}, KCol<float, LK>{Bk});
       wt.each([&](int r, int d, float& x) {
@@ -265,7 +267,7 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
       __syncthreads();
 #pragma unroll
       for (int pc = 0; pc < doin.N; ++pc) {
-        const int idx = thread_x() + pc * 512, r = idx / PR, c = (idx - r * PR) * 4;
+        const int idx = thread_x() + pc * NT, r = idx / PR, c = (idx - r * PR) * 4;
         if (c / PW == ps) *reinterpret_cast<uint4*>(Ks + r * LK + (c - ps * PW)) = keep16(r < cp.len, doin.u[pc]);
       }
       __syncthreads();
@@ -285,7 +287,7 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
 #pragma unroll
       for (int pc = 0; pc < vin[t].N; ++pc) {
         constexpr int PR = VS / 4;
-        const int idx = thread_x() + pc * 512, r = idx / PR, c = (idx - r * PR) * 4;
+        const int idx = thread_x() + pc * NT, r = idx / PR, c = (idx - r * PR) * 4;
         float4 x = __builtin_bit_cast(float4, keep16(r < cp.len, vin[t].u[pc]));
         if (w) {
           const float4 y = __builtin_bit_cast(float4, win[t].u[pc]);
@@ -294,7 +296,7 @@ __global__ __launch_bounds__(512) void k_cw_prep(Geo geo, int H, const float* __
         *reinterpret_cast<float4*>(Vw + r * LV + c) = x;
       }
       __syncthreads();
-      Tiles<CH, VS, 4, 2> uu;
+      Tiles<CH, VS, 4, WN> uu;
       uu.zero();
       uu.template mma<float, CH>(KRow<float, LC>{Tf}, KCol<float, LV>{Vw});
       const int l = lane_id();
@@ -601,7 +603,7 @@ static hipError_t launch_cw_fwd_t(const CwFwdArgs& a) {
     if (e != hipSuccess) return e;
   }
   if (geo.total_chunks > 0)
-    hipLaunchKernelGGL((k_cw_prep<DK, DV, false>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
+    hipLaunchKernelGGL((k_cw_prep<DK, DV, false>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream, geo, H,
                        a.q, a.k, a.v, a.g, a.b, a.w, (const float*)nullptr, w.gC, w.P, w.Qg, w.KhT, w.W, w.U,
                        (float*)nullptr, (float*)nullptr, (float*)nullptr);
   stage_mark(a.events, 1, a.stream);
@@ -628,7 +630,7 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
     if (e != hipSuccess) return e;
   }
   if (geo.total_chunks > 0)
-    hipLaunchKernelGGL((k_cw_prep<DK, DV, true>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
+    hipLaunchKernelGGL((k_cw_prep<DK, DV, true>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream, geo, H,
                        a.q, a.k, a.v, a.g, a.b, a.w, a.dO, w.gC, w.PT, w.QgT, w.Kh, w.WT, (float*)nullptr, w.T,
                        w.KbG, w.dOT);
   stage_mark(a.events, 1, a.stream);

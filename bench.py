@@ -34,8 +34,20 @@ BF16_PEAK_TFLOPS = 2500.0
 CH = 64
 ROOT = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bf16_B4_T4096_H16_d128.json")
+CW_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cw_f32_B4_T4096_H16_d128.json")
 STAGE_OF_KERNEL = {"k_prep_fwd": "fwd_prep", "k_scan_fwd": "fwd_scan", "k_prep_bwd": "bwd_prep",
                    "k_scan_bwd": "bwd_scan", "k_grad_bf": "bwd_grad"}
+
+
+def cw_stage_of(name: str):
+    """Stage of a channel-wise kernel name (mangled or demangled), or None."""
+    if "k_cw_prep" in name:
+        return "cw_bwd_prep" if ("true>" in name or "Lb1E" in name) else "cw_fwd_prep"
+    for k, st in (("k_scan_fwd", "cw_fwd_scan"), ("k_scan_bwd", "cw_bwd_scan"),
+                  ("k_cw_grad_v", "cw_bwd_grad_v"), ("k_cw_grad_d", "cw_bwd_grad_d")):
+        if k in name:
+            return st
+    return None
 COPY_BYTES = 256 * 1024 * 1024
 
 
@@ -52,11 +64,11 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(stage: str):
+def measured_traffic(stage: str, path: str = TRAFFIC_FILE):
     """HBM bytes per launch of `stage` from the committed counter summary, or None
     when there is none or the kernels changed since it was taken."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(path) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
@@ -76,17 +88,25 @@ def _counter_rows(d):
     return out
 
 
-def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, command):
+def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, command, cw=False):
     """Turn FETCH_SIZE / WRITE_SIZE passes (KiB per dispatch) over the bench and
     over a plain copy of COPY_BYTES into HBM bytes per launch of each stage."""
+    def stage_of(name):
+        if cw:
+            return cw_stage_of(name)
+        for k, st in STAGE_OF_KERNEL.items():
+            if k in name:
+                return st
+        return None
+
     def per_kernel(d, counter):
         acc = {}
         for r in _counter_rows(d):
             if r["Counter_Name"] != counter:
                 continue
-            for k, st in STAGE_OF_KERNEL.items():
-                if k in r["Kernel_Name"]:
-                    acc.setdefault(st, []).append(float(r["Counter_Value"]))
+            st = stage_of(r["Kernel_Name"])
+            if st is not None:
+                acc.setdefault(st, []).append(float(r["Counter_Value"]))
         return {st: sum(v) / len(v) for st, v in acc.items()}
 
     def copy_kib(d, counter):
@@ -95,7 +115,7 @@ def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, c
     fscale = COPY_BYTES / 1024.0 / copy_kib(calib_fetch_dir, "FETCH_SIZE")
     wscale = COPY_BYTES / 1024.0 / copy_kib(calib_write_dir, "WRITE_SIZE")
     f, w = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
-    km = kernel_model(4, 4096, 16, 128, 128, 2)
+    km = cw_kernel_model(4, 4096, 16, 128, 128) if cw else kernel_model(4, 4096, 16, 128, 128, 2)
     kern = {}
     for st in sorted(f):
         b = (f[st] * fscale + w.get(st, 0.0) * wscale) * 1024.0
@@ -306,7 +326,8 @@ def bench_cw(a):
         "config": {"workload": "channel-wise gated delta rule fwd+bwd (full GDN gates), fp32 I/O and state, "
                                "B=4 T=4096 H=16 dk=dv=128 chunk=64", "B": B, "T": T, "H": H, "dk": dk, "dv": dv},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(dom, CW_TRAFFIC_FILE),
                      "algorithmic_bytes_per_launch": int(km[dom][0]), "avg_launch_ms": round(stage_ms[dom], 4),
                      "mfma_tflops": round(km[dom][1] / dom_s / 1e12, 1)},
         "timing": {"cold_caches": True, "note": "mean of per-step HIP event intervals, each step after a "
@@ -436,8 +457,8 @@ def main(argv=None):
         print(md)
         return 0
     if a.summarize_counters:
-        t = summarize_counters(*a.summarize_counters, a.command)
-        with open(TRAFFIC_FILE, "w") as fh:
+        t = summarize_counters(*a.summarize_counters, a.command, cw=a.cw)
+        with open(CW_TRAFFIC_FILE if a.cw else TRAFFIC_FILE, "w") as fh:
             json.dump(t, fh, indent=1)
         print(json.dumps(t))
         return 0

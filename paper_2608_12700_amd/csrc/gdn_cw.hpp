@@ -462,9 +462,15 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
   __shared__ __align__(16) float Qs[CH * LS], Ks[CH * LS], Bs[CH * LS], Gs[CH * LS];
   float* dGs = Qs;  // dG and Khat * dKhat take Q's and K's tiles once every wave is done with them
   float* Zs = Ks;
-  const int ci = blockIdx.x, h = blockIdx.y, d0 = blockIdx.z * DS;
+  // The channel slices of one (chunk, head) tile re-read its dP and dA: they
+  // get block ids b, b + 8, b + 16, ... (blocks are dealt to the 8 XCDs round
+  // robin), so they run together on one XCD and share its L2.
+  constexpr int NSL = DK / DS;
+  const int bid = blockIdx.x, grp = bid / (8 * NSL), within = bid - grp * 8 * NSL;
+  const long tile = (long)grp * 8 + (within & 7);
+  if (tile >= (long)geo.total_chunks * H) return;  // whole block: the grid is rounded up to groups of 8 tiles
+  const int ci = (int)(tile / H), h = (int)(tile - (long)ci * H), d0 = (within >> 3) * DS;
   const ChunkPos cp = chunk_pos(geo, ci);
-  const long tile = (long)ci * H + h;
   const long rsk = (long)H * DK, bk = (cp.row0 * H + h) * DK + d0;
   {
     RowsIn<DS, 512, float> qin, kin, gin, bin;
@@ -645,7 +651,8 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
                        a.dO, a.states, (const float*)w.T, (const float*)w.KbG, (const float*)w.dh,
                        (const float*)w.dUT, a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg, w.dKh, w.hdh);
     stage_mark(a.events, 3, a.stream);
-    hipLaunchKernelGGL((k_cw_grad_d<DK>), dim3(geo.total_chunks, H, DK / 32), dim3(512), 0, a.stream, geo, H, a.q,
+    const long tiles = (long)geo.total_chunks * H;
+    hipLaunchKernelGGL((k_cw_grad_d<DK>), dim3((unsigned)((tiles + 7) / 8 * 8 * (DK / 32))), dim3(512), 0, a.stream, geo, H, a.q,
                        a.k, a.g, a.b, (const float*)w.dP, (const float*)w.dA, (const float*)w.X,
                        (const float*)w.dQg, (const float*)w.dKh, (const float*)w.hdh, a.dq, a.dk_, a.dg, a.db);
   } else {

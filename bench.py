@@ -88,7 +88,7 @@ def _counter_rows(d):
     return out
 
 
-def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, command, cw=False):
+def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, command, cw=False, cw_es=2):
     """Turn FETCH_SIZE / WRITE_SIZE passes (KiB per dispatch) over the bench and
     over a plain copy of COPY_BYTES into HBM bytes per launch of each stage."""
     def stage_of(name):
@@ -115,7 +115,7 @@ def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, c
     fscale = COPY_BYTES / 1024.0 / copy_kib(calib_fetch_dir, "FETCH_SIZE")
     wscale = COPY_BYTES / 1024.0 / copy_kib(calib_write_dir, "WRITE_SIZE")
     f, w = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
-    km = cw_kernel_model(4, 4096, 16, 128, 128) if cw else kernel_model(4, 4096, 16, 128, 128, 2)
+    km = cw_kernel_model(4, 4096, 16, 128, 128, es=cw_es) if cw else kernel_model(4, 4096, 16, 128, 128, 2)
     kern = {}
     for st in sorted(f):
         b = (f[st] * fscale + w.get(st, 0.0) * wscale) * 1024.0
@@ -212,28 +212,30 @@ def kernel_model(B, T, H, dk, dv, es, N=None):
     return out
 
 
-def cw_kernel_model(B, T, H, dk, dv, N=None):
-    """Algorithmic bytes and flops per launch of the channel-wise stages (fp32:
-    each kernel's own inputs and outputs moved once)."""
+def cw_kernel_model(B, T, H, dk, dv, N=None, es=4):
+    """Algorithmic bytes and flops per launch of the channel-wise stages (each
+    kernel's own inputs and outputs moved once; the activations q, k, v, o, dO
+    and their gradients at es bytes, everything else fp32)."""
     N = B if N is None else N
     tiles = B * (-(-T // CH)) * H
     ck, cv, cc, st, vk = CH * dk * 4, CH * dv * 4, CH * CH * 4, dk * dv * 4, dk * 4
+    ak, av = CH * dk * es, CH * dv * es  # activation tiles
     per = {
         # q, k, g, b, v, w -> G_last, P, e^G Q, Khat^T, W, U
-        "cw_fwd_prep": (4 * ck + 2 * cv + vk + cc + 3 * ck + cv,
+        "cw_fwd_prep": (2 * ak + 2 * ck + av + cv + vk + cc + 3 * ck + cv,
                         2 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dk + 2 * CH * CH * dv),
         # e^G Q, W, Khat^T, P, U, G_last -> chunk states, o
-        "cw_fwd_scan": (3 * ck + cc + cv + vk + st + cv, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
+        "cw_fwd_scan": (3 * ck + cc + cv + vk + st + av, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
         # q, k, g, b, dO -> G_last, P^T, (e^G Q)^T, Khat, W^T, T, Gamma*b*k, dO^T
-        "cw_bwd_prep": (4 * ck + cv + vk + 2 * cc + 4 * ck + cv,
+        "cw_bwd_prep": (2 * ak + 2 * ck + av + vk + 2 * cc + 4 * ck + cv,
                         2 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dk),
         # Khat, W^T, (e^G Q)^T, dO^T, P^T, G_last -> dh, dU'^T
         "cw_bwd_scan": (3 * ck + cv + cc + vk + st + cv, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
         # v, w, dO, state, T, Gamma*b*k, dh, dU'^T -> dv, dw, dP, dA, X, dQg, dKhat, <h, dh>
-        "cw_bwd_grad_v": (3 * cv + st + cc + ck + st + cv + 2 * cv + 2 * cc + 3 * ck + vk,
+        "cw_bwd_grad_v": (2 * av + cv + st + cc + ck + st + cv + av + cv + 2 * cc + 3 * ck + vk,
                           2 * CH * dk * dv + 3 * 2 * CH * CH * dv + 3 * 2 * CH * dk * dv),
         # q, k, g, b, dP, dA, X, dQg, dKhat, <h, dh> -> dq, dk, dg, db
-        "cw_bwd_grad_d": (4 * ck + 2 * cc + 3 * ck + vk + 4 * ck, 4 * 2 * CH * CH * dk),
+        "cw_bwd_grad_d": (2 * ak + 2 * ck + 2 * cc + 3 * ck + vk + 2 * ak + 2 * ck, 4 * 2 * CH * CH * dk),
     }
     out = {k: (b * tiles, f * tiles) for k, (b, f) in per.items()}
     sio = 2 * N * H * dk * dv * 4
@@ -243,7 +245,7 @@ def cw_kernel_model(B, T, H, dk, dv, N=None):
 
 
 def bench_cw(a):
-    """The channel-wise path (per-channel g, b, w; fp32) on B4 T4096 H16 d128: one JSON line."""
+    """The channel-wise path (per-channel g, b, w) on B4 T4096 H16 d128: one JSON line."""
     import time
 
     import numpy as np
@@ -253,7 +255,8 @@ def bench_cw(a):
     from paper_2608_12700_amd import gdn
 
     B, T, H, dk, dv = 4, 4096, 16, 128, 128
-    case = W.make_cw_case("cw_B4_T4096_H16_d128", B, T, H, dk, dv, gates="gbw", seed=6)
+    bf = a.cw_io == "bf16"
+    case = W.make_cw_case("cw_B4_T4096_H16_d128", B, T, H, dk, dv, gates="gbw", seed=6, io_dtype=a.cw_io)
     cpu = None
     if not a.no_cpu_baseline:
         # the oracle on one (b, h) stream of the same inputs, one core
@@ -271,7 +274,10 @@ def bench_cw(a):
     torch.cuda.set_device(dev)
     t = {n: (None if getattr(case, n) is None else torch.from_numpy(getattr(case, n)).to(dev))
          for n in ("q", "k", "v", "g", "b", "w", "S0", "dO", "dS_T")}
-    p = gdn.make_problem(B, T, H, dk, dv, io_dtype=gdn.GDN_F32)
+    if bf:
+        for n in ("q", "k", "v", "dO"):
+            t[n] = t[n].to(torch.bfloat16)
+    p = gdn.make_problem(B, T, H, dk, dv, io_dtype=gdn.GDN_BF16 if bf else gdn.GDN_F32)
     nch = gdn.gdn_num_chunks(p)
     o = torch.empty_like(t["v"])
     S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
@@ -312,19 +318,20 @@ def bench_cw(a):
                 if nm is not None:
                     stage_ms[nm] = stage_ms.get(nm, 0.0) + hip.ms(e[j], e[j + 1]) / a.steps
     ok = all(bool(torch.isfinite(x).all()) for x in [o, S_T] + grads)
-    km = cw_kernel_model(B, T, H, dk, dv)
+    km = cw_kernel_model(B, T, H, dk, dv, es=2 if bf else 4)
     dom = max(km, key=lambda n: stage_ms[n])
     dom_s = stage_ms[dom] / 1e3
     ach = km[dom][0] / dom_s / 1e9
     res = {
-        "metric": "GDN channel-wise (per-channel g, b, w) fwd+bwd tokens/s at B4 T4096 H16 d128 fp32",
+        "metric": f"GDN channel-wise (per-channel g, b, w) fwd+bwd tokens/s at B4 T4096 H16 d128 {a.cw_io}",
         "value": round(B * T / (ms_step / 1e3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32",
+        "vs_baseline": None, "dtype": "f32 (activations " + a.cw_io + ")",
         "data": "synthetic (seeded: q,k L2-normalised N(0,1); v,dO N(0,1); g=-softplus(N) per channel; "
                 "b=sigmoid(N) per channel; w=1.5*sigmoid(N) per channel; S0 N(0,0.1^2); dS_T N(0,1))",
-        "config": {"workload": "channel-wise gated delta rule fwd+bwd (full GDN gates), fp32 I/O and state, "
-                               "B=4 T=4096 H=16 dk=dv=128 chunk=64", "B": B, "T": T, "H": H, "dk": dk, "dv": dv},
+        "config": {"workload": f"channel-wise gated delta rule fwd+bwd (full GDN gates), {a.cw_io} activations, "
+                               "fp32 gates, state and operands, B=4 T=4096 H=16 dk=dv=128 chunk=64",
+                   "B": B, "T": T, "H": H, "dk": dk, "dv": dv, "io": a.cw_io},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(dom, CW_TRAFFIC_FILE),
@@ -441,7 +448,9 @@ def main(argv=None):
                     "rocprofv3 --kernel-trace --stats --output-format csv folder")
     ap.add_argument("--command", default="", help="the profiling command recorded in the summary")
     ap.add_argument("--cw", action="store_true",
-                    help="measure the channel-wise path (per-channel g, b, w; fp32) instead")
+                    help="measure the channel-wise path (per-channel g, b, w) instead")
+    ap.add_argument("--cw-io", choices=("bf16", "f32"), default="bf16",
+                    help="activation dtype of the channel-wise measurement")
     ap.add_argument("--trace-out", default="kernel_trace_bf16_B4_T4096_H16_d128.md",
                     help="file name under profiles/ for --summarize-trace")
     a = ap.parse_args(argv)
@@ -457,7 +466,7 @@ def main(argv=None):
         print(md)
         return 0
     if a.summarize_counters:
-        t = summarize_counters(*a.summarize_counters, a.command, cw=a.cw)
+        t = summarize_counters(*a.summarize_counters, a.command, cw=a.cw, cw_es=2 if a.cw_io == "bf16" else 4)
         with open(CW_TRAFFIC_FILE if a.cw else TRAFFIC_FILE, "w") as fh:
             json.dump(t, fh, indent=1)
         print(json.dumps(t))

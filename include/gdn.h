@@ -173,9 +173,11 @@ gdn_status gdn_bwd_ex(const gdn_problem* p, const void* q, const void* k, const 
  * full GDN (all three), KDA (b = w = beta_t broadcast over the channels),
  * GLA (g only), LA (none).
  *
- * Layouts as above, with g, b [B,T,H,d_k] and w [B,T,H,d_v] fp32 row-major
- * (packed sequences: B = 1 and cu_seqlens as above).  Activations are fp32:
- * io_dtype must be GDN_F32 (else GDN_ERR_UNSUPPORTED); `variant` is not read.
+ * Layouts as above, with g, b [B,T,H,d_k] and w [B,T,H,d_v] (and dg, db, dw)
+ * fp32 row-major (packed sequences: B = 1 and cu_seqlens as above).  q, k, v,
+ * o, dO, dq, dk, dv are in io_dtype (fp32 or bf16); every operand inside the
+ * chunked algorithm is fp32 (fp32 matrix cores) either way.  `variant` is not
+ * read.
  * chunk_states has the layout and meaning of gdn_fwd's.  The chunked kernels
  * form each decay exp(G_r - G_i) either per term or split at a reference row
  * between r and i, so for a decay (every g <= 0) no factor exceeds 1; a g > 0
@@ -189,17 +191,17 @@ size_t gdn_cw_fwd_workspace_size(const gdn_problem* p);
 size_t gdn_cw_bwd_workspace_size(const gdn_problem* p);
 
 /* Forward: o [B,T,H,d_v], S_T and chunk_states as gdn_fwd. */
-gdn_status gdn_cw_fwd(const gdn_problem* p, const float* q, const float* k, const float* v,
-                      const float* g, const float* b, const float* w, const float* S0, float* o,
+gdn_status gdn_cw_fwd(const gdn_problem* p, const void* q, const void* k, const void* v,
+                      const float* g, const float* b, const float* w, const float* S0, void* o,
                       float* S_T, float* chunk_states, void* workspace, size_t workspace_bytes,
                       void* stream);
 
 /* Backward of the loss sum(dO * o) + <dS_T, S_T> (dS_T may be NULL = zero).
  * dg, db, dw have the shapes of g, b, w and must be non-NULL exactly when the
  * gate is (else GDN_ERR_VARIANT); dq, dk, dv, dS0 as gdn_bwd. */
-gdn_status gdn_cw_bwd(const gdn_problem* p, const float* q, const float* k, const float* v,
+gdn_status gdn_cw_bwd(const gdn_problem* p, const void* q, const void* k, const void* v,
                       const float* g, const float* b, const float* w, const float* chunk_states,
-                      const float* dO, const float* dS_T, float* dq, float* dk, float* dv, float* dg,
+                      const void* dO, const float* dS_T, void* dq, void* dk, void* dv, float* dg,
                       float* db, float* dw, float* dS0, void* workspace, size_t workspace_bytes,
                       void* stream);
 
@@ -207,13 +209,13 @@ gdn_status gdn_cw_bwd(const gdn_problem* p, const float* q, const float* k, cons
  * prep, 1 state scan with the chunk output, 2 and 3 empty.  Backward: 0 chunk
  * prep, 1 reverse state scan, 2 value-slice gradients (dv, dw and the chunk
  * products), 3 channel gradients (dq, dk, dg, db). */
-gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const float* q, const float* k, const float* v,
-                         const float* g, const float* b, const float* w, const float* S0, float* o,
+gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
+                         const float* g, const float* b, const float* w, const float* S0, void* o,
                          float* S_T, float* chunk_states, void* workspace, size_t workspace_bytes,
                          void* stream, void* const* events);
-gdn_status gdn_cw_bwd_ex(const gdn_problem* p, const float* q, const float* k, const float* v,
+gdn_status gdn_cw_bwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
                          const float* g, const float* b, const float* w, const float* chunk_states,
-                         const float* dO, const float* dS_T, float* dq, float* dk, float* dv, float* dg,
+                         const void* dO, const float* dS_T, void* dq, void* dk, void* dv, float* dg,
                          float* db, float* dw, float* dS0, void* workspace, size_t workspace_bytes,
                          void* stream, void* const* events);
 

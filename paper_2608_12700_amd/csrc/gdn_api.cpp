@@ -196,13 +196,9 @@ void layout_cw_bwd(const Shape& s, char* base, CwBwdWs* w, size_t* total) {
   *total = b.off;
 }
 
-// The channel-wise entry points take fp32 activations only; the problem's
-// variant is not read (the gate pointers select the member).
-gdn_status check_cw_problem(const gdn_problem* p, Shape* s) {
-  const gdn_status st = check_problem(p, s);
-  if (st != GDN_OK) return st;
-  return p->io_dtype == GDN_F32 ? GDN_OK : GDN_ERR_UNSUPPORTED;
-}
+// The channel-wise entry points: the problem's variant is not read (the gate
+// pointers select the member).
+gdn_status check_cw_problem(const gdn_problem* p, Shape* s) { return check_problem(p, s); }
 
 Geo make_geo(const Shape& s, const gdn_problem* p, const int* chunk_off) {
   Geo g;
@@ -400,15 +396,15 @@ size_t gdn_cw_bwd_workspace_size(const gdn_problem* p) {
   return total;
 }
 
-gdn_status gdn_cw_fwd(const gdn_problem* p, const float* q, const float* k, const float* v, const float* g,
-                      const float* b, const float* w, const float* S0, float* o, float* S_T,
+gdn_status gdn_cw_fwd(const gdn_problem* p, const void* q, const void* k, const void* v, const float* g,
+                      const float* b, const float* w, const float* S0, void* o, float* S_T,
                       float* chunk_states, void* workspace, size_t workspace_bytes, void* stream) {
   return gdn_cw_fwd_ex(p, q, k, v, g, b, w, S0, o, S_T, chunk_states, workspace, workspace_bytes, stream,
                        nullptr);
 }
 
-gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const float* q, const float* k, const float* v,
-                         const float* g, const float* b, const float* w, const float* S0, float* o,
+gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
+                         const float* g, const float* b, const float* w, const float* S0, void* o,
                          float* S_T, float* chunk_states, void* workspace, size_t workspace_bytes,
                          void* stream, void* const* events) {
   try {
@@ -416,7 +412,8 @@ gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const float* q, const float* k, c
     gdn_status st = check_cw_problem(p, &s);
     if (st != GDN_OK) return st;
     const size_t tok = (size_t)s.B * s.T * s.H;
-    const size_t qk_b = tok * s.dk * 4, v_b = tok * s.dv * 4;
+    const size_t qk_b = tok * s.dk * s.es, v_b = tok * s.dv * s.es;  // activations
+    const size_t gk_b = tok * s.dk * 4, gv_b = tok * s.dv * 4;        // gates (fp32)
     const size_t state_b = (size_t)s.N * s.H * s.dk * s.dv * sizeof(float);
     const size_t states_b = (size_t)s.chunks * s.H * s.dk * s.dv * sizeof(float);
     if (!need(q, qk_b) || !need(k, qk_b) || !need(v, v_b) || !need(o, v_b) || !need(S_T, state_b) ||
@@ -427,8 +424,8 @@ gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const float* q, const float* k, c
     layout_cw_fwd(s, nullptr, &ws, &ws_need);
     if (!workspace || workspace_bytes < ws_need || ((uintptr_t)workspace & (kAlign - 1)))
       return GDN_ERR_WORKSPACE;
-    const Region in[] = {{q, qk_b}, {k, qk_b}, {v, v_b}, {g, g ? qk_b : 0}, {b, b ? qk_b : 0},
-                         {w, w ? v_b : 0}, {S0, S0 ? state_b : 0},
+    const Region in[] = {{q, qk_b}, {k, qk_b}, {v, v_b}, {g, g ? gk_b : 0}, {b, b ? gk_b : 0},
+                         {w, w ? gv_b : 0}, {S0, S0 ? state_b : 0},
                          {s.packed ? p->cu_seqlens_dev : nullptr, s.packed ? (size_t)(s.N + 1) * 4 : 0}};
     const Region out[] = {{o, v_b}, {S_T, state_b}, {chunk_states, states_b}, {workspace, ws_need}};
     st = check_alias(in, 8, out, 4);
@@ -437,7 +434,7 @@ gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const float* q, const float* k, c
     layout_cw_fwd(s, static_cast<char*>(workspace), &ws, &ws_need);
     CwFwdArgs a;
     a.geo = make_geo(s, p, ws.chunk_off);
-    a.dk = (int)s.dk; a.dv = (int)s.dv;
+    a.dk = (int)s.dk; a.dv = (int)s.dv; a.io = p->io_dtype == GDN_BF16 ? DT_BF16 : DT_F32;
     a.q = q; a.k = k; a.v = v; a.g = g; a.b = b; a.w = w; a.S0 = S0;
     a.o = o; a.ST = S_T; a.states = chunk_states; a.ws = ws;
     a.stream = static_cast<hipStream_t>(stream);
@@ -452,17 +449,17 @@ gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const float* q, const float* k, c
   }
 }
 
-gdn_status gdn_cw_bwd(const gdn_problem* p, const float* q, const float* k, const float* v, const float* g,
-                      const float* b, const float* w, const float* chunk_states, const float* dO,
-                      const float* dS_T, float* dq, float* dk, float* dv, float* dg, float* db, float* dw,
+gdn_status gdn_cw_bwd(const gdn_problem* p, const void* q, const void* k, const void* v, const float* g,
+                      const float* b, const float* w, const float* chunk_states, const void* dO,
+                      const float* dS_T, void* dq, void* dk, void* dv, float* dg, float* db, float* dw,
                       float* dS0, void* workspace, size_t workspace_bytes, void* stream) {
   return gdn_cw_bwd_ex(p, q, k, v, g, b, w, chunk_states, dO, dS_T, dq, dk, dv, dg, db, dw, dS0, workspace,
                        workspace_bytes, stream, nullptr);
 }
 
-gdn_status gdn_cw_bwd_ex(const gdn_problem* p, const float* q, const float* k, const float* v,
+gdn_status gdn_cw_bwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
                          const float* g, const float* b, const float* w, const float* chunk_states,
-                         const float* dO, const float* dS_T, float* dq, float* dk, float* dv, float* dg,
+                         const void* dO, const float* dS_T, void* dq, void* dk, void* dv, float* dg,
                          float* db, float* dw, float* dS0, void* workspace, size_t workspace_bytes,
                          void* stream, void* const* events) {
   try {
@@ -470,7 +467,8 @@ gdn_status gdn_cw_bwd_ex(const gdn_problem* p, const float* q, const float* k, c
     gdn_status st = check_cw_problem(p, &s);
     if (st != GDN_OK) return st;
     const size_t tok = (size_t)s.B * s.T * s.H;
-    const size_t qk_b = tok * s.dk * 4, v_b = tok * s.dv * 4;
+    const size_t qk_b = tok * s.dk * s.es, v_b = tok * s.dv * s.es;  // activations
+    const size_t gk_b = tok * s.dk * 4, gv_b = tok * s.dv * 4;        // gates (fp32)
     const size_t state_b = (size_t)s.N * s.H * s.dk * s.dv * sizeof(float);
     const size_t states_b = (size_t)s.chunks * s.H * s.dk * s.dv * sizeof(float);
     // a gradient is written exactly for the gates that are given
@@ -485,18 +483,18 @@ gdn_status gdn_cw_bwd_ex(const gdn_problem* p, const float* q, const float* k, c
     layout_cw_bwd(s, nullptr, &ws, &ws_need);
     if (!workspace || workspace_bytes < ws_need || ((uintptr_t)workspace & (kAlign - 1)))
       return GDN_ERR_WORKSPACE;
-    const Region in[] = {{q, qk_b}, {k, qk_b}, {v, v_b}, {g, g ? qk_b : 0}, {b, b ? qk_b : 0},
-                         {w, w ? v_b : 0}, {chunk_states, states_b}, {dO, v_b}, {dS_T, dS_T ? state_b : 0},
+    const Region in[] = {{q, qk_b}, {k, qk_b}, {v, v_b}, {g, g ? gk_b : 0}, {b, b ? gk_b : 0},
+                         {w, w ? gv_b : 0}, {chunk_states, states_b}, {dO, v_b}, {dS_T, dS_T ? state_b : 0},
                          {s.packed ? p->cu_seqlens_dev : nullptr, s.packed ? (size_t)(s.N + 1) * 4 : 0}};
-    const Region out[] = {{dq, qk_b}, {dk, qk_b}, {dv, v_b}, {dg, dg ? qk_b : 0}, {db, db ? qk_b : 0},
-                          {dw, dw ? v_b : 0}, {dS0, state_b}, {workspace, ws_need}};
+    const Region out[] = {{dq, qk_b}, {dk, qk_b}, {dv, v_b}, {dg, dg ? gk_b : 0}, {db, db ? gk_b : 0},
+                          {dw, dw ? gv_b : 0}, {dS0, state_b}, {workspace, ws_need}};
     st = check_alias(in, 10, out, 8);
     if (st != GDN_OK) return st;
 
     layout_cw_bwd(s, static_cast<char*>(workspace), &ws, &ws_need);
     CwBwdArgs a;
     a.geo = make_geo(s, p, ws.chunk_off);
-    a.dk = (int)s.dk; a.dv = (int)s.dv;
+    a.dk = (int)s.dk; a.dv = (int)s.dv; a.io = p->io_dtype == GDN_BF16 ? DT_BF16 : DT_F32;
     a.q = q; a.k = k; a.v = v; a.g = g; a.b = b; a.w = w; a.states = chunk_states; a.dO = dO; a.dST = dS_T;
     a.dq = dq; a.dk_ = dk; a.dv_ = dv; a.dg = dg; a.db = db; a.dw = dw; a.dS0 = dS0; a.ws = ws;
     a.stream = static_cast<hipStream_t>(stream);

@@ -5,7 +5,8 @@
 //   S_t = (I - k_t (b_t * k_t)^T) Diag(e^{g_t}) S_{t-1} + k_t (w_t * v_t)^T,  o_t = S_t^T q_t
 //
 // with g_t, b_t in R^{d_k} and w_t in R^{d_v}; a NULL gate is neutral (g = 0,
-// b = 0, w = 1).  fp32 operands throughout (fp32 matrix cores).
+// b = 0, w = 1).  Activations (q, k, v, dO and their gradients, o) are fp32 or
+// bf16 (IO); every operand inside is fp32 (fp32 matrix cores).
 //
 // Chunked form (Sec. 4.2), per chunk of 64 tokens with G_r = sum_{s<=r} g_s (a
 // d_k-vector per row), Gamma = e^G, Kb = b * K, Khat_r = e^{G_last - G_r} * k_r:
@@ -65,6 +66,68 @@ struct TileIn {
   }
 };
 
+// Rows [0, len) of a 64 x D tile of T (fp32 or bf16; rows rs elements apart
+// in HBM), read in one batch like TileIn and staged to LDS as fp32 (rows past
+// len are zero).  Pieces are 16 bytes; when they do not divide evenly over the
+// NT threads the spare threads load a valid piece and stage nothing.
+template <int D, int NT, typename T>
+struct CwRows {
+  static constexpr int V = 16 / (int)sizeof(T), PER_ROW = D / V, TOT = CH * PER_ROW;
+  static constexpr int N = (TOT + NT - 1) / NT;
+  uint4 u[N];
+  __device__ __forceinline__ static void where(int t, int& idx, int& r, int& c) {
+    idx = thread_x() + t * NT;
+    const int i = idx < TOT ? idx : TOT - 1;
+    r = i / PER_ROW;
+    c = (i - r * PER_ROW) * V;
+  }
+  __device__ __forceinline__ void load(const T* __restrict__ src, long rs, int len) {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, r, c;
+      where(t, idx, r, c);
+      u[t] = *reinterpret_cast<const uint4*>(src + clamp_row(r, len) * rs + c);
+    }
+  }
+  // columns [lo, hi) of the tile (piece-aligned) to dst[r * LD + c - lo]
+  template <int LD>
+  __device__ __forceinline__ void stage(float* dst, int len, int lo = 0, int hi = D) const {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, r, c;
+      where(t, idx, r, c);
+      if (idx >= TOT || c < lo || c >= hi) continue;
+      const uint4 x = keep16(r < len, u[t]);
+      float* d = dst + r * LD + (c - lo);
+      if constexpr (sizeof(T) == 4) {
+        *reinterpret_cast<uint4*>(d) = x;
+      } else {
+        float f[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = to_f(elem16<bf16>(x, j));
+        *reinterpret_cast<float4*>(d) = float4{f[0], f[1], f[2], f[3]};
+        *reinterpret_cast<float4*>(d + 4) = float4{f[4], f[5], f[6], f[7]};
+      }
+    }
+  }
+  // multiply the staged tile by this one's values (same layout, fp32 pieces)
+  template <int LD>
+  __device__ __forceinline__ void scale(float* dst, int len) const {
+    static_assert(sizeof(T) == 4, "fp32 factors");
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, r, c;
+      where(t, idx, r, c);
+      if (idx >= TOT) continue;
+      const float4 y = __builtin_bit_cast(float4, keep16(r < len, u[t]));
+      float4* d = reinterpret_cast<float4*>(dst + r * LD + c);
+      float4 x = *d;
+      x.x *= y.x; x.y *= y.y; x.z *= y.z; x.w *= y.w;
+      *d = x;
+    }
+  }
+};
+
 // The reference log-decay of 16-row block R (row 16R - 1; 0 for R = 0).
 template <int LD>
 __device__ __forceinline__ float cw_ref(const float* Gs, int R, int d) {
@@ -76,11 +139,11 @@ __device__ __forceinline__ float cw_ref(const float* Gs, int R, int d) {
 // those of the reverse scan and the gradient kernels (P^T, (Gamma Q)^T,
 // Khat, W^T, T, Gamma * Kb, dO^T).  Both write G_last per channel.
 constexpr int CW_PREP_THREADS = 1024;  // 16 waves: one block per CU (LDS), so all its latency hiding is in-block
-template <int DK, int DV, bool BWD>
-__global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, const float* __restrict__ q,
-                                                 const float* __restrict__ k, const float* __restrict__ v,
+template <int DK, int DV, bool BWD, typename IO>
+__global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, const IO* __restrict__ q,
+                                                 const IO* __restrict__ k, const IO* __restrict__ v,
                                                  const float* __restrict__ g, const float* __restrict__ b,
-                                                 const float* __restrict__ w, const float* __restrict__ dO,
+                                                 const float* __restrict__ w, const IO* __restrict__ dO,
                                                  float* __restrict__ gC, float* __restrict__ Pg,
                                                  float* __restrict__ Qgg, float* __restrict__ Khg,
                                                  float* __restrict__ Wg, float* __restrict__ Ug,
@@ -106,9 +169,11 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   // forward's v and w slices (or the backward's dO)
   constexpr int NSL = BWD ? 1 : DV / VS;
   constexpr int NT = CW_PREP_THREADS, WN = NT / 256;  // wave columns of the 64-row products
-  RowsIn<DK, NT, float> qin, kin, gin, bin;
-  RowsIn<VS, NT, float> vin[NSL], win[NSL];
-  RowsIn<DV, NT, float> doin;
+  CwRows<DK, NT, IO> qin, kin;
+  CwRows<DK, NT, float> gin, bin;
+  CwRows<VS, NT, IO> vin[NSL];
+  CwRows<VS, NT, float> win[NSL];
+  CwRows<DV, NT, IO> doin;
   qin.load(q + bk, rsk, cp.len);
   kin.load(k + bk, rsk, cp.len);
   if (g) gin.load(g + bk, rsk, cp.len);
@@ -128,7 +193,7 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   else
     for (int i = thread_x(); i < CH * LK; i += blockDim.x) Gs[i] = 0.f;
   if (b) bin.template stage<LK>(Bk, cp.len);
-  __syncthreads();
+  __syncthreads();  // (stage writes fp32 tiles: the LDS layout below is the same for both I/O types)
   if (g) cw_cumsum_columns<DK, LK>(Gs);
   if (b)
     for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
@@ -259,17 +324,13 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   // once W is formed), then written down its columns so each store instruction
   // covers whole rows of dO^T
   if constexpr (BWD) {
-    constexpr int PW = 64, PR = DV / 4;
+    constexpr int PW = 64;
     static_assert(PW <= LK && DV % PW == 0, "a pass fits K's tile");
     float* Dt = dOTg + tile * DV * CH;
 #pragma unroll
     for (int ps = 0; ps < DV / PW; ++ps) {
       __syncthreads();
-#pragma unroll
-      for (int pc = 0; pc < doin.N; ++pc) {
-        const int idx = thread_x() + pc * NT, r = idx / PR, c = (idx - r * PR) * 4;
-        if (c / PW == ps) *reinterpret_cast<uint4*>(Ks + r * LK + (c - ps * PW)) = keep16(r < cp.len, doin.u[pc]);
-      }
+      doin.template stage<LK>(Ks, cp.len, ps * PW, (ps + 1) * PW);
       __syncthreads();
       for (int i = thread_x(); i < PW * CH; i += blockDim.x) {
         const int vv = i / CH, r = i - vv * CH;
@@ -284,16 +345,10 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
     for (int t = 0; t < NSL; ++t) {
       const int c0 = t * VS;
       __syncthreads();  // K (first pass) or the previous slice is no longer read
-#pragma unroll
-      for (int pc = 0; pc < vin[t].N; ++pc) {
-        constexpr int PR = VS / 4;
-        const int idx = thread_x() + pc * NT, r = idx / PR, c = (idx - r * PR) * 4;
-        float4 x = __builtin_bit_cast(float4, keep16(r < cp.len, vin[t].u[pc]));
-        if (w) {
-          const float4 y = __builtin_bit_cast(float4, win[t].u[pc]);
-          x.x *= y.x; x.y *= y.y; x.z *= y.z; x.w *= y.w;
-        }
-        *reinterpret_cast<float4*>(Vw + r * LV + c) = x;
+      vin[t].template stage<LV>(Vw, cp.len);
+      if (w) {
+        __syncthreads();
+        win[t].template scale<LV>(Vw, cp.len);
       }
       __syncthreads();
       Tiles<CH, VS, 4, WN> uu;
@@ -318,12 +373,12 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
 //   dP = dO U'^T (i <= r),  dA = -Y U'^T (i < r: the solve's VJP in its short
 //   form, -T^T (dU' R^T) T^T = -Y U'^T),  X = -Y h^T,  dQg = dO h^T,
 //   dKhat = U' dh^T,  <h, dh> per row d.
-template <int DK, int DV>
-__global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* __restrict__ v,
-                                                   const float* __restrict__ w, const float* __restrict__ dO,
+template <int DK, int DV, typename IO>
+__global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __restrict__ v,
+                                                   const float* __restrict__ w, const IO* __restrict__ dO,
                                                    const float* __restrict__ states, const float* __restrict__ Tg,
                                                    const float* __restrict__ KbGg, const float* __restrict__ dhg,
-                                                   const float* __restrict__ dUTg, float* __restrict__ dvo,
+                                                   const float* __restrict__ dUTg, IO* __restrict__ dvo,
                                                    float* __restrict__ dwo, float* __restrict__ dPg,
                                                    float* __restrict__ dAg, float* __restrict__ Xg,
                                                    float* __restrict__ dQgg, float* __restrict__ dKhg,
@@ -341,7 +396,8 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
   const long rsv = (long)H * DV, bv = (cp.row0 * H + h) * DV;
   // the tiles of one value slice, requested in one batch
   struct Slice {
-    RowsIn<VS, 512, float> v, w, dO;
+    CwRows<VS, 512, IO> v, dO;
+    CwRows<VS, 512, float> w;
     TileIn<DK, VS, 512> h, dh;
     TileIn<VS, CH, 512> dut;
   };
@@ -404,7 +460,7 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
         Ys[r * LV + vv] = x;
         if (r < cp.len) {
           const long o = bv + (long)r * rsv + c0 + vv;
-          dvo[o] = (w ? Ws[r * LV + vv] : 1.f) * x;
+          dvo[o] = from_f<IO>((w ? Ws[r * LV + vv] : 1.f) * x);
           if (w) dwo[o] = Vs[r * LV + vv] * x;
         }
       });
@@ -448,14 +504,14 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
 // (elementwise), with e^{G_last} <h, dh>_d + sum_r Khat_rd dKhat_rd added on the
 // last row; dg is its reverse cumulative sum down each channel (one wave per
 // channel, fixed order).
-template <int DK>
-__global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* __restrict__ q,
-                                                   const float* __restrict__ k, const float* __restrict__ g,
+template <int DK, typename IO>
+__global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const IO* __restrict__ q,
+                                                   const IO* __restrict__ k, const float* __restrict__ g,
                                                    const float* __restrict__ b, const float* __restrict__ dPg,
                                                    const float* __restrict__ dAg, const float* __restrict__ Xg,
                                                    const float* __restrict__ dQgg, const float* __restrict__ dKhg,
-                                                   const float* __restrict__ hdhg, float* __restrict__ dq,
-                                                   float* __restrict__ dk, float* __restrict__ dg,
+                                                   const float* __restrict__ hdhg, IO* __restrict__ dq,
+                                                   IO* __restrict__ dk, float* __restrict__ dg,
                                                    float* __restrict__ db) {
   constexpr int DS = 32, LS = DS + 4, LC = CH + 4;
   __shared__ __align__(16) float dPs[CH * LC], dAs[CH * LC];
@@ -473,7 +529,8 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
   const ChunkPos cp = chunk_pos(geo, ci);
   const long rsk = (long)H * DK, bk = (cp.row0 * H + h) * DK + d0;
   {
-    RowsIn<DS, 512, float> qin, kin, gin, bin;
+    CwRows<DS, 512, IO> qin, kin;
+    CwRows<DS, 512, float> gin, bin;
     TileIn<CH, CH, 512> pin, ain;
     qin.load(q + bk, rsk, cp.len);
     kin.load(k + bk, rsk, cp.len);
@@ -568,8 +625,8 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
       Zv[j] = khdkh;
       if (r < cp.len) {
         const long o = bk + (long)r * rsk + dl;
-        dq[o] = gam * dqg + dqP;
-        dk[o] = dte * dkh + dkP + dkA + bv * dkb;
+        dq[o] = from_f<IO>(gam * dqg + dqP);
+        dk[o] = from_f<IO>(dte * dkh + dkP + dkA + bv * dkb);
         if (b) db[o] = kv * dkb;
       }
     }
@@ -597,7 +654,7 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const float* 
   }
 }
 
-template <int DK, int DV>
+template <int DK, int DV, typename IO>
 static hipError_t launch_cw_fwd_t(const CwFwdArgs& a) {
   constexpr int BV = SCAN_BV, NVT = DV / BV;
   const Geo& geo = a.geo;
@@ -609,22 +666,24 @@ static hipError_t launch_cw_fwd_t(const CwFwdArgs& a) {
     if (e != hipSuccess) return e;
   }
   if (geo.total_chunks > 0)
-    hipLaunchKernelGGL((k_cw_prep<DK, DV, false>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream, geo, H,
-                       a.q, a.k, a.v, a.g, a.b, a.w, (const float*)nullptr, w.gC, w.P, w.Qg, w.KhT, w.W, w.U,
+    hipLaunchKernelGGL((k_cw_prep<DK, DV, false, IO>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream,
+                       geo, H, (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, (const IO*)nullptr,
+                       w.gC, w.P, w.Qg, w.KhT, w.W, w.U,
                        (float*)nullptr, (float*)nullptr, (float*)nullptr);
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0)
-    hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, float, VAR_GATED, true>), dim3(NS * NVT), dim3(256), 0, a.stream,
-                       geo, H, (const float*)w.Qg, a.v, a.S0, w.gC, (const float*)w.W, (const float*)w.KhT,
-                       (const float*)w.P, (const float*)w.U, a.states, a.ST, a.o, w.flag_scan);
+    hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, float, VAR_GATED, true, IO>), dim3(NS * NVT), dim3(256), 0,
+                       a.stream, geo, H, (const float*)w.Qg, (const float*)nullptr, a.S0, w.gC, (const float*)w.W,
+                       (const float*)w.KhT, (const float*)w.P, (const float*)w.U, a.states, a.ST, (IO*)a.o,
+                       w.flag_scan);
   stage_mark(a.events, 2, a.stream);
   stage_mark(a.events, 3, a.stream);
   stage_mark(a.events, 4, a.stream);
   return hipGetLastError();
 }
 
-template <int DK, int DV>
+template <int DK, int DV, typename IO>
 static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
   constexpr int BV = SCAN_BV, NVT = DV / BV;
   const Geo& geo = a.geo;
@@ -636,8 +695,9 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
     if (e != hipSuccess) return e;
   }
   if (geo.total_chunks > 0)
-    hipLaunchKernelGGL((k_cw_prep<DK, DV, true>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream, geo, H,
-                       a.q, a.k, a.v, a.g, a.b, a.w, a.dO, w.gC, w.PT, w.QgT, w.Kh, w.WT, (float*)nullptr, w.T,
+    hipLaunchKernelGGL((k_cw_prep<DK, DV, true, IO>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream,
+                       geo, H, (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, (const IO*)a.dO,
+                       w.gC, w.PT, w.QgT, w.Kh, w.WT, (float*)nullptr, w.T,
                        w.KbG, w.dOT);
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
@@ -647,14 +707,14 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
                        (const float*)w.dOT, (const float*)w.PT, w.dh, w.dUT, a.dS0, w.flag_scan);
   stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0) {
-    hipLaunchKernelGGL((k_cw_grad_v<DK, DV>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H, a.v, a.w,
-                       a.dO, a.states, (const float*)w.T, (const float*)w.KbG, (const float*)w.dh,
-                       (const float*)w.dUT, a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg, w.dKh, w.hdh);
+    hipLaunchKernelGGL((k_cw_grad_v<DK, DV, IO>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
+                       (const IO*)a.v, a.w, (const IO*)a.dO, a.states, (const float*)w.T, (const float*)w.KbG, (const float*)w.dh,
+                       (const float*)w.dUT, (IO*)a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg, w.dKh, w.hdh);
     stage_mark(a.events, 3, a.stream);
     const long tiles = (long)geo.total_chunks * H;
-    hipLaunchKernelGGL((k_cw_grad_d<DK>), dim3((unsigned)((tiles + 7) / 8 * 8 * (DK / 32))), dim3(512), 0, a.stream, geo, H, a.q,
-                       a.k, a.g, a.b, (const float*)w.dP, (const float*)w.dA, (const float*)w.X,
-                       (const float*)w.dQg, (const float*)w.dKh, (const float*)w.hdh, a.dq, a.dk_, a.dg, a.db);
+    hipLaunchKernelGGL((k_cw_grad_d<DK, IO>), dim3((unsigned)((tiles + 7) / 8 * 8 * (DK / 32))), dim3(512), 0,
+                       a.stream, geo, H, (const IO*)a.q, (const IO*)a.k, a.g, a.b, (const float*)w.dP, (const float*)w.dA, (const float*)w.X,
+                       (const float*)w.dQg, (const float*)w.dKh, (const float*)w.hdh, (IO*)a.dq, (IO*)a.dk_, a.dg, a.db);
   } else {
     stage_mark(a.events, 3, a.stream);
   }

@@ -267,14 +267,14 @@ __global__ __launch_bounds__(512) void k_prep_fwd(Geo geo, int H, const OP* __re
 // (two barriers per chunk).
 // CWD (channel-wise decay): the carry decays row by row, h[d, :] *= e^{G_last[d]},
 // with gcum holding each chunk's d_k values of G_last instead of the 64 in-chunk
-// values of a scalar G.
-template <int DK, int DV, int BV, typename OP, int VAR, bool CWD = false>
+// values of a scalar G.  OUT: the element type of o (the operand type by default).
+template <int DK, int DV, int BV, typename OP, int VAR, bool CWD = false, typename OUT = OP>
 __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __restrict__ Qgg,
                                                   const OP* __restrict__ v, const float* __restrict__ S0,
                                                   const float* __restrict__ gcum, const OP* __restrict__ Wg,
                                                   const OP* __restrict__ KhTg, const OP* __restrict__ Pg,
                                                   const OP* __restrict__ Ug, float* __restrict__ states,
-                                                  float* __restrict__ ST, OP* __restrict__ o,
+                                                  float* __restrict__ ST, OUT* __restrict__ o,
                                                   int* __restrict__ flag) {
   static_assert(BV == SCAN_BV, "U is laid out for the scan's value tiles");
   constexpr int NVT = DV / BV;
@@ -437,13 +437,13 @@ __global__ __launch_bounds__(256) void k_scan_fwd(Geo geo, int H, const OP* __re
     }
     hs.template mma<OP, CH>(cur.kh, KRow<OP, LU>{UsT});
     ot.template mma<OP, CH>(cur.pf, KRow<OP, LU>{UsT});  // + P U'
-    OP* op = o + (row0 * H + h) * DV + v0;
+    OUT* op = o + (row0 * H + h) * DV + v0;
 #pragma unroll
     for (int b = 0; b < UT::TN; ++b)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = UT::m0(0) + (l >> 4) * 4 + j;
-        if (r < len) op[(long)r * H * DV + UT::n0(b) + (l & 15)] = from_f<OP>(ot.acc[0][b][j]);
+        if (r < len) op[(long)r * H * DV + UT::n0(b) + (l & 15)] = from_f<OUT>(ot.acc[0][b][j]);
       }
   };
   const int nch = sp.nch;

@@ -91,8 +91,8 @@ constexpr int grad_region_bytes(int dk, int es) {
   return (m + 255) / 256 * 256;
 }
 
-// Channel-wise members (per-channel g, b, w; fp32 operands).  A NULL gate is
-// neutral: g = 0, b = 0 (no erase), w = 1.
+// Channel-wise members (per-channel g, b, w; fp32 operands inside, fp32 or
+// bf16 activations).  A NULL gate is neutral: g = 0, b = 0 (no erase), w = 1.
 struct CwFwdWs {
   int* chunk_off;
   int* flag_scan;  // [N*H*NVT] written by the generic scan, not read
@@ -106,9 +106,11 @@ struct CwFwdWs {
 
 struct CwFwdArgs {
   Geo geo;
-  int dk, dv;
-  const float *q, *k, *v, *g, *b, *w, *S0;
-  float *o, *ST, *states;
+  int dk, dv, io;  // io: DT_F32 or DT_BF16 (q, k, v, o)
+  const void *q, *k, *v;
+  const float *g, *b, *w, *S0;
+  void* o;
+  float *ST, *states;
   CwFwdWs ws;
   hipStream_t stream;
   hipEvent_t const* events;
@@ -137,9 +139,11 @@ struct CwBwdWs {
 
 struct CwBwdArgs {
   Geo geo;
-  int dk, dv;
-  const float *q, *k, *v, *g, *b, *w, *states, *dO, *dST;
-  float *dq, *dk_, *dv_, *dg, *db, *dw, *dS0;
+  int dk, dv, io;  // io: DT_F32 or DT_BF16 (q, k, v, dO, dq, dk, dv)
+  const void *q, *k, *v, *dO;
+  const float *g, *b, *w, *states, *dST;
+  void *dq, *dk_, *dv_;
+  float *dg, *db, *dw, *dS0;
   CwBwdWs ws;
   hipStream_t stream;
   hipEvent_t const* events;

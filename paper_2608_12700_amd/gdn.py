@@ -308,12 +308,14 @@ def _packed_of(cu_seqlens, dev):
 
 
 def cw_fwd(q, k, v, g=None, b=None, w=None, S0=None, *, cu_seqlens=None, workspace=None):
-    """Channel-wise forward (fp32): returns (o, S_T, chunk_states).  g, b [B,T,H,d_k] and
-    w [B,T,H,d_v] may each be None (neutral gate).  See include/gdn.h."""
+    """Channel-wise forward: returns (o, S_T, chunk_states).  q, k, v fp32 or bf16 (o follows);
+    g, b [B,T,H,d_k] and w [B,T,H,d_v] fp32, each may be None (neutral gate).  See include/gdn.h."""
     dev = q.device
     packed = _packed_of(cu_seqlens, dev)
     p = _problem_for(q, v, "gated_delta", packed)
-    for name, t in (("q", q), ("k", k), ("v", v), ("g", g), ("b", b), ("w", w), ("S0", S0)):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, name, q.dtype, dev)
+    for name, t in (("g", g), ("b", b), ("w", w), ("S0", S0)):
         if t is not None:
             _check(t, name, torch.float32, dev)
     B, T, H, dk = q.shape
@@ -321,7 +323,7 @@ def cw_fwd(q, k, v, g=None, b=None, w=None, S0=None, *, cu_seqlens=None, workspa
     nch = gdn_num_chunks(p)
     if nch < 0:
         raise GdnError(nch, "gdn_num_chunks")
-    o = torch.empty((B, T, H, dv), dtype=torch.float32, device=dev)
+    o = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
     S_T = torch.empty((p.num_seqs, H, dk, dv), dtype=torch.float32, device=dev)
     states = torch.empty((nch, H, dk, dv), dtype=torch.float32, device=dev)
     wsb = gdn_cw_fwd_workspace_size(p)
@@ -334,13 +336,14 @@ def cw_fwd(q, k, v, g=None, b=None, w=None, S0=None, *, cu_seqlens=None, workspa
 
 
 def cw_bwd(q, k, v, g, b, w, chunk_states, dO, dS_T=None, *, cu_seqlens=None, workspace=None):
-    """Channel-wise backward (fp32): returns (dq, dk, dv, dg, db, dw, dS0); a gate's gradient
-    is None when the gate is None."""
+    """Channel-wise backward: returns (dq, dk, dv, dg, db, dw, dS0); dq, dk, dv in the dtype of q,
+    a gate's gradient (fp32) is None when the gate is None."""
     dev = q.device
     packed = _packed_of(cu_seqlens, dev)
     p = _problem_for(q, v, "gated_delta", packed)
-    for name, t in (("q", q), ("k", k), ("v", v), ("dO", dO), ("g", g), ("b", b), ("w", w),
-                    ("chunk_states", chunk_states), ("dS_T", dS_T)):
+    for name, t in (("q", q), ("k", k), ("v", v), ("dO", dO)):
+        _check(t, name, q.dtype, dev)
+    for name, t in (("g", g), ("b", b), ("w", w), ("chunk_states", chunk_states), ("dS_T", dS_T)):
         if t is not None:
             _check(t, name, torch.float32, dev)
     B, T, H, dk = q.shape

@@ -1,11 +1,13 @@
 """Channel-wise members on the GPU against the float64 channel-wise oracle.
 
 Every case calls the C ABI (gdn_cw_fwd / gdn_cw_bwd through the binding) on
-seeded fp32 inputs and compares every output with the oracle at the fp32
-bar (rel-L2 <= 1e-4 per tensor):
+seeded inputs and compares every output with the oracle at the bar of its
+activation dtype (rel-L2 <= 1e-4 per tensor for fp32, 1e-2 for bf16; the
+oracle sees the same once-rounded values):
 
 * full GDN gates (per-channel g, b, w), KDA (b = w = beta broadcast), GLA
   (g only), LA (no gates), each over several chunks and a ragged tail;
+* bf16 activations for every member and for packed sequences;
 * d_k / d_v in {64, 128, 256} combinations, packed variable-length
   sequences (including a one-token sequence), a T shorter than one chunk;
 * a strong decay (mean log-decay about -4 per token and channel, tails near
@@ -33,12 +35,15 @@ def _dev(x):
 
 
 def _np(x):
-    return None if x is None else x.detach().cpu().numpy().astype(np.float64)
+    return None if x is None else x.detach().float().cpu().numpy().astype(np.float64)
 
 
 def run_device(c: W.CwCase):
     from paper_2608_12700_amd import gdn
     t = {n: _dev(getattr(c, n)) for n in ("q", "k", "v", "g", "b", "w", "S0", "dO", "dS_T")}
+    if c.io_dtype == "bf16":  # the arrays hold bf16 values already: the cast is exact
+        for n in ("q", "k", "v", "dO"):
+            t[n] = t[n].to(torch.bfloat16)
     cu = None if c.cu_seqlens is None else c.cu_seqlens
     o, S_T, st = gdn.cw_fwd(t["q"], t["k"], t["v"], t["g"], t["b"], t["w"], t["S0"], cu_seqlens=cu)
     r = gdn.cw_bwd(t["q"], t["k"], t["v"], t["g"], t["b"], t["w"], st, t["dO"], t["dS_T"], cu_seqlens=cu)
@@ -62,7 +67,7 @@ def check(c: W.CwCase, heads=None):
     names = tuple(n for n in NAMES if ref.get(n) is not None or dev.get(n) is not None)
     res = Hn.compare(dev, ref, heads=heads, names=names)
     print(res, flush=True)
-    Hn.assert_parity(res, TOL, c.name)
+    Hn.assert_parity(res, Hn.TOL[c.io_dtype], c.name)
     return dev
 
 
@@ -74,6 +79,17 @@ def test_members_small(gates):
 @pytest.mark.parametrize("dk,dv", [(128, 128), (128, 64), (64, 256), (128, 256)])
 def test_dims_full_gates(dk, dv):
     check(W.make_cw_case(f"cw_d{dk}_{dv}", 1, 131, 2, dk, dv, gates="gbw", seed=2))
+
+
+@pytest.mark.parametrize("gates", ["gbw", "kda", "g", ""])
+def test_members_bf16_io(gates):
+    check(W.make_cw_case(f"cw_bf16_{gates or 'la'}", 2, 200, 2, 128, 128, gates=gates, seed=12, io_dtype="bf16"))
+
+
+def test_packed_sequences_bf16_io():
+    cu = np.array([0, 1, 65, 200, 331], dtype=np.int32)
+    check(W.make_cw_case("cw_packed_bf16", 1, 331, 2, 64, 256, gates="gbw", seed=13, cu_seqlens=cu,
+                         io_dtype="bf16"))
 
 
 def test_packed_sequences():
@@ -91,8 +107,9 @@ def test_strong_decay():
     check(W.make_cw_case("cw_strong", 1, 192, 2, 128, 128, gates="gbw", seed=5, decay=5.0))
 
 
-def test_throughput_shape_sampled_heads():
-    c = W.make_cw_case("cw_B4_T4096_H16_d128", 4, 4096, 16, 128, 128, gates="gbw", seed=6)
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_throughput_shape_sampled_heads(io):
+    c = W.make_cw_case("cw_B4_T4096_H16_d128", 4, 4096, 16, 128, 128, gates="gbw", seed=6, io_dtype=io)
     check(c, heads=[0, 11])
 
 

@@ -270,7 +270,8 @@ def describe(case: Case) -> str:
 # L2-normalised per (token, head).  Everything is rounded once to float32.
 # ``gates`` names the gates present: "gbw" (full GDN), "kda" (b = w = a scalar
 # beta per token broadcast over the channels, g per channel), "g" (GLA), ""
-# (LA).  Absent gates are None.
+# (LA).  Absent gates are None.  For bf16 I/O the activations q, k, v, dO are
+# rounded once more to bfloat16 (RNE); gates and states stay fp32.
 # ---------------------------------------------------------------------------
 
 @dataclasses.dataclass
@@ -292,6 +293,7 @@ class CwCase:
     dO: np.ndarray
     dS_T: np.ndarray
     cu_seqlens: Optional[np.ndarray] = None
+    io_dtype: str = "f32"
 
     @property
     def N(self) -> int:
@@ -299,7 +301,7 @@ class CwCase:
 
 
 def make_cw_case(name, B, T, H, dk, dv, *, gates="gbw", seed=0, decay=1.0, cu_seqlens=None,
-                 S0_std=0.1, dST_std=1.0) -> CwCase:
+                 S0_std=0.1, dST_std=1.0, io_dtype="f32") -> CwCase:
     if cu_seqlens is not None:
         assert B == 1 and int(cu_seqlens[-1]) == T
     rng = np.random.Generator(np.random.PCG64(seed))
@@ -327,8 +329,12 @@ def make_cw_case(name, B, T, H, dk, dv, *, gates="gbw", seed=0, decay=1.0, cu_se
         beta = f32(_sigmoid(b_logit[..., 0]))
         b = f32(np.repeat(beta[..., None], dk, axis=-1))
         w = f32(np.repeat(beta[..., None], dv, axis=-1))
+    if io_dtype == "bf16":
+        q, k, v, dO = (round_bf16(x) for x in (q, k, v, dO))
+    elif io_dtype != "f32":
+        raise ValueError(f"io_dtype {io_dtype!r}")
     return CwCase(name, B, T, H, dk, dv, gates, q, k, v, g, b, w, S0, dO, dS_T,
-                  None if cu_seqlens is None else np.asarray(cu_seqlens, dtype=np.int32))
+                  None if cu_seqlens is None else np.asarray(cu_seqlens, dtype=np.int32), io_dtype)
 
 
 __all__ = [

@@ -34,7 +34,7 @@ BF16_PEAK_TFLOPS = 2500.0
 CH = 64
 ROOT = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bf16_B4_T4096_H16_d128.json")
-CW_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cw_f32_B4_T4096_H16_d128.json")
+CW_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cw_bf16_B4_T4096_H16_d128.json")
 STAGE_OF_KERNEL = {"k_prep_fwd": "fwd_prep", "k_scan_fwd": "fwd_scan", "k_prep_bwd": "bwd_prep",
                    "k_scan_bwd": "bwd_scan", "k_grad_bf": "bwd_grad"}
 
@@ -459,8 +459,8 @@ def main(argv=None):
         return 0
     if a.summarize_trace:
         md = summarize_trace(a.summarize_trace, a.command, *(
-            ["channel-wise gated delta rule fwd+bwd (per-channel g, b, w), fp32, B=4 T=4096 H=16 dk=dv=128"]
-            if a.cw else []))
+            [f"channel-wise gated delta rule fwd+bwd (per-channel g, b, w), {a.cw_io} activations, "
+             "B=4 T=4096 H=16 dk=dv=128"] if a.cw else []))
         with open(os.path.join(ROOT, "profiles", a.trace_out), "w") as fh:
             fh.write(md)
         print(md)

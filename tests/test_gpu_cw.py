@@ -7,7 +7,8 @@ oracle sees the same once-rounded values):
 
 * full GDN gates (per-channel g, b, w), KDA (b = w = beta broadcast), GLA
   (g only), LA (no gates), each over several chunks and a ragged tail;
-* bf16 activations for every member and for packed sequences;
+* bf16 activations for every member and for packed sequences; empty
+  sequences (inside a packed batch, and T = 0);
 * d_k / d_v in {64, 128, 256} combinations, packed variable-length
   sequences (including a one-token sequence), a T shorter than one chunk;
 * a strong decay (mean log-decay about -4 per token and channel, tails near
@@ -95,6 +96,14 @@ def test_packed_sequences_bf16_io():
 def test_packed_sequences():
     cu = np.array([0, 70, 71, 200, 333], dtype=np.int32)
     check(W.make_cw_case("cw_packed", 1, 333, 2, 128, 128, gates="gbw", seed=3, cu_seqlens=cu))
+
+
+def test_empty_sequences():
+    # an empty sequence inside a packed batch carries S0 to S_T and dS_T to dS0;
+    # T = 0 overall leaves nothing but the states
+    cu = np.array([0, 70, 70, 71, 200], dtype=np.int32)
+    check(W.make_cw_case("cw_packed_empty", 1, 200, 2, 64, 128, gates="gbw", seed=14, cu_seqlens=cu))
+    check(W.make_cw_case("cw_T0", 2, 0, 2, 64, 64, gates="kda", seed=15))
 
 
 def test_shorter_than_one_chunk():

@@ -25,7 +25,10 @@
 // can overflow; the operand is zeroed (before the exponential) outside those
 // blocks.  Contractions down the columns (the transposed gradients) use the
 // last row of the block instead.  Pairs inside one block are summed exactly
-// on the vector ALUs with e^{G_r - G_i} formed per term.
+// on the vector ALUs with e^{G_r - G_i} formed per term -- only for blocks whose log-decay moves by more than
+// CW_SPREAD from the reference; the others take the block's reference on the
+// matrix cores too (factors within e^{+-2 CW_SPREAD}: no overflow, no
+// denormals, the same per-term rounding).
 #pragma once
 
 #include "gdn_bwd.hpp"
@@ -34,11 +37,28 @@
 namespace gdn {
 
 // G (cumulative log-decay per channel) in place down each column of a 64 x D
-// LDS tile with row stride LD: one wave per column, rows on lanes.
+// LDS tile with row stride LD: one wave per column, rows on lanes.  With
+// wide, also sets bit R of *wide when some |G_r - G_ref| in 16-row block R
+// (G_ref that of the row before the block, 0 for R = 0) exceeds CW_SPREAD or
+// is not finite: such a block's in-block pairs are summed exactly.
+constexpr float CW_SPREAD = 32.f;
 template <int D, int LD>
-__device__ __forceinline__ void cw_cumsum_columns(float* Gs) {
-  const int nw = (int)blockDim.x / WAVE, l = lane_id();
-  for (int d = wave_id(); d < D; d += nw) Gs[l * LD + d] = wave_incl_scan(Gs[l * LD + d]);
+__device__ __forceinline__ void cw_cumsum_columns(float* Gs, int* wide = nullptr) {
+  const int nw = (int)blockDim.x / WAVE, l = lane_id(), src = l >= 16 ? (l & ~15) - 1 : 0;
+  bool big = false;
+  for (int d = wave_id(); d < D; d += nw) {
+    const float x = wave_incl_scan(Gs[l * LD + d]);
+    Gs[l * LD + d] = x;
+    const float rf = shfl_idx(x, src);
+    big |= !(fabsf(x - (l >= 16 ? rf : 0.f)) <= CW_SPREAD);
+  }
+  if (wide) {
+    const unsigned long long m = __ballot(big);
+    int f = 0;
+#pragma unroll
+    for (int R = 0; R < 4; ++R) f |= ((m >> (16 * R)) & 0xFFFFull) ? 1 << R : 0;
+    if (l == 0 && f) atomicOr(wide, f);  // integer OR: order-free
+  }
 }
 
 // A ROWS x D fp32 tile (rows rs floats apart in HBM), read by NT threads in
@@ -128,12 +148,6 @@ struct CwRows {
   }
 };
 
-// The reference log-decay of 16-row block R (row 16R - 1; 0 for R = 0).
-template <int LD>
-__device__ __forceinline__ float cw_ref(const float* Gs, int R, int d) {
-  return R > 0 ? Gs[(16 * R - 1) * LD + d] : 0.f;
-}
-
 // One block per (chunk, head).  Forward mode writes the operands of the
 // generic forward scan (P, diag-scaled Q, Khat^T, W, U); backward mode writes
 // those of the reverse scan and the gradient kernels (P^T, (Gamma Q)^T,
@@ -156,7 +170,8 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   __shared__ __align__(16) float Gs[CH * LK];  // G
   __shared__ __align__(16) float Bk[CH * LK];  // b * K, then Gamma * b * K
   __shared__ __align__(16) float As[CH * LC];  // A
-  __shared__ __align__(16) float Pd[4 * 16 * 16];  // P inside the four diagonal 16 x 16 blocks
+  __shared__ __align__(16) float Pd[4 * 16 * 16];  // P inside the four diagonal 16 x 16 blocks (wide blocks)
+  __shared__ int wide;                              // blocks summed exactly (bit R: block R)
   float* Tf = Qs;
   float* Vw = Ks;
 
@@ -169,6 +184,7 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   // forward's v and w slices (or the backward's dO)
   constexpr int NSL = BWD ? 1 : DV / VS;
   constexpr int NT = CW_PREP_THREADS, WN = NT / 256;  // wave columns of the 64-row products
+  static_assert(NT / WAVE == 16, "sixteen 16 x 16 tiles of P and A, one per wave");
   CwRows<DK, NT, IO> qin, kin;
   CwRows<DK, NT, float> gin, bin;
   CwRows<VS, NT, IO> vin[NSL];
@@ -187,6 +203,7 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   } else {
     doin.load(dO + bv, rsv, cp.len);
   }
+  if (thread_x() == 0) wide = 0;
   qin.template stage<LK>(Qs, cp.len);
   kin.template stage<LK>(Ks, cp.len);
   if (g) gin.template stage<LK>(Gs, cp.len);
@@ -194,7 +211,7 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
     for (int i = thread_x(); i < CH * LK; i += blockDim.x) Gs[i] = 0.f;
   if (b) bin.template stage<LK>(Bk, cp.len);
   __syncthreads();  // (stage writes fp32 tiles: the LDS layout below is the same for both I/O types)
-  if (g) cw_cumsum_columns<DK, LK>(Gs);
+  if (g) cw_cumsum_columns<DK, LK>(Gs, &wide);
   if (b)
     for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
       const int r = i / DK, d = i - r * DK;
@@ -202,64 +219,100 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
     }
   __syncthreads();
 
-  // Pairs inside one 16-row block, exactly, spread over the whole block: pair
-  // q of block RB is (rl, il) with il <= rl; one exponential per term serves P
-  // and A.  A's sums land in As at their own positions (the A product's owner
-  // lane adds its part there), P's in Pd.
-  for (int pi = thread_x(); pi < 4 * 136; pi += blockDim.x) {
-    const int RB = pi / 136, q = pi - RB * 136;
-    int rl = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
-    while ((rl + 1) * (rl + 2) / 2 <= q) ++rl;
-    while (rl * (rl + 1) / 2 > q) --rl;
-    const int il = q - rl * (rl + 1) / 2, r = 16 * RB + rl, i = 16 * RB + il;
-    float sp = 0.f, sa = 0.f;
+  // Pairs inside a wide 16-row block, exactly, spread over the whole block:
+  // pair q of block RB is (rl, il) with il <= rl; one exponential per term
+  // serves P and A.  A's sums land in As at their own positions, P's in Pd.
+  const int wideb = wide;
+  if (wideb) {
+    for (int pi = thread_x(); pi < 4 * 136; pi += blockDim.x) {
+      const int RB = pi / 136, q = pi - RB * 136;
+      if (!((wideb >> RB) & 1)) continue;
+      int rl = (int)((sqrtf(8.f * q + 1.f) - 1.f) * 0.5f);
+      while ((rl + 1) * (rl + 2) / 2 <= q) ++rl;
+      while (rl * (rl + 1) / 2 > q) --rl;
+      const int il = q - rl * (rl + 1) / 2, r = 16 * RB + rl, i = 16 * RB + il;
+      float sp = 0.f, sa = 0.f;
 #pragma unroll 4
-    for (int d = 0; d < DK; d += 4) {
-      const float4 qr = *reinterpret_cast<const float4*>(Qs + r * LK + d);
-      const float4 ki = *reinterpret_cast<const float4*>(Ks + i * LK + d);
-      const float4 gr = *reinterpret_cast<const float4*>(Gs + r * LK + d);
-      const float4 gi = *reinterpret_cast<const float4*>(Gs + i * LK + d);
-      const float e0 = __expf(gr.x - gi.x), e1 = __expf(gr.y - gi.y), e2 = __expf(gr.z - gi.z), e3 = __expf(gr.w - gi.w);
-      const float k0 = ki.x * e0, k1 = ki.y * e1, k2 = ki.z * e2, k3 = ki.w * e3;
-      sp += qr.x * k0 + qr.y * k1 + qr.z * k2 + qr.w * k3;
-      if (b) {
-        const float4 br = *reinterpret_cast<const float4*>(Bk + r * LK + d);
-        sa += br.x * k0 + br.y * k1 + br.z * k2 + br.w * k3;
+      for (int d = 0; d < DK; d += 4) {
+        const float4 qr = *reinterpret_cast<const float4*>(Qs + r * LK + d);
+        const float4 ki = *reinterpret_cast<const float4*>(Ks + i * LK + d);
+        const float4 gr = *reinterpret_cast<const float4*>(Gs + r * LK + d);
+        const float4 gi = *reinterpret_cast<const float4*>(Gs + i * LK + d);
+        const float e0 = __expf(gr.x - gi.x), e1 = __expf(gr.y - gi.y), e2 = __expf(gr.z - gi.z), e3 = __expf(gr.w - gi.w);
+        const float k0 = ki.x * e0, k1 = ki.y * e1, k2 = ki.z * e2, k3 = ki.w * e3;
+        sp += qr.x * k0 + qr.y * k1 + qr.z * k2 + qr.w * k3;
+        if (b) {
+          const float4 br = *reinterpret_cast<const float4*>(Bk + r * LK + d);
+          sa += br.x * k0 + br.y * k1 + br.z * k2 + br.w * k3;
+        }
+      }
+      Pd[(RB * 16 + rl) * 16 + il] = sp;
+      if (b && il < rl) As[r * LC + i] = sa;
+    }
+    __syncthreads();
+  }
+
+  // P and A by 16 x 16 tiles (R, c) of output rows 16R.. and columns 16c..:
+  // waves 0..9 take the ten tiles c <= R (both products share the scaled K
+  // fragment), waves 10..15 write the six zero tiles c > R.  Lane l holds
+  // rows 16R + 4 (l >> 4) + j, column 16c + (l & 15).
+  {
+    const int wv = wave_id(), l = lane_id();
+    float* Pt = Pg + tile * CH * CH;
+    int R, c;
+    if (wv < 10) {
+      R = wv < 1 ? 0 : wv < 3 ? 1 : wv < 6 ? 2 : 3;
+      c = wv - R * (R + 1) / 2;
+    } else {  // (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
+      const int u = wv - 10;
+      R = u < 3 ? 0 : u < 5 ? 1 : 2;
+      c = u - (R == 0 ? 0 : R == 1 ? 3 : 5) + R + 1;
+    }
+    const bool lower = c <= R, exact = c == R && ((wideb >> R) & 1);
+    f32x4 ap = {0.f, 0.f, 0.f, 0.f}, aa = {0.f, 0.f, 0.f, 0.f};
+    if (lower && !exact) {
+      const int r = 16 * R + (l & 15), i = 16 * c + (l & 15);
+      const float* Gref = Gs + (R > 0 ? 16 * R - 1 : 0) * LK;
+#pragma unroll 2
+      for (int k16 = 0; k16 < DK; k16 += 16) {
+        const int d = k16 + 4 * (l >> 4);
+        const float4 rf = R > 0 ? *reinterpret_cast<const float4*>(Gref + d) : float4{0.f, 0.f, 0.f, 0.f};
+        const float4 gr = *reinterpret_cast<const float4*>(Gs + r * LK + d);
+        const float4 gi = *reinterpret_cast<const float4*>(Gs + i * LK + d);
+        const float4 qr = *reinterpret_cast<const float4*>(Qs + r * LK + d);
+        const float4 ki = *reinterpret_cast<const float4*>(Ks + i * LK + d);
+        const float er[4] = {__expf(gr.x - rf.x), __expf(gr.y - rf.y), __expf(gr.z - rf.z), __expf(gr.w - rf.w)};
+        const float kk[4] = {ki.x * __expf(rf.x - gi.x), ki.y * __expf(rf.y - gi.y), ki.z * __expf(rf.z - gi.z),
+                             ki.w * __expf(rf.w - gi.w)};
+        const float qq[4] = {qr.x * er[0], qr.y * er[1], qr.z * er[2], qr.w * er[3]};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) ap = Mma<float>::mma(qq[t], kk[t], ap);
+        if (b) {
+          const float4 br = *reinterpret_cast<const float4*>(Bk + r * LK + d);
+          const float bb[4] = {br.x * er[0], br.y * er[1], br.z * er[2], br.w * er[3]};
+#pragma unroll
+          for (int t = 0; t < 4; ++t) aa = Mma<float>::mma(bb[t], kk[t], aa);
+        }
       }
     }
-    Pd[(RB * 16 + rl) * 16 + il] = sp;
-    if (b && il < rl) As[r * LC + i] = sa;
-  }
-  __syncthreads();
-
-  // P and A: wave (R, ·) of Tiles<64, 64, 4, WN> owns 16-row block R
-  const int R = wave_id() / WN;
-  auto ref = [&](int d) { return cw_ref<LK>(Gs, R, d); };
-  auto kcol = kfun<float>([&](int i, int d) {
-    return i < 16 * R ? Ks[i * LK + d] * __expf(ref(d) - Gs[i * LK + d]) : 0.f;
-  });
-  {
-    Tiles<CH, CH, 4, WN> p;
-    p.zero();
-    p.template mma<float, DK>(kfun<float>([&](int r, int d) { return Qs[r * LK + d] * __expf(Gs[r * LK + d] - ref(d)); }),
-                              kcol);
-    float* Pt = Pg + tile * CH * CH;
-    p.each([&](int r, int i, float& x) {
-      const float dg = (r >> 4) == (i >> 4) ? Pd[(r * 16) + (i & 15)] : 0.f;
-      const float val = i <= r ? x + dg : 0.f;
-      if (BWD) Pt[i * CH + r] = val;
-      else Pt[r * CH + i] = val;
-    });
-  }
-  if (b) {
-    Tiles<CH, CH, 4, WN> a;
-    a.zero();
-    a.template mma<float, DK>(kfun<float>([&](int r, int d) { return Bk[r * LK + d] * __expf(Gs[r * LK + d] - ref(d)); }),
-                              kcol);
-    a.each([&](int r, int i, float& x) {
-      const float dg = (r >> 4) == (i >> 4) && i < r ? As[r * LC + i] : 0.f;
-      As[r * LC + i] = i < r ? x + dg : 0.f;
-    });
+    const int i = 16 * c + (l & 15), r0 = 16 * R + 4 * (l >> 4);
+    float pv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = r0 + j;
+      const float x = exact ? Pd[(R * 16 + (r & 15)) * 16 + (i & 15)] : ap[j];
+      pv[j] = lower && i <= r ? x : 0.f;
+      if (b) {
+        const float y = exact ? As[r * LC + i] : aa[j];
+        As[r * LC + i] = lower && i < r ? y : 0.f;
+      }
+    }
+    if (BWD) {
+      *reinterpret_cast<float4*>(Pt + i * CH + r0) = float4{pv[0], pv[1], pv[2], pv[3]};
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) Pt[(r0 + j) * CH + i] = pv[j];
+    }
   }
   // Gamma * Q and Khat = e^{G_last - G} * K, each in the layout its scan reads
   {
@@ -516,6 +569,7 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const IO* __r
   constexpr int DS = 32, LS = DS + 4, LC = CH + 4;
   __shared__ __align__(16) float dPs[CH * LC], dAs[CH * LC];
   __shared__ __align__(16) float Qs[CH * LS], Ks[CH * LS], Bs[CH * LS], Gs[CH * LS];
+  __shared__ int wide;  // 16-row blocks whose in-block pairs are summed exactly (bit R: block R)
   float* dGs = Qs;  // dG and Khat * dKhat take Q's and K's tiles once every wave is done with them
   float* Zs = Ks;
   // The channel slices of one (chunk, head) tile re-read its dP and dA: they
@@ -538,6 +592,7 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const IO* __r
     if (b) bin.load(b + bk, rsk, cp.len);
     pin.load(dPg + tile * CH * CH, CH);
     ain.load(dAg + tile * CH * CH, CH);
+    if (thread_x() == 0) wide = 0;
     qin.template stage<LS>(Qs, cp.len);
     kin.template stage<LS>(Ks, cp.len);
     if (g) gin.template stage<LS>(Gs, cp.len);
@@ -551,23 +606,20 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const IO* __r
   }
   __syncthreads();
   if (g) {
-    cw_cumsum_columns<DS, LS>(Gs);
+    cw_cumsum_columns<DS, LS>(Gs, &wide);
     __syncthreads();
   }
 
-  typedef Tiles<CH, DS, 4, 2> TD;  // one 16 x 16 output tile per wave
+  typedef Tiles<CH, DS, 4, 2> TD;  // the 16 x 16 output tile of each wave
   static_assert(TD::TM == 1 && TD::TN == 1, "one tile per wave");
   const int R = wave_id() / 2;     // the wave's 16-row block
-  auto ref = [&](int d) { return cw_ref<LS>(Gs, R, d); };
-  auto last = [&](int d) { return Gs[(16 * R + 15) * LS + d]; };
-  // K rows of earlier blocks, scaled to the reference before block R
-  auto kdown = kfun<float>([&](int d, int i) {
-    return i < 16 * R ? Ks[i * LS + d] * __expf(ref(d) - Gs[i * LS + d]) : 0.f;
-  });
+  const bool exact = (wide >> R) & 1;
+  const int l = lane_id(), dl = TD::n0(0) + (l & 15);
+  const float rf = R > 0 ? Gs[(16 * R - 1) * LS + dl] : 0.f;  // reference before block R
+  const float lst = Gs[(16 * R + 15) * LS + dl];               // reference at its last row
   // this lane's X, dQg, dKhat (issued ahead of the products)
   float xin[4], qgin[4], khin[4];
   {
-    const int l = lane_id(), dl = TD::n0(0) + (l & 15);
     const long base = tile * CH * DK + d0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -577,25 +629,44 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const IO* __r
       khin[j] = dKhg[base + r * DK + dl];
     }
   }
-  TD aP, aA, bP, bA;
-  aP.zero(); aA.zero(); bP.zero(); bA.zero();
-  aP.template mma<float, CH>(KRow<float, LC>{dPs}, kdown);
-  bP.template mma<float, CH>(KCol<float, LC>{dPs}, kfun<float>([&](int d, int r) {
-    return r >= 16 * (R + 1) ? Qs[r * LS + d] * __expf(Gs[r * LS + d] - last(d)) : 0.f;
-  }));
-  if (b) {
-    aA.template mma<float, CH>(KRow<float, LC>{dAs}, kdown);
-    bA.template mma<float, CH>(KCol<float, LC>{dAs}, kfun<float>([&](int d, int r) {
-      return r >= 16 * (R + 1) ? Bs[r * LS + d] * Ks[r * LS + d] * __expf(Gs[r * LS + d] - last(d)) : 0.f;
-    }));
+  // Row sums (output rows r of block R, channel dl) over i in blocks before R
+  // and, unless block R is summed exactly, in R (dP and dA are zero above
+  // their diagonals): K_id e^{G_ref - G_id}, shared by dP and dA.  Column sums
+  // (output rows i of block R) over r in blocks after R, and in R likewise:
+  // e^{G_rd - G_last} shared by Q and Kb.  Lane l supplies contraction index
+  // 16 cb + 4 (l >> 4) + t at sub-step t on both sides of each product.
+  f32x4 aP = {0.f, 0.f, 0.f, 0.f}, aA = aP, bP = aP, bA = aP;
+  {
+    const int own = 16 * R + (l & 15);
+    for (int cb = 0; cb < (exact ? R : R + 1); ++cb) {
+      const int i0 = 16 * cb + 4 * (l >> 4);
+      const float4 pr = *reinterpret_cast<const float4*>(dPs + own * LC + i0);
+      const float4 ar = *reinterpret_cast<const float4*>(dAs + own * LC + i0);
+      const float pv[4] = {pr.x, pr.y, pr.z, pr.w}, av[4] = {ar.x, ar.y, ar.z, ar.w};
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int i = i0 + t;
+        const float kt = Ks[i * LS + dl] * __expf(rf - Gs[i * LS + dl]);
+        aP = Mma<float>::mma(pv[t], kt, aP);
+        if (b) aA = Mma<float>::mma(av[t], kt, aA);
+      }
+    }
+    for (int cb = exact ? R + 1 : R; cb < 4; ++cb) {
+      const int r0 = 16 * cb + 4 * (l >> 4);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int r = r0 + t;
+        const float e = __expf(Gs[r * LS + dl] - lst);
+        bP = Mma<float>::mma(dPs[r * LC + own], Qs[r * LS + dl] * e, bP);
+        if (b) bA = Mma<float>::mma(dAs[r * LC + own], Bs[r * LS + dl] * Ks[r * LS + dl] * e, bA);
+      }
+    }
   }
-  // the pairs inside block R are summed exactly below: row sums over
-  // i in [16R, r] (a) and column sums over r in [i, 16R + 15] (b), one
-  // exponential e^{G_r - G_i} per term shared by the dP and dA sums
+  // in a block summed exactly: row sums over i in [16R, r] and column sums
+  // over r in [i, 16R + 15], one exponential e^{G_r - G_i} per term shared by
+  // the dP and dA sums
   float dGv[4], Zv[4];
   {
-    const int l = lane_id();
-    const int dl = TD::n0(0) + (l & 15);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = TD::m0(0) + (l >> 4) * 4 + j;
@@ -603,22 +674,24 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const IO* __r
       const float gam = __expf(G), dte = __expf(GL - G);
       const float qv = Qs[r * LS + dl], kv = Ks[r * LS + dl], bv = Bs[r * LS + dl], kb = bv * kv;
       const float xv = xin[j], dqg = qgin[j], dkh = khin[j];
-      float dqP = 0.f, dkbA = 0.f;  // row sums inside the block
-      for (int i = 16 * R; i <= r; ++i) {
-        const float ke = Ks[i * LS + dl] * __expf(G - Gs[i * LS + dl]);
-        dqP += dPs[r * LC + i] * ke;
-        dkbA += dAs[r * LC + i] * ke;  // dA is zero on the diagonal
+      float dqP = 0.f, dkbA = 0.f, dkP = 0.f, dkA = 0.f;
+      if (exact) {
+        for (int i = 16 * R; i <= r; ++i) {
+          const float ke = Ks[i * LS + dl] * __expf(G - Gs[i * LS + dl]);
+          dqP += dPs[r * LC + i] * ke;
+          dkbA += dAs[r * LC + i] * ke;  // dA is zero on the diagonal
+        }
+        for (int rr = r; rr <= 16 * R + 15; ++rr) {  // row r plays i
+          const float e = __expf(Gs[rr * LS + dl] - G);
+          dkP += dPs[rr * LC + r] * Qs[rr * LS + dl] * e;
+          dkA += dAs[rr * LC + r] * Bs[rr * LS + dl] * Ks[rr * LS + dl] * e;  // zero at rr == r
+        }
       }
-      float dkP = 0.f, dkA = 0.f;  // column sums inside the block (row r plays i)
-      for (int rr = r; rr <= 16 * R + 15; ++rr) {
-        const float e = __expf(Gs[rr * LS + dl] - G);
-        dkP += dPs[rr * LC + r] * Qs[rr * LS + dl] * e;
-        dkA += dAs[rr * LC + r] * Bs[rr * LS + dl] * Ks[rr * LS + dl] * e;  // zero at rr == r
-      }
-      dqP += aP.acc[0][0][j] * __expf(G - ref(dl));
-      dkP += bP.acc[0][0][j] * __expf(last(dl) - G);
-      dkbA = b ? dkbA + aA.acc[0][0][j] * __expf(G - ref(dl)) : 0.f;
-      dkA = b ? dkA + bA.acc[0][0][j] * __expf(last(dl) - G) : 0.f;
+      const float ea = __expf(G - rf), eb = __expf(lst - G);
+      dqP += aP[j] * ea;
+      dkP += bP[j] * eb;
+      dkbA = b ? dkbA + aA[j] * ea : 0.f;
+      dkA = b ? dkA + bA[j] * eb : 0.f;
       const float dkb = gam * xv + dkbA;
       const float khdkh = dte * kv * dkh;
       dGv[j] = gam * qv * dqg + qv * dqP - kv * dkP + kb * dkbA - kv * dkA + gam * kb * xv - khdkh;

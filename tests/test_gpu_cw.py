@@ -13,6 +13,8 @@ oracle sees the same once-rounded values):
   sequences (including a one-token sequence), a T shorter than one chunk;
 * a strong decay (mean log-decay about -4 per token and channel, tails near
   -15): the chunked kernels split every decay so that no factor exceeds 1;
+  and strong and weak 16-token blocks mixed inside each chunk (exact and
+  matrix-core in-block sums side by side);
 * the throughput shape (B4 T4096 H16 d128) in the launch configuration the
   bench times, checked on sampled heads;
 * run-to-run bitwise determinism, and fwd + bwd captured in a HIP graph with
@@ -114,6 +116,16 @@ def test_strong_decay():
     # a 16-token block decays by ~65 on average and by far more in the tails:
     # a single reference per block would overflow fp32 here
     check(W.make_cw_case("cw_strong", 1, 192, 2, 128, 128, gates="gbw", seed=5, decay=5.0))
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_mixed_decay_blocks(io):
+    # every third 16-token block decays strongly (its in-block pairs are summed
+    # exactly), the others weakly (they go to the matrix cores), inside the
+    # same chunks; the ragged tail ends in a strong block
+    T = 200
+    scale = np.where((np.arange(T) // 16) % 3 == 0, 8.0, 0.3)
+    check(W.make_cw_case(f"cw_mixed_{io}", 2, T, 2, 128, 128, gates="gbw", seed=16, decay=scale, io_dtype=io))
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])

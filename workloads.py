@@ -320,7 +320,11 @@ def make_cw_case(name, B, T, H, dk, dv, *, gates="gbw", seed=0, decay=1.0, cu_se
     S0 = f32(S0_std * rng.standard_normal((N, H, dk, dv)))
     dO = f32(rng.standard_normal((B, T, H, dv)))
     dS_T = f32(dST_std * rng.standard_normal((N, H, dk, dv)))
-    g = f32(-decay * _softplus(g_raw)) if gates in ("gbw", "kda", "g") else None
+    # decay: a scale of the log-decay, one number or one per token (shape [T])
+    dscale = np.asarray(decay, dtype=np.float64)
+    if dscale.ndim == 1:
+        dscale = dscale[None, :, None, None]
+    g = f32(-dscale * _softplus(g_raw)) if gates in ("gbw", "kda", "g") else None
     b = w = None
     if gates == "gbw":
         b = f32(_sigmoid(b_logit))

@@ -215,24 +215,26 @@ def kernel_model(B, T, H, dk, dv, es, N=None):
 def cw_kernel_model(B, T, H, dk, dv, N=None, es=4):
     """Algorithmic bytes and flops per launch of the channel-wise stages (each
     kernel's own inputs and outputs moved once; the activations q, k, v, o, dO
-    and their gradients at es bytes, everything else fp32)."""
+    and their gradients, and the operands the scans read or write (P, e^G Q,
+    Khat, W, U, dO^T, dh, dU'^T), at es bytes; everything else fp32)."""
     N = B if N is None else N
     tiles = B * (-(-T // CH)) * H
     ck, cv, cc, st, vk = CH * dk * 4, CH * dv * 4, CH * CH * 4, dk * dv * 4, dk * 4
     ak, av = CH * dk * es, CH * dv * es  # activation tiles
+    ok, ov, oc, ost = CH * dk * es, CH * dv * es, CH * CH * es, dk * dv * es  # scan operands
     per = {
         # q, k, g, b, v, w -> G_last, P, e^G Q, Khat^T, W, U
-        "cw_fwd_prep": (2 * ak + 2 * ck + av + cv + vk + cc + 3 * ck + cv,
+        "cw_fwd_prep": (2 * ak + 2 * ck + av + cv + vk + oc + 3 * ok + ov,
                         2 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dk + 2 * CH * CH * dv),
         # e^G Q, W, Khat^T, P, U, G_last -> chunk states, o
-        "cw_fwd_scan": (3 * ck + cc + cv + vk + st + av, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
-        # q, k, g, b, dO -> G_last, P^T, (e^G Q)^T, Khat, W^T, T, Gamma*b*k, dO^T
-        "cw_bwd_prep": (2 * ak + 2 * ck + av + vk + 2 * cc + 4 * ck + cv,
+        "cw_fwd_scan": (3 * ok + oc + ov + vk + st + av, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
+        # q, k, g, b, dO -> G_last, P^T, T, (e^G Q)^T, Khat, W^T, Gamma*b*k, dO^T
+        "cw_bwd_prep": (2 * ak + 2 * ck + av + vk + oc + cc + 3 * ok + ck + ov,
                         2 * 2 * CH * CH * dk + CH ** 3 / 3 + 2 * CH * CH * dk),
         # Khat, W^T, (e^G Q)^T, dO^T, P^T, G_last -> dh, dU'^T
-        "cw_bwd_scan": (3 * ck + cv + cc + vk + st + cv, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
+        "cw_bwd_scan": (3 * ok + ov + oc + vk + ost + ov, 3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
         # v, w, dO, state, T, Gamma*b*k, dh, dU'^T -> dv, dw, dP, dA, X, dQg, dKhat, <h, dh>
-        "cw_bwd_grad_v": (2 * av + cv + st + cc + ck + st + cv + av + cv + 2 * cc + 3 * ck + vk,
+        "cw_bwd_grad_v": (2 * av + cv + st + cc + ck + ost + ov + av + cv + 2 * cc + 3 * ck + vk,
                           2 * CH * dk * dv + 3 * 2 * CH * CH * dv + 3 * 2 * CH * dk * dv),
         # q, k, g, b, dP, dA, X, dQg, dKhat, <h, dh> -> dq, dk, dg, db
         "cw_bwd_grad_d": (2 * ak + 2 * ck + 2 * cc + 3 * ck + vk + 2 * ak + 2 * ck, 4 * 2 * CH * CH * dk),

@@ -175,12 +175,18 @@ gdn_status gdn_bwd_ex(const gdn_problem* p, const void* q, const void* k, const 
  *
  * Layouts as above, with g, b [B,T,H,d_k] and w [B,T,H,d_v] (and dg, db, dw)
  * fp32 row-major (packed sequences: B = 1 and cu_seqlens as above).  q, k, v,
- * o, dO, dq, dk, dv are in io_dtype (fp32 or bf16); every operand inside the
- * chunked algorithm is fp32 (fp32 matrix cores) either way.  `variant` is not
- * read.
+ * o, dO, dq, dk, dv are in io_dtype (fp32 or bf16).  With GDN_F32 every
+ * operand inside the chunked algorithm is fp32 (fp32 matrix cores).  With
+ * GDN_BF16 the two scans take bf16 operands, as gdn_fwd / gdn_bwd do (fp32
+ * state and accumulation; the state gradients between the reverse scan and
+ * the gradient kernels are bf16), and the prep and gradient kernels compute in
+ * fp32.  `variant` is not read.
  * chunk_states has the layout and meaning of gdn_fwd's.  The chunked kernels
- * form each decay exp(G_r - G_i) either per term or split at a reference row
- * between r and i, so for a decay (every g <= 0) no factor exceeds 1; a g > 0
+ * form each decay exp(G_r - G_i) split at a reference row: for r and i in
+ * different 16-token blocks a row between them, so for a decay (every g <= 0)
+ * no factor exceeds 1; inside a block the row before it, used only where the
+ * block's log-decay moves by at most 32 from that row in every channel
+ * (factors within e^{+-64}), else exp(G_r - G_i) is formed per term.  A g > 0
  * (growth) is computed the same way and overflows where the true values do.
  * Non-finite inputs propagate through the chunked arithmetic; there is no
  * token-serial exact pass on this path.

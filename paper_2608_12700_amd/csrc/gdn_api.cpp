@@ -163,11 +163,12 @@ void layout_cw_fwd(const Shape& s, char* base, CwFwdWs* w, size_t* total) {
   w->chunk_off = b.take<int>(s.packed ? s.N + 1 : 0);
   w->flag_scan = b.take<int>((size_t)s.N * s.H * (s.dv / SCAN_BV));
   w->gC = b.take<float>(tiles * s.dk);
-  w->W = b.take<float>(tiles * kChunk * s.dk);
-  w->U = b.take<float>(tiles * kChunk * s.dv);
-  w->KhT = b.take<float>(tiles * kChunk * s.dk);
-  w->P = b.take<float>(tiles * kChunk * kChunk);
-  w->Qg = b.take<float>(tiles * kChunk * s.dk);
+  // the scan's operands in the activation dtype
+  w->W = b.take<char>(tiles * kChunk * s.dk * s.es);
+  w->U = b.take<char>(tiles * kChunk * s.dv * s.es);
+  w->KhT = b.take<char>(tiles * kChunk * s.dk * s.es);
+  w->P = b.take<char>(tiles * kChunk * kChunk * s.es);
+  w->Qg = b.take<char>(tiles * kChunk * s.dk * s.es);
   *total = b.off;
 }
 
@@ -178,15 +179,17 @@ void layout_cw_bwd(const Shape& s, char* base, CwBwdWs* w, size_t* total) {
   w->chunk_off = b.take<int>(s.packed ? s.N + 1 : 0);
   w->flag_scan = b.take<int>((size_t)s.N * s.H * (s.dv / SCAN_BV));
   w->gC = b.take<float>(tiles * s.dk);
-  w->WT = b.take<float>(ck);
-  w->QgT = b.take<float>(ck);
-  w->dOT = b.take<float>(cv);
-  w->PT = b.take<float>(cc);
+  // the reverse scan's operands and outputs in the activation dtype
+  w->WT = b.take<char>(ck * s.es);
+  w->QgT = b.take<char>(ck * s.es);
+  w->dOT = b.take<char>(cv * s.es);
+  w->PT = b.take<char>(cc * s.es);
+  w->Kh = b.take<char>(ck * s.es);
+  w->dh = b.take<char>(tiles * (size_t)s.dk * s.dv * s.es);
+  w->dUT = b.take<char>(cv * s.es);
+  // fp32 for the gradient kernels
   w->T = b.take<float>(cc);
-  w->Kh = b.take<float>(ck);
   w->KbG = b.take<float>(ck);
-  w->dh = b.take<float>(tiles * (size_t)s.dk * s.dv);
-  w->dUT = b.take<float>(cv);
   w->dP = b.take<float>(cc);
   w->dA = b.take<float>(cc);
   w->X = b.take<float>(ck);

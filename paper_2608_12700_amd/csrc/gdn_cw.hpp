@@ -6,7 +6,9 @@
 //
 // with g_t, b_t in R^{d_k} and w_t in R^{d_v}; a NULL gate is neutral (g = 0,
 // b = 0, w = 1).  Activations (q, k, v, dO and their gradients, o) are fp32 or
-// bf16 (IO); every operand inside is fp32 (fp32 matrix cores).
+// bf16 (IO).  The prep and gradient kernels compute in fp32 (fp32 matrix
+// cores); the two scans take their operands in IO, so with bf16 activations
+// they run on bf16 matrix cores with an fp32 carry, as the scalar-gate path.
 //
 // Chunked form (Sec. 4.2), per chunk of 64 tokens with G_r = sum_{s<=r} g_s (a
 // d_k-vector per row), Gamma = e^G, Kb = b * K, Khat_r = e^{G_last - G_r} * k_r:
@@ -30,6 +32,8 @@
 // matrix cores too (factors within e^{+-2 CW_SPREAD}: no overflow, no
 // denormals, the same per-term rounding).
 #pragma once
+
+#include <type_traits>
 
 #include "gdn_bwd.hpp"
 #include "gdn_fwd.hpp"
@@ -148,21 +152,100 @@ struct CwRows {
   }
 };
 
+// Scan operands (P, diag-scaled Q, Khat, W, dO^T) in the activation dtype,
+// laid out by op_off: row-major for fp32, MFMA fragment blocks for bf16.
+// Piece idx (8 consecutive k of one row m) of a M x K operand: consecutive
+// pieces are consecutive 16-byte runs of the bf16 layout (whole 1 KiB
+// fragment blocks per wave) and consecutive runs of a row for fp32.
+template <typename OP, int K>
+__device__ __forceinline__ void op_piece(int idx, int& m, int& k0) {
+  if constexpr (sizeof(OP) == 2) {
+    const int f = idx >> 6, ll = idx & 63;
+    m = (f / (K / 32)) * 16 + (ll & 15);
+    k0 = (f % (K / 32)) * 32 + (ll >> 4) * 8;
+  } else {
+    m = idx / (K / 8);
+    k0 = (idx - m * (K / 8)) * 8;
+  }
+}
+template <typename OP, int K>
+__device__ __forceinline__ void put_op8(OP* base, int m, int k0, const float* x) {
+  OP* p = base + op_off<OP, K>(m, k0);
+  if constexpr (sizeof(OP) == 2) {
+    OP v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = from_f<OP>(x[j]);
+    *reinterpret_cast<uint4*>(p) = pack16<OP>(v);
+  } else {
+    *reinterpret_cast<float4*>(p) = float4{x[0], x[1], x[2], x[3]};
+    *reinterpret_cast<float4*>(p + 4) = float4{x[4], x[5], x[6], x[7]};
+  }
+}
+// four consecutive k (k0 % 4 == 0) of row m
+template <typename OP, int K>
+__device__ __forceinline__ void put_op4(OP* base, int m, int k0, const float* x) {
+  OP v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] = from_f<OP>(x[j]);
+  *reinterpret_cast<typename vec4_of<OP>::type*>(base + op_off<OP, K>(m, k0)) = pack4<OP>(v);
+}
+
+// Rows [m0, m0 + MR) x columns [k0, k0 + KC) of a bf16 operand laid out by
+// op_off<bf16, K> (m0 % 16 == 0, k0 % 32 == 0, KC % 32 == 0), read by NT
+// threads in one batch (whole 1 KiB fragment blocks) and staged to LDS as fp32
+// [m - m0][k - k0].
+template <int MR, int KC, int K, int NT>
+struct OpIn16 {
+  static constexpr int PIECES = MR * KC / 8, N = (PIECES + NT - 1) / NT;
+  static_assert(MR % 16 == 0 && KC % 32 == 0, "whole fragment blocks");
+  uint4 u[N];
+  __device__ __forceinline__ static void where(int t, int& idx, int& m, int& k) {
+    idx = thread_x() + t * NT;
+    const int i = idx < PIECES ? idx : PIECES - 1, f = i >> 6, ll = i & 63;
+    m = (f / (KC / 32)) * 16 + (ll & 15);
+    k = (f % (KC / 32)) * 32 + (ll >> 4) * 8;
+  }
+  __device__ __forceinline__ void load(const bf16* __restrict__ base, int m0, int k0) {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, m, k;
+      where(t, idx, m, k);
+      u[t] = *reinterpret_cast<const uint4*>(base + op_off<bf16, K>(m0 + m, k0 + k));
+    }
+  }
+  template <int LD>
+  __device__ __forceinline__ void stage(float* dst) const {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, m, k;
+      where(t, idx, m, k);
+      if (idx >= PIECES) continue;
+      float f[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) f[j] = to_f(elem16<bf16>(u[t], j));
+      *reinterpret_cast<float4*>(dst + m * LD + k) = float4{f[0], f[1], f[2], f[3]};
+      *reinterpret_cast<float4*>(dst + m * LD + k + 4) = float4{f[4], f[5], f[6], f[7]};
+    }
+  }
+};
+
 // One block per (chunk, head).  Forward mode writes the operands of the
 // generic forward scan (P, diag-scaled Q, Khat^T, W, U); backward mode writes
 // those of the reverse scan and the gradient kernels (P^T, (Gamma Q)^T,
-// Khat, W^T, T, Gamma * Kb, dO^T).  Both write G_last per channel.
+// Khat, W^T, T, Gamma * Kb, dO^T).  Both write G_last per channel.  The
+// scans' operands are written in the activation dtype IO (op_off layout);
+// T and Gamma * Kb, read by the gradient kernel, stay fp32.
 constexpr int CW_PREP_THREADS = 1024;  // 16 waves: one block per CU (LDS), so all its latency hiding is in-block
 template <int DK, int DV, bool BWD, typename IO>
 __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, const IO* __restrict__ q,
                                                  const IO* __restrict__ k, const IO* __restrict__ v,
                                                  const float* __restrict__ g, const float* __restrict__ b,
                                                  const float* __restrict__ w, const IO* __restrict__ dO,
-                                                 float* __restrict__ gC, float* __restrict__ Pg,
-                                                 float* __restrict__ Qgg, float* __restrict__ Khg,
-                                                 float* __restrict__ Wg, float* __restrict__ Ug,
+                                                 float* __restrict__ gC, IO* __restrict__ Pg,
+                                                 IO* __restrict__ Qgg, IO* __restrict__ Khg,
+                                                 IO* __restrict__ Wg, IO* __restrict__ Ug,
                                                  float* __restrict__ Tg, float* __restrict__ KbGg,
-                                                 float* __restrict__ dOTg) {
+                                                 IO* __restrict__ dOTg) {
   constexpr int LK = DK + 4, LC = CH + 4, VS = 64, LV = VS + 4;
   static_assert(CH * LC <= CH * LK && CH * LV <= CH * LK, "T and the w * V slices reuse Q's and K's tiles");
   __shared__ __align__(16) float Qs[CH * LK];  // Q, then T (stride LC)
@@ -258,7 +341,7 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   // rows 16R + 4 (l >> 4) + j, column 16c + (l & 15).
   {
     const int wv = wave_id(), l = lane_id();
-    float* Pt = Pg + tile * CH * CH;
+    IO* Pt = Pg + tile * CH * CH;
     int R, c;
     if (wv < 10) {
       R = wv < 1 ? 0 : wv < 3 ? 1 : wv < 6 ? 2 : 3;
@@ -308,27 +391,36 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
       }
     }
     if (BWD) {
-      *reinterpret_cast<float4*>(Pt + i * CH + r0) = float4{pv[0], pv[1], pv[2], pv[3]};
+      put_op4<IO, CH>(Pt, i, r0, pv);
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) Pt[(r0 + j) * CH + i] = pv[j];
+      for (int j = 0; j < 4; ++j) Pt[op_off<IO, CH>(r0 + j, i)] = from_f<IO>(pv[j]);
     }
   }
   // Gamma * Q and Khat = e^{G_last - G} * K, each in the layout its scan reads
   {
-    float* Qt = Qgg + tile * CH * DK;
-    float* Kt = Khg + tile * CH * DK;
-    for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
-      // row-major [r][d] outputs walk d fastest, transposed [d][r] ones r fastest
-      const int r1 = i / DK, d1 = i - r1 * DK, d2 = i / CH, r2 = i - d2 * CH;
-      const float G1 = Gs[r1 * LK + d1], G2 = Gs[r2 * LK + d2];
-      if (BWD) {
-        Qt[d2 * CH + r2] = __expf(G2) * Qs[r2 * LK + d2];
-        Kt[r1 * DK + d1] = __expf(Gs[(CH - 1) * LK + d1] - G1) * Ks[r1 * LK + d1];
-      } else {
-        Qt[r1 * DK + d1] = __expf(G1) * Qs[r1 * LK + d1];
-        Kt[d2 * CH + r2] = __expf(Gs[(CH - 1) * LK + d2] - G2) * Ks[r2 * LK + d2];
+    IO* Qt = Qgg + tile * CH * DK;
+    IO* Kt = Khg + tile * CH * DK;
+    // pieces of 8: rows r of the [r][d] output (forward Gamma * Q, backward
+    // Khat), columns r of the [d][r] one (forward Khat^T, backward (Gamma Q)^T)
+    for (int i = thread_x(); i < CH * DK / 8; i += blockDim.x) {
+      int r, d0;
+      op_piece<IO, DK>(i, r, d0);
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float G = Gs[r * LK + d0 + j];
+        x[j] = BWD ? __expf(Gs[(CH - 1) * LK + d0 + j] - G) * Ks[r * LK + d0 + j] : __expf(G) * Qs[r * LK + d0 + j];
       }
+      put_op8<IO, DK>(BWD ? Kt : Qt, r, d0, x);
+      int d, r0;
+      op_piece<IO, CH>(i, d, r0);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float G = Gs[(r0 + j) * LK + d];
+        x[j] = BWD ? __expf(G) * Qs[(r0 + j) * LK + d] : __expf(Gs[(CH - 1) * LK + d] - G) * Ks[(r0 + j) * LK + d];
+      }
+      put_op8<IO, CH>(BWD ? Qt : Kt, d, r0, x);
     }
     for (int d = thread_x(); d < DK; d += blockDim.x) gC[tile * DK + d] = Gs[(CH - 1) * LK + d];
   }
@@ -360,17 +452,27 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   __syncthreads();
   // W = T (Gamma * Kb)
   {
-    float* Wt = Wg + tile * CH * DK;
+    IO* Wt = Wg + tile * CH * DK;
     if (b) {
       Tiles<CH, DK, 4, WN> wt;
       wt.zero();
       wt.template mma<float, CH>(KRow<float, LC>{Tf}, KCol<float, LK>{Bk});
-      wt.each([&](int r, int d, float& x) {
-        if (BWD) Wt[d * CH + r] = x;
-        else Wt[r * DK + d] = x;
-      });
+      const int l = lane_id();
+#pragma unroll
+      for (int a = 0; a < wt.TM; ++a)
+#pragma unroll
+        for (int bb = 0; bb < wt.TN; ++bb) {
+          const int r0 = wt.m0(a) + (l >> 4) * 4, d = wt.n0(bb) + (l & 15);
+          const float x4[4] = {wt.acc[a][bb][0], wt.acc[a][bb][1], wt.acc[a][bb][2], wt.acc[a][bb][3]};
+          if (BWD) {
+            put_op4<IO, CH>(Wt, d, r0, x4);
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) Wt[op_off<IO, DK>(r0 + j, d)] = from_f<IO>(x4[j]);
+          }
+        }
     } else {
-      for (int i = thread_x(); i < CH * DK; i += blockDim.x) Wt[i] = 0.f;
+      for (int i = thread_x(); i < CH * DK; i += blockDim.x) Wt[i] = from_f<IO>(0.f);
     }
   }
   // dO^T [v][r]: 64 columns of dO at a time staged row-major in K's tile (free
@@ -379,21 +481,26 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   if constexpr (BWD) {
     constexpr int PW = 64;
     static_assert(PW <= LK && DV % PW == 0, "a pass fits K's tile");
-    float* Dt = dOTg + tile * DV * CH;
+    IO* Dt = dOTg + tile * DV * CH;
 #pragma unroll
     for (int ps = 0; ps < DV / PW; ++ps) {
       __syncthreads();
       doin.template stage<LK>(Ks, cp.len, ps * PW, (ps + 1) * PW);
       __syncthreads();
-      for (int i = thread_x(); i < PW * CH; i += blockDim.x) {
-        const int vv = i / CH, r = i - vv * CH;
-        Dt[(long)(ps * PW + vv) * CH + r] = Ks[r * LK + vv];
+      // the pass's rows v of dO^T are one contiguous range of pieces
+      for (int i = thread_x(); i < PW * CH / 8; i += blockDim.x) {
+        int vr, r0;
+        op_piece<IO, CH>(ps * PW * CH / 8 + i, vr, r0);
+        float x[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = Ks[(r0 + j) * LK + vr - ps * PW];
+        put_op8<IO, CH>(Dt, vr, r0, x);
       }
     }
   }
   // U = T (w * V) in the forward scan's accumulator-tile layout
   if constexpr (!BWD) {
-    float* Ut = Ug + tile * CH * DV;
+    IO* Ut = Ug + tile * CH * DV;
 #pragma unroll
     for (int t = 0; t < NSL; ++t) {
       const int c0 = t * VS;
@@ -411,8 +518,10 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
 #pragma unroll
       for (int bb = 0; bb < uu.TN; ++bb) {
         const int r0 = uu.m0(0) + (l >> 4) * 4, vcol = c0 + uu.n0(bb) + (l & 15);
-        const float u4[4] = {uu.acc[0][bb][0], uu.acc[0][bb][1], uu.acc[0][bb][2], uu.acc[0][bb][3]};
-        *reinterpret_cast<uint4*>(Ut + cfrag_off<SCAN_BV>(r0, vcol)) = pack4<float>(u4);
+        IO u4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) u4[j] = from_f<IO>(uu.acc[0][bb][j]);
+        *reinterpret_cast<typename vec4_of<IO>::type*>(Ut + cfrag_off<SCAN_BV>(r0, vcol)) = pack4<IO>(u4);
       }
     }
   }
@@ -430,8 +539,8 @@ template <int DK, int DV, typename IO>
 __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __restrict__ v,
                                                    const float* __restrict__ w, const IO* __restrict__ dO,
                                                    const float* __restrict__ states, const float* __restrict__ Tg,
-                                                   const float* __restrict__ KbGg, const float* __restrict__ dhg,
-                                                   const float* __restrict__ dUTg, IO* __restrict__ dvo,
+                                                   const float* __restrict__ KbGg, const IO* __restrict__ dhg,
+                                                   const IO* __restrict__ dUTg, IO* __restrict__ dvo,
                                                    float* __restrict__ dwo, float* __restrict__ dPg,
                                                    float* __restrict__ dAg, float* __restrict__ Xg,
                                                    float* __restrict__ dQgg, float* __restrict__ dKhg,
@@ -439,31 +548,39 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __r
   constexpr int LK = DK + 4, LC = CH + 4, VS = 32, LV = VS + 4;
   __shared__ __align__(16) float Ts[CH * LC];
   __shared__ __align__(16) float KbG[CH * LK];
-  __shared__ __align__(16) float Vs[CH * LV], Ws[CH * LV], dOs[CH * LV], Rs[CH * LV], Ups[CH * LV], Ys[CH * LV];
-  __shared__ __align__(16) float dUT[VS * LC];
+  __shared__ __align__(16) float Vs[CH * LV], Ws[CH * LV], dOs[CH * LV], Ups[CH * LV], Ys[CH * LV];
+  __shared__ __align__(16) float dUT[VS * LC], RT[VS * LC];  // dU'^T and R^T: [v][r]
   __shared__ __align__(16) float hs[DK * LV], dhs[DK * LV];
 
   const int ci = blockIdx.x, h = blockIdx.y;
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
   const long rsv = (long)H * DV, bv = (cp.row0 * H + h) * DV;
-  // the tiles of one value slice, requested in one batch
+  // the tiles of one value slice, requested in one batch (dh and dU'^T come
+  // from the reverse scan in the activation dtype, op_off layout)
+  constexpr bool B16 = sizeof(IO) == 2;
   struct Slice {
     CwRows<VS, 512, IO> v, dO;
     CwRows<VS, 512, float> w;
-    TileIn<DK, VS, 512> h, dh;
-    TileIn<VS, CH, 512> dut;
+    TileIn<DK, VS, 512> h;
+    std::conditional_t<B16, OpIn16<DK, VS, DV, 512>, TileIn<DK, VS, 512>> dh;
+    std::conditional_t<B16, OpIn16<VS, CH, CH, 512>, TileIn<VS, CH, 512>> dut;
   };
   const float* hp = states + tile * DK * DV;
-  const float* dhp = dhg + tile * DK * DV;
-  const float* dUp = dUTg + tile * DV * CH;
+  const IO* dhp = dhg + tile * DK * DV;
+  const IO* dUp = dUTg + tile * DV * CH;
   auto load_slice = [&](Slice& sl, int c0) {
     sl.v.load(v + bv + c0, rsv, cp.len);
     if (w) sl.w.load(w + bv + c0, rsv, cp.len);
     sl.dO.load(dO + bv + c0, rsv, cp.len);
     sl.h.load(hp + c0, DV);
-    sl.dh.load(dhp + c0, DV);
-    sl.dut.load(dUp + (long)c0 * CH, CH);
+    if constexpr (B16) {
+      sl.dh.load(dhp, 0, c0);
+      sl.dut.load(dUp, c0, 0);
+    } else {
+      sl.dh.load(dhp + c0, DV);
+      sl.dut.load(dUp + (long)c0 * CH, CH);
+    }
   };
   {
     TileIn<CH, CH, 512> tin;
@@ -475,6 +592,11 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __r
   }
   Slice cur, nxt;
   load_slice(cur, 0);
+  __syncthreads();
+  // T^T fragments of this wave's rows, for Y = T^T dU' in every slice
+  typedef Tiles<CH, VS, 4, 2> TV;
+  typename TV::template AFr<float, CH> tT;
+  tT.load(KCol<float, LC>{Ts});
   Tiles<CH, CH, 4, 2> dP, dA;
   Tiles<CH, DK, 4, 2> X, dQg, dKh;
   dP.zero(); dA.zero(); X.zero(); dQg.zero(); dKh.zero();
@@ -497,18 +619,18 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __r
       for (int c = 0; c < VS; ++c) hdh += hs[d * LV + c] * dhs[d * LV + c];
     }
     {
-      Tiles<CH, VS, 4, 2> rr;
+      TV rr;
       rr.zero();
       rr.template mma<float, DK>(KRow<float, LK>{KbG}, KCol<float, LV>{hs});
       rr.each([&](int r, int vv, float& x) {
         const float wv = w ? Ws[r * LV + vv] : 1.f;
-        Rs[r * LV + vv] = wv * Vs[r * LV + vv] - x;
+        RT[vv * LC + r] = wv * Vs[r * LV + vv] - x;
       });
     }
     {
-      Tiles<CH, VS, 4, 2> y;
+      TV y;
       y.zero();
-      y.template mma<float, CH>(KCol<float, LC>{Ts}, KRow<float, LC>{dUT});
+      y.template mma<float, CH>(tT, KRow<float, LC>{dUT});
       y.each([&](int r, int vv, float& x) {
         Ys[r * LV + vv] = x;
         if (r < cp.len) {
@@ -520,9 +642,9 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __r
     }
     __syncthreads();
     {
-      Tiles<CH, VS, 4, 2> up;
+      TV up;
       up.zero();
-      up.template mma<float, CH>(KRow<float, LC>{Ts}, KCol<float, LV>{Rs});
+      up.template mma<float, CH>(KRow<float, LC>{Ts}, KRow<float, LC>{RT});
       up.each([&](int r, int vv, float& x) { Ups[r * LV + vv] = x; });
     }
     __syncthreads();
@@ -741,14 +863,14 @@ static hipError_t launch_cw_fwd_t(const CwFwdArgs& a) {
   if (geo.total_chunks > 0)
     hipLaunchKernelGGL((k_cw_prep<DK, DV, false, IO>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream,
                        geo, H, (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, (const IO*)nullptr,
-                       w.gC, w.P, w.Qg, w.KhT, w.W, w.U,
-                       (float*)nullptr, (float*)nullptr, (float*)nullptr);
+                       w.gC, (IO*)w.P, (IO*)w.Qg, (IO*)w.KhT, (IO*)w.W, (IO*)w.U,
+                       (float*)nullptr, (float*)nullptr, (IO*)nullptr);
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0)
-    hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, float, VAR_GATED, true, IO>), dim3(NS * NVT), dim3(256), 0,
-                       a.stream, geo, H, (const float*)w.Qg, (const float*)nullptr, a.S0, w.gC, (const float*)w.W,
-                       (const float*)w.KhT, (const float*)w.P, (const float*)w.U, a.states, a.ST, (IO*)a.o,
+    hipLaunchKernelGGL((k_scan_fwd<DK, DV, BV, IO, VAR_GATED, true, IO>), dim3(NS * NVT), dim3(256), 0,
+                       a.stream, geo, H, (const IO*)w.Qg, (const IO*)nullptr, a.S0, w.gC, (const IO*)w.W,
+                       (const IO*)w.KhT, (const IO*)w.P, (const IO*)w.U, a.states, a.ST, (IO*)a.o,
                        w.flag_scan);
   stage_mark(a.events, 2, a.stream);
   stage_mark(a.events, 3, a.stream);
@@ -770,19 +892,19 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
   if (geo.total_chunks > 0)
     hipLaunchKernelGGL((k_cw_prep<DK, DV, true, IO>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream,
                        geo, H, (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, (const IO*)a.dO,
-                       w.gC, w.PT, w.QgT, w.Kh, w.WT, (float*)nullptr, w.T,
-                       w.KbG, w.dOT);
+                       w.gC, (IO*)w.PT, (IO*)w.QgT, (IO*)w.Kh, (IO*)w.WT, (IO*)nullptr, w.T,
+                       w.KbG, (IO*)w.dOT);
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0)
-    hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, float, VAR_GATED, true>), dim3(NS * NVT), dim3(256), 0, a.stream,
-                       geo, H, (const float*)w.Kh, a.dST, w.gC, (const float*)w.WT, (const float*)w.QgT,
-                       (const float*)w.dOT, (const float*)w.PT, w.dh, w.dUT, a.dS0, w.flag_scan);
+    hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, IO, VAR_GATED, true>), dim3(NS * NVT), dim3(256), 0, a.stream,
+                       geo, H, (const IO*)w.Kh, a.dST, w.gC, (const IO*)w.WT, (const IO*)w.QgT,
+                       (const IO*)w.dOT, (const IO*)w.PT, (IO*)w.dh, (IO*)w.dUT, a.dS0, w.flag_scan);
   stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0) {
     hipLaunchKernelGGL((k_cw_grad_v<DK, DV, IO>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
-                       (const IO*)a.v, a.w, (const IO*)a.dO, a.states, (const float*)w.T, (const float*)w.KbG, (const float*)w.dh,
-                       (const float*)w.dUT, (IO*)a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg, w.dKh, w.hdh);
+                       (const IO*)a.v, a.w, (const IO*)a.dO, a.states, (const float*)w.T, (const float*)w.KbG, (const IO*)w.dh,
+                       (const IO*)w.dUT, (IO*)a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg, w.dKh, w.hdh);
     stage_mark(a.events, 3, a.stream);
     const long tiles = (long)geo.total_chunks * H;
     hipLaunchKernelGGL((k_cw_grad_d<DK, IO>), dim3((unsigned)((tiles + 7) / 8 * 8 * (DK / 32))), dim3(512), 0,

@@ -91,17 +91,18 @@ constexpr int grad_region_bytes(int dk, int es) {
   return (m + 255) / 256 * 256;
 }
 
-// Channel-wise members (per-channel g, b, w; fp32 operands inside, fp32 or
-// bf16 activations).  A NULL gate is neutral: g = 0, b = 0 (no erase), w = 1.
+// Channel-wise members (per-channel g, b, w; fp32 or bf16 activations; the
+// scans' operands in the activation dtype, everything else fp32).  A NULL gate is neutral: g = 0, b = 0 (no erase), w = 1.
 struct CwFwdWs {
   int* chunk_off;
   int* flag_scan;  // [N*H*NVT] written by the generic scan, not read
   float* gC;       // [chunks*H*dk]    G of each chunk's last row, per channel
-  float* W;        // [chunks*H*64*dk] T (Gamma * b * K)
-  float* U;        // [chunks*H*64*dv] T (w * V), accumulator-tile layout
-  float* KhT;      // [chunks*H*dk*64] (e^{G_last - G} * K)^T
-  float* P;        // [chunks*H*64*64] decay-weighted Q K^T, i <= r
-  float* Qg;       // [chunks*H*64*dk] e^G * Q
+  // the scan's operands, in the activation dtype, op_off layout (U: accumulator tiles)
+  void* W;         // [chunks*H*64*dk] T (Gamma * b * K)
+  void* U;         // [chunks*H*64*dv] T (w * V)
+  void* KhT;       // [chunks*H*dk*64] (e^{G_last - G} * K)^T
+  void* P;         // [chunks*H*64*64] decay-weighted Q K^T, i <= r
+  void* Qg;        // [chunks*H*64*dk] e^G * Q
 };
 
 struct CwFwdArgs {
@@ -120,15 +121,17 @@ struct CwBwdWs {
   int* chunk_off;
   int* flag_scan;
   float* gC;   // [chunks*H*dk]
-  float* WT;   // [chunks*H*dk*64]
-  float* QgT;  // [chunks*H*dk*64]
-  float* dOT;  // [chunks*H*dv*64]
-  float* PT;   // [chunks*H*64*64]
+  // the reverse scan's operands and outputs, in the activation dtype, op_off layout
+  void* WT;    // [chunks*H*dk*64]
+  void* QgT;   // [chunks*H*dk*64]
+  void* dOT;   // [chunks*H*dv*64]
+  void* PT;    // [chunks*H*64*64]
+  void* Kh;    // [chunks*H*64*dk]
+  void* dh;    // [chunks*H*dk*dv]
+  void* dUT;   // [chunks*H*dv*64]
+  // fp32, for the gradient kernels
   float* T;    // [chunks*H*64*64]
-  float* Kh;   // [chunks*H*64*dk]
   float* KbG;  // [chunks*H*64*dk] Gamma * b * K
-  float* dh;   // [chunks*H*dk*dv]
-  float* dUT;  // [chunks*H*dv*64]
   float* dP;   // [chunks*H*64*64]
   float* dA;   // [chunks*H*64*64]
   float* X;    // [chunks*H*64*dk]

@@ -134,8 +134,9 @@ def test_throughput_shape_sampled_heads(io):
     check(c, heads=[0, 11])
 
 
-def test_deterministic_bitwise():
-    c = W.make_cw_case("cw_det", 1, 300, 3, 128, 128, gates="gbw", seed=7)
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_deterministic_bitwise(io):
+    c = W.make_cw_case(f"cw_det_{io}", 1, 300, 3, 128, 128, gates="gbw", seed=7, io_dtype=io)
     a, b = run_device(c), run_device(c)
     for n in NAMES:
         if a[n] is not None:

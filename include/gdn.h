@@ -177,10 +177,11 @@ gdn_status gdn_bwd_ex(const gdn_problem* p, const void* q, const void* k, const 
  * fp32 row-major (packed sequences: B = 1 and cu_seqlens as above).  q, k, v,
  * o, dO, dq, dk, dv are in io_dtype (fp32 or bf16).  With GDN_F32 every
  * operand inside the chunked algorithm is fp32 (fp32 matrix cores).  With
- * GDN_BF16 the two scans take bf16 operands, as gdn_fwd / gdn_bwd do (fp32
- * state and accumulation; the state gradients between the reverse scan and
- * the gradient kernels are bf16), and the prep and gradient kernels compute in
- * fp32.  `variant` is not read.
+ * GDN_BF16 the two scans and the value-part gradient products take bf16
+ * operands, as gdn_fwd / gdn_bwd do (fp32 state and accumulation), while the
+ * prep (cumulative decays, the decay-weighted products, the triangular
+ * inverse) and the channel-part gradients compute in fp32.  `variant` is not
+ * read.
  * chunk_states has the layout and meaning of gdn_fwd's.  The chunked kernels
  * form each decay exp(G_r - G_i) split at a reference row: for r and i in
  * different 16-token blocks a row between them, so for a decay (every g <= 0)

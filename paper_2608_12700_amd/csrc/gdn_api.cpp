@@ -187,9 +187,10 @@ void layout_cw_bwd(const Shape& s, char* base, CwBwdWs* w, size_t* total) {
   w->Kh = b.take<char>(ck * s.es);
   w->dh = b.take<char>(tiles * (size_t)s.dk * s.dv * s.es);
   w->dUT = b.take<char>(cv * s.es);
-  // fp32 for the gradient kernels
-  w->T = b.take<float>(cc);
-  w->KbG = b.take<float>(ck);
+  // the value-part gradient kernel's T and Gamma * Kb, also in the activation dtype
+  w->T = b.take<char>(cc * s.es);
+  w->KbG = b.take<char>(ck * s.es);
+  // fp32 between the two gradient kernels
   w->dP = b.take<float>(cc);
   w->dA = b.take<float>(cc);
   w->X = b.take<float>(ck);

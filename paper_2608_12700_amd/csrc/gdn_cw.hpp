@@ -6,9 +6,10 @@
 //
 // with g_t, b_t in R^{d_k} and w_t in R^{d_v}; a NULL gate is neutral (g = 0,
 // b = 0, w = 1).  Activations (q, k, v, dO and their gradients, o) are fp32 or
-// bf16 (IO).  The prep and gradient kernels compute in fp32 (fp32 matrix
-// cores); the two scans take their operands in IO, so with bf16 activations
-// they run on bf16 matrix cores with an fp32 carry, as the scalar-gate path.
+// bf16 (IO).  The prep and the channel-part gradients compute in fp32 (fp32
+// matrix cores); the prep writes the operands of the later kernels in IO, so
+// with bf16 activations the two scans (fp32 carry) and the value-part
+// gradient products run on bf16 matrix cores, as the scalar-gate path.
 //
 // Chunked form (Sec. 4.2), per chunk of 64 tokens with G_r = sum_{s<=r} g_s (a
 // d_k-vector per row), Gamma = e^G, Kb = b * K, Khat_r = e^{G_last - G_r} * k_r:
@@ -88,6 +89,16 @@ struct TileIn {
       *reinterpret_cast<float4*>(dst + r * LD + c) = u[t];
     }
   }
+  // rounded to bf16: one 8-byte store per piece
+  template <int LD>
+  __device__ __forceinline__ void stage16(bf16* dst) const {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      const int idx = thread_x() + t * NT, r = idx / PER_ROW, c = (idx - r * PER_ROW) * 4;
+      const bf16 x[4] = {from_f<bf16>(u[t].x), from_f<bf16>(u[t].y), from_f<bf16>(u[t].z), from_f<bf16>(u[t].w)};
+      *reinterpret_cast<uint2*>(dst + r * LD + c) = pack4<bf16>(x);
+    }
+  }
 };
 
 // Rows [0, len) of a 64 x D tile of T (fp32 or bf16; rows rs elements apart
@@ -132,6 +143,18 @@ struct CwRows {
         *reinterpret_cast<float4*>(d) = float4{f[0], f[1], f[2], f[3]};
         *reinterpret_cast<float4*>(d + 4) = float4{f[4], f[5], f[6], f[7]};
       }
+    }
+  }
+  // the same, kept in 16-bit (T = bf16 only): one 16-byte store per piece
+  template <int LD>
+  __device__ __forceinline__ void stage16(bf16* dst, int len) const {
+    static_assert(sizeof(T) == 2, "bf16 pieces");
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, r, c;
+      where(t, idx, r, c);
+      if (idx >= TOT) continue;
+      *reinterpret_cast<uint4*>(dst + r * LD + c) = keep16(r < len, u[t]);
     }
   }
   // multiply the staged tile by this one's values (same layout, fp32 pieces)
@@ -227,14 +250,25 @@ struct OpIn16 {
       *reinterpret_cast<float4*>(dst + m * LD + k + 4) = float4{f[4], f[5], f[6], f[7]};
     }
   }
+  // kept in bf16: one 16-byte store per piece
+  template <int LD>
+  __device__ __forceinline__ void stage16(bf16* dst) const {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, m, k;
+      where(t, idx, m, k);
+      if (idx >= PIECES) continue;
+      *reinterpret_cast<uint4*>(dst + m * LD + k) = u[t];
+    }
+  }
 };
 
 // One block per (chunk, head).  Forward mode writes the operands of the
 // generic forward scan (P, diag-scaled Q, Khat^T, W, U); backward mode writes
 // those of the reverse scan and the gradient kernels (P^T, (Gamma Q)^T,
-// Khat, W^T, T, Gamma * Kb, dO^T).  Both write G_last per channel.  The
-// scans' operands are written in the activation dtype IO (op_off layout);
-// T and Gamma * Kb, read by the gradient kernel, stay fp32.
+// Khat, W^T, T, Gamma * Kb, dO^T).  Both write G_last per channel.  Every
+// operand is written in the activation dtype IO: the scans' in the op_off
+// layout, T and Gamma * Kb (read by the gradient kernel) row-major.
 constexpr int CW_PREP_THREADS = 1024;  // 16 waves: one block per CU (LDS), so all its latency hiding is in-block
 template <int DK, int DV, bool BWD, typename IO>
 __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, const IO* __restrict__ q,
@@ -244,7 +278,7 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
                                                  float* __restrict__ gC, IO* __restrict__ Pg,
                                                  IO* __restrict__ Qgg, IO* __restrict__ Khg,
                                                  IO* __restrict__ Wg, IO* __restrict__ Ug,
-                                                 float* __restrict__ Tg, float* __restrict__ KbGg,
+                                                 IO* __restrict__ Tg, IO* __restrict__ KbGg,
                                                  IO* __restrict__ dOTg) {
   constexpr int LK = DK + 4, LC = CH + 4, VS = 64, LV = VS + 4;
   static_assert(CH * LC <= CH * LK && CH * LV <= CH * LK, "T and the w * V slices reuse Q's and K's tiles");
@@ -441,12 +475,12 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
       Bk[r * LK + d] *= __expf(Gs[r * LK + d]);
     }
   if (BWD) {
-    float* Tt = Tg + tile * CH * CH;
-    for (int i = thread_x(); i < CH * CH; i += blockDim.x) Tt[i] = Tf[(i / CH) * LC + (i % CH)];
-    float* Kb = KbGg + tile * CH * DK;
+    IO* Tt = Tg + tile * CH * CH;
+    for (int i = thread_x(); i < CH * CH; i += blockDim.x) Tt[i] = from_f<IO>(Tf[(i / CH) * LC + (i % CH)]);
+    IO* Kb = KbGg + tile * CH * DK;
     for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
       const int r = i / DK, d = i - r * DK;
-      Kb[i] = b ? Bk[r * LK + d] : 0.f;
+      Kb[i] = from_f<IO>(b ? Bk[r * LK + d] : 0.f);
     }
   }
   __syncthreads();
@@ -527,20 +561,20 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
   }
 }
 
-// Gradient kernel, value part: one block per (chunk, head), value slices of 32
-// columns.  With h the chunk's entry state, dh the state gradient after it and
+// Gradient kernel, value part (fp32 activations; k_cw_grad_v_bf below is the
+// bf16 one): one block per (chunk, head), value slices of 32 columns.  With h the chunk's entry state, dh the state gradient after it and
 // dU' from the reverse scan:
 //   R = w * V - (Gamma * Kb) h,  U' = T R,  Y = T^T dU'  ->  dv = w * Y, dw = v * Y
 // and, summed over the slices,
 //   dP = dO U'^T (i <= r),  dA = -Y U'^T (i < r: the solve's VJP in its short
 //   form, -T^T (dU' R^T) T^T = -Y U'^T),  X = -Y h^T,  dQg = dO h^T,
 //   dKhat = U' dh^T,  <h, dh> per row d.
-template <int DK, int DV, typename IO>
-__global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __restrict__ v,
-                                                   const float* __restrict__ w, const IO* __restrict__ dO,
+template <int DK, int DV>
+__global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* __restrict__ v,
+                                                   const float* __restrict__ w, const float* __restrict__ dO,
                                                    const float* __restrict__ states, const float* __restrict__ Tg,
-                                                   const float* __restrict__ KbGg, const IO* __restrict__ dhg,
-                                                   const IO* __restrict__ dUTg, IO* __restrict__ dvo,
+                                                   const float* __restrict__ KbGg, const float* __restrict__ dhg,
+                                                   const float* __restrict__ dUTg, float* __restrict__ dvo,
                                                    float* __restrict__ dwo, float* __restrict__ dPg,
                                                    float* __restrict__ dAg, float* __restrict__ Xg,
                                                    float* __restrict__ dQgg, float* __restrict__ dKhg,
@@ -556,31 +590,22 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __r
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
   const long rsv = (long)H * DV, bv = (cp.row0 * H + h) * DV;
-  // the tiles of one value slice, requested in one batch (dh and dU'^T come
-  // from the reverse scan in the activation dtype, op_off layout)
-  constexpr bool B16 = sizeof(IO) == 2;
+  // the tiles of one value slice, requested in one batch
   struct Slice {
-    CwRows<VS, 512, IO> v, dO;
-    CwRows<VS, 512, float> w;
-    TileIn<DK, VS, 512> h;
-    std::conditional_t<B16, OpIn16<DK, VS, DV, 512>, TileIn<DK, VS, 512>> dh;
-    std::conditional_t<B16, OpIn16<VS, CH, CH, 512>, TileIn<VS, CH, 512>> dut;
+    CwRows<VS, 512, float> v, dO, w;
+    TileIn<DK, VS, 512> h, dh;
+    TileIn<VS, CH, 512> dut;
   };
   const float* hp = states + tile * DK * DV;
-  const IO* dhp = dhg + tile * DK * DV;
-  const IO* dUp = dUTg + tile * DV * CH;
+  const float* dhp = dhg + tile * DK * DV;
+  const float* dUp = dUTg + tile * DV * CH;
   auto load_slice = [&](Slice& sl, int c0) {
     sl.v.load(v + bv + c0, rsv, cp.len);
     if (w) sl.w.load(w + bv + c0, rsv, cp.len);
     sl.dO.load(dO + bv + c0, rsv, cp.len);
     sl.h.load(hp + c0, DV);
-    if constexpr (B16) {
-      sl.dh.load(dhp, 0, c0);
-      sl.dut.load(dUp, c0, 0);
-    } else {
-      sl.dh.load(dhp + c0, DV);
-      sl.dut.load(dUp + (long)c0 * CH, CH);
-    }
+    sl.dh.load(dhp + c0, DV);
+    sl.dut.load(dUp + (long)c0 * CH, CH);
   };
   {
     TileIn<CH, CH, 512> tin;
@@ -635,7 +660,7 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __r
         Ys[r * LV + vv] = x;
         if (r < cp.len) {
           const long o = bv + (long)r * rsv + c0 + vv;
-          dvo[o] = from_f<IO>((w ? Ws[r * LV + vv] : 1.f) * x);
+          dvo[o] = (w ? Ws[r * LV + vv] : 1.f) * x;
           if (w) dwo[o] = Vs[r * LV + vv] * x;
         }
       });
@@ -656,6 +681,137 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const IO* __r
     __syncthreads();
     cur = nxt;
   }
+  float* dPt = dPg + tile * CH * CH;
+  float* dAt = dAg + tile * CH * CH;
+  dP.each([&](int r, int i, float& x) { dPt[r * CH + i] = i <= r ? x : 0.f; });
+  dA.each([&](int r, int i, float& x) { dAt[r * CH + i] = i < r ? -x : 0.f; });
+  float* Xt = Xg + tile * CH * DK;
+  float* Qt = dQgg + tile * CH * DK;
+  float* Kt = dKhg + tile * CH * DK;
+  X.each([&](int r, int d, float& x) { Xt[r * DK + d] = -x; });
+  dQg.each([&](int r, int d, float& x) { Qt[r * DK + d] = x; });
+  dKh.each([&](int r, int d, float& x) { Kt[r * DK + d] = x; });
+  if (thread_x() < DK) hdhg[tile * DK + thread_x()] = hdh;
+}
+
+// Gradient kernel, value part, bf16 activations: the products of k_cw_grad_v
+// on bf16 matrix cores (fp32 accumulation).  Every operand is staged to LDS in
+// bf16 -- T and Gamma * Kb as the prep wrote them, dh and dU'^T as the reverse
+// scan wrote them, v and dO as given, h (the fp32 chunk state) rounded -- and
+// R, U' and Y are rounded where they feed a product; w stays fp32, and dv, dw
+// are formed from the fp32 Y.  T^T and h (for R) are read down their columns
+// with the transposing LDS load.
+template <int DK, int DV>
+__global__ __launch_bounds__(512) void k_cw_grad_v_bf(Geo geo, int H, const bf16* __restrict__ v,
+                                                      const float* __restrict__ w, const bf16* __restrict__ dO,
+                                                      const float* __restrict__ states, const bf16* __restrict__ Tg,
+                                                      const bf16* __restrict__ KbGg, const bf16* __restrict__ dhg,
+                                                      const bf16* __restrict__ dUTg, bf16* __restrict__ dvo,
+                                                      float* __restrict__ dwo, float* __restrict__ dPg,
+                                                      float* __restrict__ dAg, float* __restrict__ Xg,
+                                                      float* __restrict__ dQgg, float* __restrict__ dKhg,
+                                                      float* __restrict__ hdhg) {
+  constexpr int VS = 32, PD = pad_of<bf16>(), LK = DK + PD, LC = CH + PD, LV = VS + PD, LW = VS + 4;
+  __shared__ __align__(16) bf16 Ts[CH * LC];                                 // T [i][r]
+  __shared__ __align__(16) bf16 KbG[CH * LK];                                // Gamma * Kb [r][d]
+  __shared__ __align__(16) bf16 Vs[CH * LV], dOs[CH * LV], Ups[CH * LV], Ys[CH * LV];  // [r][v]
+  __shared__ __align__(16) float Ws[CH * LW];                                // w [r][v]
+  __shared__ __align__(16) bf16 dUT[VS * LC], RT[VS * LC];                   // dU'^T, R^T [v][r]
+  __shared__ __align__(16) bf16 hs[DK * LV], dhs[DK * LV];                   // h, dh [d][v]
+
+  const int ci = blockIdx.x, h = blockIdx.y;
+  const ChunkPos cp = chunk_pos(geo, ci);
+  const long tile = (long)ci * H + h;
+  const long rsv = (long)H * DV, bv = (cp.row0 * H + h) * DV;
+  struct Slice {
+    CwRows<VS, 512, bf16> v, dO;
+    CwRows<VS, 512, float> w;
+    TileIn<DK, VS, 512> h;
+    OpIn16<DK, VS, DV, 512> dh;
+    OpIn16<VS, CH, CH, 512> dut;
+  };
+  const float* hp = states + tile * DK * DV;
+  const bf16* dhp = dhg + tile * DK * DV;
+  const bf16* dUp = dUTg + tile * DV * CH;
+  auto load_slice = [&](Slice& sl, int c0) {
+    sl.v.load(v + bv + c0, rsv, cp.len);
+    if (w) sl.w.load(w + bv + c0, rsv, cp.len);
+    sl.dO.load(dO + bv + c0, rsv, cp.len);
+    sl.h.load(hp + c0, DV);
+    sl.dh.load(dhp, 0, c0);
+    sl.dut.load(dUp, c0, 0);
+  };
+  {
+    CwRows<CH, 512, bf16> tin;
+    CwRows<DK, 512, bf16> kin;
+    tin.load(Tg + tile * CH * CH, CH, CH);
+    kin.load(KbGg + tile * CH * DK, DK, CH);
+    tin.template stage16<LC>(Ts, CH);
+    kin.template stage16<LK>(KbG, CH);
+  }
+  Slice cur, nxt;
+  load_slice(cur, 0);
+  typedef Tiles<CH, VS, 4, 2> TV;
+  Tiles<CH, CH, 4, 2> dP, dA;
+  Tiles<CH, DK, 4, 2> X, dQg, dKh;
+  dP.zero(); dA.zero(); X.zero(); dQg.zero(); dKh.zero();
+  float hdh = 0.f;  // thread d < DK: sum over v of h[d][v] dh[d][v]
+#pragma unroll
+  for (int c0 = 0; c0 < DV; c0 += VS) {
+    cur.v.template stage16<LV>(Vs, cp.len);
+    if (w) cur.w.template stage<LW>(Ws, cp.len);
+    cur.dO.template stage16<LV>(dOs, cp.len);
+    cur.h.template stage16<LV>(hs);
+    cur.dh.template stage16<LV>(dhs);
+    cur.dut.template stage16<LC>(dUT);
+    // the next slice's tiles load under this slice's products (the last slice
+    // re-reads itself, so the count of loads in flight never changes)
+    load_slice(nxt, c0 + VS < DV ? c0 + VS : c0);
+    __syncthreads();
+    if (thread_x() < DK) {
+      const int d = thread_x();
+#pragma unroll 8
+      for (int c = 0; c < VS; ++c) hdh += to_f(hs[d * LV + c]) * to_f(dhs[d * LV + c]);
+    }
+    {
+      TV rr;
+      rr.zero();
+      rr.template mma<bf16, DK>(KRow<bf16, LK>{KbG}, KColTr<LV>{hs, nullptr});
+      rr.each([&](int r, int vv, float& x) {
+        const float wv = w ? Ws[r * LW + vv] : 1.f;
+        RT[vv * LC + r] = from_f<bf16>(wv * to_f(Vs[r * LV + vv]) - x);
+      });
+    }
+    {
+      TV y;
+      y.zero();
+      y.template mma<bf16, CH>(KColTr<LC>{Ts, nullptr}, KRow<bf16, LC>{dUT});
+      y.each([&](int r, int vv, float& x) {
+        Ys[r * LV + vv] = from_f<bf16>(x);
+        if (r < cp.len) {
+          const long o = bv + (long)r * rsv + c0 + vv;
+          dvo[o] = from_f<bf16>((w ? Ws[r * LW + vv] : 1.f) * x);
+          if (w) dwo[o] = to_f(Vs[r * LV + vv]) * x;
+        }
+      });
+    }
+    __syncthreads();
+    {
+      TV up;
+      up.zero();
+      up.template mma<bf16, CH>(KRow<bf16, LC>{Ts}, KRow<bf16, LC>{RT});
+      up.each([&](int r, int vv, float& x) { Ups[r * LV + vv] = from_f<bf16>(x); });
+    }
+    __syncthreads();
+    dP.template mma<bf16, VS>(KRow<bf16, LV>{dOs}, KRow<bf16, LV>{Ups});
+    dA.template mma<bf16, VS>(KRow<bf16, LV>{Ys}, KRow<bf16, LV>{Ups});
+    X.template mma<bf16, VS>(KRow<bf16, LV>{Ys}, KRow<bf16, LV>{hs});
+    dQg.template mma<bf16, VS>(KRow<bf16, LV>{dOs}, KRow<bf16, LV>{hs});
+    dKh.template mma<bf16, VS>(KRow<bf16, LV>{Ups}, KRow<bf16, LV>{dhs});
+    __syncthreads();
+    cur = nxt;
+  }
+  // the same fp32 outputs as k_cw_grad_v
   float* dPt = dPg + tile * CH * CH;
   float* dAt = dAg + tile * CH * CH;
   dP.each([&](int r, int i, float& x) { dPt[r * CH + i] = i <= r ? x : 0.f; });
@@ -864,7 +1020,7 @@ static hipError_t launch_cw_fwd_t(const CwFwdArgs& a) {
     hipLaunchKernelGGL((k_cw_prep<DK, DV, false, IO>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream,
                        geo, H, (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, (const IO*)nullptr,
                        w.gC, (IO*)w.P, (IO*)w.Qg, (IO*)w.KhT, (IO*)w.W, (IO*)w.U,
-                       (float*)nullptr, (float*)nullptr, (IO*)nullptr);
+                       (IO*)nullptr, (IO*)nullptr, (IO*)nullptr);
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0)
@@ -892,8 +1048,8 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
   if (geo.total_chunks > 0)
     hipLaunchKernelGGL((k_cw_prep<DK, DV, true, IO>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream,
                        geo, H, (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, (const IO*)a.dO,
-                       w.gC, (IO*)w.PT, (IO*)w.QgT, (IO*)w.Kh, (IO*)w.WT, (IO*)nullptr, w.T,
-                       w.KbG, (IO*)w.dOT);
+                       w.gC, (IO*)w.PT, (IO*)w.QgT, (IO*)w.Kh, (IO*)w.WT, (IO*)nullptr, (IO*)w.T,
+                       (IO*)w.KbG, (IO*)w.dOT);
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0)
@@ -902,9 +1058,16 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
                        (const IO*)w.dOT, (const IO*)w.PT, (IO*)w.dh, (IO*)w.dUT, a.dS0, w.flag_scan);
   stage_mark(a.events, 2, a.stream);
   if (geo.total_chunks > 0) {
-    hipLaunchKernelGGL((k_cw_grad_v<DK, DV, IO>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
-                       (const IO*)a.v, a.w, (const IO*)a.dO, a.states, (const float*)w.T, (const float*)w.KbG, (const IO*)w.dh,
-                       (const IO*)w.dUT, (IO*)a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg, w.dKh, w.hdh);
+    if constexpr (sizeof(IO) == 2)
+      hipLaunchKernelGGL((k_cw_grad_v_bf<DK, DV>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
+                         (const bf16*)a.v, a.w, (const bf16*)a.dO, a.states, (const bf16*)w.T, (const bf16*)w.KbG,
+                         (const bf16*)w.dh, (const bf16*)w.dUT, (bf16*)a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg,
+                         w.dKh, w.hdh);
+    else
+      hipLaunchKernelGGL((k_cw_grad_v<DK, DV>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
+                         (const float*)a.v, a.w, (const float*)a.dO, a.states, (const float*)w.T,
+                         (const float*)w.KbG, (const float*)w.dh, (const float*)w.dUT, (float*)a.dv_, a.dw, w.dP,
+                         w.dA, w.X, w.dQg, w.dKh, w.hdh);
     stage_mark(a.events, 3, a.stream);
     const long tiles = (long)geo.total_chunks * H;
     hipLaunchKernelGGL((k_cw_grad_d<DK, IO>), dim3((unsigned)((tiles + 7) / 8 * 8 * (DK / 32))), dim3(512), 0,

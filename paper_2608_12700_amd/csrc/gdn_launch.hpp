@@ -129,9 +129,10 @@ struct CwBwdWs {
   void* Kh;    // [chunks*H*64*dk]
   void* dh;    // [chunks*H*dk*dv]
   void* dUT;   // [chunks*H*dv*64]
-  // fp32, for the gradient kernels
-  float* T;    // [chunks*H*64*64]
-  float* KbG;  // [chunks*H*64*dk] Gamma * b * K
+  // activation dtype, row-major, for the value-part gradient kernel
+  void* T;     // [chunks*H*64*64]
+  void* KbG;   // [chunks*H*64*dk] Gamma * b * K
+  // fp32, between the two gradient kernels
   float* dP;   // [chunks*H*64*64]
   float* dA;   // [chunks*H*64*64]
   float* X;    // [chunks*H*64*dk]

@@ -157,6 +157,33 @@ struct CwRows {
       *reinterpret_cast<uint4*>(dst + r * LD + c) = keep16(r < len, u[t]);
     }
   }
+  // transposed: element (r, c) to dst[c * LD + r] (rows past len zero)
+  template <int LD>
+  __device__ __forceinline__ void stageT(float* dst, int len) const {
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, r, c;
+      where(t, idx, r, c);
+      if (idx >= TOT) continue;
+      const uint4 x = keep16(r < len, u[t]);
+#pragma unroll
+      for (int j = 0; j < V; ++j) dst[(c + j) * LD + r] = to_f(elem16<T>(x, j));
+    }
+  }
+  // multiply a tile staged by stageT by this one's values (fp32 pieces)
+  template <int LD>
+  __device__ __forceinline__ void scaleT(float* dst, int len) const {
+    static_assert(sizeof(T) == 4, "fp32 factors");
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, r, c;
+      where(t, idx, r, c);
+      if (idx >= TOT) continue;
+      const uint4 x = keep16(r < len, u[t]);
+#pragma unroll
+      for (int j = 0; j < V; ++j) dst[(c + j) * LD + r] *= elem16<float>(x, j);
+    }
+  }
   // multiply the staged tile by this one's values (same layout, fp32 pieces)
   template <int LD>
   __device__ __forceinline__ void scale(float* dst, int len) const {
@@ -173,6 +200,19 @@ struct CwRows {
       *d = x;
     }
   }
+};
+
+// Element (o, k) of a fp32 LDS array of rows of 64, its 16-byte groups
+// XOR-swizzled by o & 15: a wave's float4 reads of 16 rows at one k hit 16
+// different bank groups, with no padding.
+struct KRowSw64 {
+  const float* p;
+  static constexpr bool kVec = true;
+  __device__ __forceinline__ static int off(int o, int k) {
+    return o * 64 + ((((k >> 2) ^ (o & 15)) << 2) | (k & 3));
+  }
+  __device__ __forceinline__ float get(int o, int k) const { return p[off(o, k)]; }
+  __device__ __forceinline__ const float* ptr(int o, int k) const { return p + off(o, k); }
 };
 
 // Scan operands (P, diag-scaled Q, Khat, W, dO^T) in the activation dtype,
@@ -280,12 +320,12 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
                                                  IO* __restrict__ Wg, IO* __restrict__ Ug,
                                                  IO* __restrict__ Tg, IO* __restrict__ KbGg,
                                                  IO* __restrict__ dOTg) {
-  constexpr int LK = DK + 4, LC = CH + 4, VS = 64, LV = VS + 4;
-  static_assert(CH * LC <= CH * LK && CH * LV <= CH * LK, "T and the w * V slices reuse Q's and K's tiles");
+  constexpr int LK = DK + 4, LC = CH + 4, VS = 64;
+  static_assert(CH * LC <= CH * LK && VS * LC <= CH * LK, "T and the (w * V)^T slices reuse Q's and K's tiles");
   __shared__ __align__(16) float Qs[CH * LK];  // Q, then T (stride LC)
-  __shared__ __align__(16) float Ks[CH * LK];  // K, then slices of w * V (stride LV)
-  __shared__ __align__(16) float Gs[CH * LK];  // G
-  __shared__ __align__(16) float Bk[CH * LK];  // b * K, then Gamma * b * K
+  __shared__ __align__(16) float Ks[CH * LK];  // K, then slices of (w * V)^T [v][i] (stride LC)
+  __shared__ __align__(16) float Gs[CH * LK];  // G, then (Gamma * Kb)^T (swizzled rows of 64)
+  __shared__ __align__(16) float Bk[CH * LK];  // b * K
   __shared__ __align__(16) float As[CH * LC];  // A
   __shared__ __align__(16) float Pd[4 * 16 * 16];  // P inside the four diagonal 16 x 16 blocks (wide blocks)
   __shared__ int wide;                              // blocks summed exactly (bit R: block R)
@@ -468,21 +508,31 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
     }
     __syncthreads();
   }
-  // Gamma * Kb (A has been formed from b * K above)
-  if (b)
-    for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
-      const int r = i / DK, d = i - r * DK;
-      Bk[r * LK + d] *= __expf(Gs[r * LK + d]);
-    }
+  // Gamma * Kb (A has been formed from b * K above), held in registers and
+  // then written transposed, [d][i] swizzled, over G's tile (G is dead)
+  constexpr int NG = CH * DK / NT;
+  static_assert(CH * DK % NT == 0 && DK * 64 <= CH * LK, "whole pieces; Gamma * Kb^T fits G's tile");
+  float gk[NG];
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    const int i = thread_x() + j * NT, r = i / DK, d = i - r * DK;
+    gk[j] = b ? Bk[r * LK + d] * __expf(Gs[r * LK + d]) : 0.f;
+  }
   if (BWD) {
     IO* Tt = Tg + tile * CH * CH;
     for (int i = thread_x(); i < CH * CH; i += blockDim.x) Tt[i] = from_f<IO>(Tf[(i / CH) * LC + (i % CH)]);
     IO* Kb = KbGg + tile * CH * DK;
-    for (int i = thread_x(); i < CH * DK; i += blockDim.x) {
-      const int r = i / DK, d = i - r * DK;
-      Kb[i] = from_f<IO>(b ? Bk[r * LK + d] : 0.f);
-    }
+#pragma unroll
+    for (int j = 0; j < NG; ++j) Kb[thread_x() + j * NT] = from_f<IO>(gk[j]);
   }
+  __syncthreads();  // every read of G is done
+  float* GkT = Gs;
+  if (b)
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+      const int i = thread_x() + j * NT, r = i / DK, d = i - r * DK;
+      GkT[KRowSw64::off(d, r)] = gk[j];
+    }
   __syncthreads();
   // W = T (Gamma * Kb)
   {
@@ -490,7 +540,7 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
     if (b) {
       Tiles<CH, DK, 4, WN> wt;
       wt.zero();
-      wt.template mma<float, CH>(KRow<float, LC>{Tf}, KCol<float, LK>{Bk});
+      wt.template mma<float, CH>(KRow<float, LC>{Tf}, KRowSw64{GkT});
       const int l = lane_id();
 #pragma unroll
       for (int a = 0; a < wt.TM; ++a)
@@ -539,15 +589,15 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
     for (int t = 0; t < NSL; ++t) {
       const int c0 = t * VS;
       __syncthreads();  // K (first pass) or the previous slice is no longer read
-      vin[t].template stage<LV>(Vw, cp.len);
+      vin[t].template stageT<LC>(Vw, cp.len);
       if (w) {
         __syncthreads();
-        win[t].template scale<LV>(Vw, cp.len);
+        win[t].template scaleT<LC>(Vw, cp.len);
       }
       __syncthreads();
       Tiles<CH, VS, 4, WN> uu;
       uu.zero();
-      uu.template mma<float, CH>(KRow<float, LC>{Tf}, KCol<float, LV>{Vw});
+      uu.template mma<float, CH>(KRow<float, LC>{Tf}, KRow<float, LC>{Vw});
       const int l = lane_id();
 #pragma unroll
       for (int bb = 0; bb < uu.TN; ++bb) {

@@ -945,8 +945,13 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const IO* __r
   const int l = lane_id(), dl = TD::n0(0) + (l & 15);
   const float rf = R > 0 ? Gs[(16 * R - 1) * LS + dl] : 0.f;  // reference before block R
   const float lst = Gs[(16 * R + 15) * LS + dl];               // reference at its last row
-  // this lane's X, dQg, dKhat (issued ahead of the products)
-  float xin[4], qgin[4], khin[4];
+  // this lane's X, dQg, dKhat and the <h, dh> of the channels whose dg this
+  // wave scans at the end (issued ahead of the products)
+  constexpr int NWG = 512 / WAVE;
+  static_assert(DS % NWG == 0, "whole dg channels per wave");
+  float xin[4], qgin[4], khin[4], hdv[DS / NWG];
+#pragma unroll
+  for (int it = 0; it < DS / NWG; ++it) hdv[it] = g ? hdhg[tile * DK + d0 + wave_id() + NWG * it] : 0.f;
   {
     const long base = tile * CH * DK + d0;
 #pragma unroll
@@ -1044,13 +1049,23 @@ __global__ __launch_bounds__(512) void k_cw_grad_d(Geo geo, int H, const IO* __r
       }
     }
     __syncthreads();
-    const int r = lane_id(), nw = (int)blockDim.x / WAVE;
-    for (int dl = wave_id(); dl < DS; dl += nw) {
+    const int r = lane_id();
+#pragma unroll
+    for (int it = 0; it < DS / NWG; ++it) {
+      const int dl = wave_id() + NWG * it;
       const float tot = wave_sum(Zs[r * LS + dl]);
       float x = dGs[r * LS + dl];
-      if (r == CH - 1) x += __expf(Gs[(CH - 1) * LS + dl]) * hdhg[tile * DK + d0 + dl] + tot;
-      const float dgv = wave_reverse(wave_incl_scan(wave_reverse(x)));
-      if (r < cp.len) dg[bk + (long)r * rsk + dl] = dgv;
+      if (r == CH - 1) x += __expf(Gs[(CH - 1) * LS + dl]) * hdv[it] + tot;
+      dGs[r * LS + dl] = wave_reverse(wave_incl_scan(wave_reverse(x)));  // in place: this lane's own entry
+    }
+    __syncthreads();
+    // dg leaves as whole 128-byte row segments (a wave's column would be 64
+    // scattered 4-byte stores)
+    static_assert(CH * DS / 4 <= 512, "one piece per thread");
+    {
+      const int i = thread_x(), rr = i / (DS / 4), c = (i - rr * (DS / 4)) * 4;
+      if (i < CH * DS / 4 && rr < cp.len)
+        *reinterpret_cast<float4*>(dg + bk + (long)rr * rsk + c) = *reinterpret_cast<const float4*>(dGs + rr * LS + c);
     }
   }
 }

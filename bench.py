@@ -338,7 +338,8 @@ def bench_cw(a):
         "metric": f"GDN channel-wise (per-channel g, b, w) fwd+bwd tokens/s at B4 T4096 H16 d128 {a.cw_io}",
         "value": round(B * T / (ms_step / 1e3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32 (activations " + a.cw_io + ")",
+        "vs_baseline": None, "dtype": ("bf16+f32 (bf16 activations; scans and value-part gradients on bf16 matrix cores, "
+                                             "prep and channel gradients in f32)" if bf else "f32"),
         "data": "synthetic (seeded: q,k L2-normalised N(0,1); v,dO N(0,1); g=-softplus(N) per channel; "
                 "b=sigmoid(N) per channel; w=1.5*sigmoid(N) per channel; S0 N(0,0.1^2); dS_T N(0,1))",
         "config": {"workload": f"channel-wise gated delta rule fwd+bwd (full GDN gates), {a.cw_io} activations, "

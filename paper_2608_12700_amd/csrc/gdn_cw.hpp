@@ -657,16 +657,17 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
     sl.dh.load(dhp + c0, DV);
     sl.dut.load(dUp + (long)c0 * CH, CH);
   };
+  Slice cur, nxt;
   {
+    // T, Gamma * Kb and the first value slice in flight together
     TileIn<CH, CH, 512> tin;
     TileIn<CH, DK, 512> kin;
     tin.load(Tg + tile * CH * CH, CH);
     kin.load(KbGg + tile * CH * DK, DK);
+    load_slice(cur, 0);
     tin.template stage<LC>(Ts);
     kin.template stage<LK>(KbG);
   }
-  Slice cur, nxt;
-  load_slice(cur, 0);
   __syncthreads();
   // T^T fragments of this wave's rows, for Y = T^T dU' in every slice
   typedef Tiles<CH, VS, 4, 2> TV;
@@ -791,16 +792,17 @@ __global__ __launch_bounds__(512) void k_cw_grad_v_bf(Geo geo, int H, const bf16
     sl.dh.load(dhp, 0, c0);
     sl.dut.load(dUp, c0, 0);
   };
+  Slice cur, nxt;
   {
+    // T, Gamma * Kb and the first value slice in flight together
     CwRows<CH, 512, bf16> tin;
     CwRows<DK, 512, bf16> kin;
     tin.load(Tg + tile * CH * CH, CH, CH);
     kin.load(KbGg + tile * CH * DK, DK, CH);
+    load_slice(cur, 0);
     tin.template stage16<LC>(Ts, CH);
     kin.template stage16<LK>(KbG, CH);
   }
-  Slice cur, nxt;
-  load_slice(cur, 0);
   typedef Tiles<CH, VS, 4, 2> TV;
   Tiles<CH, CH, 4, 2> dP, dA;
   Tiles<CH, DK, 4, 2> X, dQg, dKh;

@@ -205,13 +205,50 @@ def _stream_handle(device) -> int:
     return torch.cuda.current_stream(device).cuda_stream
 
 
-def _check(t: torch.Tensor, name: str, dtype, device):
+def _check(t: torch.Tensor, name: str, dtype, device, shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
     if t.device != device:
         raise ValueError(f"{name} must be on {device}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+
+
+def _io_dtype(q: torch.Tensor):
+    """The activation dtype code of q: bf16 or fp32 only."""
+    if not isinstance(q, torch.Tensor):
+        raise TypeError(f"q must be a torch.Tensor, got {type(q).__name__}")
+    if q.dtype == torch.bfloat16:
+        return GDN_BF16
+    if q.dtype == torch.float32:
+        return GDN_F32
+    raise TypeError(f"activations must be torch.bfloat16 or torch.float32, got {q.dtype}")
+
+
+def _dims(q, v):
+    """(B, T, H, dk, dv) from q [B,T,H,dk] and v [B,T,H,dv]."""
+    if q.dim() != 4:
+        raise ValueError(f"q must be [B, T, H, d_k], got shape {tuple(q.shape)}")
+    if not isinstance(v, torch.Tensor) or v.dim() != 4:
+        raise ValueError(f"v must be [B, T, H, d_v], got shape {tuple(getattr(v, 'shape', ()))}")
+    B, T, H, dk = q.shape
+    return B, T, H, dk, v.shape[-1]
+
+
+def _num_chunks(B, T, packed):
+    if packed is None:
+        return B * (-(-T // CHUNK))
+    cu = [int(x) for x in packed.host]
+    return sum(-(-max(cu[n + 1] - cu[n], 0) // CHUNK) for n in range(len(cu) - 1))
+
+
+def _on_gpu(q):
+    if q.device.type != "cuda":
+        raise ValueError(f"tensors must be on a GPU device, got {q.device}: the library reads device memory")
 
 
 class Packed:
@@ -232,9 +269,8 @@ class Packed:
 
 
 def _problem_for(q, v, variant, packed: Optional[Packed]):
-    B, T, H, dk = q.shape
-    dv = v.shape[-1]
-    io = GDN_BF16 if q.dtype == torch.bfloat16 else GDN_F32
+    B, T, H, dk, dv = _dims(q, v)
+    io = _io_dtype(q)
     if packed is None:
         return make_problem(B, T, H, dk, dv, io_dtype=io, variant=variant)
     return make_problem(B, T, H, dk, dv, io_dtype=io, variant=variant, cu_host=packed.host,
@@ -247,14 +283,14 @@ def fwd(q, k, v, g, beta, S0=None, *, variant="gated_delta", cu_seqlens=None, wo
     packed = None if cu_seqlens is None else (cu_seqlens if isinstance(cu_seqlens, Packed)
                                               else Packed(cu_seqlens, dev))
     p = _problem_for(q, v, variant, packed)
-    for name, t in (("q", q), ("k", k), ("v", v)):
-        _check(t, name, q.dtype, dev)
-    for name, t in (("g", g), ("beta", beta), ("S0", S0)):
-        if t is not None:
-            _check(t, name, torch.float32, dev)
-    B, T, H, dk = q.shape
-    dv = v.shape[-1]
+    B, T, H, dk, dv = _dims(q, v)
     N = p.num_seqs
+    for name, t, shp in (("q", q, (B, T, H, dk)), ("k", k, (B, T, H, dk)), ("v", v, (B, T, H, dv))):
+        _check(t, name, q.dtype, dev, shp)
+    for name, t, shp in (("g", g, (B, T, H)), ("beta", beta, (B, T, H)), ("S0", S0, (N, H, dk, dv))):
+        if t is not None:
+            _check(t, name, torch.float32, dev, shp)
+    _on_gpu(q)
     nch = gdn_num_chunks(p)
     if nch < 0:
         raise GdnError(nch, "gdn_num_chunks")
@@ -277,14 +313,17 @@ def bwd(q, k, v, g, beta, chunk_states, dO, dS_T=None, *, variant="gated_delta",
     packed = None if cu_seqlens is None else (cu_seqlens if isinstance(cu_seqlens, Packed)
                                               else Packed(cu_seqlens, dev))
     p = _problem_for(q, v, variant, packed)
-    for name, t in (("q", q), ("k", k), ("v", v), ("dO", dO)):
-        _check(t, name, q.dtype, dev)
-    for name, t in (("g", g), ("beta", beta), ("chunk_states", chunk_states), ("dS_T", dS_T)):
-        if t is not None:
-            _check(t, name, torch.float32, dev)
-    B, T, H, dk = q.shape
-    dv = v.shape[-1]
+    B, T, H, dk, dv = _dims(q, v)
     N = p.num_seqs
+    nch = _num_chunks(B, T, packed)
+    for name, t, shp in (("q", q, (B, T, H, dk)), ("k", k, (B, T, H, dk)), ("v", v, (B, T, H, dv)),
+                         ("dO", dO, (B, T, H, dv))):
+        _check(t, name, q.dtype, dev, shp)
+    _check(chunk_states, "chunk_states", torch.float32, dev, (nch, H, dk, dv))
+    for name, t, shp in (("g", g, (B, T, H)), ("beta", beta, (B, T, H)), ("dS_T", dS_T, (N, H, dk, dv))):
+        if t is not None:
+            _check(t, name, torch.float32, dev, shp)
+    _on_gpu(q)
     dq = torch.empty_like(q)
     dk_ = torch.empty_like(k)
     dvv = torch.empty_like(v)
@@ -313,13 +352,15 @@ def cw_fwd(q, k, v, g=None, b=None, w=None, S0=None, *, cu_seqlens=None, workspa
     dev = q.device
     packed = _packed_of(cu_seqlens, dev)
     p = _problem_for(q, v, "gated_delta", packed)
-    for name, t in (("q", q), ("k", k), ("v", v)):
-        _check(t, name, q.dtype, dev)
-    for name, t in (("g", g), ("b", b), ("w", w), ("S0", S0)):
+    B, T, H, dk, dv = _dims(q, v)
+    N = p.num_seqs
+    for name, t, shp in (("q", q, (B, T, H, dk)), ("k", k, (B, T, H, dk)), ("v", v, (B, T, H, dv))):
+        _check(t, name, q.dtype, dev, shp)
+    for name, t, shp in (("g", g, (B, T, H, dk)), ("b", b, (B, T, H, dk)), ("w", w, (B, T, H, dv)),
+                         ("S0", S0, (N, H, dk, dv))):
         if t is not None:
-            _check(t, name, torch.float32, dev)
-    B, T, H, dk = q.shape
-    dv = v.shape[-1]
+            _check(t, name, torch.float32, dev, shp)
+    _on_gpu(q)
     nch = gdn_num_chunks(p)
     if nch < 0:
         raise GdnError(nch, "gdn_num_chunks")
@@ -341,13 +382,18 @@ def cw_bwd(q, k, v, g, b, w, chunk_states, dO, dS_T=None, *, cu_seqlens=None, wo
     dev = q.device
     packed = _packed_of(cu_seqlens, dev)
     p = _problem_for(q, v, "gated_delta", packed)
-    for name, t in (("q", q), ("k", k), ("v", v), ("dO", dO)):
-        _check(t, name, q.dtype, dev)
-    for name, t in (("g", g), ("b", b), ("w", w), ("chunk_states", chunk_states), ("dS_T", dS_T)):
+    B, T, H, dk, dv = _dims(q, v)
+    N = p.num_seqs
+    nch = _num_chunks(B, T, packed)
+    for name, t, shp in (("q", q, (B, T, H, dk)), ("k", k, (B, T, H, dk)), ("v", v, (B, T, H, dv)),
+                         ("dO", dO, (B, T, H, dv))):
+        _check(t, name, q.dtype, dev, shp)
+    _check(chunk_states, "chunk_states", torch.float32, dev, (nch, H, dk, dv))
+    for name, t, shp in (("g", g, (B, T, H, dk)), ("b", b, (B, T, H, dk)), ("w", w, (B, T, H, dv)),
+                         ("dS_T", dS_T, (N, H, dk, dv))):
         if t is not None:
-            _check(t, name, torch.float32, dev)
-    B, T, H, dk = q.shape
-    dv = v.shape[-1]
+            _check(t, name, torch.float32, dev, shp)
+    _on_gpu(q)
     like = lambda t: None if t is None else torch.empty_like(t)
     dq, dk_, dvv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     dg, db, dw = like(g), like(b), like(w)

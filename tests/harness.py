@@ -88,7 +88,11 @@ def compare(dev: dict, ref: dict, heads=None, names=OUT_NAMES):
         m = np.isfinite(x) & np.isfinite(y)
         ny = np.linalg.norm(y[m])
         err = np.linalg.norm(x[m] - y[m])
-        rel = float(err / ny) if ny > 0 else float(err)
+        if ny > 0:
+            rel = float(err / ny)
+        else:
+            # an all-zero reference must be met exactly: any nonzero entry fails
+            rel = 0.0 if not np.any(x[m]) else float("inf")
         res[nm] = (rel, cls_ok, int(m.sum()))
     return res
 

@@ -40,6 +40,9 @@ def fake(i):
     return ctypes.c_void_p(FAKE + (i << 32))
 
 
+NO_WS = object()  # pass a NULL workspace pointer
+
+
 def call_fwd(p, ptrs=None, ws_bytes=None, ws=None, **over):
     args = dict(q=fake(1), k=fake(2), v=fake(3), g=fake(4), beta=fake(5), S0=None, o=fake(6),
                 S_T=fake(7), states=fake(8))
@@ -50,7 +53,8 @@ def call_fwd(p, ptrs=None, ws_bytes=None, ws=None, **over):
     args.update(over)
     wsb = gdn.gdn_fwd_workspace_size(p) if ws_bytes is None else ws_bytes
     return gdn.gdn_fwd(p, args["q"], args["k"], args["v"], args["g"], args["beta"], args["S0"],
-                       args["o"], args["S_T"], args["states"], fake(9) if ws is None else ws, wsb, None)
+                       args["o"], args["S_T"], args["states"],
+                       None if ws is NO_WS else (fake(9) if ws is None else ws), wsb, None)
 
 
 def call_bwd(p, **over):
@@ -118,7 +122,8 @@ def test_workspace_checks():
     assert need > 0 and need % 256 == 0
     assert call_fwd(p, ws_bytes=need - 1) == -5
     assert call_fwd(p, ws=ctypes.c_void_p(FAKE + 128)) == -5  # misaligned
-    assert call_fwd(p, ws=None, ws_bytes=need) == -5 or True
+    assert call_fwd(p, ws=NO_WS, ws_bytes=need) == -5         # NULL workspace
+    assert call_fwd(p, ws=NO_WS, ws_bytes=0) == -5
 
 
 def test_alias_rejected():

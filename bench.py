@@ -12,11 +12,15 @@ reported step time is the mean over K steps that each start with cold caches
 same K steps run back to back are reported beside it.
 
 The JSON line carries, besides tokens/s:
-  roofline      the dominant kernel (largest average duration among the
-                forward and backward stages), its algorithmic bytes per launch
-                divided by its average launch duration, measured live with HIP
-                events recorded on the launch stream around each stage of the
-                timed steps, against MI355X's 8 TB/s HBM peak;
+  roofline      the training backward (gdn_bwd), whose binding roofline is
+                HBM: its compulsory bytes (every tensor of the call read or
+                written once at its dtype, 2,832 B per token-head here; workspace
+                traffic is not counted) divided by its duration, measured live
+                with HIP events recorded on the launch stream around each stage
+                of the timed steps, against MI355X's 8 TB/s HBM peak.  The
+                dominant kernel (the chunk-gradient kernel) is reported inside
+                it on the same basis, and as kernel_io_frac on its own inputs
+                and outputs including workspace operands;
   cpu_baseline  the float64 oracle (fwd + bwd) on the host cores, on a bounded
                 sample of the same workload's (b, h) streams.
 """
@@ -246,6 +250,40 @@ def cw_kernel_model(B, T, H, dk, dv, N=None, es=4):
     return out
 
 
+def _cw_oracle_stream(args):
+    """One (b, h) stream of the channel-wise oracle: backward (which runs the forward)."""
+    os.environ["OMP_NUM_THREADS"] = os.environ["OPENBLAS_NUM_THREADS"] = "1"
+    os.environ["MKL_NUM_THREADS"] = "1"
+    import numpy as np
+    from oracle import cw_oracle as CWO
+    q, k, v, g, b, w, S0, dO, dST = args
+    f = lambda x: None if x is None else x[None].astype(np.float64)
+    CWO.cw_fwd_streams(f(q), f(k), f(v), f(g), f(b), f(w), f(S0))
+    CWO.cw_bwd_streams(f(q), f(k), f(v), f(g), f(b), f(w), f(S0), f(dO), f(dST))
+    return q.shape[0]
+
+
+def cw_cpu_baseline(case, budget_s=15.0):
+    """The channel-wise oracle on a bounded sample of the workload's streams, all host cores."""
+    import multiprocessing as mp
+    cores, affinity = host_workers()
+    streams = [(b, h) for b in range(case.B) for h in range(case.H)]
+    per_stream_s = 3.0 * (case.T / 4096) * (case.dk * case.dv / 16384)
+    n = min(len(streams), int(max(cores, budget_s * cores / per_stream_s)))
+    sl = lambda x, b, h: None if x is None else x[b, :, h]
+    tasks = [(sl(case.q, b, h), sl(case.k, b, h), sl(case.v, b, h), sl(case.g, b, h), sl(case.b, b, h),
+              sl(case.w, b, h), case.S0[b, h], sl(case.dO, b, h), case.dS_T[b, h]) for (b, h) in streams[:n]]
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(cores) as pool:
+        done = sum(pool.map(_cw_oracle_stream, tasks, chunksize=1))
+    wall = time.perf_counter() - t0
+    return {"value": round(done / case.H / wall, 1), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": (f"{n} of {len(streams)} (b,h) streams, full T={case.T} each, float64 token-serial fwd+bwd, "
+                       f"one process per core ({cores} workers: the host's CPU share for one GPU; {affinity} "
+                       f"cores in the affinity mask); tokens/s counts all {case.H} heads ({wall:.1f} s)")}
+
+
 def bench_cw(a):
     """The channel-wise path (per-channel g, b, w) on B4 T4096 H16 d128: one JSON line."""
     import time
@@ -259,29 +297,7 @@ def bench_cw(a):
     B, T, H, dk, dv = 4, 4096, 16, 128, 128
     bf = a.cw_io == "bf16"
     case = W.make_cw_case("cw_B4_T4096_H16_d128", B, T, H, dk, dv, gates="gbw", seed=6, io_dtype=a.cw_io)
-    cpu = None
-    if not a.no_cpu_baseline:
-        # the oracle on (b, h) streams of the same inputs, one after another on
-        # one core, until about a.cpu_budget seconds of work
-        from oracle import cw_oracle as CWO
-        t0 = time.perf_counter()
-        done = 0
-        for bi in range(B):
-            for hi in range(H):
-                sl = lambda x: np.ascontiguousarray(x[bi:bi + 1, :, hi:hi + 1], dtype=np.float64)
-                args = [None if getattr(case, n) is None else sl(getattr(case, n))
-                        for n in ("q", "k", "v", "g", "b", "w")]
-                CWO.cw_oracle_bwd(*args, case.S0[bi:bi + 1, hi:hi + 1].astype(np.float64), sl(case.dO),
-                                  case.dS_T[bi:bi + 1, hi:hi + 1].astype(np.float64))  # recomputes the forward
-                done += 1
-                if time.perf_counter() - t0 >= a.cpu_budget:
-                    break
-            if time.perf_counter() - t0 >= a.cpu_budget:
-                break
-        dt = time.perf_counter() - t0
-        cpu = {"value": round(done * T / H / dt, 1), "unit": "tokens/s", "cores": 1, "kind": "oracle",
-               "sample": f"{done} of {B * H} (b,h) streams, full T={T} each, float64 token-serial fwd+bwd, "
-                         f"one after another on one core ({dt:.1f} s); tokens/s counts all {H} heads"}
+    cpu = None if a.no_cpu_baseline else cw_cpu_baseline(case, a.cpu_budget)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     t = {n: (None if getattr(case, n) is None else torch.from_numpy(getattr(case, n)).to(dev))
@@ -403,6 +419,13 @@ class Hip:
         return float(x.value)
 
 
+def host_workers():
+    """(workers, cores in the affinity mask): one worker per core, at most 16 (the
+    CPU share of one GPU on the measurement hosts)."""
+    aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    return max(1, min(aff, 16)), aff
+
+
 def _oracle_stream(args):
     """One (b, h) stream through the float64 oracle: forward then backward."""
     os.environ["OMP_NUM_THREADS"] = os.environ["OPENBLAS_NUM_THREADS"] = "1"
@@ -419,8 +442,7 @@ def _oracle_stream(args):
 def cpu_baseline(case, budget_s=15.0):
     """Time the oracle on a bounded sample of the workload's streams, all host cores."""
     import multiprocessing as mp
-    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
-    cores = max(1, min(cores, 16))
+    cores, affinity = host_workers()
     streams = [(b, h) for b in range(case.B) for h in range(case.H)]
     per_stream_s = 2.5 * (case.T / 4096) * (case.dk * case.dv / 16384)
     n = int(max(cores, min(len(streams), budget_s * cores / max(per_stream_s, 1e-3))))
@@ -440,8 +462,9 @@ def cpu_baseline(case, budget_s=15.0):
         "cores": cores,
         "kind": "oracle",
         "sample": (f"{n} of {len(streams)} (b,h) streams of the workload, full T={case.T} each, "
-                   f"float64 token-serial fwd+bwd, one process per core; tokens/s counts all "
-                   f"{case.H} heads ({token_heads} token-heads in {wall:.1f} s)"),
+                   f"float64 token-serial fwd+bwd, one process per core ({cores} workers: the "
+                   f"host's CPU share for one GPU; {affinity} cores in the affinity mask); tokens/s "
+                   f"counts all {case.H} heads ({token_heads} token-heads in {wall:.1f} s)"),
     }
 
 
@@ -586,8 +609,14 @@ def main(argv=None):
     dom = max(km, key=lambda n: stage_ms[n])
     dom_bytes, dom_flops = km[dom]
     dom_s = stage_ms[dom] / 1e3
-    ach = dom_bytes / dom_s / 1e9
     fwd_b, bwd_b = path_model(B, T, H, dk, dv, 2)
+    # the backward against its compulsory API bytes (each tensor of the gdn_bwd
+    # call read or written once at its dtype; workspace traffic excluded)
+    bwd_s = bwd_ms / 1e3
+    ach = bwd_b / bwd_s / 1e9
+    state_io = 2 * B * H * dk * dv * 4  # dS_T in, dS0 out: moved by the reverse scan
+    grad_api = bwd_b - state_io         # everything else passes through the gradient kernel
+    bwd_traffic = [measured_traffic(st) for st in ("bwd_prep", "bwd_scan", "bwd_grad")]
 
     tokens = B * T
     res = {
@@ -607,11 +636,23 @@ def main(argv=None):
         "config": {"workload": "gated delta rule fwd+bwd, bf16 I/O, fp32 state, B=4 T=4096 H=16 "
                                "dk=dv=128 chunk=64", "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "chunk": CH, "global_batch": B, "seq_len": T, "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom),
-                     "algorithmic_bytes_per_launch": int(dom_bytes),
-                     "avg_launch_ms": round(stage_ms[dom], 4),
-                     "mfma_tflops": round(dom_flops / dom_s / 1e12, 1)},
+        "roofline": {"bound": "hbm", "kernel": "gdn_bwd (bwd_prep + bwd_scan + bwd_grad + bwd_exact)",
+                     "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(ach / HBM_PEAK_GBS, 4),
+                     "traffic": (sum(bwd_traffic) if all(x is not None for x in bwd_traffic) else None),
+                     "algorithmic_bytes_per_launch": int(bwd_b),
+                     "bytes_per_token_head": round(bwd_b / (B * T * H), 1),
+                     "avg_launch_ms": round(bwd_ms, 4),
+                     "stage_ms": {n: round(stage_ms[n], 4) for n in gdn.BWD_STAGES},
+                     "dominant_kernel": {
+                         "kernel": dom, "avg_launch_ms": round(stage_ms[dom], 4),
+                         "compulsory_bytes": int(grad_api),
+                         "achieved": round(grad_api / dom_s / 1e9, 1),
+                         "frac": round(grad_api / dom_s / 1e9 / HBM_PEAK_GBS, 4),
+                         "kernel_io_bytes": int(dom_bytes),
+                         "kernel_io_frac": round(dom_bytes / dom_s / 1e9 / HBM_PEAK_GBS, 4),
+                         "traffic": measured_traffic(dom),
+                         "mfma_tflops": round(dom_flops / dom_s / 1e12, 1)}},
         "timing": {"cold_caches": True, "median_ms": round(q_(0.5), 4),
                    "iqr_ms": [round(q_(0.25), 4), round(q_(0.75), 4)],
                    "back_to_back_ms_per_step": round(ms_step_warm, 4),

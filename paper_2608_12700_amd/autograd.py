@@ -57,7 +57,8 @@ def gated_delta_rule(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: Optio
 
 
 class ChannelwiseRule(torch.autograd.Function):
-    """The channel-wise members (per-channel g, b, w; fp32): one gdn_cw_fwd and one gdn_cw_bwd."""
+    """The channel-wise members (per-channel g, b, w; bf16 or fp32 activations, fp32
+    gates): one gdn_cw_fwd and one gdn_cw_bwd."""
 
     @staticmethod
     def forward(ctx, q, k, v, g, b, w, S0, cu_seqlens):
@@ -80,8 +81,10 @@ def channelwise_rule(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: Optio
                      b: Optional[torch.Tensor] = None, w: Optional[torch.Tensor] = None,
                      S0: Optional[torch.Tensor] = None, *, cu_seqlens=None):
     """(o, S_T) of S_t = (I - k_t (b_t * k_t)^T) Diag(e^{g_t}) S_{t-1} + k_t (w_t * v_t)^T,
-    o_t = S_t^T q_t, differentiable in every tensor argument.  fp32, contiguous:
-    q, k, g, b [B,T,H,d_k]; v, w [B,T,H,d_v]; S0 [N,H,d_k,d_v].  A gate left None is
+    o_t = S_t^T q_t, differentiable in every tensor argument.  Contiguous: q, k
+    [B,T,H,d_k] and v [B,T,H,d_v] in bf16 or fp32 (one dtype; o and the activation
+    gradients follow it); g, b [B,T,H,d_k], w [B,T,H,d_v] and S0 [N,H,d_k,d_v] fp32.
+    A gate left None is
     neutral (g = 0, b = 0, w = 1): KDA passes b = w = beta broadcast over the
     channels, GLA passes g alone, LA none."""
     return ChannelwiseRule.apply(q, k, v, g, b, w, S0, cu_seqlens)

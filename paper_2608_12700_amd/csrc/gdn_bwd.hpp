@@ -1176,6 +1176,10 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
   __shared__ float hdh_w[NW];
   __shared__ __align__(16) char ub[C::UB];
   __shared__ __align__(16) bf16 Hs[HL ? DK * LH : 8];
+  // with two slices, P and (K K^T) * E wait in LDS from phase 0 to phase 2 (one
+  // column per thread, 2 * TN * 4 entries each), keeping phase 1 within 256 VGPRs
+  constexpr int NSTASH = HL ? 1 : 2 * TC::TN * 4;
+  __shared__ float stash[NSTASH][HL ? 1 : NT];
 
   // the loop-safe thread index reads this word: it is stored before any use
   if (threadIdx.x == 0) gdn_tid_bias = 0;
@@ -1209,7 +1213,7 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
   struct PreA {
     uint4 dov[NDO];                      // dO slice, staged to LDS
     bf16x8 du[CH / 32][TY::TM];          // dU'^T rows: A fragments of Y^T
-    float hk[DK / 32][TY::TM][8];        // h^T: A fragments of (K h)^T
+    bf16x8 hk[DK / 32][TY::TM];          // h^T: A fragments of (K h)^T (two slices only)
     uint2 vb[TY::TM][TY::TN];            // v[r][v0..v0+3] in the Y^T accumulator layout
   };
   struct PreB {
@@ -1262,7 +1266,8 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
         }
     }
   };
-  // h^T of a value slice
+  // h^T of a value slice, in bf16 (loaded right before its product: the fp32
+  // values are held only until they are converted)
   auto load_a2 = [&](PreA& p, const Tile& x, int c0) {
     const int l = lane_id(), lg = l >> 4, lc = l & 15;
     const float* hp = states + x.t * DK * DV;
@@ -1270,9 +1275,12 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
 #pragma unroll
       for (int s = 0; s < DK / 32; ++s)
 #pragma unroll
-        for (int a = 0; a < TY::TM; ++a)
+        for (int a = 0; a < TY::TM; ++a) {
+          float f[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) p.hk[s][a][j] = hp[(32 * s + 8 * lg + j) * DV + c0 + TY::m0(a) + lc];
+          for (int j = 0; j < 8; ++j) f[j] = hp[(32 * s + 8 * lg + j) * DV + c0 + TY::m0(a) + lc];
+          p.hk[s][a] = cvt8(f);
+        }
     }
   };
   auto load_h = [&](PreB& p, const Tile& x, int c0) {
@@ -1330,7 +1338,7 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
   PreB pb;
   load_0(p0, cur);
   load_a1(pa, cur, 0);
-  if constexpr (HL) load_b(pb, cur, 0); else load_a2(pa, cur, 0);
+  if constexpr (HL) load_b(pb, cur, 0);
   for (int tt = blockIdx.x; tt < ntiles; tt += gridDim.x) {
   const int w = wave_id(), l = lane_id(), lg = l >> 4, lc = l & 15;
   const ChunkPos cp = cur.cp;
@@ -1418,6 +1426,15 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
         ae.acc[0][b][j] = i < r ? ae.acc[0][b][j] * dd[b][j] : 0.f;
       }
   }
+  if constexpr (!HL) {
+#pragma unroll
+    for (int b = 0; b < TC::TN; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        stash[b * 4 + j][thread_x()] = pm.acc[0][b][j];
+        stash[TC::TN * 4 + b * 4 + j][thread_x()] = DT_ ? ae.acc[0][b][j] : 0.f;
+      }
+  }
 
   // ================= phase 1: value slices
   bf16* Rs = reinterpret_cast<bf16*>(ub);  // R, row-major
@@ -1435,8 +1452,8 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
     if (c0 > 0) {
       __syncthreads();  // the previous slice's LDS operands are consumed
       load_a1(pa, cur, c0);
-      load_a2(pa, cur, c0);
     }
+    if constexpr (!HL) load_a2(pa, cur, c0);
     if constexpr (DT_) {
       // R = diag(beta) (V - diag(e^G) K h), computed transposed, (K h)^T = h^T K^T,
       // so that a lane needs v[r][v0..v0+3] as one 8-byte piece (the same
@@ -1449,7 +1466,7 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
 #pragma unroll
         for (int a = 0; a < TY::TM; ++a) {
           if constexpr (HL) fa[a] = lds_frag_tr<LH>(Hs, TY::m0(a), 32 * s);
-          else fa[a] = cvt8(pa.hk[s][a]);
+          else fa[a] = pa.hk[s][a];
         }
 #pragma unroll
         for (int b = 0; b < TY::TN; ++b) {
@@ -1597,13 +1614,27 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
     }
   }
   __syncthreads();  // phase-1 LDS operands are consumed
-  // the next tile's value-slice operands (and, with two slices, q, k, T, gates)
-  if constexpr (!HL) load_0(p0, nxt);
-  load_a1(pa, nxt, 0);
+  // the next tile's value-slice operands.  With two slices (fewer waves, more
+  // accumulators per wave) they, and the next q, k, T and gates, wait until
+  // phase 2's accumulators are in LDS, so no register is held through phase 2.
+  if constexpr (HL) load_a1(pa, nxt, 0);
 
   // ================= phase 2: the chunk-level gradients
   bf16* dPmT = reinterpret_cast<bf16*>(ub);  // (dP * D)^T
   bf16* dBT = dPmT + CH * LT;                 // dB^T, dB = dA * beta_r * E (strict lower)
+  if constexpr (!HL) {
+    // this thread's own entries (no other thread writes them)
+#pragma unroll
+    for (int b = 0; b < TC::TN; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        pm.acc[0][b][j] = stash[b * 4 + j][thread_x()];
+        ae.acc[0][b][j] = stash[TC::TN * 4 + b * 4 + j][thread_x()];
+        // the decay mask is formed again rather than held through phase 1
+        const int r = TC::m0(0) + 4 * lg + j, i = TC::n0(b) + lc;
+        dd[b][j] = i <= r ? __expf(Gs[r] - Gs[i]) : 0.f;
+      }
+  }
   TC zs;  // Z = dA * A + dP * P
   float rowA_l[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1724,8 +1755,14 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
       *reinterpret_cast<uint2*>(dqst + r * LK + d0) = pack4<bf16>(q4);
       *reinterpret_cast<uint2*>(dkst + r * LK + d0) = pack4<bf16>(k4);
     }
-  // the accumulators are free: the next tile's h and dh (or h^T with two slices)
-  if constexpr (HL) load_b(pb, nxt, 0); else load_a2(pa, nxt, 0);
+  // the accumulators are free: the next tile's h and dh (with two slices: q, k,
+  // T, gates and the first slice's dO, dU'^T and v)
+  if constexpr (HL) {
+    load_b(pb, nxt, 0);
+  } else {
+    load_0(p0, nxt);
+    load_a1(pa, nxt, 0);
+  }
   __syncthreads();
   if (w == 0) {
     // dg (reverse cumsum of dG) and dbeta, while the other waves store dq, dk

@@ -11,6 +11,16 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running case")
+    # The float64 oracle's worker pool for the whole-workload comparisons is
+    # forked here, before anything in this process touches the GPU.
+    if "not gpu" not in (config.getoption("-m") or ""):
+        from tests import oracle_pool
+        oracle_pool.start()
+
+
+def pytest_unconfigure(config):
+    from tests import oracle_pool
+    oracle_pool.close()
 
 
 def _gpu_available():

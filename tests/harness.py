@@ -27,8 +27,9 @@ def device_inputs(case: W.Case, device="cuda"):
                 S0=f32(case.S0), dO=act(case.dO), dS_T=f32(case.dS_T))
 
 
-def run_device(case: W.Case, device="cuda", keep_torch=False):
-    """Forward then backward on the HIP path; returns float64 numpy outputs."""
+def run_device(case: W.Case, device="cuda", keep_torch=False, dtype=np.float64):
+    """Forward then backward on the HIP path; returns numpy outputs (float64 by
+    default; float32 holds every device value exactly too)."""
     import torch
     from paper_2608_12700_amd import gdn
     t = device_inputs(case, device)
@@ -41,7 +42,7 @@ def run_device(case: W.Case, device="cuda", keep_torch=False):
     outs = dict(o=o, S_T=S_T, states=st, dq=dq, dk=dk, dv=dv, dg=dg, dbeta=db, dS0=dS0)
     if keep_torch:
         return outs
-    return {k: (None if x is None else x.float().cpu().numpy().astype(np.float64)) for k, x in outs.items()}
+    return {k: (None if x is None else x.float().cpu().numpy().astype(dtype, copy=False)) for k, x in outs.items()}
 
 
 def run_oracle(case: W.Case, heads=None):

@@ -6,9 +6,10 @@
 * graph capture: fwd + bwd recorded once into a HIP graph and replayed several
   times, with eager work and synchronisations between replays; every replay
   must reproduce the eager outputs bit for bit;
-* a 300-step synthetic training run at L = 256 (the paper's training length):
-  a one-layer gated-delta-rule model fitted to a fixed random teacher of the
-  same architecture; the loss must fall and stay finite.
+* 300-step synthetic training runs at L = 256 (the paper's training length)
+  for the gated delta rule and the scalar-decay (SSD) member: a one-layer
+  model fitted to a fixed random teacher of the same architecture; the loss
+  must fall and stay finite.
 """
 import ctypes
 
@@ -126,9 +127,9 @@ def test_graph_capture_replay_bitwise():
 class _GDNLayer(torch.nn.Module):
     """x -> projections -> gated delta rule (HIP) -> output projection."""
 
-    def __init__(self, D, H, dk, dv):
+    def __init__(self, D, H, dk, dv, variant="gated_delta"):
         super().__init__()
-        self.H, self.dk, self.dv = H, dk, dv
+        self.H, self.dk, self.dv, self.variant = H, dk, dv, variant
         self.wq = torch.nn.Linear(D, H * dk, bias=False)
         self.wk = torch.nn.Linear(D, H * dk, bias=False)
         self.wv = torch.nn.Linear(D, H * dv, bias=False)
@@ -144,18 +145,27 @@ class _GDNLayer(torch.nn.Module):
         v = self.wv(x).view(B, L, self.H, self.dv)
         g = -0.1 * F.softplus(self.wg(x))
         beta = torch.sigmoid(self.wb(x))
+        if self.variant == "decay_only":
+            # the scalar-decay (SSD) member: no erase, so keep the state's growth
+            # in check with the key scale
+            beta = None
+            k = k * 0.5
         bf = torch.bfloat16
+        c = lambda t: None if t is None else t.float().contiguous()
         o, _ = gated_delta_rule(q.to(bf).contiguous(), k.to(bf).contiguous(), v.to(bf).contiguous(),
-                                g.float().contiguous(), beta.float().contiguous())
+                                c(g), c(beta), variant=self.variant)
         return self.wo(o.float().reshape(B, L, self.H * self.dv))
 
 
-def test_training_smoke_l256():
+@pytest.mark.parametrize("variant", ["gated_delta", "decay_only"])
+def test_training_smoke_l256(variant):
+    """300 Adam steps at L = 256: the gated delta rule and the scalar-decay (SSD)
+    member, both through the native forward and backward."""
     torch.manual_seed(0)
     dev = torch.device("cuda")
     D, H, dk, dv, B, L = 64, 2, 64, 64, 4, 256
-    teacher = _GDNLayer(D, H, dk, dv).to(dev)
-    student = _GDNLayer(D, H, dk, dv).to(dev)
+    teacher = _GDNLayer(D, H, dk, dv, variant).to(dev)
+    student = _GDNLayer(D, H, dk, dv, variant).to(dev)
     for prm in teacher.parameters():
         prm.requires_grad_(False)
     opt = torch.optim.Adam(student.parameters(), lr=3e-3)
@@ -172,5 +182,5 @@ def test_training_smoke_l256():
         losses.append(loss.item())
         assert np.isfinite(losses[-1]), (it, losses[-1])
     first, last = np.mean(losses[:10]), np.mean(losses[-10:])
-    print(f"training smoke: relative loss {first:.4f} -> {last:.4f}", flush=True)
+    print(f"training smoke {variant}: relative loss {first:.4f} -> {last:.4f}", flush=True)
     assert last < 0.2 * first, (first, last)

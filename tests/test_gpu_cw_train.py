@@ -4,7 +4,7 @@ every family member trains on the real kernels).
 * autograd (``channelwise_rule``, one gdn_cw_fwd + one gdn_cw_bwd) against the
   float64 channel-wise oracle;
 * 300-step synthetic training runs at L = 256 for the full GDN gates, KDA
-  (a scalar beta broadcast as b = w) and GLA: a one-layer model fitted to a
+  (a scalar beta broadcast as b = w), GLA and plain linear attention (LA): a one-layer model fitted to a
   fixed random teacher of the same architecture; the loss must fall and stay
   finite.
 """
@@ -63,7 +63,7 @@ class _Layer(torch.nn.Module):
         q = F.normalize(self.wq(x).view(B, L, H, dk), dim=-1)
         k = F.normalize(self.wk(x).view(B, L, H, dk), dim=-1)
         v = self.wv(x).view(B, L, H, dv)
-        g = (-0.1 * F.softplus(self.wg(x))).view(B, L, H, dk)
+        g = (-0.1 * F.softplus(self.wg(x))).view(B, L, H, dk) if self.member else None
         b = w = None
         if self.member == "gbw":
             b = torch.sigmoid(self.wb(x)).view(B, L, H, dk)
@@ -77,7 +77,13 @@ class _Layer(torch.nn.Module):
         return self.wo(o.reshape(B, L, H * dv))
 
 
-@pytest.mark.parametrize("member", ["gbw", "kda", "g"])
+# The paper notes plain linear attention (no gates) as the poorly conditioned
+# member: its state only grows, so it is held to a weaker bar (the loss must
+# still fall by a third and stay finite).
+BAR = {"gbw": 0.2, "kda": 0.2, "g": 0.2, "": 0.67}
+
+
+@pytest.mark.parametrize("member", ["gbw", "kda", "g", ""])
 def test_training_smoke_l256(member):
     torch.manual_seed(0)
     dev = torch.device("cuda")
@@ -100,5 +106,5 @@ def test_training_smoke_l256(member):
         losses.append(loss.item())
         assert np.isfinite(losses[-1]), (it, losses[-1])
     first, last = np.mean(losses[:10]), np.mean(losses[-10:])
-    print(f"{member}: relative loss {first:.4f} -> {last:.4f}", flush=True)
-    assert last < 0.2 * first, (first, last)
+    print(f"{member or 'la'}: relative loss {first:.4f} -> {last:.4f}", flush=True)
+    assert last < BAR[member] * first, (first, last)

@@ -38,6 +38,20 @@ def test_parity_small(io, B, T, H, dk, dv):
     Hn.assert_parity(res, Hn.TOL[io], case.name)
 
 
+@pytest.mark.parametrize("dv", [64, 128, 256])
+@pytest.mark.parametrize("dk", [64, 128])
+@pytest.mark.parametrize("variant", ["gated_delta", "delta", "decay_only"])
+@pytest.mark.parametrize("io", ["bf16", "f32"])
+def test_parity_every_instantiation(io, variant, dk, dv):
+    """Every compiled (dtype, member, d_k, d_v) combination: two sequences of 130
+    tokens (two whole chunks and a 2-token tail), two heads."""
+    case = _case(io, 2, 130, 2, dk, dv, variant=variant, seed=dk + dv)
+    print("case", W.describe(case), flush=True)
+    res = Hn.compare(Hn.run_device(case), Hn.run_oracle(case))
+    print({k: f"{v[0]:.2e}" for k, v in res.items()}, flush=True)
+    Hn.assert_parity(res, Hn.TOL[io], case.name)
+
+
 @pytest.mark.parametrize("variant", ["delta", "decay_only"])
 @pytest.mark.parametrize("io", ["bf16", "f32"])
 def test_parity_variants_small(variant, io):

@@ -30,14 +30,33 @@ def test_bitwise_determinism_five_runs():
             assert torch.equal(_bits(x), _bits(again[nm])), (rep, nm)
 
 
-def test_determinism_packed_and_variants():
+def _same_bits_runs(case, runs):
     import torch
-    for case in (W.config3("delta"), W.config3("decay_only")):
-        a = Hn.run_device(case, keep_torch=True)
-        b = Hn.run_device(case, keep_torch=True)
-        for nm, x in a.items():
+    first = Hn.run_device(case, keep_torch=True)
+    for rep in range(runs - 1):
+        again = Hn.run_device(case, keep_torch=True)
+        for nm, x in first.items():
             if x is not None:
-                assert torch.equal(_bits(x), _bits(b[nm])), (case.name, nm)
+                assert torch.equal(_bits(x), _bits(again[nm])), (case.name, rep, nm)
+
+
+def test_determinism_packed_and_variants():
+    cu = np.array([0, 5, 70, 71, 135, 135, 300], np.int32)
+    packed = W.make_case("bf16_packed_det", B=1, T=int(cu[-1]), H=3, dk=128, dv=256, cu_seqlens=cu)
+    for case in (W.config3("delta"), W.config3("decay_only"), W.config3("nan_elem"), packed):
+        print("case", W.describe(case), flush=True)
+        _same_bits_runs(case, 2)
+
+
+@pytest.mark.parametrize("which", ["config0", "config2_T65536", "config2_T65473", "config4"])
+def test_determinism_other_workloads(which):
+    """dg, dbeta and every other output bitwise equal over three runs on the
+    small fp32 workload, the long sequence (full and ragged tail) and the packed
+    variable-length batch."""
+    case = {"config0": W.config0, "config4": W.config4}.get(which) or (lambda: W.config2(int(which.split("T")[1])))
+    case = case()
+    print("case", W.describe(case), flush=True)
+    _same_bits_runs(case, 3)
 
 
 SENT = {"bf16": 0x7FA1, "f32": 0x7FC0DEAD}  # NaN payloads nothing in the path produces

@@ -91,8 +91,10 @@ typedef enum {
   GDN_ERR_ALIAS = -6,       /* an output overlaps an input or another output */
   GDN_ERR_VARLEN = -7,      /* cu_seqlens not 0-based, non-decreasing, ending at T */
   GDN_ERR_HIP = -8,         /* a kernel launch failed */
-  GDN_ERR_VARIANT = -9      /* unknown variant, or a gate pointer that the
+  GDN_ERR_VARIANT = -9,     /* unknown variant, or a gate pointer that the
                                variant forbids / requires */
+  GDN_ERR_TOO_LARGE = -10   /* gdn_fwd_noalloc: the problem's workspace exceeds
+                               GDN_NOALLOC_SCRATCH_BYTES */
 } gdn_status;
 
 typedef enum { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
@@ -136,6 +138,24 @@ gdn_status gdn_bwd(const gdn_problem* p, const void* q, const void* k, const voi
                    const float* g, const float* beta, const float* chunk_states, const void* dO,
                    const float* dS_T, void* dq, void* dk, void* dv, float* dg, float* dbeta,
                    float* dS0, void* workspace, size_t workspace_bytes, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): gdn_fwd with
+ * its workspace in a fixed array of GDN_NOALLOC_SCRATCH_BYTES that the library
+ * itself holds in device memory, one per GPU, from its first use on that GPU
+ * until the process ends.  Arguments, outputs, kernels and results are those
+ * of gdn_fwd (bitwise); the caller still provides inputs and outputs.  The
+ * call allocates and frees nothing.  A problem whose workspace
+ * (gdn_fwd_workspace_size) exceeds the array returns GDN_ERR_TOO_LARGE before
+ * anything is launched; a failed lookup of the array's device address returns
+ * GDN_ERR_HIP.  All calls on one GPU share its array: calls that overlap in
+ * time on one GPU (different streams or threads without ordering) race and
+ * must be serialised by the caller.  The array keeps the last call's contents,
+ * which no call depends on. */
+#define GDN_NOALLOC_SCRATCH_BYTES (64u << 20)
+gdn_status gdn_fwd_noalloc(const gdn_problem* p, const void* q, const void* k, const void* v,
+                           const float* g, const float* beta, const float* S0, void* o, float* S_T,
+                           float* chunk_states, void* stream);
 
 /* Stages that gdn_fwd_ex / gdn_bwd_ex can bracket with events.  Forward:
  * 0 chunk prep (UT transform and the masked in-chunk scores), 1 forward state

@@ -525,6 +525,7 @@ const char* gdn_status_str(gdn_status s) {
     case GDN_ERR_VARLEN: return "malformed cu_seqlens";
     case GDN_ERR_HIP: return "kernel launch failed";
     case GDN_ERR_VARIANT: return "unknown variant or gate pointers inconsistent with it";
+    case GDN_ERR_TOO_LARGE: return "workspace larger than the no-allocation scratch array";
   }
   return "unknown status";
 }

@@ -25,7 +25,8 @@ LIB_PATH = os.path.join(_PKG, "libgdn.so")
 GDN_OK = 0
 STATUS = {0: "GDN_OK", -1: "GDN_ERR_NULL", -2: "GDN_ERR_SHAPE", -3: "GDN_ERR_UNSUPPORTED",
           -4: "GDN_ERR_DTYPE", -5: "GDN_ERR_WORKSPACE", -6: "GDN_ERR_ALIAS", -7: "GDN_ERR_VARLEN",
-          -8: "GDN_ERR_HIP", -9: "GDN_ERR_VARIANT"}
+          -8: "GDN_ERR_HIP", -9: "GDN_ERR_VARIANT", -10: "GDN_ERR_TOO_LARGE"}
+NOALLOC_SCRATCH_BYTES = 64 << 20  # GDN_NOALLOC_SCRATCH_BYTES
 GDN_F32, GDN_BF16 = 0, 1
 VARIANTS = {"gated_delta": 0, "delta": 1, "decay_only": 2}
 CHUNK = 64
@@ -51,7 +52,7 @@ class Problem(ctypes.Structure):
 EXPORTED = ("gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_fwd",
             "gdn_bwd", "gdn_fwd_ex", "gdn_bwd_ex", "gdn_cw_fwd_workspace_size",
             "gdn_cw_bwd_workspace_size", "gdn_cw_fwd", "gdn_cw_bwd", "gdn_cw_fwd_ex", "gdn_cw_bwd_ex",
-            "gdn_status_str", "gdn_version")
+            "gdn_status_str", "gdn_version", "gdn_fwd_noalloc")
 CW_BWD_STAGES = ("cw_bwd_prep", "cw_bwd_scan", "cw_bwd_grad_v", "cw_bwd_grad_d")
 NUM_STAGES = 4
 FWD_STAGES = ("fwd_prep", "fwd_scan", "fwd_exact", None)  # the output is fused into the scan
@@ -96,6 +97,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.gdn_cw_fwd_ex.restype = ctypes.c_int
     lib.gdn_cw_bwd_ex.argtypes = [P] + [vp] * 16 + [vp, sz, vp, vp]
     lib.gdn_cw_bwd_ex.restype = ctypes.c_int
+    lib.gdn_fwd_noalloc.argtypes = [P] + [vp] * 9 + [vp]
+    lib.gdn_fwd_noalloc.restype = ctypes.c_int
     lib.gdn_status_str.argtypes = [ctypes.c_int]
     lib.gdn_status_str.restype = ctypes.c_char_p
     lib.gdn_version.argtypes = []
@@ -145,6 +148,10 @@ def gdn_bwd(p, q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg, dbeta, dS0, w
             stream) -> int:
     return int(load().gdn_bwd(ctypes.byref(p), q, k, v, g, beta, states, dO, dS_T, dq, dk, dv, dg,
                               dbeta, dS0, ws, ws_bytes, stream))
+
+
+def gdn_fwd_noalloc(p, q, k, v, g, beta, S0, o, S_T, states, stream) -> int:
+    return int(load().gdn_fwd_noalloc(ctypes.byref(p), q, k, v, g, beta, S0, o, S_T, states, stream))
 
 
 def gdn_fwd_ex(p, q, k, v, g, beta, S0, o, S_T, states, ws, ws_bytes, stream, events) -> int:
@@ -409,7 +416,7 @@ def cw_bwd(q, k, v, g, b, w, chunk_states, dO, dS_T=None, *, cu_seqlens=None, wo
 
 
 __all__ = ["load", "make_problem", "Problem", "Packed", "GdnError", "fwd", "bwd", "gdn_fwd", "gdn_bwd",
-           "gdn_fwd_ex", "gdn_bwd_ex", "NUM_STAGES", "FWD_STAGES", "BWD_STAGES",
+           "gdn_fwd_ex", "gdn_bwd_ex", "gdn_fwd_noalloc", "NOALLOC_SCRATCH_BYTES", "NUM_STAGES", "FWD_STAGES", "BWD_STAGES",
            "gdn_num_chunks", "gdn_fwd_workspace_size", "gdn_bwd_workspace_size", "gdn_status_str",
            "gdn_version", "EXPORTED", "LIB_PATH", "VARIANTS", "cw_fwd", "cw_bwd", "gdn_cw_fwd", "gdn_cw_bwd",
            "gdn_cw_fwd_ex", "gdn_cw_bwd_ex", "gdn_cw_fwd_workspace_size", "gdn_cw_bwd_workspace_size",

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_function():
 
 def test_status_strings_and_version():
     assert "gfx950" in gdn.gdn_version()
-    for code in range(0, -10, -1):
+    for code in range(0, -11, -1):
         assert gdn.gdn_status_str(code) != "unknown status"
 
 
@@ -211,3 +211,13 @@ def test_channelwise_null_alias_and_workspace():
     big = gdn.make_problem(2, 640, 4, 128, 128, io_dtype=gdn.GDN_F32)
     assert gdn.gdn_cw_fwd_workspace_size(big) > need
     assert gdn.gdn_cw_bwd_workspace_size(big) > gdn.gdn_cw_fwd_workspace_size(big)
+
+
+def test_noalloc_rejects_oversized_problems_on_the_host():
+    # the size check runs before any HIP call: no GPU is needed to see it
+    big = gdn.make_problem(4, 4096, 16, 128, 128)
+    assert gdn.gdn_fwd_workspace_size(big) > gdn.NOALLOC_SCRATCH_BYTES
+    args = [fake(i) for i in range(1, 6)] + [None] + [fake(i) for i in range(6, 9)]
+    assert gdn.gdn_fwd_noalloc(big, *args, None) == -10
+    bad = gdn.make_problem(1, 64, 1, 96, 64)
+    assert gdn.gdn_fwd_noalloc(bad, *args, None) == -3

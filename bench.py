@@ -198,10 +198,10 @@ def kernel_model(B, T, H, dk, dv, es, N=None):
         # q, W, Khat^T, P, U, gcum -> chunk states, o
         "fwd_scan": (3 * qk + pp + vv + g4 + st + vv,
                      3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
-        # q, k, g, beta, dO -> gcum, W^T, (diag(e^G) Q)^T, dO^T, P^T, T
-        "bwd_prep": (2 * qk + 2 * g4 + vv + g4 + 2 * qk + vv + 2 * pp,
+        # q, k, g, beta -> gcum, W^T, (diag(e^G) Q)^T, P^T, T
+        "bwd_prep": (2 * qk + 2 * g4 + g4 + 2 * qk + 2 * pp,
                      3 * 2 * CH * CH * dk + CH ** 3 / 3),
-        # k, gcum, W^T, Qg^T, dO^T, P^T -> dh (I/O dtype), dU'^T
+        # k, gcum, W^T, Qg^T, dO, P^T -> dh (I/O dtype), dU'^T
         "bwd_scan": (3 * qk + g4 + vv + pp + dk * dv * es + vv,
                      3 * 2 * CH * dk * dv + 2 * CH * CH * dv),
         # q, k, v, g, beta, T, states, dO, dh, dU'^T -> dq, dk, dv, dg, dbeta
@@ -641,7 +641,6 @@ def main(argv=None):
                      "frac": round(ach / HBM_PEAK_GBS, 4),
                      "traffic": (sum(bwd_traffic) if all(x is not None for x in bwd_traffic) else None),
                      "algorithmic_bytes_per_launch": int(bwd_b),
-                     "bytes_per_token_head": round(bwd_b / (B * T * H), 1),
                      "avg_launch_ms": round(bwd_ms, 4),
                      "stage_ms": {n: round(stage_ms[n], 4) for n in gdn.BWD_STAGES},
                      "dominant_kernel": {

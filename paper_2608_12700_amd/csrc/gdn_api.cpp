@@ -139,7 +139,7 @@ void layout_bwd(const Shape& s, char* base, BwdWs* w, size_t* total) {
   w->gcum = b.take<float>(tiles * kChunk);
   w->W = b.take<char>(tiles * kChunk * s.dk * s.es);
   w->QgT = b.take<char>(tiles * kChunk * s.dk * s.es);
-  w->dOT = b.take<char>(tiles * kChunk * s.dv * s.es);
+  w->dOT = b.take<char>(s.es == 2 ? 0 : tiles * kChunk * s.dv * s.es);  // the bf16 scan reads dO
   w->PT = b.take<char>(tiles * kChunk * kChunk * s.es);
   w->T = b.take<char>(tiles * kChunk * kChunk * s.es);
   w->Kh = b.take<char>(s.es == 2 ? 0 : tiles * kChunk * s.dk * s.es);  // the bf16 scan reads k

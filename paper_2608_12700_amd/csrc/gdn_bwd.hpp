@@ -46,17 +46,19 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   constexpr int LK = DK + pad_of<OP>();
   constexpr int LC = CH + 4;
   constexpr int LT = CH + pad_of<OP>();
-  constexpr int VS = TR ? DV : 64;  // value columns per slice of dO
+  // dO^T is laid out only for the fp32 scan; the bf16 scan reads dO's rows itself
+  constexpr bool DOT = !TR;
+  constexpr int VS = 64;  // value columns per slice of dO
   constexpr int LVS = VS + pad_of<OP>();
   constexpr int VE = 16 / (int)sizeof(OP);
   typedef typename vec4_of<OP>::type V4;
   // LDS regions are reused by lifetime so that two blocks fit on a CU:
   //   R1: Q, then T in fp32;  R2: K (bf16: alive through W; fp32: then T);
-  //   R3: bf16: T in bf16; fp32: (diag(beta e^G) K)^T;  R4: A in fp32, then dO.
+  //   R3: bf16: T in bf16; fp32: (diag(beta e^G) K)^T;  R4: A in fp32 (fp32: then dO).
   constexpr int R1 = CH * LK * (int)sizeof(OP) > CH * LC * 4 ? CH * LK * (int)sizeof(OP) : CH * LC * 4;
   constexpr int R2 = CH * LK * (int)sizeof(OP);
   constexpr int R3 = !DT_ ? 16 : (TR ? CH * LT * (int)sizeof(OP) : DK * LT * (int)sizeof(OP));
-  constexpr int R4 = CH * LC * 4 > CH * LVS * (int)sizeof(OP) ? CH * LC * 4 : CH * LVS * (int)sizeof(OP);
+  constexpr int R4 = (!DOT || CH * LC * 4 > CH * LVS * (int)sizeof(OP)) ? CH * LC * 4 : CH * LVS * (int)sizeof(OP);
   static_assert(TR || CH * LT * (int)sizeof(OP) <= R2, "T fits where K was");
   __shared__ __align__(16) char r1[R1];
   __shared__ __align__(16) char r2[R2];
@@ -75,21 +77,23 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
   const ChunkPos cp = chunk_pos(geo, ci);
   const long tile = (long)ci * H + h;
   const int l = lane_id(), wv = wave_id();
-  // every input row of the block is requested up front: q, k, then the dO
-  // slices (slice t of VS columns is piece t of each thread)
+  // every input row of the block is requested up front: q, k, then (fp32)
+  // the dO slices (slice t of VS columns is piece t of each thread)
   RowsIn<DK, 512, OP> qin, kin;
   qin.load(q + (cp.row0 * H + h) * DK, (long)H * DK, cp.len);
   kin.load(k + (cp.row0 * H + h) * DK, (long)H * DK, cp.len);
   const OP* dop = dO + (cp.row0 * H + h) * DV;
-  constexpr int NSL = DV / VS, NPS = CH * VS / VE / 512;  // slices; pieces per thread and slice
+  constexpr int NSL = DOT ? DV / VS : 1, NPS = DOT ? CH * VS / VE / 512 : 1;  // slices; pieces per thread and slice
   uint4 din[NSL][NPS];
+  if constexpr (DOT) {
 #pragma unroll
-  for (int t = 0; t < NSL; ++t)
+    for (int t = 0; t < NSL; ++t)
 #pragma unroll
-    for (int p = 0; p < NPS; ++p) {
-      const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), c = t * VS + (idx % (VS / VE)) * VE;
-      din[t][p] = *reinterpret_cast<const uint4*>(dop + (long)clamp_row(i, cp.len) * H * DV + c);
-    }
+      for (int p = 0; p < NPS; ++p) {
+        const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), c = t * VS + (idx % (VS / VE)) * VE;
+        din[t][p] = *reinterpret_cast<const uint4*>(dop + (long)clamp_row(i, cp.len) * H * DV + c);
+      }
+  }
   bool ok = load_gates<VAR>(g, beta, cp.row0, H, h, cp.len, Gs, Bs);
   ok &= qin.template stage<LK>(Qs, cp.len);
   ok &= kin.template stage<LK>(Ks, cp.len);
@@ -192,16 +196,6 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
       const int r = idx / (CH / VE), c = (idx - r * (CH / VE)) * VE;
       *reinterpret_cast<uint4*>(Tg + tile * CH * CH + r * CH + c) = *reinterpret_cast<const uint4*>(Tp + r * LTT + c);
     }
-    if constexpr (TR) {
-      // A is dead: stage dO row-major for its transpose below
-#pragma unroll
-      for (int p = 0; p < NPS; ++p) {
-        const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
-        const uint4 x = keep16(i < cp.len, din[0][p]);
-        ok &= finite16B<OP>(x);
-        *reinterpret_cast<uint4*>(dOs + i * LVS + v0) = x;
-      }
-    }
     // W = T diag(beta e^G) K, written transposed (d, r)
     Tiles<CH, DK, 4, 2> w;
     w.zero();
@@ -218,27 +212,12 @@ __global__ __launch_bounds__(512) void k_prep_bwd(Geo geo, int H, const OP* __re
       for (int j = 0; j < 4; ++j) v4[j] = from_f<OP>(w.acc[0][b][j]);
       *reinterpret_cast<V4*>(Wt + op_off<OP, CH>(d, r0)) = pack4<OP>(v4);
     }
-  } else if constexpr (TR) {
-    // no A: dO goes straight into its region
-#pragma unroll
-    for (int p = 0; p < NPS; ++p) {
-      const int idx = threadIdx.x + p * 512, i = idx / (VS / VE), v0 = (idx % (VS / VE)) * VE;
-      const uint4 x = keep16(i < cp.len, din[0][p]);
-      ok &= finite16B<OP>(x);
-      *reinterpret_cast<uint4*>(dOs + i * LVS + v0) = x;
-    }
   }
-  // dO^T, the scan's A operand for the injection term
-  OP* dOt = dOTg + tile * DV * CH;
-  __syncthreads();
-  if constexpr (TR) {
-#pragma unroll
-    for (int t = 0; t < DV * CH / (512 * 8); ++t) {
-      const int f = wv + 8 * t, mt = f / (CH / 32), s = f % (CH / 32);
-      *reinterpret_cast<bf16x8*>(dOt + ((long)f * 64 + l) * 8) = lds_frag_tr<LVS>(dOs, 16 * mt, 32 * s);
-    }
-  } else {
-    // in slices of VS value columns (dO slices reuse the A region)
+  if constexpr (DOT) {
+    // dO^T, the fp32 scan's A operand for the injection term, in slices of VS
+    // value columns (dO slices reuse the A region)
+    OP* dOt = dOTg + tile * DV * CH;
+    __syncthreads();
 #pragma unroll
     for (int t = 0; t < NSL; ++t) {
       const int c0 = t * VS;
@@ -442,12 +421,15 @@ __global__ __launch_bounds__(256) void k_scan_bwd(Geo geo, int H, const OP* __re
 
 // The reverse scan for bf16 operands, split into four chain waves and four
 // copy waves (the layout of the forward scan's split): every per-chunk
-// operand of the carry (K, (diag(e^G) Q)^T, W^T, this block's slice of dO^T,
+// operand of the carry (K, (diag(e^G) Q)^T, W^T, this block's columns of dO,
 // P^T and the chunk's G) goes through LDS in 1 KiB blocks, which the copy
 // waves move into one of two LDS buffers with global_load_lds_dwordx4 a chunk
 // ahead (warming L2 two chunks ahead): the prep kernel's outputs are stored
-// as MFMA fragment blocks in HBM, and k's token-major rows (the contraction
-// index d_k is contiguous there) are gathered a line at a time (RowLines).
+// as MFMA fragment blocks in HBM, k's token-major rows (the contraction
+// index d_k is contiguous there) are gathered a line at a time (RowLines),
+// and dO's rows are gathered as this block's 64 bytes of each (16 rows per
+// block, row-major), whose B fragments the chain reads down the columns with
+// the transposing load.
 // The copy waves also write the dh
 // entering each chunk out of LDS.  Per chunk:
 //   chain: dh -> LDS | barrier | inj = Qg^T dO,
@@ -458,10 +440,13 @@ template <int DK, int DV, int BV, int VAR>
 __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16* __restrict__ k,
                                                      const float* __restrict__ dST, const float* __restrict__ gcum,
                                                      const bf16* __restrict__ WTg, const bf16* __restrict__ QgTg,
-                                                     const bf16* __restrict__ dOTg, const bf16* __restrict__ PTg,
+                                                     const bf16* __restrict__ dO, const bf16* __restrict__ PTg,
                                                      bf16* __restrict__ dhg, bf16* __restrict__ dUTg,
                                                      float* __restrict__ dS0, int* __restrict__ flag) {
   static_assert(BV == SCAN_BV, "value tiles");
+  // one row of this block's dO columns is BV bf16 = 4 pieces of 16 bytes: a
+  // 1 KiB block holds 16 rows, row-major
+  static_assert(BV * 2 == 64, "four 16-byte pieces per dO row");
   constexpr int NVT = DV / BV;
   constexpr bool DT_ = VAR != VAR_DECAY;  // delta term present
   typedef RowLines<DK> KL;
@@ -470,7 +455,7 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
   typedef Tiles<DK, BV, 4, 1> HT;  // dh slice (chain waves)
   typedef Tiles<CH, BV, 4, 1> UT;  // dU' slice (chain waves)
   constexpr int NKh = (CH / 16) * (DK / 32), NQ = (DK / 16) * (CH / 32), NWT = DT_ ? NQ : 0;
-  constexpr int ND = (BV / 16) * (CH / 32), NP = (CH / 16) * (CH / 32);
+  constexpr int ND = CH * BV * 2 / 1024, NP = (CH / 16) * (CH / 32);
   constexpr int OKh = 0, OQ = OKh + NKh, OW = OQ + NQ, OD = OW + NWT, OP_ = OD + ND, NB = OP_ + NP;
   constexpr int BUF = NB * 1024 + CH * 4;  // + the chunk's G (64 fp32)
   __shared__ __align__(1024) char buf[2][BUF];
@@ -494,11 +479,16 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
     const int len = min(CH, sp.len - c * CH);
     return k + ((sp.row0 + (long)c * CH + clamp_row(r, len)) * H + h) * DK;
   };
-  // start of prep-written block j (j >= OQ)
+  // row r of this block's dO columns in chunk c (rows past the chunk's end
+  // repeat its last row; they meet zero rows of P and of (diag(e^G) Q))
+  auto do_row = [&](int c, int r) -> const bf16* {
+    const int len = min(CH, sp.len - c * CH);
+    return dO + ((sp.row0 + (long)c * CH + clamp_row(r, len)) * H + h) * DV + v0;
+  };
+  // start of prep-written block j (j >= OQ, outside the dO blocks)
   auto src_of = [&](long tile, int j) -> const bf16* {
     if (j < OW) return QgTg + tile * DK * CH + (j - OQ) * 512;
     if (j < OD) return WTg + tile * DK * CH + (j - OW) * 512;
-    if (j < OP_) return dOTg + tile * DV * CH + op_off<bf16, CH>(v0, 0) + (j - OD) * 512;
     return PTg + tile * CH * CH + (j - OP_) * 512;
   };
   // copy waves: chunk c's operands into buffer b (wave w - 4 takes every fourth block)
@@ -513,6 +503,8 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
           int r, e;
           KL::src(j - OKh, l, r, e);
           src = k_row(c, r) + e;
+        } else if (j >= OD && j < OP_) {
+          src = do_row(c, 16 * (j - OD) + (l >> 2)) + 8 * (l & 3);
         } else {
           src = src_of(tile, j) + l * 8;
         }
@@ -522,11 +514,12 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
     if (w == 4) __builtin_amdgcn_global_load_lds((gvoid*)(gcum + tile * CH + l), (lvoid*)(buf[b] + NB * 1024), 4, 0, 0);
   };
   // L2 warm-up: the NVT blocks of a stream split the shared blocks (all but
-  // the dO^T slice) and each warms its own dO^T slice, touching every
-  // 128-byte line once: one 4-byte load per lane (64 lines per instruction)
+  // the dO rows), touching every 128-byte line once, and each warms the 64
+  // lines its own dO columns lie in: one 4-byte load per lane (64 lines per
+  // instruction)
   constexpr int NSHB = NB - ND;
   constexpr int NSH = (NSHB + NVT - 1) / NVT;
-  constexpr int NWL = (NSH + ND) * 8;
+  constexpr int NWL = NSH * 8 + CH;
   constexpr int NWARM = (NWL + 255) / 256;
   auto warm = [&](int c) {
     const long tile = (long)(sp.c0 + c) * H + h;
@@ -534,24 +527,25 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
     for (int t = 0; t < NWARM; ++t) {
       int L = ((w - 4) + 4 * t) * 64 + l;
       L = L < NWL ? L : NWL - 1;
-      const int e = L >> 3;
-      int j;
-      if (e < NSH) {
-        j = e * NVT + vt;                 // index among the shared blocks
-        j = j < NSHB ? j : NSHB - 1;
-        j = j < OD ? j : j + ND;          // skip the dO^T slice
-      } else {
-        j = OD + (e - NSH);
-      }
+      // lanes past the shared lines take dO's rows: one load per lane either
+      // way (the address is selected, the load is not branched around: every
+      // iteration issues exactly one load, which the wait counts rely on)
+      const bool own = L >= NSH * 8;
+      const int Ls = own ? 0 : L;
+      const int e = Ls >> 3;
+      int j = e * NVT + vt;                 // index among the shared blocks
+      j = j < NSHB ? j : NSHB - 1;
+      j = j < OD ? j : j + ND;              // skip the dO rows
       const bf16* src;
       if (j < OQ) {
         // line (L & 7) of k block j - OKh
         int r, e;
-        KL::src(j - OKh, (L & 7) << 3, r, e);
+        KL::src(j - OKh, (Ls & 7) << 3, r, e);
         src = k_row(c, r) + (e & ~63);
       } else {
-        src = src_of(tile, j) + (L & 7) * 64;
+        src = src_of(tile, j) + (Ls & 7) * 64;
       }
+      src = own ? do_row(c, L - NSH * 8) : src;
       __builtin_amdgcn_global_load_lds((gvoid*)src, (lvoid*)sink, 4, 0, 0);
     }
   };
@@ -599,13 +593,13 @@ __global__ __launch_bounds__(512) void k_scan_bwd_ws(Geo geo, int H, const bf16*
           er[j] = r < len ? __expf(Gc[CH - 1] - Gc[r]) : 0.f;
         }
       }
-      const bf16x8* Df = reinterpret_cast<const bf16x8*>(B + OD * 1024);
+      const bf16* Drows = reinterpret_cast<const bf16*>(B + OD * 1024);  // dO[r][v], row stride BV
       const bf16x8* Pf = reinterpret_cast<const bf16x8*>(B + OP_ * 1024);
-      bf16x8 fd[CH / 32][HT::TN];  // dO^T slice: B fragments of both products
+      bf16x8 fd[CH / 32][HT::TN];  // dO columns: B fragments of both products
 #pragma unroll
       for (int st = 0; st < CH / 32; ++st)
 #pragma unroll
-        for (int bb = 0; bb < HT::TN; ++bb) fd[st][bb] = Df[((HT::n0(bb) >> 4) * (CH / 32) + st) * 64 + l];
+        for (int bb = 0; bb < HT::TN; ++bb) fd[st][bb] = lds_frag_tr<BV>(Drows, HT::n0(bb), 32 * st);
       HT inj;  // (diag(e^G) Q)^T dO, independent of the carry
       inj.zero();
 #pragma unroll
@@ -1774,6 +1768,10 @@ __global__ __launch_bounds__(DV <= 128 ? 1024 : 512) void k_grad_bf(Geo geo, int
       rx += rxp[i][r];
       rk += rkp[i][r];
     }
+    // dO is first read in full by this kernel: a NaN or Inf in row r of dO
+    // makes every entry of row r of dO h^T non-finite (Inf times 0 is NaN), and
+    // with it q_r . (dO h^T)_r, so that sum flags it
+    ok &= finite_f(rq);
     float dbv = 0.f;
 #pragma unroll
     for (int i = 0; i < C::WNv; ++i) dbv += dbYp[i][r];
@@ -1856,7 +1854,7 @@ static hipError_t launch_bwd_t(const BwdArgs& a) {
     if constexpr (sizeof(OP) == 2) {
       hipLaunchKernelGGL((k_scan_bwd_ws<DK, DV, BV, VAR>), dim3(NS * NVT), dim3(512), 0, a.stream, geo, H,
                          (const bf16*)a.k, a.dST, w.gcum, (const bf16*)w.W, (const bf16*)w.QgT,
-                         (const bf16*)w.dOT, (const bf16*)w.PT, (bf16*)w.dh, (bf16*)w.dUT, a.dS0, w.flag_scan);
+                         (const bf16*)a.dO, (const bf16*)w.PT, (bf16*)w.dh, (bf16*)w.dUT, a.dS0, w.flag_scan);
     } else {
       hipLaunchKernelGGL((k_scan_bwd<DK, DV, BV, OP, VAR>), dim3(NS * NVT), dim3(256), 0, a.stream, geo, H,
                          (const OP*)w.Kh, a.dST, w.gcum, (const OP*)w.W, (const OP*)w.QgT, (const OP*)w.dOT,

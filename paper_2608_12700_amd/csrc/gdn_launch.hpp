@@ -37,13 +37,13 @@ struct FwdArgs {
 
 struct BwdWs {
   int* chunk_off;
-  int* flag_prep;  // [chunks*H]   non-finite q, k, v, g, beta, dO in the chunk
-  int* flag_grad;  // [chunks*H]   non-finite chunk state in the chunk
+  int* flag_prep;  // [chunks*H]   non-finite q, k, g, beta (fp32: and dO) in the chunk
+  int* flag_grad;  // [chunks*H]   non-finite chunk state, v or (bf16) dO in the chunk
   int* flag_scan;  // [N*H*NVT]    non-finite dS_T slice
   float* gcum;     // [chunks*H*64]
   void* W;         // [chunks*H*dk*64] operand dtype, W^T
   void* QgT;       // [chunks*H*dk*64] operand dtype, (diag(e^G) Q)^T
-  void* dOT;       // [chunks*H*dv*64] operand dtype, dO^T
+  void* dOT;       // [chunks*H*dv*64] operand dtype, dO^T (fp32 operands only)
   void* PT;        // [chunks*H*64*64] operand dtype, P^T
   void* T;         // [chunks*H*64*64] operand dtype, T = (I + A)^{-1}
   void* Kh;        // [chunks*H*64*dk] operand dtype, diag(e^{G_last - G}) K

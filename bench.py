@@ -179,12 +179,12 @@ def copy_kernel():
     print(f"copied {COPY_BYTES} bytes x3", flush=True)
 
 
-def kernel_model(B, T, H, dk, dv, es, N=None):
+def kernel_model(B, T, H, dk, dv, es, N=None, nch=None):
     """Algorithmic bytes and flops per launch of every stage (compulsory traffic
     of the kernel's own inputs and outputs, each moved once at its stored dtype).
     """
     N = B if N is None else N
-    nch = B * (-(-T // CH))
+    nch = B * (-(-T // CH)) if nch is None else nch
     tiles = nch * H
     g4 = 4 * CH  # one fp32 per token of a chunk
     st = dk * dv * 4
@@ -338,7 +338,7 @@ def bench_cw(a):
         step(*evs[i])
     torch.cuda.synchronize()
     ms_step = sum(hip.ms(ef[0], eb[ns - 1]) for ef, eb in evs) / a.steps
-    fwd_names = ("cw_fwd_prep", "cw_fwd_scan", None, None)
+    fwd_names = ("cw_fwd_prep", "cw_fwd_scan", "cw_fwd_exact", None)
     stage_ms = {}
     for ef, eb in evs:
         for j in range(gdn.NUM_STAGES):
@@ -381,11 +381,12 @@ def bench_cw(a):
     return 0
 
 
-def path_model(B, T, H, dk, dv, es, N=None):
-    """The API's compulsory bytes for the forward and the backward."""
+def path_model(B, T, H, dk, dv, es, N=None, nch=None):
+    """The API's compulsory bytes for the forward and the backward (nch: the
+    number of chunk states, sum over sequences of ceil(L_n / 64))."""
     N = B if N is None else N
     tok = B * T * H
-    nch = B * (-(-T // CH))
+    nch = B * (-(-T // CH)) if nch is None else nch
     states = nch * H * dk * dv * 4
     s = N * H * dk * dv * 4
     fwd = tok * (2 * dk * es + dv * es + 8) + s + tok * dv * es + s + states
@@ -487,6 +488,10 @@ def main(argv=None):
                     help="measure the channel-wise path (per-channel g, b, w) instead")
     ap.add_argument("--cw-io", choices=("bf16", "f32"), default="bf16",
                     help="activation dtype of the channel-wise measurement")
+    ap.add_argument("--workload", choices=("throughput", "long", "varlen"), default="throughput",
+                    help="throughput: the metric workload (B4 T4096 H16 d128); long: B1 T65536 H16 d128 "
+                         "(1024-chunk reverse scan); varlen: 16 packed sequences, T=32768, dk=128, dv=256")
+    ap.add_argument("--long-T", type=int, default=65536, help="T of the long workload")
     ap.add_argument("--trace-out", default="kernel_trace_bf16_B4_T4096_H16_d128.md",
                     help="file name under profiles/ for --summarize-trace")
     a = ap.parse_args(argv)
@@ -521,9 +526,15 @@ def main(argv=None):
     import workloads as W
     from paper_2608_12700_amd import gdn
 
-    case = W.config1()
+    if a.workload == "long":
+        case = W.config2(a.long_T)
+    elif a.workload == "varlen":
+        case = W.config4()
+    else:
+        case = W.config1()
     # the oracle's worker processes are forked before anything touches the GPU
-    cpu = None if a.no_cpu_baseline else cpu_baseline(case, a.cpu_budget)
+    # (the CPU baseline is the metric workload's; other workloads are secondary lines)
+    cpu = None if (a.no_cpu_baseline or a.workload != "throughput") else cpu_baseline(case, a.cpu_budget)
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -534,10 +545,14 @@ def main(argv=None):
     q, k, v, dO = act(case.q), act(case.k), act(case.v), act(case.dO)
     g, beta, S0, dST = f32(case.g), f32(case.beta), f32(case.S0), f32(case.dS_T)
 
-    p = gdn.make_problem(B, T, H, dk, dv, io_dtype=gdn.GDN_BF16, variant="gated_delta")
+    packed = None if case.cu_seqlens is None else gdn.Packed(case.cu_seqlens, dev)
+    p = (gdn.make_problem(B, T, H, dk, dv, io_dtype=gdn.GDN_BF16, variant="gated_delta") if packed is None else
+         gdn.make_problem(B, T, H, dk, dv, io_dtype=gdn.GDN_BF16, variant="gated_delta", cu_host=packed.host,
+                          cu_dev_ptr=packed.dev.data_ptr()))
     nch = gdn.gdn_num_chunks(p)
+    N = case.N
     o = torch.empty_like(v)
-    S_T = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev)
+    S_T = torch.empty((N, H, dk, dv), dtype=torch.float32, device=dev)
     states = torch.empty((nch, H, dk, dv), dtype=torch.float32, device=dev)
     dq, dk_, dv_ = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     dg, db = torch.empty_like(g), torch.empty_like(beta)
@@ -605,18 +620,20 @@ def main(argv=None):
 
     ok = all(bool(torch.isfinite(x).all()) for x in (o, S_T, dq, dk_, dv_, dg, db, dS0))
 
-    km = kernel_model(B, T, H, dk, dv, 2)
+    km = kernel_model(B, T, H, dk, dv, 2, N=N, nch=nch)
     dom = max(km, key=lambda n: stage_ms[n])
     dom_bytes, dom_flops = km[dom]
     dom_s = stage_ms[dom] / 1e3
-    fwd_b, bwd_b = path_model(B, T, H, dk, dv, 2)
+    fwd_b, bwd_b = path_model(B, T, H, dk, dv, 2, N=N, nch=nch)
+    main = a.workload == "throughput"
+    traffic = measured_traffic if main else (lambda st: None)  # counters were taken on the metric workload
     # the backward against its compulsory API bytes (each tensor of the gdn_bwd
     # call read or written once at its dtype; workspace traffic excluded)
     bwd_s = bwd_ms / 1e3
     ach = bwd_b / bwd_s / 1e9
-    state_io = 2 * B * H * dk * dv * 4  # dS_T in, dS0 out: moved by the reverse scan
+    state_io = 2 * N * H * dk * dv * 4  # dS_T in, dS0 out: moved by the reverse scan
     grad_api = bwd_b - state_io         # everything else passes through the gradient kernel
-    bwd_traffic = [measured_traffic(st) for st in ("bwd_prep", "bwd_scan", "bwd_grad")]
+    bwd_traffic = [traffic(st) for st in ("bwd_prep", "bwd_scan", "bwd_grad")]
 
     tokens = B * T
     res = {
@@ -650,7 +667,7 @@ def main(argv=None):
                          "frac": round(grad_api / dom_s / 1e9 / HBM_PEAK_GBS, 4),
                          "kernel_io_bytes": int(dom_bytes),
                          "kernel_io_frac": round(dom_bytes / dom_s / 1e9 / HBM_PEAK_GBS, 4),
-                         "traffic": measured_traffic(dom),
+                         "traffic": traffic(dom),
                          "mfma_tflops": round(dom_flops / dom_s / 1e12, 1)}},
         "timing": {"cold_caches": True, "median_ms": round(q_(0.5), 4),
                    "iqr_ms": [round(q_(0.25), 4), round(q_(0.75), 4)],
@@ -666,6 +683,22 @@ def main(argv=None):
                  "stage_ms": {k_: round(x, 4) for k_, x in stage_ms.items()},
                  "outputs_finite": ok},
     }
+    # the reverse scan's serial chain: time per chunk step of the longest stream
+    max_nch = max(-(-L // CH) for (_, _, L) in case.seq_bounds())
+    res["path"]["chunks_per_stream"] = max_nch
+    res["path"]["fwd_scan_us_per_chunk"] = round(stage_ms["fwd_scan"] * 1e3 / max_nch, 3)
+    res["path"]["bwd_scan_us_per_chunk"] = round(stage_ms["bwd_scan"] * 1e3 / max_nch, 3)
+    if not main:
+        # a secondary line: the same measurement on another specified workload
+        what = {"long": f"B1 T{T} H16 d128 bf16 (long-sequence reverse-state stress, g=-0.02*softplus(N))",
+                "varlen": "packed varlen 16 sequences T32768 H16 dk128 dv256 bf16"}[a.workload]
+        res["metric"] = f"GDN fwd+bwd tokens/s at {what}; % of binding roofline"
+        res["data"] = res["data"].replace("g=-0.1", "g=-0.02") if a.workload == "long" else res["data"]
+        res["config"] = {"workload": f"gated delta rule fwd+bwd, {what}, chunk=64", "B": B, "T": T, "H": H,
+                         "dk": dk, "dv": dv, "chunk": CH, "num_seqs": N, "chunk_states": nch,
+                         "parallelism": "none (1 GPU)"}
+        if a.workload == "varlen":
+            res["config"]["cu_seqlens"] = [int(x) for x in case.cu_seqlens]
     if a.stages:
         for nm in names:
             b_, f_ = km.get(nm, (0, 0))

@@ -209,8 +209,11 @@ gdn_status gdn_bwd_ex(const gdn_problem* p, const void* q, const void* k, const 
  * block's log-decay moves by at most 32 from that row in every channel
  * (factors within e^{+-64}), else exp(G_r - G_i) is formed per term.  A g > 0
  * (growth) is computed the same way and overflows where the true values do.
- * Non-finite inputs propagate through the chunked arithmetic; there is no
- * token-serial exact pass on this path.
+ * Non-finite inputs: a (sequence, head) stream whose inputs (q, k, v, g, b, w,
+ * S0, and in the backward dO, dS_T and its chunk states) hold a NaN or Inf is
+ * recomputed token by token in fp32 in the operation order written above, as
+ * gdn_fwd / gdn_bwd do, so NaN/Inf land on exactly the outputs that order
+ * determines; the workspace holds that pass's per-block scratch.
  * Ownership, workspace, aliasing and stream rules are those of gdn_fwd /
  * gdn_bwd; the workspace sizes come from the two functions below.
  * ------------------------------------------------------------------------- */
@@ -233,9 +236,10 @@ gdn_status gdn_cw_bwd(const gdn_problem* p, const void* q, const void* k, const 
                       void* stream);
 
 /* With per-stage events as gdn_fwd_ex / gdn_bwd_ex.  Forward stages: 0 chunk
- * prep, 1 state scan with the chunk output, 2 and 3 empty.  Backward: 0 chunk
- * prep, 1 reverse state scan, 2 value-slice gradients (dv, dw and the chunk
- * products), 3 channel gradients (dq, dk, dg, db). */
+ * prep, 1 state scan with the chunk output, 2 exact token-serial pass for
+ * non-finite streams, 3 empty.  Backward: 0 chunk prep, 1 reverse state scan,
+ * 2 value-slice gradients (dv, dw and the chunk products), 3 channel gradients
+ * (dq, dk, dg, db) followed by the exact pass for non-finite streams. */
 gdn_status gdn_cw_fwd_ex(const gdn_problem* p, const void* q, const void* k, const void* v,
                          const float* g, const float* b, const float* w, const float* S0, void* o,
                          float* S_T, float* chunk_states, void* workspace, size_t workspace_bytes,

@@ -161,6 +161,7 @@ void layout_cw_fwd(const Shape& s, char* base, CwFwdWs* w, size_t* total) {
   Bump b{base};
   const size_t tiles = (size_t)s.chunks * s.H;
   w->chunk_off = b.take<int>(s.packed ? s.N + 1 : 0);
+  w->flag_prep = b.take<int>(tiles);
   w->flag_scan = b.take<int>((size_t)s.N * s.H * (s.dv / SCAN_BV));
   w->gC = b.take<float>(tiles * s.dk);
   // the scan's operands in the activation dtype
@@ -177,6 +178,8 @@ void layout_cw_bwd(const Shape& s, char* base, CwBwdWs* w, size_t* total) {
   const size_t tiles = (size_t)s.chunks * s.H;
   const size_t ck = tiles * kChunk * s.dk, cv = tiles * kChunk * s.dv, cc = tiles * kChunk * kChunk;
   w->chunk_off = b.take<int>(s.packed ? s.N + 1 : 0);
+  w->flag_prep = b.take<int>(tiles);
+  w->flag_grad = b.take<int>(tiles);
   w->flag_scan = b.take<int>((size_t)s.N * s.H * (s.dv / SCAN_BV));
   w->gC = b.take<float>(tiles * s.dk);
   // the reverse scan's operands and outputs in the activation dtype
@@ -197,6 +200,7 @@ void layout_cw_bwd(const Shape& s, char* base, CwBwdWs* w, size_t* total) {
   w->dQg = b.take<float>(ck);
   w->dKh = b.take<float>(ck);
   w->hdh = b.take<float>(tiles * s.dk);
+  w->exact = b.take<float>(exact_scratch_floats(s));
   *total = b.off;
 }
 

@@ -37,6 +37,7 @@
 #include <type_traits>
 
 #include "gdn_bwd.hpp"
+#include "gdn_cw_exact.hpp"
 #include "gdn_fwd.hpp"
 
 namespace gdn {
@@ -144,6 +145,17 @@ struct CwRows {
         *reinterpret_cast<float4*>(d + 4) = float4{f[4], f[5], f[6], f[7]};
       }
     }
+  }
+  // whether every loaded element of rows [0, len) is finite
+  __device__ __forceinline__ bool finite(int len) const {
+    bool ok = true;
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+      int idx, r, c;
+      where(t, idx, r, c);
+      if (idx < TOT && r < len) ok &= finite16B<T>(u[t]);
+    }
+    return ok;
   }
   // the same, kept in 16-bit (T = bf16 only): one 16-byte store per piece
   template <int LD>
@@ -319,7 +331,7 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
                                                  IO* __restrict__ Qgg, IO* __restrict__ Khg,
                                                  IO* __restrict__ Wg, IO* __restrict__ Ug,
                                                  IO* __restrict__ Tg, IO* __restrict__ KbGg,
-                                                 IO* __restrict__ dOTg) {
+                                                 IO* __restrict__ dOTg, int* __restrict__ flag) {
   constexpr int LK = DK + 4, LC = CH + 4, VS = 64;
   static_assert(CH * LC <= CH * LK && VS * LC <= CH * LK, "T and the (w * V)^T slices reuse Q's and K's tiles");
   __shared__ __align__(16) float Qs[CH * LK];  // Q, then T (stride LC)
@@ -361,6 +373,11 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
     doin.load(dO + bv, rsv, cp.len);
   }
   if (thread_x() == 0) wide = 0;
+  // non-finite inputs send the stream to the exact token-serial pass
+  bool ok = qin.finite(cp.len) && kin.finite(cp.len);
+  if (g) ok &= gin.finite(cp.len);
+  if (b) ok &= bin.finite(cp.len);
+  if constexpr (BWD) ok &= doin.finite(cp.len);
   qin.template stage<LK>(Qs, cp.len);
   kin.template stage<LK>(Ks, cp.len);
   if (g) gin.template stage<LK>(Gs, cp.len);
@@ -589,6 +606,8 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
     for (int t = 0; t < NSL; ++t) {
       const int c0 = t * VS;
       __syncthreads();  // K (first pass) or the previous slice is no longer read
+      ok &= vin[t].finite(cp.len);
+      if (w) ok &= win[t].finite(cp.len);
       vin[t].template stageT<LC>(Vw, cp.len);
       if (w) {
         __syncthreads();
@@ -609,6 +628,8 @@ __global__ __launch_bounds__(CW_PREP_THREADS) void k_cw_prep(Geo geo, int H, con
       }
     }
   }
+  const int bad = __syncthreads_or(!ok);
+  if (thread_x() == 0) flag[tile] = bad;
 }
 
 // Gradient kernel, value part (fp32 activations; k_cw_grad_v_bf below is the
@@ -628,7 +649,7 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
                                                    float* __restrict__ dwo, float* __restrict__ dPg,
                                                    float* __restrict__ dAg, float* __restrict__ Xg,
                                                    float* __restrict__ dQgg, float* __restrict__ dKhg,
-                                                   float* __restrict__ hdhg) {
+                                                   float* __restrict__ hdhg, int* __restrict__ flag) {
   constexpr int LK = DK + 4, LC = CH + 4, VS = 32, LV = VS + 4;
   __shared__ __align__(16) float Ts[CH * LC];
   __shared__ __align__(16) float KbG[CH * LK];
@@ -677,8 +698,11 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
   Tiles<CH, DK, 4, 2> X, dQg, dKh;
   dP.zero(); dA.zero(); X.zero(); dQg.zero(); dKh.zero();
   float hdh = 0.f;  // thread d < DK: sum over v of h[d][v] dh[d][v]
+  bool ok = true;   // v and w finite (the chunk state through <h, dh>)
 #pragma unroll
   for (int c0 = 0; c0 < DV; c0 += VS) {
+    ok &= cur.v.finite(cp.len);
+    if (w) ok &= cur.w.finite(cp.len);
     cur.v.template stage<LV>(Vs, cp.len);
     if (w) cur.w.template stage<LV>(Ws, cp.len);
     cur.dO.template stage<LV>(dOs, cp.len);
@@ -743,6 +767,10 @@ __global__ __launch_bounds__(512) void k_cw_grad_v(Geo geo, int H, const float* 
   dQg.each([&](int r, int d, float& x) { Qt[r * DK + d] = x; });
   dKh.each([&](int r, int d, float& x) { Kt[r * DK + d] = x; });
   if (thread_x() < DK) hdhg[tile * DK + thread_x()] = hdh;
+  // a non-finite element of h (or dh) leaves its row's <h, dh> non-finite
+  if (thread_x() < DK) ok &= finite_f(hdh);
+  const int bad = __syncthreads_or(!ok);
+  if (thread_x() == 0) flag[tile] = bad;
 }
 
 // Gradient kernel, value part, bf16 activations: the products of k_cw_grad_v
@@ -761,7 +789,7 @@ __global__ __launch_bounds__(512) void k_cw_grad_v_bf(Geo geo, int H, const bf16
                                                       float* __restrict__ dwo, float* __restrict__ dPg,
                                                       float* __restrict__ dAg, float* __restrict__ Xg,
                                                       float* __restrict__ dQgg, float* __restrict__ dKhg,
-                                                      float* __restrict__ hdhg) {
+                                                      float* __restrict__ hdhg, int* __restrict__ flag) {
   constexpr int VS = 32, PD = pad_of<bf16>(), LK = DK + PD, LC = CH + PD, LV = VS + PD, LW = VS + 4;
   __shared__ __align__(16) bf16 Ts[CH * LC];                                 // T [i][r]
   __shared__ __align__(16) bf16 KbG[CH * LK];                                // Gamma * Kb [r][d]
@@ -808,8 +836,11 @@ __global__ __launch_bounds__(512) void k_cw_grad_v_bf(Geo geo, int H, const bf16
   Tiles<CH, DK, 4, 2> X, dQg, dKh;
   dP.zero(); dA.zero(); X.zero(); dQg.zero(); dKh.zero();
   float hdh = 0.f;  // thread d < DK: sum over v of h[d][v] dh[d][v]
+  bool ok = true;   // v and w finite (the chunk state through <h, dh>)
 #pragma unroll
   for (int c0 = 0; c0 < DV; c0 += VS) {
+    ok &= cur.v.finite(cp.len);
+    if (w) ok &= cur.w.finite(cp.len);
     cur.v.template stage16<LV>(Vs, cp.len);
     if (w) cur.w.template stage<LW>(Ws, cp.len);
     cur.dO.template stage16<LV>(dOs, cp.len);
@@ -875,6 +906,10 @@ __global__ __launch_bounds__(512) void k_cw_grad_v_bf(Geo geo, int H, const bf16
   dQg.each([&](int r, int d, float& x) { Qt[r * DK + d] = x; });
   dKh.each([&](int r, int d, float& x) { Kt[r * DK + d] = x; });
   if (thread_x() < DK) hdhg[tile * DK + thread_x()] = hdh;
+  // a non-finite element of h (or dh) leaves its row's <h, dh> non-finite
+  if (thread_x() < DK) ok &= finite_f(hdh);
+  const int bad = __syncthreads_or(!ok);
+  if (thread_x() == 0) flag[tile] = bad;
 }
 
 // Gradient kernel, channel part: one block per (chunk, head, 32 channels).
@@ -1087,7 +1122,7 @@ static hipError_t launch_cw_fwd_t(const CwFwdArgs& a) {
     hipLaunchKernelGGL((k_cw_prep<DK, DV, false, IO>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream,
                        geo, H, (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, (const IO*)nullptr,
                        w.gC, (IO*)w.P, (IO*)w.Qg, (IO*)w.KhT, (IO*)w.W, (IO*)w.U,
-                       (IO*)nullptr, (IO*)nullptr, (IO*)nullptr);
+                       (IO*)nullptr, (IO*)nullptr, (IO*)nullptr, w.flag_prep);
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0)
@@ -1096,6 +1131,10 @@ static hipError_t launch_cw_fwd_t(const CwFwdArgs& a) {
                        (const IO*)w.KhT, (const IO*)w.P, (const IO*)w.U, a.states, a.ST, (IO*)a.o,
                        w.flag_scan);
   stage_mark(a.events, 2, a.stream);
+  if (NS > 0)
+    hipLaunchKernelGGL((k_cw_exact_fwd<DK, DV, IO>), dim3(NS), dim3(DV), 0, a.stream, geo, (const IO*)a.q,
+                       (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, a.S0, (IO*)a.o, a.ST, a.states,
+                       w.flag_prep, w.flag_scan, NVT);
   stage_mark(a.events, 3, a.stream);
   stage_mark(a.events, 4, a.stream);
   return hipGetLastError();
@@ -1116,7 +1155,7 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
     hipLaunchKernelGGL((k_cw_prep<DK, DV, true, IO>), dim3(geo.total_chunks, H), dim3(CW_PREP_THREADS), 0, a.stream,
                        geo, H, (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, (const IO*)a.dO,
                        w.gC, (IO*)w.PT, (IO*)w.QgT, (IO*)w.Kh, (IO*)w.WT, (IO*)nullptr, (IO*)w.T,
-                       (IO*)w.KbG, (IO*)w.dOT);
+                       (IO*)w.KbG, (IO*)w.dOT, w.flag_prep);
   stage_mark(a.events, 1, a.stream);
   const int NS = geo.N * H;
   if (NS > 0)
@@ -1129,12 +1168,12 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
       hipLaunchKernelGGL((k_cw_grad_v_bf<DK, DV>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
                          (const bf16*)a.v, a.w, (const bf16*)a.dO, a.states, (const bf16*)w.T, (const bf16*)w.KbG,
                          (const bf16*)w.dh, (const bf16*)w.dUT, (bf16*)a.dv_, a.dw, w.dP, w.dA, w.X, w.dQg,
-                         w.dKh, w.hdh);
+                         w.dKh, w.hdh, w.flag_grad);
     else
       hipLaunchKernelGGL((k_cw_grad_v<DK, DV>), dim3(geo.total_chunks, H), dim3(512), 0, a.stream, geo, H,
                          (const float*)a.v, a.w, (const float*)a.dO, a.states, (const float*)w.T,
                          (const float*)w.KbG, (const float*)w.dh, (const float*)w.dUT, (float*)a.dv_, a.dw, w.dP,
-                         w.dA, w.X, w.dQg, w.dKh, w.hdh);
+                         w.dA, w.X, w.dQg, w.dKh, w.hdh, w.flag_grad);
     stage_mark(a.events, 3, a.stream);
     const long tiles = (long)geo.total_chunks * H;
     hipLaunchKernelGGL((k_cw_grad_d<DK, IO>), dim3((unsigned)((tiles + 7) / 8 * 8 * (DK / 32))), dim3(512), 0,
@@ -1143,6 +1182,11 @@ static hipError_t launch_cw_bwd_t(const CwBwdArgs& a) {
   } else {
     stage_mark(a.events, 3, a.stream);
   }
+  if (NS > 0)
+    hipLaunchKernelGGL((k_cw_exact_bwd<DK, DV, IO>), dim3(EXACT_SLOTS), dim3(DV), 0, a.stream, geo,
+                       (const IO*)a.q, (const IO*)a.k, (const IO*)a.v, a.g, a.b, a.w, a.states, (const IO*)a.dO,
+                       a.dST, (IO*)a.dq, (IO*)a.dk_, (IO*)a.dv_, a.dg, a.db, a.dw, a.dS0, w.flag_prep,
+                       w.flag_grad, w.flag_scan, NVT, w.exact);
   stage_mark(a.events, 4, a.stream);
   return hipGetLastError();
 }

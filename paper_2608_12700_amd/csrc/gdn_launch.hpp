@@ -95,7 +95,8 @@ constexpr int grad_region_bytes(int dk, int es) {
 // scans' operands in the activation dtype, everything else fp32).  A NULL gate is neutral: g = 0, b = 0 (no erase), w = 1.
 struct CwFwdWs {
   int* chunk_off;
-  int* flag_scan;  // [N*H*NVT] written by the generic scan, not read
+  int* flag_prep;  // [chunks*H]   non-finite q, k, v, g, b, w in the chunk
+  int* flag_scan;  // [N*H*NVT]    non-finite S0 slice
   float* gC;       // [chunks*H*dk]    G of each chunk's last row, per channel
   // the scan's operands, in the activation dtype, op_off layout (U: accumulator tiles)
   void* W;         // [chunks*H*64*dk] T (Gamma * b * K)
@@ -119,7 +120,9 @@ struct CwFwdArgs {
 
 struct CwBwdWs {
   int* chunk_off;
-  int* flag_scan;
+  int* flag_prep;  // [chunks*H]   non-finite q, k, g, b, dO in the chunk
+  int* flag_grad;  // [chunks*H]   non-finite v, w or chunk state in the chunk
+  int* flag_scan;  // [N*H*NVT]    non-finite dS_T slice
   float* gC;   // [chunks*H*dk]
   // the reverse scan's operands and outputs, in the activation dtype, op_off layout
   void* WT;    // [chunks*H*dk*64]
@@ -139,6 +142,7 @@ struct CwBwdWs {
   float* dQg;  // [chunks*H*64*dk]
   float* dKh;  // [chunks*H*64*dk]
   float* hdh;  // [chunks*H*dk]
+  float* exact;  // the exact backward's per-slot chunk replay
 };
 
 struct CwBwdArgs {

@@ -19,7 +19,7 @@ import pytest
 from paper_2608_12700_amd import build as Bld
 
 LDS_BYTES = 160 * 1024
-EXEMPT = ("k_exact_fwd", "k_exact_bwd")
+EXEMPT = ("k_exact_fwd", "k_exact_bwd", "k_cw_exact_fwd", "k_cw_exact_bwd")
 
 
 def _short(mangled):

@@ -132,6 +132,48 @@ def summarize_counters(fetch_dir, write_dir, calib_fetch_dir, calib_write_dir, c
             "kernels": kern}
 
 
+SQ_FILE = os.path.join(ROOT, "profiles", "sq_counters_bf16_B4_T4096_H16_d128.json")
+
+
+def summarize_sq(dirs, command):
+    """Per stage of the metric workload: SQ instruction counters from rocprofv3
+    --pmc passes (one folder per pass), averaged over dispatches, as totals per
+    launch and per wave; plus the ratios the kernel designs are judged by."""
+    acc = {}
+    for d in dirs:
+        for r in _counter_rows(d):
+            st = None
+            for k, stg in STAGE_OF_KERNEL.items():
+                if k in r["Kernel_Name"]:
+                    st = stg
+            if st is None:
+                continue
+            acc.setdefault(st, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    km = kernel_model(4, 4096, 16, 128, 128, 2)
+    out = {}
+    for st, cs in sorted(acc.items()):
+        avg = {c: sum(v) / len(v) for c, v in cs.items()}
+        waves = avg.get("SQ_WAVES", 0.0)
+        e = {"per_launch": {c: round(x) for c, x in avg.items()}}
+        if waves:
+            e["per_wave"] = {c: round(x / waves, 1) for c, x in avg.items()
+                             if c.startswith("SQ_INSTS") or c.startswith("SQ_LDS")}
+        if avg.get("SQ_INSTS_MFMA"):
+            e["valu_per_mfma"] = round(avg.get("SQ_INSTS_VALU", 0.0) / avg["SQ_INSTS_MFMA"], 2)
+        if avg.get("SQ_ACTIVE_INST_LDS"):
+            e["lds_bank_conflict_per_lds_active_cycle"] = round(
+                avg.get("SQ_LDS_BANK_CONFLICT", 0.0) / avg["SQ_ACTIVE_INST_LDS"], 3)
+        if avg.get("SQ_BUSY_CYCLES"):
+            e["valu_mfma_busy_per_busy_cycle"] = round(avg.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / avg["SQ_BUSY_CYCLES"], 4)
+        if st in km:
+            e["model_flops_per_launch"] = int(km[st][1])
+        out[st] = e
+    return {"source_digest": source_digest(), "command": command,
+            "note": "SQ_* counters summed over the device per dispatch (rocprofv3 --pmc), averaged over the "
+                    "dispatches of the run; per_wave = per launch / SQ_WAVES",
+            "stages": out}
+
+
 def summarize_trace(trace_dir, command, title="gated delta rule fwd+bwd, bf16 I/O, B=4 T=4096 H=16 dk=dv=128"):
     """Markdown table of a `rocprofv3 --kernel-trace --stats --output-format csv` run."""
     import csv
@@ -483,6 +525,8 @@ def main(argv=None):
                     help="write the traffic summary from four rocprofv3 --pmc output folders")
     ap.add_argument("--summarize-trace", metavar="TRACE", help="write the kernel-trace summary of a "
                     "rocprofv3 --kernel-trace --stats --output-format csv folder")
+    ap.add_argument("--summarize-sq", nargs="+", metavar="DIR", help="write the SQ counter summary of "
+                    "rocprofv3 --pmc output folders (one per pass)")
     ap.add_argument("--command", default="", help="the profiling command recorded in the summary")
     ap.add_argument("--cw", action="store_true",
                     help="measure the channel-wise path (per-channel g, b, w) instead")
@@ -505,6 +549,12 @@ def main(argv=None):
         with open(os.path.join(ROOT, "profiles", a.trace_out), "w") as fh:
             fh.write(md)
         print(md)
+        return 0
+    if a.summarize_sq:
+        t = summarize_sq(a.summarize_sq, a.command)
+        with open(SQ_FILE, "w") as fh:
+            json.dump(t, fh, indent=1)
+        print(json.dumps(t)[:2000])
         return 0
     if a.summarize_counters:
         t = summarize_counters(*a.summarize_counters, a.command, cw=a.cw, cw_es=2 if a.cw_io == "bf16" else 4)

@@ -414,6 +414,9 @@ def bench_cw(a):
     }
     if a.stages:
         for nm, x in stage_ms.items():
+            if nm not in km:  # the exact pass (reads its flags; recomputes flagged streams only)
+                print(f"{nm:14s} {x*1e3:9.1f} us", file=sys.stderr)
+                continue
             b_, f_ = km[nm]
             print(f"{nm:14s} {x*1e3:9.1f} us  {b_/(x/1e3)/1e9:8.1f} GB/s  {f_/(x/1e3)/1e12:7.1f} TFLOP/s",
                   file=sys.stderr)
